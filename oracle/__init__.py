@@ -1,0 +1,202 @@
+"""CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+ctypes wrapper around ``liboracle.so`` (built from ``oracle.cpp`` with g++).
+Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its binding) never loads it.
+
+Every routine follows the paper "Learning to Optimize Tensor Programs":
+templates and knobs (Section 2), loop-context features (Appendix A.2), the
+gradient-boosted tree model (Section 3.1), parallel simulated annealing
+(Section 3.3, Algorithm 1).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+
+def build() -> str:
+    """Compile the oracle (single-threaded, no FMA contraction, no fast-math)."""
+    cmd = ["g++", "-O2", "-std=c++17", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-o", _LIB + ".tmp", _SRC]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64
+        L.or_space_create.argtypes = [i32, vp, i32, ctypes.POINTER(vp)]
+        L.or_space_destroy.argtypes = [vp]
+        L.or_space_destroy.restype = None
+        L.or_space_info.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.or_knob_split.argtypes = [vp, i32, i64, vp]
+        L.or_decode.argtypes = [vp, u64, vp]
+        L.or_encode.argtypes = [vp, vp, vp]
+        L.or_loop_quantities.argtypes = [vp, u64, vp]
+        L.or_features.argtypes = [vp, vp, i64, vp]
+        L.or_predict.argtypes = [i32, i32, i32, vp, vp, vp, vp, i64, vp, vp]
+        L.or_philox.argtypes = [u64, vp, vp]
+        L.or_philox.restype = None
+        L.or_thresholds.argtypes = [u64, i64, i64, u64, i32, vp]
+        L.or_sa_run.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp, vp, u64, i64, i64, i32,
+                                i32, vp, i32, vp, vp, vp, vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(st: int, what: str):
+    if st != 0:
+        raise ValueError(f"oracle {what} failed with status {st}")
+
+
+TOP_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("valid", "<u4")])
+
+
+class Space:
+    """A schedule space: template + shape (Section 2)."""
+
+    def __init__(self, template: int, shape):
+        self.template = int(template)
+        self.shape = tuple(int(s) for s in shape)
+        sh = np.asarray(self.shape, dtype=np.int64)
+        h = ctypes.c_void_p()
+        _check(lib().or_space_create(self.template, _p(sh), len(sh), ctypes.byref(h)), "space_create")
+        self._h = h
+        nk, nl, nf = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        nc = ctypes.c_uint64()
+        sizes = np.zeros(16, dtype=np.int64)
+        lib().or_space_info(h, ctypes.byref(nk), _p(sizes), ctypes.byref(nl), ctypes.byref(nf), ctypes.byref(nc))
+        self.n_knobs = nk.value
+        self.knob_sizes = sizes[: nk.value].copy()
+        self.n_loops = nl.value
+        self.n_features = nf.value
+        self.n_configs = nc.value
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and _lib is not None:
+            _lib.or_space_destroy(self._h)
+            self._h = None
+
+    def split(self, knob: int, idx: int) -> tuple:
+        f = np.zeros(8, dtype=np.int64)
+        k = lib().or_knob_split(self._h, knob, idx, _p(f))
+        if k < 0:
+            raise ValueError("not a split knob value")
+        return tuple(int(x) for x in f[:k])
+
+    def decode(self, cfg: int) -> np.ndarray:
+        v = np.zeros(self.n_knobs, dtype=np.int64)
+        _check(lib().or_decode(self._h, int(cfg), _p(v)), "decode")
+        return v
+
+    def encode(self, values) -> int:
+        v = np.ascontiguousarray(values, dtype=np.int64)
+        out = ctypes.c_uint64()
+        _check(lib().or_encode(self._h, _p(v), ctypes.byref(out)), "encode")
+        return out.value
+
+    def loop_quantities(self, cfg: int) -> np.ndarray:
+        """[n_loops, 3 + 3*n_buffers] raw quantities: ext, ann, bottom_up,
+        then (touched, reuse, stride) per buffer."""
+        out = np.zeros(self.n_loops * 12, dtype=np.int64)
+        _check(lib().or_loop_quantities(self._h, int(cfg), _p(out)), "loop_quantities")
+        return out.reshape(self.n_loops, 12)
+
+    def features(self, cfgs) -> np.ndarray:
+        c = np.ascontiguousarray(cfgs, dtype=np.uint64)
+        out = np.zeros((len(c), self.n_features), dtype=np.int32)
+        _check(lib().or_features(self._h, _p(c), len(c), _p(out)), "features")
+        return out
+
+
+def predict(fid, thr, leaf, feats, want_leaves=False):
+    """fp32 ensemble scores (left fold in tree order) and optionally leaf indices."""
+    fid = np.ascontiguousarray(fid, dtype=np.uint8)
+    thr = np.ascontiguousarray(thr, dtype=np.uint8)
+    leaf = np.ascontiguousarray(leaf, dtype=np.float32)
+    feats = np.ascontiguousarray(feats, dtype=np.int32)
+    T, n_int = fid.shape
+    depth = int(n_int + 1).bit_length() - 1
+    n, F = feats.shape
+    scores = np.zeros(n, dtype=np.float32)
+    leaves = np.zeros((n, T), dtype=np.uint16) if want_leaves else None
+    _check(lib().or_predict(T, depth, F, _p(fid), _p(thr), _p(leaf), _p(feats), n, _p(scores),
+                            _p(leaves) if want_leaves else None), "predict")
+    return (scores, leaves) if want_leaves else scores
+
+
+def philox(seed: int, ctr) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().or_philox(int(seed), _p(c), _p(out))
+    return out
+
+
+def thresholds(seed: int, chain0: int, n_chains: int, step_base: int, steps: int) -> np.ndarray:
+    out = np.zeros((n_chains, steps), dtype=np.float32)
+    _check(lib().or_thresholds(int(seed), chain0, n_chains, step_base, steps, _p(out)), "thresholds")
+    return out
+
+
+class Chains:
+    """Persistent annealing chain state (Section 3.3)."""
+
+    MAX_KNOBS = 8
+
+    def __init__(self, spaces, offsets, seed: int, chain0: int, topk: int):
+        self.spaces = list(spaces)
+        self.offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+        self.n = int(self.offsets[-1])
+        self.seed, self.chain0, self.topk = int(seed), int(chain0), int(topk)
+        self.knobs = np.zeros((self.n, self.MAX_KNOBS), dtype=np.int64)
+        self.score = np.zeros(self.n, dtype=np.float32)
+        self.initialised = np.zeros(self.n, dtype=np.uint8)
+        self.step_abs = np.zeros(self.n, dtype=np.uint64)
+        self.top = np.zeros((self.n, self.topk), dtype=TOP_DTYPE)
+
+    def cur_cfgs(self) -> np.ndarray:
+        out = np.zeros(self.n, dtype=np.uint64)
+        for w, sp in enumerate(self.spaces):
+            for c in range(int(self.offsets[w]), int(self.offsets[w + 1])):
+                out[c] = sp.encode(self.knobs[c, : sp.n_knobs])
+        return out
+
+    def run(self, ensemble, steps: int, thr, trace=False):
+        fid, thr_nodes, leaf = (np.ascontiguousarray(a) for a in ensemble)
+        fid = fid.astype(np.uint8, copy=False)
+        thr_nodes = thr_nodes.astype(np.uint8, copy=False)
+        leaf = leaf.astype(np.float32, copy=False)
+        T, n_int = fid.shape
+        depth = int(n_int + 1).bit_length() - 1
+        F = self.spaces[0].n_features
+        thr = np.ascontiguousarray(thr, dtype=np.float32).reshape(self.n, steps)
+        handles = (ctypes.c_void_p * len(self.spaces))(*[s._h.value for s in self.spaces])
+        tr = np.zeros((self.n, steps), dtype=TOP_DTYPE) if trace else None
+        st = lib().or_sa_run(handles, len(self.spaces), _p(self.offsets), T, depth, F,
+                             _p(fid), _p(thr_nodes), _p(leaf), self.seed, self.chain0, self.n,
+                             self.topk, steps, _p(thr), self.MAX_KNOBS, _p(self.knobs),
+                             _p(self.score), _p(self.initialised), _p(self.step_abs),
+                             _p(self.top), _p(tr) if trace else None)
+        _check(st, "sa_run")
+        return tr

@@ -1,0 +1,106 @@
+"""Seeded synthetic inputs shared by the tests, the bench and the smoke check.
+
+This module holds the workload recipes (template shapes, ensemble sizes, chain
+counts) and the seeded generators of the *inputs* the method consumes: the
+tree-ensemble arrays and the uniformly random configuration indices of the
+batched-scoring workload.  It performs none of the method's arithmetic: no
+knob decoding, no loop features, no tree traversal, no annealing.  Neither the
+HIP library nor the CPU oracle imports it; callers pass its arrays to both.
+
+Shapes follow the paper: the GEMM expression of Section 2 and the twelve
+ResNet-18 conv2d operators of Table 1.  The trained XGBoost models of the
+paper are not available, so a synthetic ensemble of full-depth trees stands in
+for them: split feature uniform over [0, F), integer threshold uniform over
+[0, 33), leaf value float32(N(0,1) * 0.05).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+GEMM = 0
+CONV2D = 1
+
+# Table 1: (H/W, IC, OC, kernel, stride) of the conv2d operators of ResNet-18.
+TABLE1 = {
+    "C1": (224, 3, 64, 7, 2),
+    "C2": (56, 64, 64, 3, 1),
+    "C3": (56, 64, 64, 1, 1),
+    "C4": (56, 64, 128, 3, 2),
+    "C5": (56, 64, 128, 1, 2),
+    "C6": (28, 128, 128, 3, 1),
+    "C7": (28, 128, 256, 3, 2),
+    "C8": (28, 128, 256, 1, 2),
+    "C9": (14, 256, 256, 3, 1),
+    "C10": (14, 256, 512, 3, 2),
+    "C11": (14, 256, 512, 1, 2),
+    "C12": (7, 512, 512, 3, 1),
+}
+
+
+def conv_shape(name: str) -> tuple:
+    """Conv shape tuple (N, C, H, W, K, KH, KW, pad, stride) for a Table 1 row.
+
+    Padding is (kernel-1)/2 (same padding), the reading that yields the output
+    sizes 112/56/28/14/7 of the ResNet-18 stages.
+    """
+    hw, ic, oc, k, s = TABLE1[name]
+    return (1, ic, hw, hw, oc, k, k, (k - 1) // 2, s)
+
+
+GEMM_512 = (512, 512, 512)
+
+# The five synthetic workloads.  "sa" workloads run annealing chains; "score"
+# scores a batch of random configurations.  Seeds: ensemble 1000+i,
+# annealing 2000+i, random configurations 3000+i.
+WORKLOADS = {
+    "gemm512_sa": dict(
+        index=0, kind="sa", spaces=[(GEMM, GEMM_512)], trees=100, depth=6,
+        chains_per_space=64, steps=500, topk=8, ens_seed=1000, sa_seed=2000),
+    "conv_c2_sa": dict(
+        index=1, kind="sa", spaces=[(CONV2D, conv_shape("C2"))], trees=500,
+        depth=8, chains_per_space=1024, steps=500, topk=16, ens_seed=1001,
+        sa_seed=2001),
+    "conv_c2_score1m": dict(
+        index=2, kind="score", spaces=[(CONV2D, conv_shape("C2"))], trees=1000,
+        depth=8, n_cfgs=1 << 20, ens_seed=1002, cfg_seed=3002),
+    "conv_c12_sa": dict(
+        index=3, kind="sa", spaces=[(CONV2D, conv_shape("C12"))], trees=2000,
+        depth=10, chains_per_space=8192, steps=1000, topk=32, ens_seed=1003,
+        sa_seed=2003),
+    "resnet18_12conv_sa": dict(
+        index=4, kind="sa",
+        spaces=[(CONV2D, conv_shape(f"C{i}")) for i in range(1, 13)],
+        trees=1000, depth=8, chains_per_space=512, steps=500, topk=16,
+        ens_seed=1004, sa_seed=2004),
+}
+
+
+def n_features_of(template: int) -> int:
+    """Loop-context feature count: 10 GEMM loops or 16 conv loops, 11 each."""
+    return 110 if template == GEMM else 176
+
+
+def make_ensemble(n_trees: int, depth: int, n_features: int, seed: int):
+    """Synthetic full-depth tree ensemble, heap-ordered nodes.
+
+    Returns (fid uint8 [T, 2^d-1], thr uint8 [T, 2^d-1], leaf float32 [T, 2^d]).
+    """
+    if not (1 <= depth <= 15 and 1 <= n_features <= 256 and n_trees >= 1):
+        raise ValueError("unsupported ensemble size")
+    rng = np.random.default_rng(seed)
+    n_int = (1 << depth) - 1
+    fid = rng.integers(0, n_features, size=(n_trees, n_int), dtype=np.int64)
+    thr = rng.integers(0, 33, size=(n_trees, n_int), dtype=np.int64)
+    leaf = (rng.standard_normal(size=(n_trees, 1 << depth)) * 0.05).astype(np.float32)
+    return fid.astype(np.uint8), thr.astype(np.uint8), leaf
+
+
+def make_configs(n: int, n_configs: int, seed: int) -> np.ndarray:
+    """n configuration indices drawn uniformly from [0, n_configs) (uint64)."""
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, n_configs, size=n, dtype=np.uint64)
+
+
+def chain_offsets(n_spaces: int, chains_per_space: int) -> np.ndarray:
+    """Contiguous chain ranges per space: space w owns [w*c, (w+1)*c)."""
+    return np.arange(n_spaces + 1, dtype=np.int64) * chains_per_space
