@@ -1,0 +1,201 @@
+/*
+ * autotensor.h -- C ABI of the MI355X (gfx950) annealing hot path of
+ * "Learning to Optimize Tensor Programs" (Chen et al., NeurIPS 2018).
+ *
+ * The library explores a schedule template's knob space with many
+ * independent simulated-annealing chains whose energy is a gradient-boosted
+ * tree cost model over loop-context features (Section 3.3, Algorithm 1;
+ * Section 3.1; Appendix A.2).  Every compute call runs hand-written HIP
+ * kernels on the GPU; nothing here falls back to the CPU.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers tagged "device" are caller-owned device allocations (HIP
+ *     device memory, e.g. PyTorch tensors); "host" pointers are ordinary
+ *     host memory.  The caller keeps every buffer alive until the stream work
+ *     that uses it has completed.
+ *   - Handles (at_space_t, at_ensemble_t, at_chains_t) are library-owned
+ *     and released with the matching *_destroy call.  A handle is bound to
+ *     the device that was current when it was created.
+ *   - Compute calls (at_extract_features, at_gbt_predict, at_sa_run,
+ *     at_sa_run_traced, at_chains_export) only enqueue work on the given
+ *     stream (0 = the null stream) and return without synchronising.
+ *     Create calls are synchronous.
+ *   - Every call returns an at_status.  Argument errors are reported before
+ *     anything is enqueued.  at_last_error() returns a thread-local message
+ *     describing the last non-OK status.
+ *   - Layouts are row-major.  Feature rows hold n_features int32 values.
+ */
+#ifndef AUTOTENSOR_H
+#define AUTOTENSOR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct at_space_s* at_space_t;
+typedef struct at_ensemble_s* at_ensemble_t;
+typedef struct at_chains_s* at_chains_t;
+typedef void* at_stream_t; /* a hipStream_t; 0 selects the null stream */
+
+typedef enum {
+    AT_OK = 0,
+    AT_E_INVALID = -1,     /* bad argument (null pointer, bad size, bad handle) */
+    AT_E_UNSUPPORTED = -2, /* shape or size the kernels do not handle */
+    AT_E_OOM = -3,         /* device or host allocation failed */
+    AT_E_HIP = -4,         /* a HIP runtime call failed */
+    AT_E_RANGE = -5,       /* a configuration index outside [0, n_configs) */
+    AT_E_MISMATCH = -6     /* space and ensemble feature counts differ, or
+                              spaces of one set use different templates */
+} at_status;
+
+/* Schedule templates (Section 2).
+ *  AT_TMPL_GEMM: C[i,j] = sum_k A[k,i] * B[k,j]; shape {M, N, K}.
+ *    Knobs: 4-level split of i, 4-level split of j, 2-level split of k,
+ *    auto_unroll_max_step in {0, 512, 1500}, unroll_explicit in {0, 1}.
+ *    Nest i1 j1 i2 j2 k1 i3 j3 k2 i4 j4 (i1/j1 -> blockIdx.y/x,
+ *    i2/j2 -> threadIdx.y/x): 10 loops, 110 features.
+ *  AT_TMPL_CONV2D_NCHW: out[k][oh][ow] = sum_{c,ry,rx}
+ *    data_pad[c][oh*S+ry][ow*S+rx] * kernel[k][c][ry][rx];
+ *    shape {N, C, H, W, K, KH, KW, pad, stride} with N == 1.
+ *    Knobs: 4-level splits of oc, oh, ow; 2-level splits of rc, ry, rx;
+ *    auto_unroll_max_step; unroll_explicit.  Nest oc1 oh1 ow1 oc2 oh2 ow2
+ *    rc1 r1 oc3 oh3 ow3 rc2 r2 oc4 oh4 ow4 (r_l fuses ry_l, rx_l; first band
+ *    -> blockIdx.z/y/x, second -> threadIdx.z/y/x): 16 loops, 176 features.
+ * Ordered splits are enumerated lexicographically (outer level first); a
+ * configuration index is the mixed-radix number of the knob values with
+ * knob 0 most significant. */
+typedef enum { AT_TMPL_GEMM = 0, AT_TMPL_CONV2D_NCHW = 1 } at_template;
+
+/* One entry of a chain's best list, or of an annealing trace. */
+typedef struct {
+    uint64_t cfg;   /* configuration index */
+    float score;    /* model score (higher is better) */
+    uint32_t flag;  /* best list: 1 = valid entry; trace: 1 = move accepted */
+} at_entry;
+
+/* Builds the schedule space S_e of an index expression e (Section 2):
+ * knob tables, loop nest and buffer index expressions, uploaded once to the
+ * current device.  shape: host [nshape] int64 (see at_template).
+ * Errors: AT_E_INVALID for bad shapes; AT_E_UNSUPPORTED when the nest's
+ * iteration count or a buffer size reaches 2^31, or the space holds 2^32 or
+ * more configurations.  Synchronous. */
+at_status at_space_create(int tmpl, const int64_t* shape, int nshape, at_space_t* out);
+
+/* Space metadata.  knob_sizes: host [at least n_knobs], may be NULL; any
+ * other output pointer may be NULL. */
+at_status at_space_info(at_space_t space, int* n_knobs, int32_t* knob_sizes, int* n_loops,
+                        int* n_features, uint64_t* n_configs);
+
+/* A set of spaces of one template, for annealing several workloads in one
+ * launch (transfer-style search over an invariant representation, Section 4).
+ * chain_offsets: host [n + 1] int64, ascending, chain_offsets[0] == 0: space
+ * i owns the chains [chain_offsets[i], chain_offsets[i+1]).  The set keeps
+ * its own copies of the member spaces' tables; members may be destroyed
+ * afterwards.  AT_E_MISMATCH if the templates differ.  Synchronous. */
+at_status at_spaceset_create(const at_space_t* spaces, int n, const int64_t* chain_offsets,
+                             at_space_t* out);
+void at_space_destroy(at_space_t space);
+
+/* Loop-context features of configurations (Appendix A.2), one row per
+ * configuration: per loop (outer to inner) bitlen(length), annotation id,
+ * then for each buffer bitlen(touch count), bitlen(reuse ratio),
+ * bitlen(stride).  bitlen(x) = 0 for x = 0, else floor(log2 x) + 1.
+ * Annotation ids: 0 serial, 1 unrolled, 2 unrolled explicitly, 3/4/5
+ * blockIdx.x/y/z, 6/7/8 threadIdx.x/y/z; a serial loop is unrolled when
+ * auto_unroll_max_step > 0 and its sub-nest has at most that many
+ * iterations.  Touch counts are distinct elements of the (padded) buffer
+ * touched by the sub-nest rooted at the loop; reuse ratio is
+ * floor(bottom-up / touch count); stride is the change of the buffer's flat
+ * index for one step of the loop variable.
+ * cfgs: device [n] uint64; feats: device [n][n_features] int32.
+ * A single space only (not a set).  Rows whose index is >= n_configs are
+ * filled with -1 and counted; at_space_errors() reports the count.
+ * n == 0 is a no-op. */
+at_status at_extract_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                              at_stream_t stream);
+
+/* Number of out-of-range configuration indices seen by at_extract_features
+ * since the last call (synchronises the device; resets the counter). */
+at_status at_space_errors(at_space_t space, uint64_t* n_out_of_range);
+
+/* Gradient-boosted tree cost model f-hat (Section 3.1): n_trees full
+ * binary trees of the given depth in heap order (node n has children 2n+1,
+ * taken when x[fid[n]] < thr[n], and 2n+2).
+ * fid, thr: host [n_trees][2^depth - 1] uint8 (fid < n_features);
+ * leaf: host [n_trees][2^depth] float.  1 <= depth <= 12,
+ * 1 <= n_features <= 256.  The tables are packed and uploaded to the
+ * current device.  Synchronous. */
+at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8_t* fid,
+                             const uint8_t* thr, const float* leaf, at_ensemble_t* out);
+void at_ensemble_destroy(at_ensemble_t ens);
+
+/* Scores of n feature rows: the fp32 sum of each tree's reached leaf,
+ * added in tree order starting from +0.0f (higher is better).
+ * feats: device [n][n_features] int32 with values in [0, 255] (values
+ * outside are clamped); scores: device [n] float; leaves: device
+ * [n][n_trees] uint16 leaf indices, or NULL.  n == 0 is a no-op. */
+at_status at_gbt_predict(at_ensemble_t ens, const int32_t* feats, int64_t n, float* scores,
+                         uint16_t* leaves, at_stream_t stream);
+
+/* Persistent state of n_chains Markov chains (Section 3.3: chain states
+ * persist across model updates): current knob values and score, absolute
+ * step counter and a best list of the topk highest-scoring distinct
+ * configurations seen.  Global chain ids are chain0 .. chain0+n_chains-1;
+ * they key the chains' random streams, so a chain's trajectory does not
+ * depend on which other chains run beside it.  For a space set, n_chains
+ * must equal the set's last chain offset.  1 <= topk <= 64.  The chains
+ * are initialised by the first at_sa_run: each knob value uniform over its
+ * range, scored once and offered to the best list.  Synchronous. */
+at_status at_chains_create(at_space_t space, int64_t chain0, int64_t n_chains, int topk,
+                           uint64_t seed, at_chains_t* out);
+void at_chains_destroy(at_chains_t chains);
+
+/* Absolute step counter of the chains (the step_base of the next run). */
+at_status at_chains_step(at_chains_t chains, uint64_t* step_abs);
+
+/* Metropolis thresholds for the next `steps` steps of chains
+ * chain0 .. chain0+n_chains-1 starting at absolute step step_base:
+ * thr[c][s] = fp32(T_s * ln(u)) computed in double, with
+ * T_s = 1 - s/(steps-1) (T = 0 when steps == 1) and u = (r2 + 0.5) / 2^32,
+ * r2 the third word of the Philox-4x32-10 block keyed by seed at counter
+ * (chain, step_base + s, 0, 0).  A move of score change d (fp32) is then
+ * accepted iff d >= thr, i.e. with probability min(1, exp(d / T_s)).
+ * thr: host [n_chains][steps] float.  Runs on the host. */
+at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint64_t step_base,
+                           int steps, float* thr);
+
+/* Runs `steps` annealing steps on every chain (Section 3.3, Algorithm 1's
+ * inner search).  Per chain and step: draw the Philox block (chain,
+ * step_abs, 0, 0); change one knob chosen uniformly among knobs with at
+ * least two values to a uniformly chosen different value; extract the
+ * candidate's features; score it with the ensemble; offer it to the best
+ * list (ordered by score descending, then index ascending; duplicates are
+ * skipped); accept it iff fp32(score - current) >= thr[c][s].
+ * thr: device [n_chains][steps] float; best: device [n_chains][topk]
+ * at_entry receiving a copy of the best lists after the run (entries with
+ * flag 0 are empty).  The ensemble's feature count must match the space's
+ * (AT_E_MISMATCH).  steps == 0 only initialises. */
+at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
+                    const float* thr, at_entry* best, at_stream_t stream);
+
+/* at_sa_run that also records, per chain and step, the proposed
+ * configuration, its score and whether it was accepted.
+ * trace: device [n_chains][steps] at_entry. */
+at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
+                           const float* thr, at_entry* best, at_entry* trace, at_stream_t stream);
+
+/* Copies the chains' current configuration indices (device [n_chains]
+ * uint64) and scores (device [n_chains] float); either may be NULL. */
+at_status at_chains_export(at_chains_t chains, uint64_t* cur_cfg, float* cur_score,
+                           at_stream_t stream);
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* at_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AUTOTENSOR_H */

@@ -1,0 +1,390 @@
+// C ABI of the autotensor library: handle lifetimes, argument checks, status
+// codes and the host-side threshold helper.  Every compute entry point
+// validates its arguments and then enqueues HIP kernels on the caller's
+// stream.
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "at_internal.h"
+
+namespace at {
+
+namespace {
+thread_local std::string g_last_error;
+
+template <class T>
+at_status upload(DeviceBuf& buf, const T* host, size_t count) {
+    buf.bytes = count * sizeof(T);
+    if (buf.bytes == 0) buf.bytes = 16;
+    hipError_t e = hipMalloc(&buf.p, buf.bytes);
+    if (e != hipSuccess) {
+        buf.p = nullptr;
+        return hip_fail(e, "hipMalloc");
+    }
+    if (count) {
+        e = hipMemcpy(buf.p, host, count * sizeof(T), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+    }
+    return AT_OK;
+}
+
+at_status alloc_zero(DeviceBuf& buf, size_t bytes) {
+    buf.bytes = bytes ? bytes : 16;
+    hipError_t e = hipMalloc(&buf.p, buf.bytes);
+    if (e != hipSuccess) {
+        buf.p = nullptr;
+        return hip_fail(e, "hipMalloc");
+    }
+    e = hipMemset(buf.p, 0, buf.bytes);
+    if (e != hipSuccess) return hip_fail(e, "hipMemset");
+    return AT_OK;
+}
+
+void release(DeviceBuf& buf) {
+    if (buf.p) (void)hipFree(buf.p);
+    buf.p = nullptr;
+    buf.bytes = 0;
+}
+
+int current_device() {
+    int d = 0;
+    (void)hipGetDevice(&d);
+    return d;
+}
+
+// Makes the handle's device current for the duration of a call.
+struct DeviceGuard {
+    int prev = 0;
+    bool switched = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) {
+            switched = hipSetDevice(dev) == hipSuccess;
+        }
+    }
+    ~DeviceGuard() {
+        if (switched) (void)hipSetDevice(prev);
+    }
+};
+
+at_status finish_launch(hipError_t e, const char* what) {
+    if (e != hipSuccess) return hip_fail(e, what);
+    return AT_OK;
+}
+
+}  // namespace
+
+at_status fail(at_status st, const std::string& msg) {
+    g_last_error = msg;
+    return st;
+}
+
+at_status hip_fail(hipError_t e, const char* what) {
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? AT_E_OOM : AT_E_HIP;
+}
+
+}  // namespace at
+
+using namespace at;
+
+extern "C" {
+
+const char* at_last_error(void) { return g_last_error.c_str(); }
+
+at_status at_space_create(int tmpl, const int64_t* shape, int nshape, at_space_t* out) {
+    if (!out) return fail(AT_E_INVALID, "at_space_create: out is NULL");
+    *out = nullptr;
+    SpaceDesc d;
+    std::vector<uint64_t> factors;
+    at_status st = build_space(tmpl, shape, nshape, d, factors);
+    if (st != AT_OK) return st;
+    at_space_s* sp = new (std::nothrow) at_space_s();
+    if (!sp) return fail(AT_E_OOM, "at_space_create: host allocation");
+    sp->device = current_device();
+    sp->tmpl = tmpl;
+    sp->n_spaces = 1;
+    sp->descs.push_back(d);
+    sp->chain_offsets = {0, 0};
+    sp->host_factors.push_back(factors);
+    int64_t offs[2] = {0, INT64_MAX};
+    if ((st = upload(sp->d_descs, &d, 1)) != AT_OK || (st = upload(sp->d_factors, factors.data(), factors.size())) != AT_OK ||
+        (st = upload(sp->d_offsets, offs, 2)) != AT_OK || (st = alloc_zero(sp->d_errors, 8)) != AT_OK) {
+        at_space_destroy(sp);
+        return st;
+    }
+    *out = sp;
+    return AT_OK;
+}
+
+at_status at_space_info(at_space_t space, int* n_knobs, int32_t* knob_sizes, int* n_loops, int* n_features,
+                        uint64_t* n_configs) {
+    if (!space) return fail(AT_E_INVALID, "at_space_info: NULL space");
+    const SpaceDesc& d = space->descs[0];
+    if (n_knobs) *n_knobs = d.n_knobs;
+    if (knob_sizes)
+        for (int j = 0; j < d.n_knobs; ++j) knob_sizes[j] = (int32_t)d.knob_size[j];
+    if (n_loops) *n_loops = d.tmpl == AT_TMPL_GEMM ? 10 : 16;
+    if (n_features) *n_features = d.n_features;
+    if (n_configs) {
+        uint64_t total = 0;
+        for (const SpaceDesc& x : space->descs) total += x.n_configs;
+        *n_configs = space->n_spaces == 1 ? d.n_configs : total;
+    }
+    return AT_OK;
+}
+
+at_status at_spaceset_create(const at_space_t* spaces, int n, const int64_t* chain_offsets, at_space_t* out) {
+    if (!out) return fail(AT_E_INVALID, "at_spaceset_create: out is NULL");
+    *out = nullptr;
+    if (!spaces || !chain_offsets || n < 1) return fail(AT_E_INVALID, "at_spaceset_create: bad arguments");
+    if (chain_offsets[0] != 0) return fail(AT_E_INVALID, "at_spaceset_create: chain_offsets[0] must be 0");
+    for (int i = 0; i < n; ++i) {
+        if (!spaces[i] || spaces[i]->n_spaces != 1) return fail(AT_E_INVALID, "at_spaceset_create: member must be a single space");
+        if (chain_offsets[i + 1] < chain_offsets[i]) return fail(AT_E_INVALID, "at_spaceset_create: offsets must ascend");
+        if (spaces[i]->tmpl != spaces[0]->tmpl) return fail(AT_E_MISMATCH, "at_spaceset_create: templates differ");
+    }
+    at_space_s* sp = new (std::nothrow) at_space_s();
+    if (!sp) return fail(AT_E_OOM, "at_spaceset_create: host allocation");
+    sp->device = current_device();
+    sp->tmpl = spaces[0]->tmpl;
+    sp->n_spaces = n;
+    std::vector<uint64_t> all;
+    for (int i = 0; i < n; ++i) {
+        SpaceDesc d = spaces[i]->descs[0];
+        const int32_t shift = (int32_t)all.size();
+        for (int a = 0; a < d.n_axes; ++a) d.split_off[a] += shift;
+        const std::vector<uint64_t>& f = spaces[i]->host_factors[0];
+        all.insert(all.end(), f.begin(), f.end());
+        sp->descs.push_back(d);
+        sp->host_factors.push_back(f);
+    }
+    sp->chain_offsets.assign(chain_offsets, chain_offsets + n + 1);
+    at_status st;
+    if ((st = upload(sp->d_descs, sp->descs.data(), sp->descs.size())) != AT_OK ||
+        (st = upload(sp->d_factors, all.data(), all.size())) != AT_OK ||
+        (st = upload(sp->d_offsets, sp->chain_offsets.data(), sp->chain_offsets.size())) != AT_OK ||
+        (st = alloc_zero(sp->d_errors, 8)) != AT_OK) {
+        at_space_destroy(sp);
+        return st;
+    }
+    *out = sp;
+    return AT_OK;
+}
+
+void at_space_destroy(at_space_t space) {
+    if (!space) return;
+    DeviceGuard g(space->device);
+    release(space->d_descs);
+    release(space->d_factors);
+    release(space->d_offsets);
+    release(space->d_errors);
+    delete space;
+}
+
+at_status at_extract_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats, at_stream_t stream) {
+    if (!space) return fail(AT_E_INVALID, "at_extract_features: NULL space");
+    if (space->n_spaces != 1) return fail(AT_E_INVALID, "at_extract_features: takes a single space, not a set");
+    if (n < 0) return fail(AT_E_INVALID, "at_extract_features: n < 0");
+    if (n == 0) return AT_OK;
+    if (!cfgs || !feats) return fail(AT_E_INVALID, "at_extract_features: NULL buffer");
+    if (n > ((int64_t)1 << 36)) return fail(AT_E_UNSUPPORTED, "at_extract_features: n too large for one call");
+    DeviceGuard g(space->device);
+    return finish_launch(launch_extract(*space, cfgs, n, feats, (hipStream_t)stream), "at_extract_features");
+}
+
+at_status at_space_errors(at_space_t space, uint64_t* n_out_of_range) {
+    if (!space || !n_out_of_range) return fail(AT_E_INVALID, "at_space_errors: NULL argument");
+    DeviceGuard g(space->device);
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    uint64_t v = 0;
+    e = hipMemcpy(&v, space->d_errors.p, 8, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+    e = hipMemset(space->d_errors.p, 0, 8);
+    if (e != hipSuccess) return hip_fail(e, "hipMemset");
+    *n_out_of_range = v;
+    return AT_OK;
+}
+
+at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8_t* fid, const uint8_t* thr,
+                             const float* leaf, at_ensemble_t* out) {
+    if (!out) return fail(AT_E_INVALID, "at_ensemble_create: out is NULL");
+    *out = nullptr;
+    if (!fid || !thr || !leaf) return fail(AT_E_INVALID, "at_ensemble_create: NULL table");
+    if (n_trees < 1 || n_trees > 65535) return fail(AT_E_INVALID, "at_ensemble_create: n_trees out of [1, 65535]");
+    if (depth < 1 || depth > 12) return fail(AT_E_UNSUPPORTED, "at_ensemble_create: depth out of [1, 12]");
+    if (n_features < 1 || n_features > 256) return fail(AT_E_UNSUPPORTED, "at_ensemble_create: n_features out of [1, 256]");
+    const size_t n_int = ((size_t)1 << depth) - 1, n_leaf = (size_t)1 << depth, W = (size_t)2 << depth;
+    std::vector<uint32_t> words;
+    try {
+        words.assign((size_t)n_trees * W, 0u);
+    } catch (...) {
+        return fail(AT_E_OOM, "at_ensemble_create: host allocation");
+    }
+    for (size_t t = 0; t < (size_t)n_trees; ++t) {
+        uint32_t* tw = words.data() + t * W;
+        for (size_t n = 0; n < n_int; ++n) {
+            const uint8_t f = fid[t * n_int + n];
+            if (f >= n_features) return fail(AT_E_INVALID, "at_ensemble_create: split feature >= n_features");
+            // heap node n (0-based) is word n + 1
+            tw[n + 1] = ((uint32_t)thr[t * n_int + n] << 16) | tile_offset(f);
+        }
+        for (size_t j = 0; j < n_leaf; ++j) {
+            uint32_t bits;
+            std::memcpy(&bits, &leaf[t * n_leaf + j], 4);
+            tw[n_leaf + j] = bits;
+        }
+    }
+    at_ensemble_s* e = new (std::nothrow) at_ensemble_s();
+    if (!e) return fail(AT_E_OOM, "at_ensemble_create: host allocation");
+    e->device = current_device();
+    at_status st = upload(e->d_words, words.data(), words.size());
+    if (st != AT_OK) {
+        at_ensemble_destroy(e);
+        return st;
+    }
+    e->desc.n_trees = n_trees;
+    e->desc.depth = depth;
+    e->desc.n_features = n_features;
+    e->desc.words_per_tree = (int32_t)W;
+    e->desc.words = static_cast<const uint32_t*>(e->d_words.p);
+    *out = e;
+    return AT_OK;
+}
+
+void at_ensemble_destroy(at_ensemble_t ens) {
+    if (!ens) return;
+    DeviceGuard g(ens->device);
+    release(ens->d_words);
+    delete ens;
+}
+
+at_status at_gbt_predict(at_ensemble_t ens, const int32_t* feats, int64_t n, float* scores, uint16_t* leaves,
+                         at_stream_t stream) {
+    if (!ens) return fail(AT_E_INVALID, "at_gbt_predict: NULL ensemble");
+    if (n < 0) return fail(AT_E_INVALID, "at_gbt_predict: n < 0");
+    if (n == 0) return AT_OK;
+    if (!feats || !scores) return fail(AT_E_INVALID, "at_gbt_predict: NULL buffer");
+    if (n > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, "at_gbt_predict: n too large");
+    DeviceGuard g(ens->device);
+    return finish_launch(launch_predict(ens->desc, feats, n, scores, leaves, (hipStream_t)stream), "at_gbt_predict");
+}
+
+at_status at_chains_create(at_space_t space, int64_t chain0, int64_t n_chains, int topk, uint64_t seed,
+                           at_chains_t* out) {
+    if (!out) return fail(AT_E_INVALID, "at_chains_create: out is NULL");
+    *out = nullptr;
+    if (!space) return fail(AT_E_INVALID, "at_chains_create: NULL space");
+    if (chain0 < 0 || n_chains < 0) return fail(AT_E_INVALID, "at_chains_create: negative chain range");
+    if (chain0 + n_chains > ((int64_t)1 << 32)) return fail(AT_E_UNSUPPORTED, "at_chains_create: chain ids must fit 32 bits");
+    if (topk < 1 || topk > 64) return fail(AT_E_INVALID, "at_chains_create: topk out of [1, 64]");
+    if (space->n_spaces > 1 && n_chains != space->chain_offsets.back())
+        return fail(AT_E_INVALID, "at_chains_create: n_chains must equal the set's last chain offset");
+    at_chains_s* ch = new (std::nothrow) at_chains_s();
+    if (!ch) return fail(AT_E_OOM, "at_chains_create: host allocation");
+    ch->device = current_device();
+    ch->chain0 = chain0;
+    ch->n_chains = n_chains;
+    ch->topk = topk;
+    ch->seed = seed;
+    ch->n_spaces = space->n_spaces;
+    ch->tmpl = space->tmpl;
+    at_status st;
+    if ((st = alloc_zero(ch->d_knobs, (size_t)n_chains * MAX_KNOBS * 2)) != AT_OK ||
+        (st = alloc_zero(ch->d_score, (size_t)n_chains * 4)) != AT_OK ||
+        (st = alloc_zero(ch->d_top, (size_t)n_chains * topk * sizeof(at_entry))) != AT_OK ||
+        (st = upload(ch->d_descs, space->descs.data(), space->descs.size())) != AT_OK) {
+        at_chains_destroy(ch);
+        return st;
+    }
+    if (space->n_spaces > 1) {
+        st = upload(ch->d_offsets, space->chain_offsets.data(), space->chain_offsets.size());
+    } else {
+        const int64_t offs[2] = {0, INT64_MAX};
+        st = upload(ch->d_offsets, offs, 2);
+    }
+    if (st != AT_OK) {
+        at_chains_destroy(ch);
+        return st;
+    }
+    *out = ch;
+    return AT_OK;
+}
+
+void at_chains_destroy(at_chains_t chains) {
+    if (!chains) return;
+    DeviceGuard g(chains->device);
+    release(chains->d_knobs);
+    release(chains->d_score);
+    release(chains->d_top);
+    release(chains->d_descs);
+    release(chains->d_offsets);
+    delete chains;
+}
+
+at_status at_chains_step(at_chains_t chains, uint64_t* step_abs) {
+    if (!chains || !step_abs) return fail(AT_E_INVALID, "at_chains_step: NULL argument");
+    *step_abs = chains->step_abs;
+    return AT_OK;
+}
+
+at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint64_t step_base, int steps,
+                           float* thr) {
+    if (steps < 1 || n_chains < 0 || chain0 < 0) return fail(AT_E_INVALID, "at_sa_thresholds: bad sizes");
+    if (n_chains > 0 && !thr) return fail(AT_E_INVALID, "at_sa_thresholds: NULL output");
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    for (int64_t c = 0; c < n_chains; ++c) {
+        const uint32_t chain = (uint32_t)(chain0 + c);
+        for (int s = 0; s < steps; ++s) {
+            const U4 r = philox(k0, k1, U4{chain, (uint32_t)(step_base + (uint64_t)s), 0u, 0u});
+            const double T = steps == 1 ? 0.0 : 1.0 - (double)s / (double)(steps - 1);
+            const double u = ((double)r.z + 0.5) / 4294967296.0;
+            thr[c * steps + s] = (float)(T * std::log(u));
+        }
+    }
+    return AT_OK;
+}
+
+static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps, const float* thr,
+                             at_entry* best, at_entry* trace, at_stream_t stream) {
+    if (!space || !ens || !chains) return fail(AT_E_INVALID, "at_sa_run: NULL handle");
+    if (steps < 0) return fail(AT_E_INVALID, "at_sa_run: steps < 0");
+    if (space->n_spaces != chains->n_spaces || space->tmpl != chains->tmpl)
+        return fail(AT_E_INVALID, "at_sa_run: chains were created for another space");
+    if (space->n_spaces > 1 && chains->n_chains != space->chain_offsets.back())
+        return fail(AT_E_INVALID, "at_sa_run: chain count does not match the space set");
+    if (ens->desc.n_features != space->descs[0].n_features)
+        return fail(AT_E_MISMATCH, "at_sa_run: ensemble and space feature counts differ");
+    if (chains->n_chains > 0 && !best) return fail(AT_E_INVALID, "at_sa_run: NULL best");
+    if (steps > 0 && chains->n_chains > 0 && !thr) return fail(AT_E_INVALID, "at_sa_run: NULL thr");
+    if (chains->step_abs + (uint64_t)steps > ((uint64_t)1 << 32))
+        return fail(AT_E_UNSUPPORTED, "at_sa_run: step counter must fit 32 bits");
+    DeviceGuard g(chains->device);
+    const bool init = !chains->initialised;
+    hipError_t e = launch_sa(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "at_sa_run");
+    chains->initialised = true;
+    chains->step_abs += (uint64_t)steps;
+    return AT_OK;
+}
+
+at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps, const float* thr,
+                    at_entry* best, at_stream_t stream) {
+    return sa_run_impl(space, ens, chains, steps, thr, best, nullptr, stream);
+}
+
+at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps, const float* thr,
+                           at_entry* best, at_entry* trace, at_stream_t stream) {
+    if (steps > 0 && chains && chains->n_chains > 0 && !trace) return fail(AT_E_INVALID, "at_sa_run_traced: NULL trace");
+    return sa_run_impl(space, ens, chains, steps, thr, best, trace, stream);
+}
+
+at_status at_chains_export(at_chains_t chains, uint64_t* cur_cfg, float* cur_score, at_stream_t stream) {
+    if (!chains) return fail(AT_E_INVALID, "at_chains_export: NULL chains");
+    if (!chains->initialised) return fail(AT_E_INVALID, "at_chains_export: chains not initialised (run at_sa_run first)");
+    DeviceGuard g(chains->device);
+    return finish_launch(launch_export(*chains, cur_cfg, cur_score, (hipStream_t)stream), "at_chains_export");
+}
+
+}  // extern "C"

@@ -1,0 +1,161 @@
+// Internal declarations of the autotensor library (not part of the C ABI).
+//
+// Device-side descriptions of schedule spaces, packed tree ensembles and
+// annealing chains, plus the Philox-4x32-10 block function shared by the
+// host threshold helper and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/autotensor.h"
+
+namespace at {
+
+constexpr int MAX_KNOBS = 8;
+constexpr int MAX_AXES = 6;
+constexpr int N_BUFFERS = 3;
+// Lanes of one feature tile in LDS.  A tile holds the u8 features of 256
+// rows "quad-major": byte (f & 3) of dword (f >> 2) * 256 + lane, so every
+// lane of a wave reads its own bank whatever feature it asks for.
+constexpr int TILE_LANES = 256;
+constexpr int MAX_TILE_QUADS = 64;   // up to 256 features
+
+// Schedule space as the kernels see it.  Split knobs come first (one per
+// axis, axis a is knob a), then auto_unroll_max_step, then unroll_explicit.
+struct SpaceDesc {
+    int32_t tmpl;
+    int32_t n_knobs;
+    int32_t n_axes;
+    int32_t n_features;
+    int32_t n_mut;                       // knobs with at least two values
+    int32_t mut[MAX_KNOBS];              // their indices, ascending
+    uint32_t knob_size[MAX_KNOBS];
+    uint64_t n_configs;
+    uint64_t radix[MAX_KNOBS];           // product of the sizes of later knobs
+    int32_t split_off[MAX_AXES];         // split choices of axis a start at
+                                         // factors[split_off[a]] (u64 each)
+    int32_t coef[N_BUFFERS][MAX_AXES];   // weight of axis a in buffer b's flat index
+    int32_t stride;                      // conv stride S (1 for GEMM)
+    int32_t pad_;
+};
+
+// Packed ensemble.  Tree t occupies words [t*W, (t+1)*W) with W = 2^(d+1):
+// word m (1 <= m < 2^d) is internal node m (1-based heap order: children 2m
+// and 2m+1) holding (thr << 16) | tile byte offset of its feature; words
+// 2^d .. 2^(d+1)-1 hold the leaf values (float bits); word 0 is unused.
+struct EnsembleDesc {
+    int32_t n_trees;
+    int32_t depth;
+    int32_t n_features;
+    int32_t words_per_tree;
+    const uint32_t* words;
+};
+
+// Tile byte offset of feature f: quad (f >> 2), byte (f & 3).
+__host__ __device__ inline uint32_t tile_offset(int f) {
+    return (uint32_t)((f >> 2) * TILE_LANES * 4 + (f & 3));
+}
+
+// --------------------------------------------------------------------------
+// Philox-4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two
+// 32x32 -> 64-bit products with multipliers 0xD2511F53 / 0xCD9E8D57 and a
+// Weyl key schedule with increments 0x9E3779B9 / 0xBB67AE85.
+// --------------------------------------------------------------------------
+struct U4 { uint32_t x, y, z, w; };
+
+__host__ __device__ inline uint32_t mul_hi32(uint32_t a, uint32_t b) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __umulhi(a, b);
+#else
+    return (uint32_t)(((uint64_t)a * b) >> 32);
+#endif
+}
+
+__host__ __device__ inline U4 philox(uint32_t k0, uint32_t k1, U4 c) {
+#pragma unroll
+    for (int i = 0; i < 10; ++i) {
+        uint32_t hi0 = mul_hi32(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+        uint32_t hi1 = mul_hi32(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+        c = U4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return c;
+}
+
+// floor(r * n / 2^32): a uniform value in [0, n) from one 32-bit word.
+__host__ __device__ inline uint32_t uniform_below(uint32_t r, uint32_t n) { return mul_hi32(r, n); }
+
+// --------------------------------------------------------------------------
+// Library handles.
+// --------------------------------------------------------------------------
+struct DeviceBuf {
+    void* p = nullptr;
+    size_t bytes = 0;
+};
+
+}  // namespace at
+
+struct at_space_s {
+    int device = 0;
+    int tmpl = 0;
+    int n_spaces = 1;                       // > 1 for a space set
+    std::vector<at::SpaceDesc> descs;       // host copies
+    std::vector<int64_t> chain_offsets;     // [n_spaces + 1] (sets only)
+    at::DeviceBuf d_descs;                  // SpaceDesc[n_spaces]
+    at::DeviceBuf d_factors;                // uint64 split factor tables
+    at::DeviceBuf d_offsets;                // int64 [n_spaces + 1]
+    at::DeviceBuf d_errors;                 // uint64 out-of-range counter
+    // per member space: its factor tables as host data (for building sets)
+    std::vector<std::vector<uint64_t>> host_factors;
+};
+
+struct at_ensemble_s {
+    int device = 0;
+    at::EnsembleDesc desc{};
+    at::DeviceBuf d_words;
+};
+
+struct at_chains_s {
+    int device = 0;
+    int64_t chain0 = 0;
+    int64_t n_chains = 0;
+    int topk = 0;
+    uint64_t seed = 0;
+    uint64_t step_abs = 0;
+    bool initialised = false;
+    int n_spaces = 1;
+    int tmpl = 0;
+    at::DeviceBuf d_knobs;    // uint16 [n_chains][MAX_KNOBS]
+    at::DeviceBuf d_score;    // float [n_chains]
+    at::DeviceBuf d_top;      // at_entry [n_chains][topk]
+    at::DeviceBuf d_descs;    // copy of the space's SpaceDesc[n_spaces]
+    at::DeviceBuf d_offsets;  // copy of the space's chain offsets
+};
+
+namespace at {
+
+// Thread-local error message helpers (at_capi.cpp).
+at_status fail(at_status st, const std::string& msg);
+at_status hip_fail(hipError_t e, const char* what);
+
+// Space construction (at_space.cpp).
+at_status build_space(int tmpl, const int64_t* shape, int nshape, SpaceDesc& desc,
+                      std::vector<uint64_t>& factors);
+
+// Kernel launchers (at_kernels.hip).
+hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                          hipStream_t stream);
+hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
+                          uint16_t* leaves, hipStream_t stream);
+hipError_t launch_sa(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
+                     bool init, const float* thr, at_entry* best, at_entry* trace,
+                     hipStream_t stream);
+hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score,
+                         hipStream_t stream);
+
+}  // namespace at

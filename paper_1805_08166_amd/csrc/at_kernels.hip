@@ -1,0 +1,663 @@
+// HIP kernels for gfx950 (CDNA4): loop-context features, tree-ensemble
+// scoring and parallel simulated annealing.
+//
+// Nothing here is a dense contraction, so there is no MFMA: the features are
+// integer bookkeeping bound by HBM writes, and the tree walk is a chain of
+// dependent LDS gathers bound by LDS and VALU issue.
+//
+// Exactness: features are integers; a score is the fp32 sum of the reached
+// leaves added one tree after another in tree order from +0.0f, exactly as
+// the model defines it, so every kernel reproduces it bit for bit.  The
+// library is compiled with -ffp-contract=off.
+#include "at_internal.h"
+
+namespace at {
+namespace {
+
+constexpr int WG = 256;   // workgroup size of every kernel (4 wave64s)
+
+// bitlen(x): bits needed to write x (0 for 0).
+__device__ __forceinline__ uint32_t bitlen(uint32_t x) { return 32u - (uint32_t)__clz((int)x); }
+
+// bitlen(floor(a / b)) for a >= b >= 1 without a division: with
+// k = bitlen(a) - bitlen(b) >= 0 the quotient lies in [2^(k-1), 2^(k+1)),
+// and it reaches 2^k exactly when floor(a / 2^k) >= b.
+__device__ __forceinline__ uint32_t bitlen_quot(uint32_t a, uint32_t b) {
+    uint32_t k = bitlen(a) - bitlen(b);
+    return k + ((a >> k) >= b ? 1u : 0u);
+}
+
+// Distinct values of S*x + y for x over A consecutive integers and y over B
+// consecutive integers: one run of (A-1)*S + B when the windows touch
+// (B >= S, or a single x), else A*B isolated windows.
+__device__ __forceinline__ uint32_t distinct_affine(uint32_t A, uint32_t B, uint32_t S) {
+    return (A == 1u || B >= S) ? (A - 1u) * S + B : A * B;
+}
+
+// --------------------------------------------------------------------------
+// Loop nests of the two templates, outer to inner.  Axis ids: GEMM i=0 j=1
+// k=2; conv oc=0 oh=1 ow=2 rc=3 ry=4 rx=5.  FUSED marks the kernel-window
+// loop r_l = (ry_l outer, rx_l inner).  Binding ids follow the annotation
+// column: 3/4/5 blockIdx.x/y/z, 6/7/8 threadIdx.x/y/z, 0 serial.
+// --------------------------------------------------------------------------
+constexpr int FUSED = -1;
+
+template <int TMPL> struct Nest;
+
+template <> struct Nest<AT_TMPL_GEMM> {
+    static constexpr int L = 10;
+    static constexpr int F = 110;
+    static constexpr int axis[L] = {0, 1, 0, 1, 2, 0, 1, 2, 0, 1};
+    static constexpr int level[L] = {0, 0, 1, 1, 0, 2, 2, 1, 3, 3};
+    static constexpr int bind[L] = {4, 3, 7, 6, 0, 0, 0, 0, 0, 0};
+    // touch counts from the per-axis ranges of a sub-nest
+    __device__ static void touched(const uint32_t (&r)[6], uint32_t, uint32_t (&t)[3]) {
+        t[0] = r[2] * r[0];   // A[k][i]
+        t[1] = r[2] * r[1];   // B[k][j]
+        t[2] = r[0] * r[1];   // C[i][j]
+    }
+};
+
+template <> struct Nest<AT_TMPL_CONV2D_NCHW> {
+    static constexpr int L = 16;
+    static constexpr int F = 176;
+    static constexpr int axis[L] = {0, 1, 2, 0, 1, 2, 3, FUSED, 0, 1, 2, 3, FUSED, 0, 1, 2};
+    static constexpr int level[L] = {0, 0, 0, 1, 1, 1, 0, 0, 2, 2, 2, 1, 1, 3, 3, 3};
+    static constexpr int bind[L] = {5, 4, 3, 8, 7, 6, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    __device__ static void touched(const uint32_t (&r)[6], uint32_t S, uint32_t (&t)[3]) {
+        // data_pad[rc][oh*S+ry][ow*S+rx], unclipped padded coordinates
+        t[0] = r[3] * distinct_affine(r[1], r[4], S) * distinct_affine(r[2], r[5], S);
+        t[1] = r[0] * r[3] * r[4] * r[5];   // kernel[oc][rc][ry][rx]
+        t[2] = r[0] * r[1] * r[2];          // output[oc][oh][ow]
+    }
+};
+
+// Factors of the chosen split of axis a: four 16-bit fields, outer level first.
+__device__ __forceinline__ void unpack_split(uint64_t w, uint32_t (&f)[4]) {
+    f[0] = (uint32_t)(w & 0xffff);
+    f[1] = (uint32_t)((w >> 16) & 0xffff);
+    f[2] = (uint32_t)((w >> 32) & 0xffff);
+    f[3] = (uint32_t)(w >> 48);
+}
+
+// Loop-context features of one schedule.  The nest is walked from the
+// innermost loop outwards so that each loop's sub-nest quantities are running
+// products: range[a] is the extent of axis a covered by the sub-nest, and a
+// loop's stride in buffer b is b's weight of the loop's axis times the range
+// of that axis strictly inside the loop.  emit(f, value) receives feature f.
+template <int TMPL, class Emit>
+__device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4],
+                                              uint32_t unroll_max, uint32_t unroll_id, Emit&& emit) {
+    using N = Nest<TMPL>;
+    uint32_t range[6] = {1u, 1u, 1u, 1u, 1u, 1u};
+    uint32_t bottom_up = 1u;
+    const uint32_t S = (uint32_t)sd.stride;
+#pragma unroll
+    for (int p = N::L - 1; p >= 0; --p) {
+        uint32_t ext, strd[3];
+        if (N::axis[p] == FUSED) {
+            const int l = N::level[p];
+            const uint32_t fy = fac[4][l], fx = fac[5][l];
+            ext = fy * fx;
+            // one step of r moves rx when rx has several values, else ry
+#pragma unroll
+            for (int b = 0; b < 3; ++b)
+                strd[b] = (fx > 1u) ? (uint32_t)sd.coef[b][5] * range[5] : (uint32_t)sd.coef[b][4] * range[4];
+            range[4] *= fy;
+            range[5] *= fx;
+        } else {
+            const int a = N::axis[p];
+            ext = fac[a][N::level[p]];
+#pragma unroll
+            for (int b = 0; b < 3; ++b) strd[b] = (uint32_t)sd.coef[b][a] * range[a];
+            range[a] *= ext;
+        }
+        bottom_up *= ext;
+        uint32_t t[3];
+        N::touched(range, S, t);
+        uint32_t ann = N::bind[p] ? (uint32_t)N::bind[p]
+                                  : ((unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u);
+        emit(p * 11 + 0, bitlen(ext));
+        emit(p * 11 + 1, ann);
+#pragma unroll
+        for (int b = 0; b < 3; ++b) {
+            emit(p * 11 + 2 + 3 * b, bitlen(t[b]));
+            emit(p * 11 + 3 + 3 * b, bitlen_quot(bottom_up, t[b]));
+            emit(p * 11 + 4 + 3 * b, bitlen(strd[b]));
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t unroll_max_of(uint32_t v) { return v == 0u ? 0u : (v == 1u ? 512u : 1500u); }
+
+// Factors of every axis for knob values kv (split knob a = axis a).
+template <int TMPL>
+__device__ __forceinline__ void gather_factors(const SpaceDesc& sd, const uint64_t* __restrict__ factors,
+                                               const uint32_t (&kv)[MAX_KNOBS], uint32_t (&fac)[6][4]) {
+    constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
+#pragma unroll
+    for (int a = 0; a < 6; ++a) {
+        if (a < A) unpack_split(factors[sd.split_off[a] + kv[a]], fac[a]);
+        else fac[a][0] = fac[a][1] = fac[a][2] = fac[a][3] = 1u;
+    }
+}
+
+// ==========================================================================
+// Feature extraction: one configuration per lane.  Rows are built as signed
+// bytes in LDS (row stride with an odd dword count so the per-lane byte
+// writes spread over the banks) and then written out as int32 with
+// consecutive lanes covering consecutive 16-byte pieces of the block, so the
+// HBM stores are fully coalesced.
+// ==========================================================================
+template <int TMPL>
+struct RowLayout {
+    static constexpr int F = Nest<TMPL>::F;
+    static constexpr int RS = ((F + 3) / 4 % 2 == 1) ? ((F + 3) / 4) * 4 : ((F + 3) / 4 + 1) * 4;
+};
+
+template <int TMPL, bool VEC>
+__global__ __launch_bounds__(WG) void k_extract(SpaceDesc sd, const uint64_t* __restrict__ factors,
+                                                const uint64_t* __restrict__ cfgs, int64_t n,
+                                                int32_t* __restrict__ feats,
+                                                unsigned long long* __restrict__ n_bad) {
+    constexpr int F = RowLayout<TMPL>::F;
+    constexpr int RS = RowLayout<TMPL>::RS;
+    __shared__ int8_t rows[WG * RS];
+    const int tid = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * WG;
+    const int64_t row = base + tid;
+    int8_t* my = rows + tid * RS;
+    if (row < n) {
+        const uint64_t cfg = cfgs[row];
+        if (cfg >= sd.n_configs) {
+            for (int f = 0; f < F; ++f) my[f] = -1;
+            atomicAdd(n_bad, 1ull);
+        } else {
+            // mixed radix, knob 0 most significant; indices fit 32 bits
+            uint32_t rest = (uint32_t)cfg;
+            uint32_t kv[MAX_KNOBS];
+#pragma unroll
+            for (int j = MAX_KNOBS - 1; j >= 0; --j) {
+                if (j < sd.n_knobs) {
+                    const uint32_t sz = sd.knob_size[j];
+                    const uint32_t q = rest / sz;
+                    kv[j] = rest - q * sz;
+                    rest = q;
+                } else {
+                    kv[j] = 0u;
+                }
+            }
+            uint32_t fac[6][4];
+            gather_factors<TMPL>(sd, factors, kv, fac);
+            constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
+            nest_features<TMPL>(sd, fac, unroll_max_of(kv[A]), 1u + kv[A + 1],
+                                [&](int f, uint32_t v) { my[f] = (int8_t)v; });
+        }
+    }
+    __syncthreads();
+    const int64_t rows_here = (n - base < WG) ? (n - base) : WG;
+    const int total = (int)rows_here * F;
+    int32_t* out = feats + base * F;
+    if (VEC) {
+        // F % 4 == 0: each thread moves 4 consecutive features of one row
+        for (int g = tid; g < total / 4; g += WG) {
+            const int e = g * 4;
+            const int r = e / F, c = e - r * F;
+            const int w = *reinterpret_cast<const int*>(rows + r * RS + c);
+            int4 v;
+            v.x = (int)(int8_t)(w & 0xff);
+            v.y = (int)(int8_t)((w >> 8) & 0xff);
+            v.z = (int)(int8_t)((w >> 16) & 0xff);
+            v.w = (int)(int8_t)((w >> 24) & 0xff);
+            *reinterpret_cast<int4*>(out + e) = v;
+        }
+    } else {
+        for (int e = tid; e < total; e += WG) {
+            const int r = e / F, c = e - r * F;
+            out[e] = (int32_t)rows[r * RS + c];
+        }
+    }
+}
+
+// ==========================================================================
+// Tree-ensemble traversal shared by scoring and annealing.
+// A workgroup holds the features of its 256 rows (chains or candidates) in
+// an LDS tile and streams the packed trees through LDS in chunks.  Each lane
+// walks every tree for its own row and adds the leaves in tree order.
+// ==========================================================================
+
+// Copies `words` packed tree words (a multiple of 4) from global to LDS.
+__device__ __forceinline__ void stage_words(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src,
+                                            int words) {
+    const uint4* s4 = reinterpret_cast<const uint4*>(src);
+    uint4* d4 = reinterpret_cast<uint4*>(dst);
+    for (int i = threadIdx.x; i < words / 4; i += WG) d4[i] = s4[i];
+}
+
+// Walks GROUP trees of depth DEPTH starting at chunk word `cb` (tree stride
+// W words) for the lane whose feature column starts at byte `fb` of the
+// tile; returns the leaf words and leaf indices.
+template <int DEPTH, int GROUP>
+__device__ __forceinline__ void walk(const uint32_t* __restrict__ chunk, const uint8_t* __restrict__ tile_b,
+                                     uint32_t fb, int cb, uint32_t (&leafw)[GROUP], uint32_t (&leafi)[GROUP]) {
+    constexpr int W = 2 << DEPTH;
+    uint32_t m[GROUP];
+#pragma unroll
+    for (int g = 0; g < GROUP; ++g) m[g] = 1u;
+#pragma unroll
+    for (int l = 0; l < DEPTH; ++l) {
+        uint32_t node[GROUP];
+#pragma unroll
+        for (int g = 0; g < GROUP; ++g) node[g] = chunk[cb + g * W + m[g]];
+#pragma unroll
+        for (int g = 0; g < GROUP; ++g) {
+            const uint32_t x = tile_b[fb + (node[g] & 0xffffu)];
+            m[g] = 2u * m[g] + (x >= (node[g] >> 16) ? 1u : 0u);
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < GROUP; ++g) {
+        leafw[g] = chunk[cb + g * W + m[g]];
+        leafi[g] = m[g] - (1u << DEPTH);
+    }
+}
+
+// Scores the row in this lane's tile column against every tree; all lanes
+// of the workgroup must call it together (it stages chunks with barriers).
+template <int DEPTH>
+__device__ __forceinline__ float score_tile(const EnsembleDesc& e, const uint32_t* __restrict__ tile, uint32_t* __restrict__ chunk,
+                            int chunk_trees, uint16_t* __restrict__ leaves_row) {
+    constexpr int W = 2 << DEPTH;
+    constexpr int G = 4;
+    const uint8_t* tile_b = reinterpret_cast<const uint8_t*>(tile);
+    const uint32_t fb = threadIdx.x * 4u;
+    float acc = 0.0f;
+    for (int t0 = 0; t0 < e.n_trees; t0 += chunk_trees) {
+        const int nt = (e.n_trees - t0 < chunk_trees) ? (e.n_trees - t0) : chunk_trees;
+        __syncthreads();
+        stage_words(chunk, e.words + (size_t)t0 * W, nt * W);
+        __syncthreads();
+        int t = 0;
+        for (; t + G <= nt; t += G) {
+            uint32_t lw[G], li[G];
+            walk<DEPTH, G>(chunk, tile_b, fb, t * W, lw, li);
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                acc = acc + __uint_as_float(lw[g]);
+                if (leaves_row) leaves_row[t0 + t + g] = (uint16_t)li[g];
+            }
+        }
+        for (; t < nt; ++t) {
+            uint32_t lw[1], li[1];
+            walk<DEPTH, 1>(chunk, tile_b, fb, t * W, lw, li);
+            acc = acc + __uint_as_float(lw[0]);
+            if (leaves_row) leaves_row[t0 + t] = (uint16_t)li[0];
+        }
+    }
+    return acc;
+}
+
+// Trees per LDS chunk: the largest count whose words fit `bytes`.
+__host__ __device__ inline int chunk_trees_for(int depth, int bytes) {
+    int w = 2 << depth;
+    int t = bytes / (w * 4);
+    return t < 1 ? 1 : t;
+}
+
+constexpr int CHUNK_BYTES = 32768;
+
+template <int DEPTH>
+__global__ __launch_bounds__(WG) void k_predict(EnsembleDesc e, const int32_t* __restrict__ feats, int64_t n,
+                                                float* __restrict__ scores, uint16_t* __restrict__ leaves,
+                                                int chunk_trees) {
+    extern __shared__ uint32_t lds[];
+    const int Q = (e.n_features + 3) / 4;
+    uint32_t* tile = lds;
+    uint32_t* chunk = lds + Q * WG;
+    const int tid = threadIdx.x;
+    const int64_t row = (int64_t)blockIdx.x * WG + tid;
+    const int F = e.n_features;
+    // own row -> tile column, 4 features per dword, clamped to [0, 255]
+    for (int q = 0; q < Q; ++q) {
+        uint32_t w = 0;
+        if (row < n) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int f = q * 4 + k;
+                if (f < F) {
+                    int x = feats[row * F + f];
+                    x = x < 0 ? 0 : (x > 255 ? 255 : x);
+                    w |= (uint32_t)x << (8 * k);
+                }
+            }
+        }
+        tile[q * WG + tid] = w;
+    }
+    uint16_t* lrow = (leaves && row < n) ? leaves + row * e.n_trees : nullptr;
+    const float s = score_tile<DEPTH>(e, tile, chunk, chunk_trees, lrow);
+    if (row < n) scores[row] = s;
+}
+
+// ==========================================================================
+// Parallel simulated annealing, one chain per lane (Section 3.3).
+// ==========================================================================
+
+// Offers (cfg, score) to a chain's best list in global memory: ordered by
+// score descending then index ascending, distinct indices, at most k.
+// count / kth_* cache the list length and its last entry in registers.
+__device__ __forceinline__ void offer(at_entry* __restrict__ list, int k, int& count, float& kth_s,
+                                      uint64_t& kth_c, uint64_t cfg, float sc) {
+    if (count == k && !(sc > kth_s || (sc == kth_s && cfg < kth_c))) return;
+    int pos = count;
+    for (int i = 0; i < count; ++i) {
+        const at_entry e = list[i];
+        if (e.cfg == cfg) return;
+        if (pos == count && (sc > e.score || (sc == e.score && cfg < e.cfg))) pos = i;
+    }
+    const int last = (count < k) ? count : k - 1;
+    for (int i = last; i > pos; --i) list[i] = list[i - 1];
+    at_entry ne;
+    ne.cfg = cfg;
+    ne.score = sc;
+    ne.flag = 1u;
+    list[pos] = ne;
+    if (count < k) ++count;
+    const at_entry tail = list[count - 1];
+    kth_s = tail.score;
+    kth_c = tail.cfg;
+}
+
+struct SaArgs {
+    const SpaceDesc* descs;
+    const int64_t* offsets;   // [n_spaces + 1]
+    int n_spaces;
+    const uint64_t* factors;
+    uint16_t* knobs;          // [n_chains][MAX_KNOBS]
+    float* cur_score;         // [n_chains]
+    at_entry* top;            // [n_chains][topk]
+    int topk;
+    int64_t n_chains;
+    uint64_t chain0;
+    uint64_t seed;
+    uint64_t step_base;
+    int steps;
+    int init;
+    const float* thr;         // [n_chains][steps]
+    at_entry* best;           // [n_chains][topk]
+    at_entry* trace;          // [n_chains][steps] or null
+    int chunk_trees;
+};
+
+template <int TMPL, int DEPTH>
+__global__ __launch_bounds__(WG) void k_sa(SaArgs a, EnsembleDesc e) {
+    constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
+    extern __shared__ uint32_t lds[];
+    const int Q = (Nest<TMPL>::F + 3) / 4;
+    uint32_t* tile = lds;
+    uint32_t* chunk = lds + Q * WG;
+    uint8_t* tile_b = reinterpret_cast<uint8_t*>(tile);
+    const int tid = threadIdx.x;
+    const int64_t c = (int64_t)blockIdx.x * WG + tid;
+    const bool active = c < a.n_chains;
+    const int64_t cc = active ? c : 0;
+    int w = 0;
+    while (w + 1 < a.n_spaces && a.offsets[w + 1] <= cc) ++w;
+    const SpaceDesc& sd = a.descs[w];
+    const uint64_t gchain = a.chain0 + (uint64_t)cc;
+    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+
+    uint32_t kv[MAX_KNOBS];
+    at_entry* list = a.top + cc * a.topk;
+    int count = 0;
+    float kth_s = 0.0f;
+    uint64_t kth_c = 0;
+    float cur = 0.0f;
+
+    // score of knob vector v: features into this lane's tile column, then the walk
+    auto evaluate = [&](const uint32_t (&v)[MAX_KNOBS]) __attribute__((always_inline)) -> float {
+        uint32_t fac[6][4];
+        gather_factors<TMPL>(sd, a.factors, v, fac);
+        nest_features<TMPL>(sd, fac, unroll_max_of(v[A]), 1u + v[A + 1], [&](int f, uint32_t x) {
+            tile_b[tile_offset(f) + tid * 4] = (uint8_t)x;
+        });
+        return score_tile<DEPTH>(e, tile, chunk, a.chunk_trees, nullptr);
+    };
+    auto cfg_of = [&](const uint32_t (&v)[MAX_KNOBS]) __attribute__((always_inline)) -> uint64_t {
+        uint64_t x = 0;
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j)
+            if (j < sd.n_knobs) x += (uint64_t)v[j] * sd.radix[j];
+        return x;
+    };
+
+    if (a.init) {
+        // each knob uniform over its values: block (chain, 0, 1, j / 4)
+        U4 r{0, 0, 0, 0};
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j) {
+            if ((j & 3) == 0) r = philox(k0, k1, U4{(uint32_t)gchain, 0u, 1u, (uint32_t)(j >> 2)});
+            const uint32_t word = (j & 3) == 0 ? r.x : (j & 3) == 1 ? r.y : (j & 3) == 2 ? r.z : r.w;
+            kv[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
+        }
+        cur = evaluate(kv);
+        if (active) {
+            for (int i = 0; i < a.topk; ++i) {
+                at_entry z;
+                z.cfg = 0;
+                z.score = 0.0f;
+                z.flag = 0u;
+                list[i] = z;
+            }
+            offer(list, a.topk, count, kth_s, kth_c, cfg_of(kv), cur);
+        }
+    } else {
+        const uint4 packed = reinterpret_cast<const uint4*>(a.knobs)[cc];
+        const uint32_t pw[4] = {packed.x, packed.y, packed.z, packed.w};
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = (pw[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+        cur = a.cur_score[cc];
+        if (active) {
+            while (count < a.topk && list[count].flag) ++count;
+            if (count > 0) {
+                kth_s = list[count - 1].score;
+                kth_c = list[count - 1].cfg;
+            }
+        }
+    }
+
+    for (int s = 0; s < a.steps; ++s) {
+        const U4 r = philox(k0, k1, U4{(uint32_t)gchain, (uint32_t)(a.step_base + (uint64_t)s), 0u, 0u});
+        uint32_t cand[MAX_KNOBS];
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j) cand[j] = kv[j];
+        if (sd.n_mut > 0) {
+            const int jm = sd.mut[uniform_below(r.x, (uint32_t)sd.n_mut)];
+            uint32_t old = 0, size = 2;
+#pragma unroll
+            for (int j = 0; j < MAX_KNOBS; ++j)
+                if (j == jm) { old = kv[j]; size = sd.knob_size[j]; }
+            uint32_t nv = uniform_below(r.y, size - 1u);
+            if (nv >= old) nv += 1u;
+#pragma unroll
+            for (int j = 0; j < MAX_KNOBS; ++j)
+                if (j == jm) cand[j] = nv;
+        }
+        const float sc = evaluate(cand);
+        if (active) {
+            const uint64_t cfg = cfg_of(cand);
+            offer(list, a.topk, count, kth_s, kth_c, cfg, sc);
+            const float delta = sc - cur;
+            const bool acc = delta >= a.thr[cc * a.steps + s];
+            if (acc) {
+                cur = sc;
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = cand[j];
+            }
+            if (a.trace) {
+                at_entry t;
+                t.cfg = cfg;
+                t.score = sc;
+                t.flag = acc ? 1u : 0u;
+                a.trace[cc * a.steps + s] = t;
+            }
+        }
+    }
+    if (active) {
+        uint4 packed;
+        packed.x = kv[0] | (kv[1] << 16);
+        packed.y = kv[2] | (kv[3] << 16);
+        packed.z = kv[4] | (kv[5] << 16);
+        packed.w = kv[6] | (kv[7] << 16);
+        reinterpret_cast<uint4*>(a.knobs)[cc] = packed;
+        a.cur_score[cc] = cur;
+        for (int i = 0; i < a.topk; ++i) a.best[cc * a.topk + i] = list[i];
+    }
+}
+
+__global__ __launch_bounds__(WG) void k_export(const SpaceDesc* descs, const int64_t* offsets, int n_spaces,
+                                               const uint16_t* knobs, const float* score, int64_t n,
+                                               uint64_t* cur_cfg, float* cur_score) {
+    const int64_t c = (int64_t)blockIdx.x * WG + threadIdx.x;
+    if (c >= n) return;
+    int w = 0;
+    while (w + 1 < n_spaces && offsets[w + 1] <= c) ++w;
+    const SpaceDesc& sd = descs[w];
+    if (cur_cfg) {
+        uint64_t x = 0;
+        for (int j = 0; j < sd.n_knobs; ++j) x += (uint64_t)knobs[c * MAX_KNOBS + j] * sd.radix[j];
+        cur_cfg[c] = x;
+    }
+    if (cur_score) cur_score[c] = score[c];
+}
+
+}  // namespace
+
+hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                          hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const SpaceDesc& sd = sp.descs[0];
+    const unsigned grid = (unsigned)((n + WG - 1) / WG);
+    const uint64_t* fac = static_cast<const uint64_t*>(sp.d_factors.p);
+    auto* bad = static_cast<unsigned long long*>(sp.d_errors.p);
+    const bool aligned = (reinterpret_cast<uintptr_t>(feats) & 15u) == 0;
+    if (sp.tmpl == AT_TMPL_GEMM) {
+        // 110 features per row: not a multiple of 4, scalar stores
+        hipLaunchKernelGGL((k_extract<AT_TMPL_GEMM, false>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs, n,
+                           feats, bad);
+    } else if (aligned) {
+        hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, true>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs,
+                           n, feats, bad);
+    } else {
+        hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, false>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs,
+                           n, feats, bad);
+    }
+    return hipGetLastError();
+}
+
+namespace {
+
+template <int DEPTH>
+hipError_t predict_depth(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores, uint16_t* leaves,
+                         hipStream_t stream) {
+    const int Q = (e.n_features + 3) / 4;
+    const int ct = chunk_trees_for(DEPTH, CHUNK_BYTES);
+    const size_t lds = (size_t)Q * WG * 4 + (size_t)ct * (2 << DEPTH) * 4;
+    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_predict<DEPTH>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    const unsigned grid = (unsigned)((n + WG - 1) / WG);
+    hipLaunchKernelGGL((k_predict<DEPTH>), dim3(grid), dim3(WG), lds, stream, e, feats, n, scores, leaves, ct);
+    return hipGetLastError();
+}
+
+template <int TMPL, int DEPTH>
+hipError_t sa_depth(const SaArgs& a0, const EnsembleDesc& e, hipStream_t stream) {
+    SaArgs a = a0;
+    const int Q = (Nest<TMPL>::F + 3) / 4;
+    a.chunk_trees = chunk_trees_for(DEPTH, CHUNK_BYTES);
+    const size_t lds = (size_t)Q * WG * 4 + (size_t)a.chunk_trees * (2 << DEPTH) * 4;
+    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sa<TMPL, DEPTH>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    const unsigned grid = (unsigned)((a.n_chains + WG - 1) / WG);
+    hipLaunchKernelGGL((k_sa<TMPL, DEPTH>), dim3(grid), dim3(WG), lds, stream, a, e);
+    return hipGetLastError();
+}
+
+template <int TMPL>
+hipError_t sa_tmpl(const SaArgs& a, const EnsembleDesc& e, hipStream_t stream) {
+    switch (e.depth) {
+        case 1: return sa_depth<TMPL, 1>(a, e, stream);
+        case 2: return sa_depth<TMPL, 2>(a, e, stream);
+        case 3: return sa_depth<TMPL, 3>(a, e, stream);
+        case 4: return sa_depth<TMPL, 4>(a, e, stream);
+        case 5: return sa_depth<TMPL, 5>(a, e, stream);
+        case 6: return sa_depth<TMPL, 6>(a, e, stream);
+        case 7: return sa_depth<TMPL, 7>(a, e, stream);
+        case 8: return sa_depth<TMPL, 8>(a, e, stream);
+        case 9: return sa_depth<TMPL, 9>(a, e, stream);
+        case 10: return sa_depth<TMPL, 10>(a, e, stream);
+        case 11: return sa_depth<TMPL, 11>(a, e, stream);
+        case 12: return sa_depth<TMPL, 12>(a, e, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
+                          uint16_t* leaves, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    switch (e.depth) {
+        case 1: return predict_depth<1>(e, feats, n, scores, leaves, stream);
+        case 2: return predict_depth<2>(e, feats, n, scores, leaves, stream);
+        case 3: return predict_depth<3>(e, feats, n, scores, leaves, stream);
+        case 4: return predict_depth<4>(e, feats, n, scores, leaves, stream);
+        case 5: return predict_depth<5>(e, feats, n, scores, leaves, stream);
+        case 6: return predict_depth<6>(e, feats, n, scores, leaves, stream);
+        case 7: return predict_depth<7>(e, feats, n, scores, leaves, stream);
+        case 8: return predict_depth<8>(e, feats, n, scores, leaves, stream);
+        case 9: return predict_depth<9>(e, feats, n, scores, leaves, stream);
+        case 10: return predict_depth<10>(e, feats, n, scores, leaves, stream);
+        case 11: return predict_depth<11>(e, feats, n, scores, leaves, stream);
+        case 12: return predict_depth<12>(e, feats, n, scores, leaves, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_sa(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps, bool init,
+                     const float* thr, at_entry* best, at_entry* trace, hipStream_t stream) {
+    SaArgs a{};
+    a.descs = static_cast<const SpaceDesc*>(sp.d_descs.p);
+    a.offsets = static_cast<const int64_t*>(sp.d_offsets.p);
+    a.n_spaces = sp.n_spaces;
+    a.factors = static_cast<const uint64_t*>(sp.d_factors.p);
+    a.knobs = static_cast<uint16_t*>(ch.d_knobs.p);
+    a.cur_score = static_cast<float*>(ch.d_score.p);
+    a.top = static_cast<at_entry*>(ch.d_top.p);
+    a.topk = ch.topk;
+    a.n_chains = ch.n_chains;
+    a.chain0 = (uint64_t)ch.chain0;
+    a.seed = ch.seed;
+    a.step_base = ch.step_abs;
+    a.steps = steps;
+    a.init = init ? 1 : 0;
+    a.thr = thr;
+    a.best = best;
+    a.trace = trace;
+    if (ch.n_chains == 0) return hipSuccess;
+    if (sp.tmpl == AT_TMPL_GEMM) return sa_tmpl<AT_TMPL_GEMM>(a, e, stream);
+    return sa_tmpl<AT_TMPL_CONV2D_NCHW>(a, e, stream);
+}
+
+hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score, hipStream_t stream) {
+    if (ch.n_chains == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((ch.n_chains + WG - 1) / WG);
+    hipLaunchKernelGGL(k_export, dim3(grid), dim3(WG), 0, stream, static_cast<const SpaceDesc*>(ch.d_descs.p),
+                       static_cast<const int64_t*>(ch.d_offsets.p), ch.n_spaces,
+                       static_cast<const uint16_t*>(ch.d_knobs.p), static_cast<const float*>(ch.d_score.p),
+                       ch.n_chains, cur_cfg, cur_score);
+    return hipGetLastError();
+}
+
+}  // namespace at
