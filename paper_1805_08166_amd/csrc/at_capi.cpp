@@ -217,8 +217,10 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     if (n_features < 1 || n_features > 256) return fail(AT_E_UNSUPPORTED, "at_ensemble_create: n_features out of [1, 256]");
     const size_t n_int = ((size_t)1 << depth) - 1, n_leaf = (size_t)1 << depth, W = (size_t)2 << depth;
     std::vector<uint32_t> words;
+    // padded to whole 32 KB blocks so that chunked prefetches stay in bounds
+    const size_t padded = ((size_t)n_trees * W + ENSEMBLE_PAD_WORDS - 1) / ENSEMBLE_PAD_WORDS * ENSEMBLE_PAD_WORDS;
     try {
-        words.assign((size_t)n_trees * W, 0u);
+        words.assign(padded, 0u);
     } catch (...) {
         return fail(AT_E_OOM, "at_ensemble_create: host allocation");
     }
@@ -320,6 +322,10 @@ void at_chains_destroy(at_chains_t chains) {
     release(chains->d_top);
     release(chains->d_descs);
     release(chains->d_offsets);
+    release(chains->d_cand);
+    release(chains->d_meta);
+    release(chains->d_fg);
+    release(chains->d_v);
     delete chains;
 }
 
@@ -362,7 +368,7 @@ static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t ch
         return fail(AT_E_UNSUPPORTED, "at_sa_run: step counter must fit 32 bits");
     DeviceGuard g(chains->device);
     const bool init = !chains->initialised;
-    hipError_t e = launch_sa(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
+    hipError_t e = launch_sa_tp(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "at_sa_run");
     chains->initialised = true;
     chains->step_abs += (uint64_t)steps;

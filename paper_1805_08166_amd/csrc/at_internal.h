@@ -23,6 +23,8 @@ constexpr int N_BUFFERS = 3;
 // lane of a wave reads its own bank whatever feature it asks for.
 constexpr int TILE_LANES = 256;
 constexpr int MAX_TILE_QUADS = 64;   // up to 256 features
+// Packed ensembles are zero-padded to a multiple of this many words.
+constexpr size_t ENSEMBLE_PAD_WORDS = 8192;
 
 // Schedule space as the kernels see it.  Split knobs come first (one per
 // axis, axis a is knob a), then auto_unroll_max_step, then unroll_explicit.
@@ -53,6 +55,14 @@ struct EnsembleDesc {
     int32_t n_features;
     int32_t words_per_tree;
     const uint32_t* words;
+};
+
+// Per-chain best-list bookkeeping kept between kernels: number of valid
+// entries and the last (k-th) entry.
+struct ChainMeta {
+    uint32_t count;
+    float kth_score;
+    uint64_t kth_cfg;
 };
 
 // Tile byte offset of feature f: quad (f >> 2), byte (f & 3).
@@ -135,6 +145,11 @@ struct at_chains_s {
     at::DeviceBuf d_top;      // at_entry [n_chains][topk]
     at::DeviceBuf d_descs;    // copy of the space's SpaceDesc[n_spaces]
     at::DeviceBuf d_offsets;  // copy of the space's chain offsets
+    // workspace of the tree-partitioned annealing path
+    at::DeviceBuf d_cand;     // uint16 [n_chains][MAX_KNOBS] candidates
+    at::DeviceBuf d_meta;     // ChainMeta [n_chains]
+    at::DeviceBuf d_fg;       // uint32 [Q][n_chains] packed candidate features
+    at::DeviceBuf d_v;        // float leaf values, [ceil(T/4)][n_chains][4]
 };
 
 namespace at {
@@ -152,9 +167,14 @@ hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n,
                           hipStream_t stream);
 hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
                           uint16_t* leaves, hipStream_t stream);
+hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
+                        uint16_t* leaves, hipStream_t stream);
 hipError_t launch_sa(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
                      bool init, const float* thr, at_entry* best, at_entry* trace,
                      hipStream_t stream);
+hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
+                        bool init, const float* thr, at_entry* best, at_entry* trace,
+                        hipStream_t stream);
 hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score,
                          hipStream_t stream);
 

@@ -135,7 +135,8 @@ def test_features_out_of_range_rows_and_unaligned_output(P):
 # ensemble scoring
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("depth,trees,F", [(1, 5, 13), (3, 37, 110), (5, 9, 176), (6, 100, 110), (8, 37, 176),
-                                           (10, 11, 176), (11, 3, 64), (12, 2, 176)])
+                                           (10, 11, 176), (11, 3, 64), (12, 2, 176), (1, 700, 176), (2, 1029, 176),
+                                           (6, 101, 176), (7, 33, 176), (8, 1, 176), (9, 6, 176), (11, 5, 176)])
 def test_predict_matches_oracle_with_leaf_indices(P, depth, trees, F):
     import torch
     say(f"predict depth {depth} trees {trees} F {F}")
