@@ -122,6 +122,58 @@ __device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_
     }
 }
 
+// The loop-context features of loop p alone (out[0..10]), for evaluating one
+// schedule with one lane per loop.  Same arithmetic as nest_features: the
+// running products over the loops at or inside p are formed by visiting every
+// loop from the innermost outwards and multiplying in only those with index
+// >= p; loop p's own quantities are captured when it is visited.
+template <int TMPL>
+__device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4], uint32_t unroll_max,
+                                              uint32_t unroll_id, int p, uint32_t (&out)[11]) {
+    using N = Nest<TMPL>;
+    uint32_t range[6] = {1u, 1u, 1u, 1u, 1u, 1u};
+    uint32_t bottom_up = 1u, ext = 1u, bind = 0u;
+    uint32_t strd[3] = {0u, 0u, 0u};
+#pragma unroll
+    for (int q = N::L - 1; q >= 0; --q) {
+        const bool in = q >= p, at = q == p;
+        uint32_t e, sq[3];
+        if (N::axis[q] == FUSED) {
+            const int l = N::level[q];
+            const uint32_t fy = fac[4][l], fx = fac[5][l];
+            e = fy * fx;
+#pragma unroll
+            for (int b = 0; b < 3; ++b)
+                sq[b] = (fx > 1u) ? (uint32_t)sd.coef[b][5] * range[5] : (uint32_t)sd.coef[b][4] * range[4];
+            range[4] *= in ? fy : 1u;
+            range[5] *= in ? fx : 1u;
+        } else {
+            const int a = N::axis[q];
+            e = fac[a][N::level[q]];
+#pragma unroll
+            for (int b = 0; b < 3; ++b) sq[b] = (uint32_t)sd.coef[b][a] * range[a];
+            range[a] *= in ? e : 1u;
+        }
+        bottom_up *= in ? e : 1u;
+        if (at) {
+            ext = e;
+            bind = (uint32_t)N::bind[q];
+#pragma unroll
+            for (int b = 0; b < 3; ++b) strd[b] = sq[b];
+        }
+    }
+    uint32_t t[3];
+    N::touched(range, (uint32_t)sd.stride, t);
+    out[0] = bitlen(ext);
+    out[1] = bind ? bind : ((unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u);
+#pragma unroll
+    for (int b = 0; b < 3; ++b) {
+        out[2 + 3 * b] = bitlen(t[b]);
+        out[3 + 3 * b] = bitlen_quot(bottom_up, t[b]);
+        out[4 + 3 * b] = bitlen(strd[b]);
+    }
+}
+
 __device__ __forceinline__ uint32_t unroll_max_of(uint32_t v) { return v == 0u ? 0u : (v == 1u ? 512u : 1500u); }
 
 // Factors of every axis for knob values kv (split knob a = axis a).

@@ -17,6 +17,8 @@
 // V is laid out in groups of four trees: the values of trees 4g..4g+3 for
 // chain c are the 16 bytes at V[(g * n + c) * 4], so the fold reads one
 // float4 per lane per group, coalesced across the wave.
+#include <cstddef>
+
 #include "at_device.h"
 
 namespace at {
@@ -25,11 +27,13 @@ namespace {
 using namespace dev;
 
 constexpr int TREE_WG = 256;
-constexpr int CHAIN_WG = 256;           // one wave of chains + three loader waves
-constexpr int CHAINS_PER_WG = 64;
-constexpr int FOLD_GROUPS = 32;         // 4-tree groups per staged chunk (32 KB)
-constexpr int LOAD_PER_THREAD = (FOLD_GROUPS * CHAINS_PER_WG + 191) / 192;
+constexpr int CHAIN_WG = 256;           // wave 0 runs the chains, all four waves move data
+constexpr int CPW = 16;                 // chains per chain-kernel workgroup
+constexpr int FOLD_GROUPS = 512;        // 4-tree groups per fold pass: 512 x 16 chains x 16 B = 128 KB
+constexpr int KMAX = 64;                // largest best list
+constexpr int FAC_MAX = 1024;           // split choices staged in LDS (8 KB)
 constexpr int TREE_LDS_BYTES = 65536;   // resident tree words per workgroup
+constexpr size_t MAX_LDS_BYTES = 163840; // LDS of one compute unit
 
 enum { FIN_NONE = 0, FIN_INIT = 1, FIN_STEP = 2 };
 enum { DRAW_NONE = 0, DRAW_INIT = 1, DRAW_PROPOSE = 2 };
@@ -61,6 +65,12 @@ struct ChainArgs {
     at_entry* best;           // copy of the best lists (last launch), or null
 };
 
+__device__ __forceinline__ int space_of(const ChainArgs& a, int64_t c) {
+    int w = 0;
+    while (w + 1 < a.n_spaces && a.offsets[w + 1] <= c) ++w;
+    return w;
+}
+
 __device__ __forceinline__ void load_knobs(const uint16_t* p, int64_t c, uint32_t (&kv)[MAX_KNOBS]) {
     const uint4 w = reinterpret_cast<const uint4*>(p)[c];
     const uint32_t pw[4] = {w.x, w.y, w.z, w.w};
@@ -77,128 +87,283 @@ __device__ __forceinline__ void store_knobs(uint16_t* p, int64_t c, const uint32
     reinterpret_cast<uint4*>(p)[c] = w;
 }
 
-// Loads chunk k of the leaf values of this workgroup's chains into vbuf:
-// element i is group (k * FOLD_GROUPS + i / 64), chain c0 + i % 64.  Called
-// by the three loader waves; all loads are issued before the LDS stores.
-__device__ __forceinline__ void load_fold_chunk(const float4* __restrict__ V4, int64_t n, int64_t c0, int nc,
-                                                int groups, int k, float4* __restrict__ dst, int ltid) {
-    float4 r[LOAD_PER_THREAD];
-#pragma unroll
-    for (int u = 0; u < LOAD_PER_THREAD; ++u) {
-        const int i = ltid + u * 192;
-        const int g = k * FOLD_GROUPS + i / CHAINS_PER_WG, j = i % CHAINS_PER_WG;
-        r[u] = (i < FOLD_GROUPS * CHAINS_PER_WG && g < groups && j < nc) ? V4[(int64_t)g * n + c0 + j]
-                                                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+// Issues the loads of groups [g0, g0+ng) of the leaf values of chains
+// c0 .. c0+15 straight into LDS: each wave instruction moves four groups of
+// the 16 chains (1 KB, lane l -> group g0 + 4*ins + l/16, chain c0 + l%16),
+// so vbuf[g * 16 + j] holds group g0+g of chain c0+j.  Addresses past the
+// last group or chain are clamped (those slots are never read).
+__device__ __forceinline__ void issue_fold_loads(const float4* __restrict__ V4, int64_t n, int64_t c0, int nc,
+                                                 int groups, int g0, int ng, float4* vbuf, int wave, int lane) {
+    const int ninstr = (ng + 3) >> 2;
+    const int j = lane & (CPW - 1);
+    const int jc = j < nc ? j : nc - 1;
+    for (int ins = wave; ins < ninstr; ins += CHAIN_WG / 64) {
+        const int g = g0 + ins * 4 + (lane >> 4);
+        const int gc = g < groups ? g : groups - 1;
+        __builtin_amdgcn_global_load_lds(V4 + (int64_t)gc * n + c0 + jc, vbuf + ins * 64, 16, 0, 0);
     }
+}
+
+__device__ __forceinline__ bool precedes(float sa, uint64_t ca, float sb, uint64_t cb) {
+    return sa > sb || (sa == sb && ca < cb);
+}
+
+// Per-chain record shared between the chain's owner lane and its group of
+// 16 lanes through LDS.
+struct ChainRec {
+    uint64_t cfg;
+    float score;
+    uint32_t count;
+    float kth_score;
+    uint32_t qual;
+    uint64_t kth_cfg;
+    uint32_t nx[MAX_KNOBS / 2];   // proposed knob values, packed in pairs
+};
+
+// Offers (cfg, sc) to the best list of one chain held in LDS, with the 16
+// lanes r = 0..15 of its group (entries are ordered by score descending then
+// index ascending, distinct indices, at most k <= 64).  Lane r looks after
+// entries r, r+16, r+32, r+48.  A wave ballot gives whether the index is
+// already listed and how many entries precede the new one (its position);
+// the entries from that position on then move down by one.  All lanes of
+// the wave must call this (the ballots are wave-wide); gm selects the
+// group's 16 bits of a ballot mask and `active` the lanes of a group whose
+// chain offers.
+__device__ __forceinline__ void group_offer(at_entry* list, ChainRec& rec, int k, int r, uint64_t gm, bool active) {
+    const uint64_t cfg = rec.cfg;
+    const float sc = rec.score;
+    const int count = active ? (int)rec.count : 0;
+    at_entry old[4], prev[4];
+    bool dup = false;
+    uint32_t pre = 0;
 #pragma unroll
-    for (int u = 0; u < LOAD_PER_THREAD; ++u) {
-        const int i = ltid + u * 192;
-        if (i < FOLD_GROUPS * CHAINS_PER_WG) dst[i] = r[u];
+    for (int u = 0; u < 4; ++u) {
+        const int i = r + 16 * u;
+        if (active && i < count) {
+            old[u] = list[i];
+            dup |= old[u].cfg == cfg;
+            pre |= precedes(old[u].score, old[u].cfg, sc, cfg) ? (1u << u) : 0u;
+        }
+        if (active && i > 0 && i <= count && i < k) prev[u] = list[i - 1];
+    }
+    const bool any_dup = (__ballot(dup) & gm) != 0;
+    int pos = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) pos += __popcll(__ballot((pre >> u) & 1u) & gm);
+    if (!active || any_dup) return;
+    // new list: entries before pos stay, the new entry goes to pos, later
+    // entries move down one place, the last one drops out when the list is full
+    const int n_new = count < k ? count + 1 : k;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = r + 16 * u;
+        if (i >= pos && i < n_new) {
+            at_entry e;
+            if (i == pos) {
+                e.cfg = cfg;
+                e.score = sc;
+                e.flag = 1u;
+            } else {
+                e = prev[u];
+            }
+            list[i] = e;
+            if (i == n_new - 1) {
+                rec.count = (uint32_t)n_new;
+                rec.kth_score = e.score;
+                rec.kth_cfg = e.cfg;
+            }
+        }
     }
 }
 
 template <int TMPL>
 __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
+    using N = Nest<TMPL>;
     constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
-    constexpr int Q = (Nest<TMPL>::F + 3) / 4;
-    __shared__ float4 vbuf[2][FOLD_GROUPS * CHAINS_PER_WG];
+    constexpr int Q = (N::F + 3) / 4;
+    constexpr int RS = Q * 4 + 4;                 // feature row stride (bytes) in LDS
+    extern __shared__ float4 vbuf[];   // min(groups rounded up to 4, FOLD_GROUPS) * CPW entries
+    __shared__ at_entry lists[CPW][KMAX + 1];
+    __shared__ ChainRec rec[CPW];
+    __shared__ uint8_t frow[CPW][RS];
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
-    const int64_t c0 = (int64_t)blockIdx.x * CHAINS_PER_WG;
-    const int nc = (a.n - c0 < CHAINS_PER_WG) ? (int)(a.n - c0) : CHAINS_PER_WG;
-    const int64_t c = c0 + (tid & 63);
+    const int64_t c0 = (int64_t)blockIdx.x * CPW;
+    const int nc = (a.n - c0 < CPW) ? (int)(a.n - c0) : CPW;
+    const bool owner = tid < nc;                 // lanes of wave 0 that own a chain
+    const int64_t c = c0 + (owner ? tid : 0);
+    const int k = a.topk;
+    // group of 16 lanes per chain for the best-list offer and the features
+    const int gj = tid >> 4, gr = tid & 15;
+    const uint64_t gmask = 0xffffull << (16 * (gj & 3));
+    const bool gvalid = gj < nc;
 
-    // score of the pending candidate: its leaves added in tree order.  The
-    // leaf values are staged through LDS in chunks by waves 1-3 while wave 0
-    // (one lane per chain) folds the previous chunk.
-    float s = 0.0f;
+    // The workgroup's space: when all its chains share one space whose split
+    // tables fit, the descriptor and tables are staged in LDS; otherwise each
+    // lane reads its own space from global memory.
+    __shared__ SpaceDesc s_desc;
+    __shared__ uint64_t s_fac[FAC_MAX];
+    const int w_lo = space_of(a, c0), w_hi = space_of(a, c0 + nc - 1);
+    int fac_lo = 0, fac_n = 0;
+    if (w_lo == w_hi) {
+        const SpaceDesc& g = a.descs[w_lo];
+        fac_lo = g.split_off[0];
+        for (int ax = 0; ax < g.n_axes; ++ax) fac_n += (int)g.knob_size[ax];
+    }
+    const bool staged = w_lo == w_hi && fac_n <= FAC_MAX;
+    if (staged) {
+        constexpr int DW = (int)(sizeof(SpaceDesc) / 4);
+        constexpr int SO = (int)(offsetof(SpaceDesc, split_off) / 4);
+        const uint32_t* gd = reinterpret_cast<const uint32_t*>(a.descs + w_lo);
+        uint32_t* ld = reinterpret_cast<uint32_t*>(&s_desc);
+        for (int i = tid; i < DW; i += CHAIN_WG)
+            ld[i] = (i >= SO && i < SO + MAX_AXES) ? gd[i] - (uint32_t)fac_lo : gd[i];
+        for (int i = tid; i < fac_n; i += CHAIN_WG) s_fac[i] = a.factors[fac_lo + i];
+    }
+    const uint64_t* facp = staged ? s_fac : a.factors;
+    // owner lanes: their chain's space; group lanes: the space of chain gj
+    const SpaceDesc* sdp = staged ? &s_desc : a.descs + space_of(a, c);
+    const SpaceDesc* gsdp = staged ? &s_desc : a.descs + space_of(a, c0 + (gvalid ? gj : 0));
+    if (a.fin == FIN_NONE) __syncthreads();   // (otherwise the fold's barrier publishes the staging)
+
+    // per-chain state, fetched before the fold so the loads overlap it
+    uint32_t cur[MAX_KNOBS], cd[MAX_KNOBS];
+    ChainMeta m;
+    m.count = 0;
+    m.kth_score = 0.0f;
+    m.kth_cfg = 0;
+    float cur_s = 0.0f, thr_v = 0.0f;
+    if (owner) {
+        load_knobs(a.knobs, c, cur);
+        if (a.fin != FIN_NONE) load_knobs(a.cand, c, cd);
+        if (a.fin == FIN_STEP) {
+            m = a.meta[c];
+            cur_s = a.cur_score[c];
+            thr_v = a.thr[c * a.steps + a.fin_step];
+        }
+    }
+
     if (a.fin != FIN_NONE) {
+        // score of the pending candidate: its leaves added in tree order.  All
+        // four waves move the leaf values of the 16 chains into LDS (up to
+        // 2048 trees per pass), then one lane per chain folds them.
         const float4* V4 = reinterpret_cast<const float4*>(a.V);
         const int groups = (a.T + 3) >> 2;
-        const int chunks = (groups + FOLD_GROUPS - 1) / FOLD_GROUPS;
-        if (wave > 0) load_fold_chunk(V4, a.n, c0, nc, groups, 0, vbuf[0], tid - 64);
-        __syncthreads();
-        for (int k = 0; k < chunks; ++k) {
-            if (wave == 0) {
-                const float4* src = vbuf[k & 1] + (tid & 63);
-                const int g_end = (groups - k * FOLD_GROUPS < FOLD_GROUPS) ? groups - k * FOLD_GROUPS : FOLD_GROUPS;
+        float s = 0.0f;
+        for (int g0 = 0; g0 < groups; g0 += FOLD_GROUPS) {
+            const int ng = (groups - g0 < FOLD_GROUPS) ? groups - g0 : FOLD_GROUPS;
+            if (g0 > 0) __syncthreads();   // the previous pass has been folded
+            issue_fold_loads(V4, a.n, c0, nc, groups, g0, ng, vbuf, wave, tid & 63);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (owner) {
+                const float4* src = vbuf + tid;
+                const bool last = g0 + ng == groups;
+                const int full = (last && (a.T & 3)) ? ng - 1 : ng;
 #pragma unroll 8
-                for (int g = 0; g < g_end; ++g) {
-                    const float4 q = src[g * CHAINS_PER_WG];
-                    const int t = (k * FOLD_GROUPS + g) * 4;
+                for (int g = 0; g < full; ++g) {
+                    const float4 q = src[g * CPW];
                     s = s + q.x;
-                    if (t + 1 < a.T) s = s + q.y;
-                    if (t + 2 < a.T) s = s + q.z;
-                    if (t + 3 < a.T) s = s + q.w;
+                    s = s + q.y;
+                    s = s + q.z;
+                    s = s + q.w;
                 }
-            } else if (k + 1 < chunks) {
-                load_fold_chunk(V4, a.n, c0, nc, groups, k + 1, vbuf[(k + 1) & 1], tid - 64);
+                if (full < ng) {
+                    const float4 q = src[full * CPW];
+                    const int r = a.T & 3;
+                    s = s + q.x;
+                    if (r > 1) s = s + q.y;
+                    if (r > 2) s = s + q.z;
+                }
+            }
+        }
+
+        // best lists: the chains whose candidate would enter their list bring
+        // it into LDS, where the chain's group of 16 lanes inserts it; the
+        // lists are then written back.  Skipped when no chain qualifies.
+        uint64_t cfg = 0;
+        int qual = 0;
+        if (owner) {
+            const SpaceDesc& sd = *sdp;
+#pragma unroll
+            for (int j = 0; j < MAX_KNOBS; ++j)
+                if (j < sd.n_knobs) cfg += (uint64_t)cd[j] * sd.radix[j];
+            qual = (a.fin == FIN_INIT || (int)m.count < k || precedes(s, cfg, m.kth_score, m.kth_cfg)) ? 1 : 0;
+            ChainRec& R = rec[tid];
+            R.cfg = cfg;
+            R.score = s;
+            R.count = m.count;
+            R.kth_score = m.kth_score;
+            R.kth_cfg = m.kth_cfg;
+            R.qual = (uint32_t)qual;
+        } else if (tid < CPW) {
+            rec[tid].qual = 0;
+        }
+        if (__syncthreads_or(qual)) {
+            for (int idx = tid; idx < CPW * k; idx += CHAIN_WG) {
+                const int j = idx / k, i = idx - j * k;
+                if (rec[j].qual) {
+                    at_entry e;
+                    if (a.fin == FIN_INIT) {
+                        e.cfg = 0;
+                        e.score = 0.0f;
+                        e.flag = 0u;
+                    } else {
+                        e = a.top[(c0 + j) * k + i];
+                    }
+                    lists[j][i] = e;
+                }
             }
             __syncthreads();
-        }
-    }
-    if (wave != 0 || (tid & 63) >= nc) return;
-
-    int w = 0;
-    while (w + 1 < a.n_spaces && a.offsets[w + 1] <= c) ++w;
-    const SpaceDesc& sd = a.descs[w];
-    const uint64_t gchain = a.chain0 + (uint64_t)c;
-    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-    at_entry* list = a.top + c * a.topk;
-
-    uint32_t cur[MAX_KNOBS];
-    load_knobs(a.knobs, c, cur);
-
-    if (a.fin != FIN_NONE) {
-        uint32_t cd[MAX_KNOBS];
-        load_knobs(a.cand, c, cd);
-        uint64_t cfg = 0;
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j)
-            if (j < sd.n_knobs) cfg += (uint64_t)cd[j] * sd.radix[j];
-        ChainMeta m;
-        if (a.fin == FIN_INIT) {
-            for (int i = 0; i < a.topk; ++i) {
-                at_entry z;
-                z.cfg = 0;
-                z.score = 0.0f;
-                z.flag = 0u;
-                list[i] = z;
-            }
-            m.count = 0;
-            m.kth_score = 0.0f;
-            m.kth_cfg = 0;
-        } else {
-            m = a.meta[c];
-        }
-        int count = (int)m.count;
-        offer(list, a.topk, count, m.kth_score, m.kth_cfg, cfg, s);
-        m.count = (uint32_t)count;
-        a.meta[c] = m;
-        bool acc;
-        if (a.fin == FIN_INIT) {
-            acc = true;
-        } else {
-            const float delta = s - a.cur_score[c];
-            acc = delta >= a.thr[c * a.steps + a.fin_step];
-            if (a.trace) {
-                at_entry t;
-                t.cfg = cfg;
-                t.score = s;
-                t.flag = acc ? 1u : 0u;
-                a.trace[c * a.steps + a.fin_step] = t;
+            group_offer(lists[gj], rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
+            __syncthreads();
+            for (int idx = tid; idx < CPW * k; idx += CHAIN_WG) {
+                const int j = idx / k, i = idx - j * k;
+                if (rec[j].qual) a.top[(c0 + j) * k + i] = lists[j][i];
             }
         }
-        if (acc) {
+        if (owner) {
+            if (qual) {
+                const ChainRec& R = rec[tid];
+                m.count = R.count;
+                m.kth_score = R.kth_score;
+                m.kth_cfg = R.kth_cfg;
+                a.meta[c] = m;
+            }
+            bool acc = true;
+            if (a.fin == FIN_STEP) {
+                const float delta = s - cur_s;
+                acc = delta >= thr_v;
+                if (a.trace) {
+                    at_entry t;
+                    t.cfg = cfg;
+                    t.score = s;
+                    t.flag = acc ? 1u : 0u;
+                    a.trace[c * a.steps + a.fin_step] = t;
+                }
+            }
+            if (acc) {
 #pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
-            store_knobs(a.knobs, c, cur);
-            a.cur_score[c] = s;
+                for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
+                store_knobs(a.knobs, c, cur);
+                a.cur_score[c] = s;
+            }
         }
     }
 
-    if (a.draw != DRAW_NONE) {
-        uint32_t cd[MAX_KNOBS];
+    if (a.best) {
+        // the lists were written back above by this workgroup
+        __syncthreads();
+        for (int idx = tid; idx < nc * k; idx += CHAIN_WG) a.best[c0 * k + idx] = a.top[c0 * k + idx];
+    }
+    if (a.draw == DRAW_NONE) return;
+
+    // proposal (owner lanes)
+    if (owner) {
+        const SpaceDesc& sd = *sdp;
+        const uint64_t gchain = a.chain0 + (uint64_t)c;
+        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+        uint32_t nx[MAX_KNOBS];
         if (a.draw == DRAW_INIT) {
             // each knob uniform over its values: block (chain, 0, 1, j / 4)
             U4 r{0, 0, 0, 0};
@@ -206,12 +371,14 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             for (int j = 0; j < MAX_KNOBS; ++j) {
                 if ((j & 3) == 0) r = philox(k0, k1, U4{(uint32_t)gchain, 0u, 1u, (uint32_t)(j >> 2)});
                 const uint32_t word = (j & 3) == 0 ? r.x : (j & 3) == 1 ? r.y : (j & 3) == 2 ? r.z : r.w;
-                cd[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
+                nx[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
             }
         } else {
+            // one knob, uniform among those with two or more values, moves to a
+            // uniformly chosen other value: block (chain, step, 0, 0)
             const U4 r = philox(k0, k1, U4{(uint32_t)gchain, a.draw_step, 0u, 0u});
 #pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j) cd[j] = cur[j];
+            for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = cur[j];
             if (sd.n_mut > 0) {
                 const int jm = sd.mut[uniform_below(r.x, (uint32_t)sd.n_mut)];
                 uint32_t old = 0, size = 2;
@@ -222,23 +389,39 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
                 if (nv >= old) nv += 1u;
 #pragma unroll
                 for (int j = 0; j < MAX_KNOBS; ++j)
-                    if (j == jm) cd[j] = nv;
+                    if (j == jm) nx[j] = nv;
             }
         }
-        store_knobs(a.cand, c, cd);
-        uint32_t fac[6][4];
-        gather_factors<TMPL>(sd, a.factors, cd, fac);
-        uint32_t words[Q];
+        store_knobs(a.cand, c, nx);
 #pragma unroll
-        for (int q = 0; q < Q; ++q) words[q] = 0u;
-        nest_features<TMPL>(sd, fac, unroll_max_of(cd[A]), 1u + cd[A + 1],
-                            [&](int f, uint32_t v) { words[f >> 2] |= v << (8 * (f & 3)); });
-#pragma unroll
-        for (int q = 0; q < Q; ++q) a.Fg[(int64_t)q * a.n + c] = words[q];
+        for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = nx[2 * j] | (nx[2 * j + 1] << 16);
     }
+    __syncthreads();
 
-    if (a.best) {
-        for (int i = 0; i < a.topk; ++i) a.best[c * a.topk + i] = list[i];
+    // features: lane gr of group gj evaluates loop gr of chain gj's candidate
+    if (gvalid && gr < N::L) {
+        const SpaceDesc& sd = *gsdp;
+        uint32_t nx[MAX_KNOBS];
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (rec[gj].nx[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+        uint32_t fac[6][4];
+        gather_factors<TMPL>(sd, facp, nx, fac);
+        uint32_t f[11];
+        loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f);
+#pragma unroll
+        for (int i = 0; i < 11; ++i) frow[gj][gr * 11 + i] = (uint8_t)f[i];
+    }
+    __syncthreads();
+    // packed rows out, consecutive lanes on consecutive chains
+    for (int idx = tid; idx < nc * Q; idx += CHAIN_WG) {
+        const int q = idx / nc, j = idx - q * nc;
+        uint32_t w = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int f = 4 * q + b;
+            if (f < N::F) w |= (uint32_t)frow[j][f] << (8 * b);
+        }
+        a.Fg[(int64_t)q * a.n + c0 + j] = w;
     }
 }
 
@@ -251,87 +434,123 @@ struct TreeArgs {
     int tpw;              // trees per workgroup
 };
 
+// Walks GROUP trees (local index t, LDS byte offset tree_base + t * TB) for
+// this lane's chain and stores their leaf values to V.  Trees t_global ..
+// t_global+GROUP-1 of one chain are consecutive 4-byte slots of V when they
+// lie in one group of four, so aligned groups are stored as one vector.
 template <int DEPTH, int GROUP>
-__device__ __forceinline__ void walk_store(const uint32_t* __restrict__ trees, const uint8_t* __restrict__ tile_b,
-                                           uint32_t fb, int t_local, int t_global, int64_t c, int64_t n,
-                                           float* __restrict__ V, bool active) {
-    constexpr int W = 2 << DEPTH;
+__device__ __forceinline__ void walk_store(const uint8_t* __restrict__ L, uint32_t tree_base, uint32_t fb, int t,
+                                           int t_global, int64_t c, int64_t n, float* __restrict__ V, bool active) {
+    constexpr uint32_t TB = (2u << DEPTH) * 4u;
     uint32_t lw[GROUP], li[GROUP];
-    walk<DEPTH, GROUP>(trees, tile_b, fb, t_local * W, lw, li);
-    if (active) {
+    walk_pair<DEPTH, GROUP>(L, tree_base + (uint32_t)t * TB, fb, lw, li);
+    if (!active) return;
+    float* dst = V + ((((int64_t)(t_global >> 2) * n + c) << 2) + (t_global & 3));
+    if (GROUP == 4 && (t_global & 3) == 0) {
+        *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(lw[0]), __uint_as_float(lw[1 % GROUP]),
+                                                      __uint_as_float(lw[2 % GROUP]), __uint_as_float(lw[3 % GROUP]));
+    } else if (GROUP == 2 && (t_global & 1) == 0) {
+        *reinterpret_cast<float2*>(dst) = make_float2(__uint_as_float(lw[0]), __uint_as_float(lw[1 % GROUP]));
+    } else {
 #pragma unroll
         for (int g = 0; g < GROUP; ++g) {
-            const int t = t_global + g;
-            V[(((int64_t)(t >> 2) * n + c) << 2) + (t & 3)] = __uint_as_float(lw[g]);
+            const int tg = t_global + g;
+            V[(((int64_t)(tg >> 2) * n + c) << 2) + (tg & 3)] = __uint_as_float(lw[g]);
         }
     }
 }
 
-// Walks `r` (< 2*H) trees starting at local tree t, in groups of H, H/2, ..., 1.
+// Walks r (< 2*H) remaining trees starting at local tree t, in groups of H, H/2, ..., 1.
 template <int DEPTH, int H>
-__device__ __forceinline__ void walk_rest(const uint32_t* __restrict__ trees, const uint8_t* __restrict__ tile_b,
-                                          uint32_t fb, int t, int t_global, int r, int64_t c, int64_t n,
-                                          float* __restrict__ V, bool active) {
+__device__ __forceinline__ void walk_rest(const uint8_t* __restrict__ L, uint32_t tree_base, uint32_t fb, int t,
+                                          int t_global, int r, int64_t c, int64_t n, float* __restrict__ V,
+                                          bool active) {
     if (r >= H) {
-        walk_store<DEPTH, H>(trees, tile_b, fb, t, t_global, c, n, V, active);
+        walk_store<DEPTH, H>(L, tree_base, fb, t, t_global, c, n, V, active);
         t += H;
         t_global += H;
         r -= H;
     }
-    if constexpr (H > 1) walk_rest<DEPTH, H / 2>(trees, tile_b, fb, t, t_global, r, c, n, V, active);
+    if constexpr (H > 1) walk_rest<DEPTH, H / 2>(L, tree_base, fb, t, t_global, r, c, n, V, active);
 }
 
-template <int DEPTH, int Q>
-__global__ __launch_bounds__(TREE_WG) void k_trees(TreeArgs a) {
+// LDS: NT feature tiles (Q quads x 256 chains each, quad-major) from byte 0,
+// then the workgroup's trees.  A workgroup of NT*256 threads walks NT*256
+// chains per block, thread i in tile i / 256.  The next block's features are
+// fetched into registers while the current block is walked; the fetch is
+// unconditional (the chain index is clamped) so that it is issued ahead of
+// the walk.
+template <int DEPTH, int Q, int NT>
+__global__ __launch_bounds__(NT * 256) void k_trees(TreeArgs a) {
     constexpr int W = 2 << DEPTH;
-    constexpr int G = (DEPTH <= 8) ? 8 : 4;
+    constexpr int G = 4;
+    constexpr int TW = NT * 256;
+    constexpr uint32_t TILE_BYTES = (uint32_t)Q * 256u * 4u;
     extern __shared__ uint32_t lds[];
-    uint32_t* tile = lds;
-    uint32_t* trees = lds + Q * TREE_WG;
-    const uint8_t* tile_b = reinterpret_cast<const uint8_t*>(tile);
+    const uint8_t* L = reinterpret_cast<const uint8_t*>(lds);
+    uint32_t* trees = lds + NT * Q * 256;
     const int tid = threadIdx.x;
+    const int h = tid >> 8, lane = tid & 255;
+    uint32_t* tile = lds + h * Q * 256;
     const int t0 = blockIdx.x * a.tpw;
     const int nt = (a.e.n_trees - t0 < a.tpw) ? (a.e.n_trees - t0) : a.tpw;
     if (nt <= 0) return;
-    stage_words(trees, a.e.words + (size_t)t0 * W, nt * W);
-    const uint32_t fb = tid * 4u;
-    // the next block's features are fetched into registers during the walk
+    const int64_t n = a.n;
     uint32_t pre[Q];
+    {
+        const int64_t cf = tid < n ? tid : n - 1;
 #pragma unroll
-    for (int q = 0; q < Q; ++q) pre[q] = (tid < a.n) ? a.Fg[(int64_t)q * a.n + tid] : 0u;
-    for (int64_t cb = 0; cb < a.n; cb += TREE_WG) {
+        for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cf];
+    }
+    {
+        const uint4* s4 = reinterpret_cast<const uint4*>(a.e.words + (size_t)t0 * W);
+        uint4* d4 = reinterpret_cast<uint4*>(trees);
+        for (int i = tid; i < nt * W / 4; i += TW) d4[i] = s4[i];
+    }
+    const uint32_t fb = (uint32_t)h * TILE_BYTES + (uint32_t)lane * 4u;
+    const uint32_t tree_base = NT * TILE_BYTES;
+    for (int64_t cb = 0; cb < n; cb += TW) {
         __syncthreads();
 #pragma unroll
-        for (int q = 0; q < Q; ++q) tile[q * TREE_WG + tid] = pre[q];
+        for (int q = 0; q < Q; ++q) tile[q * 256 + lane] = pre[q];
         __syncthreads();
         const int64_t c = cb + tid;
-        const bool active = c < a.n;
-        const int64_t cn = c + TREE_WG;
-        if (cb + TREE_WG < a.n) {
+        const bool active = c < n;
+        {
+            const int64_t cn = (cb + TW + tid < n) ? cb + TW + tid : n - 1;
 #pragma unroll
-            for (int q = 0; q < Q; ++q) pre[q] = (cn < a.n) ? a.Fg[(int64_t)q * a.n + cn] : 0u;
+            for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cn];
         }
         int t = 0;
-        for (; t + G <= nt; t += G) walk_store<DEPTH, G>(trees, tile_b, fb, t, t0 + t, c, a.n, a.V, active);
-        walk_rest<DEPTH, G / 2>(trees, tile_b, fb, t, t0 + t, nt - t, c, a.n, a.V, active);
+        for (; t + G <= nt; t += G) walk_store<DEPTH, G>(L, tree_base, fb, t, t0 + t, c, n, a.V, active);
+        walk_rest<DEPTH, G / 2>(L, tree_base, fb, t, t0 + t, nt - t, c, n, a.V, active);
     }
 }
 
-template <int DEPTH, int Q>
-hipError_t launch_trees_depth(const TreeArgs& a, hipStream_t stream) {
+template <int DEPTH, int Q, int NT>
+hipError_t launch_trees_nt(const TreeArgs& a, hipStream_t stream) {
     constexpr int W = 2 << DEPTH;
-    const size_t lds = (size_t)Q * TREE_WG * 4 + (size_t)a.tpw * W * 4;
+    const size_t lds = (size_t)NT * Q * 256 * 4 + (size_t)a.tpw * W * 4;
     static bool configured = false;
     if (!configured) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_trees<DEPTH, Q>),
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_trees<DEPTH, Q, NT>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             Q * TREE_WG * 4 + TREE_LDS_BYTES);
+                                             NT * Q * 256 * 4 + TREE_LDS_BYTES);
         if (err != hipSuccess) return err;
         configured = true;
     }
     const int grid = (a.e.n_trees + a.tpw - 1) / a.tpw;
-    hipLaunchKernelGGL((k_trees<DEPTH, Q>), dim3(grid), dim3(TREE_WG), lds, stream, a);
+    hipLaunchKernelGGL((k_trees<DEPTH, Q, NT>), dim3(grid), dim3(NT * 256), lds, stream, a);
     return hipGetLastError();
+}
+
+// Two tiles (512 threads) when they and the trees fit in LDS, else one.
+template <int DEPTH, int Q>
+hipError_t launch_trees_depth(const TreeArgs& a, hipStream_t stream) {
+    constexpr int W = 2 << DEPTH;
+    const size_t two = (size_t)2 * Q * 256 * 4 + (size_t)a.tpw * W * 4;
+    if (two <= MAX_LDS_BYTES) return launch_trees_nt<DEPTH, Q, 2>(a, stream);
+    return launch_trees_nt<DEPTH, Q, 1>(a, stream);
 }
 
 template <int Q>
@@ -427,12 +646,27 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     if (tpw < 1) tpw = 1;
     ta.tpw = tpw;
 
-    const unsigned chain_grid = (unsigned)((n + CHAINS_PER_WG - 1) / CHAINS_PER_WG);
+    const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
+    // whole four-group wave instructions: the last one of a pass may cover
+    // up to three groups past its end
+    const int fold_groups = groups < FOLD_GROUPS ? (groups + 3) / 4 * 4 : FOLD_GROUPS;
+    const size_t chain_lds = (size_t)fold_groups * CPW * 16;
+    static bool chain_configured = false;
+    if (!chain_configured) {
+        for (const void* f : {reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM>),
+                              reinterpret_cast<const void*>(&k_chain<AT_TMPL_CONV2D_NCHW>)}) {
+            if ((err = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           FOLD_GROUPS * CPW * 16)) != hipSuccess)
+                return err;
+        }
+        chain_configured = true;
+    }
     auto chain_kernel = [&](const ChainArgs& x) -> hipError_t {
+        const size_t lds = x.fin == FIN_NONE ? 0 : chain_lds;
         if (sp.tmpl == AT_TMPL_GEMM)
-            hipLaunchKernelGGL(k_chain<AT_TMPL_GEMM>, dim3(chain_grid), dim3(CHAIN_WG), 0, stream, x);
+            hipLaunchKernelGGL(k_chain<AT_TMPL_GEMM>, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, x);
         else
-            hipLaunchKernelGGL(k_chain<AT_TMPL_CONV2D_NCHW>, dim3(chain_grid), dim3(CHAIN_WG), 0, stream, x);
+            hipLaunchKernelGGL(k_chain<AT_TMPL_CONV2D_NCHW>, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, x);
         return hipGetLastError();
     };
 
