@@ -176,7 +176,11 @@ at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint
  * thr: device [n_chains][steps] float; best: device [n_chains][topk]
  * at_entry receiving a copy of the best lists after the run (entries with
  * flag 0 are empty).  The ensemble's feature count must match the space's
- * (AT_E_MISMATCH).  steps == 0 only initialises. */
+ * (AT_E_MISMATCH).  steps == 0 only initialises.
+ * Workspace: the first run on a chains handle, and any run with more trees
+ * than before, allocates the chains' device workspace (about
+ * n_chains * (16 * ceil(n_trees / 4) + 4 * ceil(n_features / 4) + 32)
+ * bytes), which synchronises the device; later runs allocate nothing. */
 at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
                     const float* thr, at_entry* best, at_stream_t stream);
 

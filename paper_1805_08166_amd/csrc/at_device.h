@@ -263,30 +263,5 @@ __device__ __forceinline__ void walk_pair(const uint8_t* __restrict__ L, uint32_
     }
 }
 
-// Offers (cfg, score) to a chain's best list in global memory: ordered by
-// score descending then index ascending, distinct indices, at most k.
-// count / kth_* cache the list length and its last entry in registers.
-__device__ __forceinline__ void offer(at_entry* __restrict__ list, int k, int& count, float& kth_s,
-                                      uint64_t& kth_c, uint64_t cfg, float sc) {
-    if (count == k && !(sc > kth_s || (sc == kth_s && cfg < kth_c))) return;
-    int pos = count;
-    for (int i = 0; i < count; ++i) {
-        const at_entry e = list[i];
-        if (e.cfg == cfg) return;
-        if (pos == count && (sc > e.score || (sc == e.score && cfg < e.cfg))) pos = i;
-    }
-    const int last = (count < k) ? count : k - 1;
-    for (int i = last; i > pos; --i) list[i] = list[i - 1];
-    at_entry ne;
-    ne.cfg = cfg;
-    ne.score = sc;
-    ne.flag = 1u;
-    list[pos] = ne;
-    if (count < k) ++count;
-    const at_entry tail = list[count - 1];
-    kth_s = tail.score;
-    kth_c = tail.cfg;
-}
-
 }  // namespace dev
 }  // namespace at

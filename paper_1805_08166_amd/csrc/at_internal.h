@@ -169,9 +169,6 @@ hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n
                           uint16_t* leaves, hipStream_t stream);
 hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
                         uint16_t* leaves, hipStream_t stream);
-hipError_t launch_sa(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
-                     bool init, const float* thr, at_entry* best, at_entry* trace,
-                     hipStream_t stream);
 hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
                         bool init, const float* thr, at_entry* best, at_entry* trace,
                         hipStream_t stream);

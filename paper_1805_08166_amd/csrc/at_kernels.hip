@@ -176,157 +176,6 @@ __global__ __launch_bounds__(WG) void k_predict(EnsembleDesc e, const int32_t* _
     if (row < n) scores[row] = s;
 }
 
-// ==========================================================================
-// Parallel simulated annealing, one chain per lane (Section 3.3).
-// ==========================================================================
-
-struct SaArgs {
-    const SpaceDesc* descs;
-    const int64_t* offsets;   // [n_spaces + 1]
-    int n_spaces;
-    const uint64_t* factors;
-    uint16_t* knobs;          // [n_chains][MAX_KNOBS]
-    float* cur_score;         // [n_chains]
-    at_entry* top;            // [n_chains][topk]
-    int topk;
-    int64_t n_chains;
-    uint64_t chain0;
-    uint64_t seed;
-    uint64_t step_base;
-    int steps;
-    int init;
-    const float* thr;         // [n_chains][steps]
-    at_entry* best;           // [n_chains][topk]
-    at_entry* trace;          // [n_chains][steps] or null
-    int chunk_trees;
-};
-
-template <int TMPL, int DEPTH>
-__global__ __launch_bounds__(WG) void k_sa(SaArgs a, EnsembleDesc e) {
-    constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
-    extern __shared__ uint32_t lds[];
-    const int Q = (Nest<TMPL>::F + 3) / 4;
-    uint32_t* tile = lds;
-    uint32_t* chunk = lds + Q * WG;
-    uint8_t* tile_b = reinterpret_cast<uint8_t*>(tile);
-    const int tid = threadIdx.x;
-    const int64_t c = (int64_t)blockIdx.x * WG + tid;
-    const bool active = c < a.n_chains;
-    const int64_t cc = active ? c : 0;
-    int w = 0;
-    while (w + 1 < a.n_spaces && a.offsets[w + 1] <= cc) ++w;
-    const SpaceDesc& sd = a.descs[w];
-    const uint64_t gchain = a.chain0 + (uint64_t)cc;
-    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-
-    uint32_t kv[MAX_KNOBS];
-    at_entry* list = a.top + cc * a.topk;
-    int count = 0;
-    float kth_s = 0.0f;
-    uint64_t kth_c = 0;
-    float cur = 0.0f;
-
-    // score of knob vector v: features into this lane's tile column, then the walk
-    auto evaluate = [&](const uint32_t (&v)[MAX_KNOBS]) __attribute__((always_inline)) -> float {
-        uint32_t fac[6][4];
-        gather_factors<TMPL>(sd, a.factors, v, fac);
-        nest_features<TMPL>(sd, fac, unroll_max_of(v[A]), 1u + v[A + 1], [&](int f, uint32_t x) {
-            tile_b[tile_offset(f) + tid * 4] = (uint8_t)x;
-        });
-        return score_tile<DEPTH>(e, tile, chunk, a.chunk_trees, nullptr);
-    };
-    auto cfg_of = [&](const uint32_t (&v)[MAX_KNOBS]) __attribute__((always_inline)) -> uint64_t {
-        uint64_t x = 0;
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j)
-            if (j < sd.n_knobs) x += (uint64_t)v[j] * sd.radix[j];
-        return x;
-    };
-
-    if (a.init) {
-        // each knob uniform over its values: block (chain, 0, 1, j / 4)
-        U4 r{0, 0, 0, 0};
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j) {
-            if ((j & 3) == 0) r = philox(k0, k1, U4{(uint32_t)gchain, 0u, 1u, (uint32_t)(j >> 2)});
-            const uint32_t word = (j & 3) == 0 ? r.x : (j & 3) == 1 ? r.y : (j & 3) == 2 ? r.z : r.w;
-            kv[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
-        }
-        cur = evaluate(kv);
-        if (active) {
-            for (int i = 0; i < a.topk; ++i) {
-                at_entry z;
-                z.cfg = 0;
-                z.score = 0.0f;
-                z.flag = 0u;
-                list[i] = z;
-            }
-            offer(list, a.topk, count, kth_s, kth_c, cfg_of(kv), cur);
-        }
-    } else {
-        const uint4 packed = reinterpret_cast<const uint4*>(a.knobs)[cc];
-        const uint32_t pw[4] = {packed.x, packed.y, packed.z, packed.w};
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = (pw[j >> 1] >> (16 * (j & 1))) & 0xffffu;
-        cur = a.cur_score[cc];
-        if (active) {
-            while (count < a.topk && list[count].flag) ++count;
-            if (count > 0) {
-                kth_s = list[count - 1].score;
-                kth_c = list[count - 1].cfg;
-            }
-        }
-    }
-
-    for (int s = 0; s < a.steps; ++s) {
-        const U4 r = philox(k0, k1, U4{(uint32_t)gchain, (uint32_t)(a.step_base + (uint64_t)s), 0u, 0u});
-        uint32_t cand[MAX_KNOBS];
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j) cand[j] = kv[j];
-        if (sd.n_mut > 0) {
-            const int jm = sd.mut[uniform_below(r.x, (uint32_t)sd.n_mut)];
-            uint32_t old = 0, size = 2;
-#pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j)
-                if (j == jm) { old = kv[j]; size = sd.knob_size[j]; }
-            uint32_t nv = uniform_below(r.y, size - 1u);
-            if (nv >= old) nv += 1u;
-#pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j)
-                if (j == jm) cand[j] = nv;
-        }
-        const float sc = evaluate(cand);
-        if (active) {
-            const uint64_t cfg = cfg_of(cand);
-            offer(list, a.topk, count, kth_s, kth_c, cfg, sc);
-            const float delta = sc - cur;
-            const bool acc = delta >= a.thr[cc * a.steps + s];
-            if (acc) {
-                cur = sc;
-#pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = cand[j];
-            }
-            if (a.trace) {
-                at_entry t;
-                t.cfg = cfg;
-                t.score = sc;
-                t.flag = acc ? 1u : 0u;
-                a.trace[cc * a.steps + s] = t;
-            }
-        }
-    }
-    if (active) {
-        uint4 packed;
-        packed.x = kv[0] | (kv[1] << 16);
-        packed.y = kv[2] | (kv[3] << 16);
-        packed.z = kv[4] | (kv[5] << 16);
-        packed.w = kv[6] | (kv[7] << 16);
-        reinterpret_cast<uint4*>(a.knobs)[cc] = packed;
-        a.cur_score[cc] = cur;
-        for (int i = 0; i < a.topk; ++i) a.best[cc * a.topk + i] = list[i];
-    }
-}
-
 __global__ __launch_bounds__(WG) void k_export(const SpaceDesc* descs, const int64_t* offsets, int n_spaces,
                                                const uint16_t* knobs, const float* score, int64_t n,
                                                uint64_t* cur_cfg, float* cur_score) {
@@ -383,39 +232,6 @@ hipError_t predict_depth(const EnsembleDesc& e, const int32_t* feats, int64_t n,
     return hipGetLastError();
 }
 
-template <int TMPL, int DEPTH>
-hipError_t sa_depth(const SaArgs& a0, const EnsembleDesc& e, hipStream_t stream) {
-    SaArgs a = a0;
-    const int Q = (Nest<TMPL>::F + 3) / 4;
-    a.chunk_trees = chunk_trees_for(DEPTH, CHUNK_BYTES);
-    const size_t lds = (size_t)Q * WG * 4 + (size_t)a.chunk_trees * (2 << DEPTH) * 4;
-    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sa<TMPL, DEPTH>),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (err != hipSuccess) return err;
-    const unsigned grid = (unsigned)((a.n_chains + WG - 1) / WG);
-    hipLaunchKernelGGL((k_sa<TMPL, DEPTH>), dim3(grid), dim3(WG), lds, stream, a, e);
-    return hipGetLastError();
-}
-
-template <int TMPL>
-hipError_t sa_tmpl(const SaArgs& a, const EnsembleDesc& e, hipStream_t stream) {
-    switch (e.depth) {
-        case 1: return sa_depth<TMPL, 1>(a, e, stream);
-        case 2: return sa_depth<TMPL, 2>(a, e, stream);
-        case 3: return sa_depth<TMPL, 3>(a, e, stream);
-        case 4: return sa_depth<TMPL, 4>(a, e, stream);
-        case 5: return sa_depth<TMPL, 5>(a, e, stream);
-        case 6: return sa_depth<TMPL, 6>(a, e, stream);
-        case 7: return sa_depth<TMPL, 7>(a, e, stream);
-        case 8: return sa_depth<TMPL, 8>(a, e, stream);
-        case 9: return sa_depth<TMPL, 9>(a, e, stream);
-        case 10: return sa_depth<TMPL, 10>(a, e, stream);
-        case 11: return sa_depth<TMPL, 11>(a, e, stream);
-        case 12: return sa_depth<TMPL, 12>(a, e, stream);
-        default: return hipErrorInvalidValue;
-    }
-}
-
 }  // namespace
 
 hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
@@ -439,31 +255,6 @@ hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n
         case 12: return predict_depth<12>(e, feats, n, scores, leaves, stream);
         default: return hipErrorInvalidValue;
     }
-}
-
-hipError_t launch_sa(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps, bool init,
-                     const float* thr, at_entry* best, at_entry* trace, hipStream_t stream) {
-    SaArgs a{};
-    a.descs = static_cast<const SpaceDesc*>(sp.d_descs.p);
-    a.offsets = static_cast<const int64_t*>(sp.d_offsets.p);
-    a.n_spaces = sp.n_spaces;
-    a.factors = static_cast<const uint64_t*>(sp.d_factors.p);
-    a.knobs = static_cast<uint16_t*>(ch.d_knobs.p);
-    a.cur_score = static_cast<float*>(ch.d_score.p);
-    a.top = static_cast<at_entry*>(ch.d_top.p);
-    a.topk = ch.topk;
-    a.n_chains = ch.n_chains;
-    a.chain0 = (uint64_t)ch.chain0;
-    a.seed = ch.seed;
-    a.step_base = ch.step_abs;
-    a.steps = steps;
-    a.init = init ? 1 : 0;
-    a.thr = thr;
-    a.best = best;
-    a.trace = trace;
-    if (ch.n_chains == 0) return hipSuccess;
-    if (sp.tmpl == AT_TMPL_GEMM) return sa_tmpl<AT_TMPL_GEMM>(a, e, stream);
-    return sa_tmpl<AT_TMPL_CONV2D_NCHW>(a, e, stream);
 }
 
 hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score, hipStream_t stream) {

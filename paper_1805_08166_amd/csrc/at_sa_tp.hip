@@ -26,7 +26,6 @@ namespace {
 
 using namespace dev;
 
-constexpr int TREE_WG = 256;
 constexpr int CHAIN_WG = 256;           // wave 0 runs the chains, all four waves move data
 constexpr int CPW = 16;                 // chains per chain-kernel workgroup
 constexpr int FOLD_GROUPS = 512;        // 4-tree groups per fold pass: 512 x 16 chains x 16 B = 128 KB
