@@ -238,10 +238,27 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
             tw[n_leaf + j] = bits;
         }
     }
+    // compact form for the annealing kernels (layout in at_internal.h)
+    const size_t NB = n_leaf / 2, W16 = NB + n_leaf;
+    std::vector<uint32_t> words16;
+    try {
+        words16.assign((size_t)n_trees * W16, 0u);
+    } catch (...) {
+        return fail(AT_E_OOM, "at_ensemble_create: host allocation");
+    }
+    for (size_t t = 0; t < (size_t)n_trees; ++t) {
+        uint32_t* tw = words16.data() + t * W16;
+        // heap node m (1-based) is node m - 1 of the caller's tables
+        auto node = [&](size_t m) { return node16(fid[t * n_int + m - 1], thr[t * n_int + m - 1]); };
+        tw[0] = node(1);
+        for (size_t p = 1; p < NB; ++p) tw[p] = node(2 * p) | (node(2 * p + 1) << 16);
+        std::memcpy(tw + NB, &leaf[t * n_leaf], n_leaf * 4);
+    }
     at_ensemble_s* e = new (std::nothrow) at_ensemble_s();
     if (!e) return fail(AT_E_OOM, "at_ensemble_create: host allocation");
     e->device = current_device();
     at_status st = upload(e->d_words, words.data(), words.size());
+    if (st == AT_OK) st = upload(e->d_words16, words16.data(), words16.size());
     if (st != AT_OK) {
         at_ensemble_destroy(e);
         return st;
@@ -251,6 +268,7 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     e->desc.n_features = n_features;
     e->desc.words_per_tree = (int32_t)W;
     e->desc.words = static_cast<const uint32_t*>(e->d_words.p);
+    e->desc.words16 = static_cast<const uint32_t*>(e->d_words16.p);
     *out = e;
     return AT_OK;
 }
@@ -259,6 +277,7 @@ void at_ensemble_destroy(at_ensemble_t ens) {
     if (!ens) return;
     DeviceGuard g(ens->device);
     release(ens->d_words);
+    release(ens->d_words16);
     delete ens;
 }
 

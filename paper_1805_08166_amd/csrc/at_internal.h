@@ -49,13 +49,31 @@ struct SpaceDesc {
 // word m (1 <= m < 2^d) is internal node m (1-based heap order: children 2m
 // and 2m+1) holding (thr << 16) | tile byte offset of its feature; words
 // 2^d .. 2^(d+1)-1 hold the leaf values (float bits); word 0 is unused.
+//
+// The annealing path uses a second, compact form (words16): its features
+// are loop-context bitlens, never above 31, so a split on x < thr decides
+// the same with thr clamped to 32.  Tree t occupies words16 [t*W16,
+// (t+1)*W16) with W16 = 3 * 2^(d-1): a node block of 2^(d-1) words (word 0
+// holds the root in its low half, word p >= 1 holds internal nodes 2p and
+// 2p+1 as the low and high halves) followed by the 2^d leaf values.  A
+// 16-bit node is (f & 3) | min(thr, 32) << 2 | (f >> 2) << 8.
 struct EnsembleDesc {
     int32_t n_trees;
     int32_t depth;
     int32_t n_features;
     int32_t words_per_tree;
     const uint32_t* words;
+    const uint32_t* words16;
 };
+
+// Largest threshold the compact form keeps; annealing features never exceed
+// SA_FEATURE_MAX.
+constexpr uint32_t SA_FEATURE_MAX = 31;
+constexpr uint32_t SA_THR_CLAMP = SA_FEATURE_MAX + 1;
+__host__ __device__ inline uint32_t node16(uint32_t f, uint32_t thr) {
+    const uint32_t t = thr < SA_THR_CLAMP ? thr : SA_THR_CLAMP;
+    return (f & 3u) | (t << 2) | ((f >> 2) << 8);
+}
 
 // Per-chain best-list bookkeeping kept between kernels: number of valid
 // entries and the last (k-th) entry.
@@ -128,6 +146,7 @@ struct at_ensemble_s {
     int device = 0;
     at::EnsembleDesc desc{};
     at::DeviceBuf d_words;
+    at::DeviceBuf d_words16;
 };
 
 struct at_chains_s {

@@ -6,10 +6,11 @@
 //            best list, applies the Metropolis test, then proposes the next
 //            candidate (one knob changed, Philox block (chain, step, 0, 0)),
 //            evaluates its loop-context features and writes them as packed
-//            bytes, quad-major (dword q of chain c at Fg[q * n + c]).
-//   k_trees  workgroup w holds trees [w*tpw, (w+1)*tpw) in LDS and walks
-//            them for every chain, 256 chains at a time through an LDS
-//            feature tile, writing the reached leaf values to V.
+//            bytes 4x+3, quad-major (dword q of chain c at Fg[q * n + c]).
+//   k_trees  workgroup w holds the compact form of trees [w*tpw, (w+1)*tpw)
+//            in LDS; each of its waves walks them for 64 chains at a time
+//            through its own LDS feature tile, writing the reached leaf
+//            values to V.
 // The kernel boundary is the only device-wide synchronisation: it is cheaper
 // than an in-kernel grid barrier here because the cross-XCD data (features
 // and leaf values) must be written back from the per-XCD L2 caches anyway.
@@ -31,7 +32,6 @@ constexpr int CPW = 16;                 // chains per chain-kernel workgroup
 constexpr int FOLD_GROUPS = 512;        // 4-tree groups per fold pass: 512 x 16 chains x 16 B = 128 KB
 constexpr int KMAX = 64;                // largest best list
 constexpr int FAC_MAX = 1024;           // split choices staged in LDS (8 KB)
-constexpr int TREE_LDS_BYTES = 65536;   // resident tree words per workgroup
 constexpr size_t MAX_LDS_BYTES = 163840; // LDS of one compute unit
 
 enum { FIN_NONE = 0, FIN_INIT = 1, FIN_STEP = 2 };
@@ -411,169 +411,294 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         for (int i = 0; i < 11; ++i) frow[gj][gr * 11 + i] = (uint8_t)f[i];
     }
     __syncthreads();
-    // packed rows out, consecutive lanes on consecutive chains
+    // packed rows out (4x+3 per byte, the tree kernel's tile encoding),
+    // consecutive lanes on consecutive chains
     for (int idx = tid; idx < nc * Q; idx += CHAIN_WG) {
         const int q = idx / nc, j = idx - q * nc;
         uint32_t w = 0;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             const int f = 4 * q + b;
-            if (f < N::F) w |= (uint32_t)frow[j][f] << (8 * b);
+            if (f < N::F) w |= (4u * frow[j][f] + 3u) << (8 * b);
         }
         a.Fg[(int64_t)q * a.n + c0 + j] = w;
     }
 }
 
+// ---------------------------------------------------------------------------
+// Tree kernel.  A workgroup holds the compact form of its trees in LDS and
+// walks them for every chain.  Each wave owns a feature tile of 64 chains in
+// a slot of SLOT bytes at wave * SLOT: byte (f & 3) of dword (f >> 2) * 64 +
+// lane holds 4x+3 for feature value x, so lanes read distinct banks whatever
+// features they ask for, and the tile byte address of feature f is
+// (node & mask) | (wave * SLOT + 4 * lane) for a 16-bit node of that feature,
+// mask = 3 | (SLOT - 1) & ~0xff.
+// With 4x+3 in the tile, x >= thr is (4x+3) >= (low byte of the node) for
+// x, thr <= 63.  Tiles are private to their wave, so the walk loop needs no
+// barrier; tree blocks go into the gaps after the tiles.
+// ---------------------------------------------------------------------------
+constexpr int TREES_MAX = 16;          // trees per workgroup
+constexpr int TREE_WAVES_MAX = 16;
+
 struct TreeArgs {
-    EnsembleDesc e;
-    const uint32_t* Fg;
+    const uint32_t* words16;   // compact ensemble
+    int n_trees;
+    int tpw;                   // trees per workgroup
+    const uint32_t* Fg;        // [Q][n] packed features (4x+3 per byte)
     int64_t n;
-    int Q;
     float* V;
-    int tpw;              // trees per workgroup
+    int slices;                // chain slices per tree group
+    int slice_blocks;          // 64-chain blocks per slice
+    uint32_t mask;             // node bits of a tile address: 3 | (slot - 1) & ~0xff
+    // LDS dword offsets of tree i's node block (low half) and leaf block (high half)
+    uint32_t toff[TREES_MAX];
 };
 
-// Walks GROUP trees (local index t, LDS byte offset tree_base + t * TB) for
-// this lane's chain and stores their leaf values to V.  Trees t_global ..
-// t_global+GROUP-1 of one chain are consecutive 4-byte slots of V when they
-// lie in one group of four, so aligned groups are stored as one vector.
-template <int DEPTH, int GROUP>
-__device__ __forceinline__ void walk_store(const uint8_t* __restrict__ L, uint32_t tree_base, uint32_t fb, int t,
-                                           int t_global, int64_t c, int64_t n, float* __restrict__ V, bool active) {
-    constexpr uint32_t TB = (2u << DEPTH) * 4u;
-    uint32_t lw[GROUP], li[GROUP];
-    walk_pair<DEPTH, GROUP>(L, tree_base + (uint32_t)t * TB, fb, lw, li);
+// Walks G trees for this lane's chain: nb/lb are the LDS byte offsets of the
+// trees' node and leaf blocks, mask the node bits of a tile address (held in
+// a scalar register).  Node p (1-based heap) has its children in word p of
+// the node block; the chosen child of the last internal level is leaf
+// 2p + right - 2^DEPTH.  A level is five vector instructions: the feature
+// address, the pair address, and one short sequence that compares, selects
+// the child's half of the pair and doubles p adding the comparison's carry
+// (the compiler does not form the latter two from plain code).
+template <int DEPTH, int G>
+__device__ __forceinline__ void walk16(const uint8_t* __restrict__ L, const uint32_t (&nb)[G],
+                                       const uint32_t (&lb)[G], uint32_t fb, uint32_t mask, uint32_t (&out)[G]) {
+    uint32_t node[G], p[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        node[g] = *reinterpret_cast<const uint16_t*>(L + nb[g]);
+        p[g] = 1u;
+    }
+#pragma unroll
+    for (int l = 0; l + 1 < DEPTH; ++l) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const uint32_t x4 = L[(node[g] & mask) | fb];
+            const uint32_t pr = *reinterpret_cast<const uint32_t*>(L + nb[g] + 4u * p[g]);
+            // right = (node & 0xff) <= x4; node = right ? pr >> 16 : pr & 0xffff; p = 2p + right
+            asm("v_cmp_le_u32_sdwa vcc, %0, %2 src0_sel:BYTE_0 src1_sel:DWORD\n\t"
+                "v_cndmask_b32_sdwa %0, %3, %3, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
+                "src1_sel:WORD_1\n\t"
+                "v_addc_co_u32 %1, vcc, %1, %1, vcc"
+                : "+v"(node[g]), "+v"(p[g])
+                : "v"(x4), "v"(pr)
+                : "vcc");
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const uint32_t x4 = L[(node[g] & mask) | fb];
+        uint32_t q = p[g];
+        // q = 2p + ((node & 0xff) <= x4)
+        asm("v_cmp_le_u32_sdwa vcc, %1, %2 src0_sel:BYTE_0 src1_sel:DWORD\n\t"
+            "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+            : "+v"(q)
+            : "v"(node[g]), "v"(x4)
+            : "vcc");
+        out[g] = *reinterpret_cast<const uint32_t*>(L + lb[g] + 4u * (q - (1u << DEPTH)));
+    }
+}
+
+// Walks local trees t .. t+G-1 and stores their leaf values to V (groups of
+// four trees of one chain are 16 consecutive bytes, stored as one vector
+// when aligned).
+template <int DEPTH, int G>
+__device__ __forceinline__ void walk_group(const uint8_t* __restrict__ L, const TreeArgs& a, int t, int t_global,
+                                           uint32_t fb, int64_t c, bool active) {
+    uint32_t nb[G], lb[G], v[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const uint32_t o = a.toff[t + g];
+        nb[g] = (o & 0xffffu) * 4u;
+        lb[g] = (o >> 16) * 4u;
+    }
+    walk16<DEPTH, G>(L, nb, lb, fb, a.mask, v);
     if (!active) return;
-    float* dst = V + ((((int64_t)(t_global >> 2) * n + c) << 2) + (t_global & 3));
-    if (GROUP == 4 && (t_global & 3) == 0) {
-        *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(lw[0]), __uint_as_float(lw[1 % GROUP]),
-                                                      __uint_as_float(lw[2 % GROUP]), __uint_as_float(lw[3 % GROUP]));
-    } else if (GROUP == 2 && (t_global & 1) == 0) {
-        *reinterpret_cast<float2*>(dst) = make_float2(__uint_as_float(lw[0]), __uint_as_float(lw[1 % GROUP]));
+    float* dst = a.V + ((((int64_t)(t_global >> 2) * a.n + c) << 2) + (t_global & 3));
+    if (G >= 4 && (t_global & 3) == 0) {
+#pragma unroll
+        for (int h = 0; h + 4 <= G; h += 4)
+            *reinterpret_cast<float4*>(dst + (int64_t)(h >> 2) * a.n * 4) =
+                make_float4(__uint_as_float(v[h]), __uint_as_float(v[(h + 1) % G]), __uint_as_float(v[(h + 2) % G]),
+                            __uint_as_float(v[(h + 3) % G]));
+    } else if (G == 2 && (t_global & 1) == 0) {
+        *reinterpret_cast<float2*>(dst) = make_float2(__uint_as_float(v[0]), __uint_as_float(v[1 % G]));
     } else {
 #pragma unroll
-        for (int g = 0; g < GROUP; ++g) {
+        for (int g = 0; g < G; ++g) {
             const int tg = t_global + g;
-            V[(((int64_t)(tg >> 2) * n + c) << 2) + (tg & 3)] = __uint_as_float(lw[g]);
+            a.V[(((int64_t)(tg >> 2) * a.n + c) << 2) + (tg & 3)] = __uint_as_float(v[g]);
         }
     }
 }
 
-// Walks r (< 2*H) remaining trees starting at local tree t, in groups of H, H/2, ..., 1.
+// r (< 2H) remaining trees from local tree t, in groups of H, H/2, ..., 1.
 template <int DEPTH, int H>
-__device__ __forceinline__ void walk_rest(const uint8_t* __restrict__ L, uint32_t tree_base, uint32_t fb, int t,
-                                          int t_global, int r, int64_t c, int64_t n, float* __restrict__ V,
-                                          bool active) {
+__device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const TreeArgs& a, int t, int t_global, int r,
+                                          uint32_t fb, int64_t c, bool active) {
     if (r >= H) {
-        walk_store<DEPTH, H>(L, tree_base, fb, t, t_global, c, n, V, active);
+        walk_group<DEPTH, H>(L, a, t, t_global, fb, c, active);
         t += H;
         t_global += H;
         r -= H;
     }
-    if constexpr (H > 1) walk_rest<DEPTH, H / 2>(L, tree_base, fb, t, t_global, r, c, n, V, active);
+    if constexpr (H > 1) walk_tail<DEPTH, H / 2>(L, a, t, t_global, r, fb, c, active);
 }
 
-// LDS: NT feature tiles (Q quads x 256 chains each, quad-major) from byte 0,
-// then the workgroup's trees.  A workgroup of NT*256 threads walks NT*256
-// chains per block, thread i in tile i / 256.  The next block's features are
-// fetched into registers while the current block is walked; the fetch is
-// unconditional (the chain index is clamped) so that it is issued ahead of
-// the walk.
-template <int DEPTH, int Q, int NT>
-__global__ __launch_bounds__(NT * 256) void k_trees(TreeArgs a) {
-    constexpr int W = 2 << DEPTH;
-    constexpr int G = 4;
-    constexpr int TW = NT * 256;
-    constexpr uint32_t TILE_BYTES = (uint32_t)Q * 256u * 4u;
-    extern __shared__ uint32_t lds[];
+// Workgroup b walks trees [g*tpw, g*tpw + tpw) for chain blocks (64 chains
+// each) [cs*slice_blocks, (cs+1)*slice_blocks), with g = b / slices and
+// cs = b % slices; its waves take the blocks in turn.
+template <int DEPTH, int Q, int SLOT_LOG2>
+__global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
+    constexpr uint32_t SLOT = 1u << SLOT_LOG2;
+    constexpr int NB = 1 << (DEPTH - 1), NL = 1 << DEPTH, W16 = NB + NL;
+    constexpr int G = 8;
+    __shared__ uint32_t lds[MAX_LDS_BYTES / 4];
     const uint8_t* L = reinterpret_cast<const uint8_t*>(lds);
-    uint32_t* trees = lds + NT * Q * 256;
     const int tid = threadIdx.x;
-    const int h = tid >> 8, lane = tid & 255;
-    uint32_t* tile = lds + h * Q * 256;
-    const int t0 = blockIdx.x * a.tpw;
-    const int nt = (a.e.n_trees - t0 < a.tpw) ? (a.e.n_trees - t0) : a.tpw;
-    if (nt <= 0) return;
+    const int grp = blockIdx.x / a.slices, cs = blockIdx.x - grp * a.slices;
+    const int t0 = grp * a.tpw;
+    const int nt = (a.n_trees - t0 < a.tpw) ? (a.n_trees - t0) : a.tpw;
+    // trees into LDS: all loads of a round are issued before its stores
+    if constexpr (DEPTH >= 3) {
+        // blocks are whole 16-byte pieces at 16-byte aligned offsets
+        constexpr int NB4 = NB / 4, W4 = W16 / 4;
+        const uint4* src = reinterpret_cast<const uint4*>(a.words16 + (size_t)t0 * W16);
+        const int total = nt * W4;
+        for (int base = 0; base < total; base += 8 * (int)blockDim.x) {
+            uint4 v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int j = base + k * (int)blockDim.x + tid;
+                v[k] = src[j < total ? j : total - 1];
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int j = base + k * (int)blockDim.x + tid;
+                if (j < total) {
+                    const int t = j / W4, i = j - t * W4;
+                    const uint32_t o = a.toff[t];
+                    const uint32_t d = i < NB4 ? (o & 0xffffu) + 4u * (uint32_t)i : (o >> 16) + 4u * (uint32_t)(i - NB4);
+                    *reinterpret_cast<uint4*>(lds + d) = v[k];
+                }
+            }
+        }
+    } else {
+        const uint32_t* src = a.words16 + (size_t)t0 * W16;
+        const int total = nt * W16;
+        for (int j = tid; j < total; j += (int)blockDim.x) {
+            const int t = j / W16, i = j - t * W16;
+            const uint32_t o = a.toff[t];
+            lds[i < NB ? (o & 0xffffu) + (uint32_t)i : (o >> 16) + (uint32_t)(i - NB)] = src[j];
+        }
+    }
+    __syncthreads();
+    const int wave = tid >> 6, lane = tid & 63;
+    const int nw = (int)(blockDim.x >> 6);
     const int64_t n = a.n;
+    const int64_t blocks = (n + 63) >> 6;
+    const int64_t b_end0 = (int64_t)(cs + 1) * a.slice_blocks;
+    const int64_t b_end = b_end0 < blocks ? b_end0 : blocks;
+    uint32_t* tile = lds + wave * (SLOT / 4);
+    const uint32_t fb = (uint32_t)wave * SLOT + (uint32_t)lane * 4u;
+    int64_t b = (int64_t)cs * a.slice_blocks + wave;
     uint32_t pre[Q];
     {
-        const int64_t cf = tid < n ? tid : n - 1;
+        const int64_t c = b * 64 + lane;
+        const int64_t cf = c < n ? c : n - 1;
 #pragma unroll
         for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cf];
     }
-    {
-        const uint4* s4 = reinterpret_cast<const uint4*>(a.e.words + (size_t)t0 * W);
-        uint4* d4 = reinterpret_cast<uint4*>(trees);
-        for (int i = tid; i < nt * W / 4; i += TW) d4[i] = s4[i];
-    }
-    const uint32_t fb = (uint32_t)h * TILE_BYTES + (uint32_t)lane * 4u;
-    const uint32_t tree_base = NT * TILE_BYTES;
-    for (int64_t cb = 0; cb < n; cb += TW) {
-        __syncthreads();
+    for (; b < b_end; b += nw) {
+        // the wave's own tile: earlier reads of it were issued before these
+        // writes, and LDS serves a wave's instructions in order
 #pragma unroll
-        for (int q = 0; q < Q; ++q) tile[q * 256 + lane] = pre[q];
-        __syncthreads();
-        const int64_t c = cb + tid;
+        for (int q = 0; q < Q; ++q) tile[q * 64 + lane] = pre[q];
+        const int64_t c = b * 64 + lane;
         const bool active = c < n;
         {
-            const int64_t cn = (cb + TW + tid < n) ? cb + TW + tid : n - 1;
+            const int64_t cn = (b + nw) * 64 + lane;
+            const int64_t cf = cn < n ? cn : n - 1;
 #pragma unroll
-            for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cn];
+            for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cf];
         }
         int t = 0;
-        for (; t + G <= nt; t += G) walk_store<DEPTH, G>(L, tree_base, fb, t, t0 + t, c, n, a.V, active);
-        walk_rest<DEPTH, G / 2>(L, tree_base, fb, t, t0 + t, nt - t, c, n, a.V, active);
+        for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
+        walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
     }
 }
 
-template <int DEPTH, int Q, int NT>
-hipError_t launch_trees_nt(const TreeArgs& a, hipStream_t stream) {
-    constexpr int W = 2 << DEPTH;
-    const size_t lds = (size_t)NT * Q * 256 * 4 + (size_t)a.tpw * W * 4;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_trees<DEPTH, Q, NT>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             NT * Q * 256 * 4 + TREE_LDS_BYTES);
-        if (err != hipSuccess) return err;
-        configured = true;
+// LDS plan of a tree workgroup: nw feature tiles, one per SLOT, and the
+// node and leaf blocks of tpw trees placed first-fit (largest first) in the
+// space the tiles leave free.  Returns false when they do not fit.
+bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TREES_MAX]) {
+    const uint32_t tile = (uint32_t)Q * 256u;
+    struct Gap { uint32_t lo, hi; };
+    Gap gaps[TREE_WAVES_MAX];
+    int ng = 0;
+    for (int w = 0; w < nw; ++w) {
+        const uint32_t lo = (uint32_t)w * slot + tile;
+        const uint32_t hi = (w + 1 < nw) ? (uint32_t)(w + 1) * slot : (uint32_t)MAX_LDS_BYTES;
+        if (lo > (uint32_t)MAX_LDS_BYTES) return false;
+        gaps[ng++] = Gap{lo, hi};
     }
-    const int grid = (a.e.n_trees + a.tpw - 1) / a.tpw;
-    hipLaunchKernelGGL((k_trees<DEPTH, Q, NT>), dim3(grid), dim3(NT * 256), lds, stream, a);
+    const uint32_t nbytes = 4u << (depth - 1), lbytes = 4u << depth;
+    uint32_t noff[TREES_MAX], loff[TREES_MAX];
+    auto place = [&](uint32_t bytes, uint32_t& off) {
+        for (int i = 0; i < ng; ++i) {
+            if (gaps[i].hi - gaps[i].lo >= bytes) {
+                off = gaps[i].lo;
+                gaps[i].lo += bytes;
+                return true;
+            }
+        }
+        return false;
+    };
+    for (int t = 0; t < tpw; ++t)
+        if (!place(lbytes, loff[t])) return false;
+    for (int t = 0; t < tpw; ++t)
+        if (!place(nbytes, noff[t])) return false;
+    for (int t = 0; t < tpw; ++t) toff[t] = (noff[t] / 4u) | ((loff[t] / 4u) << 16);
+    return true;
+}
+
+template <int DEPTH, int Q, int SLOT_LOG2>
+hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream) {
+    const int grid = (a.n_trees + a.tpw - 1) / a.tpw * a.slices;
+    hipLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, a);
     return hipGetLastError();
 }
 
-// Two tiles (512 threads) when they and the trees fit in LDS, else one.
-template <int DEPTH, int Q>
-hipError_t launch_trees_depth(const TreeArgs& a, hipStream_t stream) {
-    constexpr int W = 2 << DEPTH;
-    const size_t two = (size_t)2 * Q * 256 * 4 + (size_t)a.tpw * W * 4;
-    if (two <= MAX_LDS_BYTES) return launch_trees_nt<DEPTH, Q, 2>(a, stream);
-    return launch_trees_nt<DEPTH, Q, 1>(a, stream);
-}
-
-template <int Q>
-hipError_t launch_trees_q(const TreeArgs& a, hipStream_t stream) {
-    switch (a.e.depth) {
-        case 1: return launch_trees_depth<1, Q>(a, stream);
-        case 2: return launch_trees_depth<2, Q>(a, stream);
-        case 3: return launch_trees_depth<3, Q>(a, stream);
-        case 4: return launch_trees_depth<4, Q>(a, stream);
-        case 5: return launch_trees_depth<5, Q>(a, stream);
-        case 6: return launch_trees_depth<6, Q>(a, stream);
-        case 7: return launch_trees_depth<7, Q>(a, stream);
-        case 8: return launch_trees_depth<8, Q>(a, stream);
-        case 9: return launch_trees_depth<9, Q>(a, stream);
-        case 10: return launch_trees_depth<10, Q>(a, stream);
-        case 11: return launch_trees_depth<11, Q>(a, stream);
-        case 12: return launch_trees_depth<12, Q>(a, stream);
+template <int Q, int SLOT_LOG2>
+hipError_t launch_trees_q(const TreeArgs& a, int depth, int nw, hipStream_t stream) {
+    switch (depth) {
+        case 1: return launch_trees_t<1, Q, SLOT_LOG2>(a, nw, stream);
+        case 2: return launch_trees_t<2, Q, SLOT_LOG2>(a, nw, stream);
+        case 3: return launch_trees_t<3, Q, SLOT_LOG2>(a, nw, stream);
+        case 4: return launch_trees_t<4, Q, SLOT_LOG2>(a, nw, stream);
+        case 5: return launch_trees_t<5, Q, SLOT_LOG2>(a, nw, stream);
+        case 6: return launch_trees_t<6, Q, SLOT_LOG2>(a, nw, stream);
+        case 7: return launch_trees_t<7, Q, SLOT_LOG2>(a, nw, stream);
+        case 8: return launch_trees_t<8, Q, SLOT_LOG2>(a, nw, stream);
+        case 9: return launch_trees_t<9, Q, SLOT_LOG2>(a, nw, stream);
+        case 10: return launch_trees_t<10, Q, SLOT_LOG2>(a, nw, stream);
+        case 11: return launch_trees_t<11, Q, SLOT_LOG2>(a, nw, stream);
+        case 12: return launch_trees_t<12, Q, SLOT_LOG2>(a, nw, stream);
         default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_trees(const TreeArgs& a, hipStream_t stream) {
-    if (a.Q == 28) return launch_trees_q<28>(a, stream);   // GEMM: 110 features
-    if (a.Q == 44) return launch_trees_q<44>(a, stream);   // conv2d: 176 features
+// Tile slot sizes: the smallest power of two holding Q * 256 bytes.
+constexpr int GEMM_Q = 28, CONV_Q = 44;
+constexpr int GEMM_SLOT_LOG2 = 13, CONV_SLOT_LOG2 = 14;
+static_assert((GEMM_Q * 256) <= (1 << GEMM_SLOT_LOG2) && (GEMM_Q * 256) > (1 << (GEMM_SLOT_LOG2 - 1)), "slot");
+static_assert((CONV_Q * 256) <= (1 << CONV_SLOT_LOG2) && (CONV_Q * 256) > (1 << (CONV_SLOT_LOG2 - 1)), "slot");
+
+hipError_t launch_trees(const TreeArgs& a, int Q, int depth, int nw, hipStream_t stream) {
+    if (Q == GEMM_Q) return launch_trees_q<GEMM_Q, GEMM_SLOT_LOG2>(a, depth, nw, stream);
+    if (Q == CONV_Q) return launch_trees_q<CONV_Q, CONV_SLOT_LOG2>(a, depth, nw, stream);
     return hipErrorInvalidValue;
 }
 
@@ -630,20 +755,46 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     ca.trace = trace;
 
     TreeArgs ta{};
-    ta.e = e;
+    ta.words16 = e.words16;
+    ta.n_trees = e.n_trees;
     ta.Fg = ca.Fg;
     ta.n = n;
-    ta.Q = Q;
     ta.V = static_cast<float*>(ch.d_v.p);
-    // spread the trees over the compute units, within the LDS budget
+    // Tree groups of tpw trees times chain slices: a layout scores the walks
+    // in flight per compute unit (waves times trees walked together) times
+    // the share of compute units its grid fills.
     int n_cu = 256;
     (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, ch.device);
-    const int W = 2 << e.depth;
-    int tpw = (e.n_trees + n_cu - 1) / n_cu;
-    const int tpw_max = TREE_LDS_BYTES / (W * 4) > 0 ? TREE_LDS_BYTES / (W * 4) : 1;
-    if (tpw > tpw_max) tpw = tpw_max;
-    if (tpw < 1) tpw = 1;
-    ta.tpw = tpw;
+    const int slot = 1 << (Q == GEMM_Q ? GEMM_SLOT_LOG2 : CONV_SLOT_LOG2);
+    const int64_t blocks = (n + 63) / 64;
+    double best_score = -1.0;
+    int nw = 0;
+    for (int tpw = TREES_MAX; tpw >= 1; tpw /= 2) {
+        const int tg = (e.n_trees + tpw - 1) / tpw;
+        int64_t slices = n_cu / tg;
+        if (slices < 1) slices = 1;
+        if (slices > blocks) slices = blocks;
+        const int64_t sb = (blocks + slices - 1) / slices;
+        slices = (blocks + sb - 1) / sb;
+        const int cap = sb < TREE_WAVES_MAX ? (int)sb : TREE_WAVES_MAX;
+        uint32_t toff[TREES_MAX];
+        for (int w = cap; w >= 1; --w) {
+            if (!plan_trees(e.depth, Q, slot, w, tpw, toff)) continue;
+            const double grid = (double)tg * (double)slices;
+            const double score = (double)w * (tpw < 8 ? tpw : 8) * (grid < n_cu ? grid / n_cu : 1.0);
+            if (score > best_score) {
+                best_score = score;
+                nw = w;
+                ta.tpw = tpw;
+                ta.slices = (int)slices;
+                ta.slice_blocks = (int)sb;
+                for (int i = 0; i < TREES_MAX; ++i) ta.toff[i] = toff[i];
+            }
+            break;
+        }
+    }
+    if (nw == 0) return hipErrorInvalidConfiguration;
+    ta.mask = (((uint32_t)slot - 1u) & ~0xffu) | 3u;
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
     // whole four-group wave instructions: the last one of a pass may cover
@@ -675,7 +826,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
         x.fin = FIN_NONE;
         x.draw = DRAW_INIT;
         if ((err = chain_kernel(x)) != hipSuccess) return err;
-        if ((err = launch_trees(ta, stream)) != hipSuccess) return err;
+        if ((err = launch_trees(ta, Q, e.depth, nw, stream)) != hipSuccess) return err;
         pending = FIN_INIT;
     }
     for (int s = 0; s < steps; ++s) {
@@ -685,7 +836,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
         x.draw = DRAW_PROPOSE;
         x.draw_step = (uint32_t)(ch.step_abs + (uint64_t)s);
         if ((err = chain_kernel(x)) != hipSuccess) return err;
-        if ((err = launch_trees(ta, stream)) != hipSuccess) return err;
+        if ((err = launch_trees(ta, Q, e.depth, nw, stream)) != hipSuccess) return err;
         pending = FIN_STEP;
     }
     ChainArgs x = ca;
