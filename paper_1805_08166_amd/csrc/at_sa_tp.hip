@@ -53,7 +53,8 @@ struct ChainArgs {
     uint64_t seed;
     const float* V;           // leaf values, groups of 4 trees
     int T;
-    uint32_t* Fg;             // [Q][n] packed features
+    uint32_t* Fg;             // [Q][fg_stride] packed features
+    int64_t fg_stride;        // n rounded up to 64 chains
     int fin;                  // what the pending candidate is
     int fin_step;             // its local step index (thr / trace row)
     int steps;                // row length of thr and trace
@@ -421,7 +422,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             const int f = 4 * q + b;
             if (f < N::F) w |= (4u * frow[j][f] + 3u) << (8 * b);
         }
-        a.Fg[(int64_t)q * a.n + c0 + j] = w;
+        a.Fg[(int64_t)q * a.fg_stride + c0 + j] = w;
     }
 }
 
@@ -444,7 +445,8 @@ struct TreeArgs {
     const uint32_t* words16;   // compact ensemble
     int n_trees;
     int tpw;                   // trees per workgroup
-    const uint32_t* Fg;        // [Q][n] packed features (4x+3 per byte)
+    const uint32_t* Fg;        // [Q][fg_stride] packed features (4x+3 per byte)
+    int64_t fg_stride;         // n rounded up to 64 chains
     int64_t n;
     float* V;
     int slices;                // chain slices per tree group
@@ -454,49 +456,93 @@ struct TreeArgs {
     uint32_t toff[TREES_MAX];
 };
 
+// One level of four trees: for each tree, right = (node & 0xff) <= x4, node
+// becomes the right or left half of its children pair pr, p becomes 2p +
+// right (the comparison's carry), then the next feature address
+// (node & mask) | fb and pair address nb + 4p.  The compiler does not form
+// the carry and the half-word select from plain code.  A VALU write of VCC
+// is read two or more instructions later (gfx950 wait states): the first
+// compare is followed by s_nop 1, the others by the previous tree's address
+// instructions.
+// Operands: 0-3 node, 4-7 p, 8-11 feature address, 12-15 pair address,
+// 16-19 x4, 20-23 pr, 24 mask, 25 fb, 26-29 nb.
+#define AT_WALK4_ASM                                                                                       \
+    "v_cmp_le_u32_sdwa vcc, %0, %16 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32_sdwa %0, %20, %20, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %4, vcc, %4, %4, vcc\n\t"                                                               \
+    "v_cmp_le_u32_sdwa vcc, %1, %17 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %8, %0, %24, %25\n\t"                                                                    \
+    "v_lshl_add_u32 %12, %4, 2, %26\n\t"                                                                   \
+    "v_cndmask_b32_sdwa %1, %21, %21, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %5, vcc, %5, %5, vcc\n\t"                                                               \
+    "v_cmp_le_u32_sdwa vcc, %2, %18 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %9, %1, %24, %25\n\t"                                                                    \
+    "v_lshl_add_u32 %13, %5, 2, %27\n\t"                                                                   \
+    "v_cndmask_b32_sdwa %2, %22, %22, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %6, vcc, %6, %6, vcc\n\t"                                                               \
+    "v_cmp_le_u32_sdwa vcc, %3, %19 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %10, %2, %24, %25\n\t"                                                                   \
+    "v_lshl_add_u32 %14, %6, 2, %28\n\t"                                                                   \
+    "v_cndmask_b32_sdwa %3, %23, %23, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %7, vcc, %7, %7, vcc\n\t"                                                               \
+    "v_and_or_b32 %11, %3, %24, %25\n\t"                                                                   \
+    "v_lshl_add_u32 %15, %7, 2, %29"
+
 // Walks G trees for this lane's chain: nb/lb are the LDS byte offsets of the
-// trees' node and leaf blocks, mask the node bits of a tile address (held in
-// a scalar register).  Node p (1-based heap) has its children in word p of
-// the node block; the chosen child of the last internal level is leaf
-// 2p + right - 2^DEPTH.  A level is five vector instructions: the feature
-// address, the pair address, and one short sequence that compares, selects
-// the child's half of the pair and doubles p adding the comparison's carry
-// (the compiler does not form the latter two from plain code).
+// trees' node and leaf blocks, mask the node bits of a tile address.  Node
+// p (1-based heap) has its children in word p of the node block; the chosen
+// child of the last internal level is leaf 2p + right - 2^DEPTH.  A level
+// costs five vector instructions per tree when G is a multiple of four.
 template <int DEPTH, int G>
 __device__ __forceinline__ void walk16(const uint8_t* __restrict__ L, const uint32_t (&nb)[G],
                                        const uint32_t (&lb)[G], uint32_t fb, uint32_t mask, uint32_t (&out)[G]) {
-    uint32_t node[G], p[G];
+    uint32_t node[G], p[G], fa[G], pa[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         node[g] = *reinterpret_cast<const uint16_t*>(L + nb[g]);
         p[g] = 1u;
+        fa[g] = (node[g] & mask) | fb;
+        pa[g] = nb[g] + 4u;
     }
 #pragma unroll
     for (int l = 0; l + 1 < DEPTH; ++l) {
+        uint32_t x4[G], pr[G];
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-            const uint32_t x4 = L[(node[g] & mask) | fb];
-            const uint32_t pr = *reinterpret_cast<const uint32_t*>(L + nb[g] + 4u * p[g]);
-            // right = (node & 0xff) <= x4; node = right ? pr >> 16 : pr & 0xffff; p = 2p + right
-            asm("v_cmp_le_u32_sdwa vcc, %0, %2 src0_sel:BYTE_0 src1_sel:DWORD\n\t"
-                "v_cndmask_b32_sdwa %0, %3, %3, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
-                "src1_sel:WORD_1\n\t"
-                "v_addc_co_u32 %1, vcc, %1, %1, vcc"
-                : "+v"(node[g]), "+v"(p[g])
-                : "v"(x4), "v"(pr)
-                : "vcc");
+            x4[g] = L[fa[g]];
+            pr[g] = *reinterpret_cast<const uint32_t*>(L + pa[g]);
+        }
+        if constexpr (G % 4 == 0) {
+#pragma unroll
+            for (int h = 0; h < G; h += 4) {
+                asm(AT_WALK4_ASM
+                    : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
+                      "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "=&v"(fa[h]), "=&v"(fa[h + 1]),
+                      "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]), "=&v"(pa[h + 2]),
+                      "=&v"(pa[h + 3])
+                    : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"(pr[h]), "v"(pr[h + 1]),
+                      "v"(pr[h + 2]), "v"(pr[h + 3]), "s"(mask), "v"(fb), "s"(nb[h]), "s"(nb[h + 1]),
+                      "s"(nb[h + 2]), "s"(nb[h + 3])
+                    : "vcc");
+            }
+        } else {
+            // plain code for groups of one or two trees (high bits of node
+            // are left as they fall; only its low half is used)
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const bool right = x4[g] >= (node[g] & 0xffu);
+                node[g] = right ? (pr[g] >> 16) : pr[g];
+                p[g] = 2u * p[g] + (right ? 1u : 0u);
+                fa[g] = (node[g] & mask) | fb;
+                pa[g] = nb[g] + 4u * p[g];
+            }
         }
     }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        const uint32_t x4 = L[(node[g] & mask) | fb];
-        uint32_t q = p[g];
-        // q = 2p + ((node & 0xff) <= x4)
-        asm("v_cmp_le_u32_sdwa vcc, %1, %2 src0_sel:BYTE_0 src1_sel:DWORD\n\t"
-            "v_addc_co_u32 %0, vcc, %0, %0, vcc"
-            : "+v"(q)
-            : "v"(node[g]), "v"(x4)
-            : "vcc");
+        const uint32_t x4 = L[fa[g]];
+        const uint32_t q = 2u * p[g] + (x4 >= (node[g] & 0xffu) ? 1u : 0u);
         out[g] = *reinterpret_cast<const uint32_t*>(L + lb[g] + 4u * (q - (1u << DEPTH)));
     }
 }
@@ -561,37 +607,36 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     const int grp = blockIdx.x / a.slices, cs = blockIdx.x - grp * a.slices;
     const int t0 = grp * a.tpw;
     const int nt = (a.n_trees - t0 < a.tpw) ? (a.n_trees - t0) : a.tpw;
-    // trees into LDS: all loads of a round are issued before its stores
+    // trees into LDS: per round, one piece of every tree is loaded before
+    // any store.  Loads and stores are unconditional so that the loads stay
+    // in flight together: slots past the last tree and lanes past the last
+    // piece repeat the last tree's or piece's store (same value, same place).
     if constexpr (DEPTH >= 3) {
         // blocks are whole 16-byte pieces at 16-byte aligned offsets
         constexpr int NB4 = NB / 4, W4 = W16 / 4;
         const uint4* src = reinterpret_cast<const uint4*>(a.words16 + (size_t)t0 * W16);
-        const int total = nt * W4;
-        for (int base = 0; base < total; base += 8 * (int)blockDim.x) {
-            uint4 v[8];
+        for (int base = 0; base < W4; base += (int)blockDim.x) {
+            const int i = base + tid < W4 ? base + tid : W4 - 1;
+            uint4 v[TREES_MAX];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int j = base + k * (int)blockDim.x + tid;
-                v[k] = src[j < total ? j : total - 1];
-            }
+            for (int t = 0; t < TREES_MAX; ++t) v[t] = src[(t < nt ? t : nt - 1) * W4 + i];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int j = base + k * (int)blockDim.x + tid;
-                if (j < total) {
-                    const int t = j / W4, i = j - t * W4;
-                    const uint32_t o = a.toff[t];
-                    const uint32_t d = i < NB4 ? (o & 0xffffu) + 4u * (uint32_t)i : (o >> 16) + 4u * (uint32_t)(i - NB4);
-                    *reinterpret_cast<uint4*>(lds + d) = v[k];
-                }
+            for (int t = 0; t < TREES_MAX; ++t) {
+                const uint32_t o = a.toff[t < nt ? t : nt - 1];
+                const uint32_t d = i < NB4 ? (o & 0xffffu) + 4u * (uint32_t)i : (o >> 16) + 4u * (uint32_t)(i - NB4);
+                *reinterpret_cast<uint4*>(lds + d) = v[t];
             }
         }
     } else {
         const uint32_t* src = a.words16 + (size_t)t0 * W16;
-        const int total = nt * W16;
-        for (int j = tid; j < total; j += (int)blockDim.x) {
-            const int t = j / W16, i = j - t * W16;
-            const uint32_t o = a.toff[t];
-            lds[i < NB ? (o & 0xffffu) + (uint32_t)i : (o >> 16) + (uint32_t)(i - NB)] = src[j];
+        for (int i = tid; i < W16; i += (int)blockDim.x) {
+#pragma unroll
+            for (int t = 0; t < TREES_MAX; ++t) {
+                if (t < nt) {
+                    const uint32_t o = a.toff[t];
+                    lds[i < NB ? (o & 0xffffu) + (uint32_t)i : (o >> 16) + (uint32_t)(i - NB)] = src[t * W16 + i];
+                }
+            }
         }
     }
     __syncthreads();
@@ -603,27 +648,21 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     const int64_t b_end = b_end0 < blocks ? b_end0 : blocks;
     uint32_t* tile = lds + wave * (SLOT / 4);
     const uint32_t fb = (uint32_t)wave * SLOT + (uint32_t)lane * 4u;
-    int64_t b = (int64_t)cs * a.slice_blocks + wave;
-    uint32_t pre[Q];
-    {
-        const int64_t c = b * 64 + lane;
-        const int64_t cf = c < n ? c : n - 1;
+    // tile fill straight from global memory into LDS: instruction k moves
+    // quads 4k..4k+3, lane i the 16 bytes of chains 4(i & 15) .. +3 of quad
+    // 4k + i/16, which land on tile dwords 256k + 4i .. +3 = quad * 64 + chain
+    const uint32_t* fsrc = a.Fg + (int64_t)(lane >> 4) * a.fg_stride + 4 * (lane & 15);
+    static_assert(Q % 4 == 0, "whole quad groups");
+    for (int64_t b = (int64_t)cs * a.slice_blocks + wave; b < b_end; b += nw) {
+        // every earlier read of this wave's tile has returned before the
+        // tile is overwritten (s_waitcnt lgkmcnt(0))
+        __builtin_amdgcn_s_waitcnt(0xc07f);
 #pragma unroll
-        for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cf];
-    }
-    for (; b < b_end; b += nw) {
-        // the wave's own tile: earlier reads of it were issued before these
-        // writes, and LDS serves a wave's instructions in order
-#pragma unroll
-        for (int q = 0; q < Q; ++q) tile[q * 64 + lane] = pre[q];
+        for (int k = 0; k < Q / 4; ++k)
+            __builtin_amdgcn_global_load_lds(fsrc + (int64_t)(4 * k) * a.fg_stride + b * 64, tile + 256 * k, 16, 0, 0);
+        __builtin_amdgcn_s_waitcnt(0);
         const int64_t c = b * 64 + lane;
         const bool active = c < n;
-        {
-            const int64_t cn = (b + nw) * 64 + lane;
-            const int64_t cf = cn < n ? cn : n - 1;
-#pragma unroll
-            for (int q = 0; q < Q; ++q) pre[q] = a.Fg[(int64_t)q * n + cf];
-        }
         int t = 0;
         for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
         walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
@@ -730,7 +769,8 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     hipError_t err;
     if ((err = ensure(ch.d_cand, (size_t)n * MAX_KNOBS * 2)) != hipSuccess) return err;
     if ((err = ensure(ch.d_meta, (size_t)n * sizeof(ChainMeta))) != hipSuccess) return err;
-    if ((err = ensure(ch.d_fg, (size_t)Q * n * 4)) != hipSuccess) return err;
+    const int64_t fg_stride = (n + 63) / 64 * 64;
+    if ((err = ensure(ch.d_fg, (size_t)Q * fg_stride * 4)) != hipSuccess) return err;
     if ((err = ensure(ch.d_v, (size_t)groups * n * 16)) != hipSuccess) return err;
 
     ChainArgs ca{};
@@ -750,6 +790,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     ca.V = static_cast<const float*>(ch.d_v.p);
     ca.T = e.n_trees;
     ca.Fg = static_cast<uint32_t*>(ch.d_fg.p);
+    ca.fg_stride = fg_stride;
     ca.steps = steps;
     ca.thr = thr;
     ca.trace = trace;
@@ -758,6 +799,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     ta.words16 = e.words16;
     ta.n_trees = e.n_trees;
     ta.Fg = ca.Fg;
+    ta.fg_stride = fg_stride;
     ta.n = n;
     ta.V = static_cast<float*>(ch.d_v.p);
     // Tree groups of tpw trees times chain slices: a layout scores the walks
