@@ -29,7 +29,9 @@ using namespace dev;
 
 constexpr int CHAIN_WG = 256;           // wave 0 runs the chains, all four waves move data
 constexpr int CPW = 16;                 // chains per chain-kernel workgroup
-constexpr int FOLD_GROUPS = 512;        // 4-tree groups per fold pass: 512 x 16 chains x 16 B = 128 KB
+constexpr int FOLD_P = 32;              // 4-tree groups per fold pass: 32 x 16 chains x 16 B = 8 KB
+constexpr int FOLD_R = 6;               // passes in the LDS ring (five in flight while one is folded)
+constexpr size_t RING_BYTES = (size_t)FOLD_R * FOLD_P * CPW * 16;
 constexpr int KMAX = 64;                // largest best list
 constexpr int FAC_MAX = 1024;           // split choices staged in LDS (8 KB)
 constexpr size_t MAX_LDS_BYTES = 163840; // LDS of one compute unit
@@ -87,21 +89,90 @@ __device__ __forceinline__ void store_knobs(uint16_t* p, int64_t c, const uint32
     reinterpret_cast<uint4*>(p)[c] = w;
 }
 
-// Issues the loads of groups [g0, g0+ng) of the leaf values of chains
-// c0 .. c0+15 straight into LDS: each wave instruction moves four groups of
-// the 16 chains (1 KB, lane l -> group g0 + 4*ins + l/16, chain c0 + l%16),
-// so vbuf[g * 16 + j] holds group g0+g of chain c0+j.  Addresses past the
-// last group or chain are clamped (those slots are never read).
-__device__ __forceinline__ void issue_fold_loads(const float4* __restrict__ V4, int64_t n, int64_t c0, int nc,
-                                                 int groups, int g0, int ng, float4* vbuf, int wave, int lane) {
-    const int ninstr = (ng + 3) >> 2;
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4, lgkmcnt 11:8): wait for vmcnt <= n only, or for lgkmcnt 0 only.
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int WAIT_LGKM0 = (15) | (3 << 14) | (7 << 4);
+
+// Score of the pending candidates of chains c0 .. c0+nc-1: lane j < nc adds
+// its chain's leaf values in tree order (fp32, from +0.0f).  All 64 lanes of
+// the calling wave move the values into a ring of FOLD_R LDS buffers: pass p
+// (groups p*FOLD_P ..) goes to buffer p % FOLD_R, instruction i of a pass
+// moves groups 4i .. 4i+3 of the 16 chains (lane l: group 4i + l/16, chain
+// c0 + l%16), so buffer entry g * 16 + j holds group g of chain c0 + j.
+// FOLD_R - 1 passes stay in flight while one is folded.
+__device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
+                                           float4* ring, int lane) {
+    const int groups = (T + 3) >> 2;
+    const int npass = (groups + FOLD_P - 1) / FOLD_P;
     const int j = lane & (CPW - 1);
-    const int jc = j < nc ? j : nc - 1;
-    for (int ins = wave; ins < ninstr; ins += CHAIN_WG / 64) {
-        const int g = g0 + ins * 4 + (lane >> 4);
-        const int gc = g < groups ? g : groups - 1;
-        __builtin_amdgcn_global_load_lds(V4 + (int64_t)gc * n + c0 + jc, vbuf + ins * 64, 16, 0, 0);
+    const int64_t cj = c0 + (j < nc ? j : nc - 1);
+    auto issue = [&](int p) {
+        float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
+#pragma unroll
+        for (int ins = 0; ins < FOLD_P / 4; ++ins) {
+            const int g = p * FOLD_P + ins * 4 + (lane >> 4);
+            const int gc = g < groups ? g : groups - 1;
+            __builtin_amdgcn_global_load_lds(V4 + (int64_t)gc * n + cj, buf + ins * 64, 16, 0, 0);
+        }
+    };
+    for (int p = 0; p < FOLD_R - 1 && p < npass; ++p) issue(p);
+    float s = 0.0f;
+    for (int p = 0; p < npass; ++p) {
+        if (p + FOLD_R - 1 < npass) {
+            // the fold of pass p - 1 has read the buffer that pass p + R - 1 takes
+            __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+            issue(p + FOLD_R - 1);
+            __builtin_amdgcn_s_waitcnt(wait_vm(FOLD_P / 4 * (FOLD_R - 1)));
+        } else {
+            __builtin_amdgcn_s_waitcnt(wait_vm(0));
+        }
+        if (lane < nc) {
+            const float4* src = ring + (p % FOLD_R) * (FOLD_P * CPW) + lane;
+            const int ng = groups - p * FOLD_P < FOLD_P ? groups - p * FOLD_P : FOLD_P;
+            const int r = (p == npass - 1) ? (T & 3) : 0;   // trees in a last, partial group
+            const int full = r ? ng - 1 : ng;
+            if (full == FOLD_P) {
+                // whole pass: the next eight groups are read while eight are added
+                float4 cur[8], nxt[8];
+#pragma unroll
+                for (int g = 0; g < 8; ++g) cur[g] = src[g * CPW];
+#pragma unroll
+                for (int b = 0; b < FOLD_P / 8; ++b) {
+                    if (b + 1 < FOLD_P / 8) {
+#pragma unroll
+                        for (int g = 0; g < 8; ++g) nxt[g] = src[(8 * (b + 1) + g) * CPW];
+                    }
+#pragma unroll
+                    for (int g = 0; g < 8; ++g) {
+                        s = s + cur[g].x;
+                        s = s + cur[g].y;
+                        s = s + cur[g].z;
+                        s = s + cur[g].w;
+                    }
+                    if (b + 1 < FOLD_P / 8) {
+#pragma unroll
+                        for (int g = 0; g < 8; ++g) cur[g] = nxt[g];
+                    }
+                }
+            } else {
+                for (int g = 0; g < full; ++g) {
+                    const float4 q = src[g * CPW];
+                    s = s + q.x;
+                    s = s + q.y;
+                    s = s + q.z;
+                    s = s + q.w;
+                }
+                if (r) {
+                    const float4 q = src[full * CPW];
+                    s = s + q.x;
+                    if (r > 1) s = s + q.y;
+                    if (r > 2) s = s + q.z;
+                }
+            }
+        }
     }
+    return s;
 }
 
 __device__ __forceinline__ bool precedes(float sa, uint64_t ca, float sb, uint64_t cb) {
@@ -182,8 +253,8 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
     constexpr int Q = (N::F + 3) / 4;
     constexpr int RS = Q * 4 + 4;                 // feature row stride (bytes) in LDS
-    extern __shared__ float4 vbuf[];   // min(groups rounded up to 4, FOLD_GROUPS) * CPW entries
-    __shared__ at_entry lists[CPW][KMAX + 1];
+    // dynamic LDS: the fold ring, then the chains' best lists [CPW][topk]
+    extern __shared__ float4 ring[];
     __shared__ ChainRec rec[CPW];
     __shared__ uint8_t frow[CPW][RS];
     const int tid = threadIdx.x;
@@ -224,7 +295,6 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     // owner lanes: their chain's space; group lanes: the space of chain gj
     const SpaceDesc* sdp = staged ? &s_desc : a.descs + space_of(a, c);
     const SpaceDesc* gsdp = staged ? &s_desc : a.descs + space_of(a, c0 + (gvalid ? gj : 0));
-    if (a.fin == FIN_NONE) __syncthreads();   // (otherwise the fold's barrier publishes the staging)
 
     // per-chain state, fetched before the fold so the loads overlap it
     uint32_t cur[MAX_KNOBS], cd[MAX_KNOBS];
@@ -242,45 +312,36 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             thr_v = a.thr[c * a.steps + a.fin_step];
         }
     }
+    __syncthreads();   // publishes the staged space tables
 
     if (a.fin != FIN_NONE) {
-        // score of the pending candidate: its leaves added in tree order.  All
-        // four waves move the leaf values of the 16 chains into LDS (up to
-        // 2048 trees per pass), then one lane per chain folds them.
-        const float4* V4 = reinterpret_cast<const float4*>(a.V);
-        const int groups = (a.T + 3) >> 2;
+        // score of the pending candidate (wave 0); meanwhile waves 1-3 bring
+        // the chains' best lists into LDS (an initial list is empty)
+        at_entry* lists = reinterpret_cast<at_entry*>(ring + RING_BYTES / 16);
         float s = 0.0f;
-        for (int g0 = 0; g0 < groups; g0 += FOLD_GROUPS) {
-            const int ng = (groups - g0 < FOLD_GROUPS) ? groups - g0 : FOLD_GROUPS;
-            if (g0 > 0) __syncthreads();   // the previous pass has been folded
-            issue_fold_loads(V4, a.n, c0, nc, groups, g0, ng, vbuf, wave, tid & 63);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-            if (owner) {
-                const float4* src = vbuf + tid;
-                const bool last = g0 + ng == groups;
-                const int full = (last && (a.T & 3)) ? ng - 1 : ng;
-#pragma unroll 8
-                for (int g = 0; g < full; ++g) {
-                    const float4 q = src[g * CPW];
-                    s = s + q.x;
-                    s = s + q.y;
-                    s = s + q.z;
-                    s = s + q.w;
-                }
-                if (full < ng) {
-                    const float4 q = src[full * CPW];
-                    const int r = a.T & 3;
-                    s = s + q.x;
-                    if (r > 1) s = s + q.y;
-                    if (r > 2) s = s + q.z;
-                }
+        if (wave == 0) {
+            s = fold_ring(reinterpret_cast<const float4*>(a.V), a.n, a.T, c0, nc, ring, tid);
+        } else if (a.fin == FIN_STEP) {
+            const at_entry* src = a.top + c0 * k;
+            const int total = nc * k;
+            for (int ins = wave - 1; ins * 64 < total; ins += CHAIN_WG / 64 - 1) {
+                const int e = ins * 64 + (tid & 63);
+                if (e < total) __builtin_amdgcn_global_load_lds(src + e, lists + ins * 64, 16, 0, 0);
+            }
+        } else {
+            for (int e = tid - 64; e < nc * k; e += CHAIN_WG - 64) {
+                at_entry z;
+                z.cfg = 0;
+                z.score = 0.0f;
+                z.flag = 0u;
+                lists[e] = z;
             }
         }
+        __builtin_amdgcn_s_waitcnt(0);
 
-        // best lists: the chains whose candidate would enter their list bring
-        // it into LDS, where the chain's group of 16 lanes inserts it; the
-        // lists are then written back.  Skipped when no chain qualifies.
+        // best lists: the chain's group of 16 lanes inserts the candidate
+        // into its list in LDS when it qualifies; changed lists are written
+        // back.  Skipped when no chain qualifies.
         uint64_t cfg = 0;
         int qual = 0;
         if (owner) {
@@ -300,26 +361,11 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             rec[tid].qual = 0;
         }
         if (__syncthreads_or(qual)) {
-            for (int idx = tid; idx < CPW * k; idx += CHAIN_WG) {
-                const int j = idx / k, i = idx - j * k;
-                if (rec[j].qual) {
-                    at_entry e;
-                    if (a.fin == FIN_INIT) {
-                        e.cfg = 0;
-                        e.score = 0.0f;
-                        e.flag = 0u;
-                    } else {
-                        e = a.top[(c0 + j) * k + i];
-                    }
-                    lists[j][i] = e;
-                }
-            }
+            group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
             __syncthreads();
-            group_offer(lists[gj], rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
-            __syncthreads();
-            for (int idx = tid; idx < CPW * k; idx += CHAIN_WG) {
-                const int j = idx / k, i = idx - j * k;
-                if (rec[j].qual) a.top[(c0 + j) * k + i] = lists[j][i];
+            for (int idx = tid; idx < nc * k; idx += CHAIN_WG) {
+                const int j = idx / k;
+                if (rec[j].qual) a.top[c0 * k + idx] = lists[idx];
             }
         }
         if (owner) {
@@ -839,16 +885,13 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     ta.mask = (((uint32_t)slot - 1u) & ~0xffu) | 3u;
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
-    // whole four-group wave instructions: the last one of a pass may cover
-    // up to three groups past its end
-    const int fold_groups = groups < FOLD_GROUPS ? (groups + 3) / 4 * 4 : FOLD_GROUPS;
-    const size_t chain_lds = (size_t)fold_groups * CPW * 16;
+    const size_t chain_lds = RING_BYTES + (size_t)CPW * ch.topk * sizeof(at_entry);
     static bool chain_configured = false;
     if (!chain_configured) {
         for (const void* f : {reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM>),
                               reinterpret_cast<const void*>(&k_chain<AT_TMPL_CONV2D_NCHW>)}) {
             if ((err = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           FOLD_GROUPS * CPW * 16)) != hipSuccess)
+                                           (int)(RING_BYTES + (size_t)CPW * KMAX * sizeof(at_entry)))) != hipSuccess)
                 return err;
         }
         chain_configured = true;
