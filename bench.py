@@ -11,15 +11,24 @@ seed, so every step does identical work.  The headline workload is the C2
 conv2d search (1024 chains x 500 steps, 500 trees of depth 8); the other
 workloads are reported under "extra".
 
-Prints one JSON line.  Timing uses HIP events on the stream the kernels run
-on; the roofline figure divides the kernel's algorithmic LDS bytes by its
-event-timed duration.
+Prints one JSON line.  Run times come from HIP events on the stream the
+kernels run on.  The roofline object is for the dominant kernel, the tree
+walk: one further run of each workload attaches start/stop events to every
+kernel launch (at_sa_set_profiling), and the roofline divides the walk's
+algorithmic LDS bytes per launch, (2d+1) x 4 bytes per tree evaluation
+times chains times trees, by its average launch duration.  Its HBM traffic
+comes from the committed rocprofv3 counter summary while the kernel source
+it was taken from is unchanged (null otherwise).  A 256 MiB device copy runs
+once before the timed region; its FETCH_SIZE / WRITE_SIZE readings scale the
+counters.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -42,6 +51,34 @@ def tree_eval_bytes(depth: int) -> int:
     """Algorithmic LDS bytes of one tree evaluation: depth node reads, depth
     feature reads and one leaf read, 4 bytes each."""
     return (2 * depth + 1) * 4
+
+
+TREE_KERNEL_SOURCE = os.path.join(ROOT, "paper_1805_08166_amd", "csrc", "at_sa_tp.hip")
+COPY_BYTES = 256 << 20
+
+
+def calibration_copy():
+    """One device-to-device copy of known size (for scaling HBM counters)."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
+def committed_traffic(workload: str):
+    """HBM bytes per tree-kernel launch from the committed counter summary,
+    or None when there is none or the kernel source has changed since."""
+    path = os.path.join(ROOT, "profiles", f"k_trees_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    sha = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val:
+        return None
+    cur = hashlib.sha256(open(TREE_KERNEL_SOURCE, "rb").read()).hexdigest()
+    return float(val.group(1)) if sha.group(1) == cur else None
 
 
 def describe(name: str) -> str:
@@ -117,12 +154,23 @@ def bench_sa(P, name, steps, warmup):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     t = float(np.mean(ev))
+    # one profiled run: average launch durations of the two kernels
+    ch = w.make_chains(1)[0]
+    P.at_sa_set_profiling(ch, True)
+    w.run(ch)
+    kt = P.at_sa_kernel_times(ch)
+    tree_s = kt["tree_ms"] / kt["tree_launches"] * 1e-3
+    tree_bytes = w.n * w.wl["trees"] * tree_eval_bytes(w.wl["depth"])
     return w, dict(
         workload=describe(name), ms_per_run=t * 1e3, ms_min=float(np.min(ev)) * 1e3, wall_s=wall,
         evals_per_s=w.evals / t, tree_evals_per_s=w.tree_evals / t,
-        lds_bytes_per_launch=w.lds_bytes, lds_TBps=w.lds_bytes / t / 1e12,
-        lds_frac=w.lds_bytes / t / LDS_PEAK_BPS,
-        host_threshold_s=w.t_thr, host_ensemble_pack_s=w.t_pack)
+        run_lds_bytes=w.lds_bytes, run_lds_TBps=w.lds_bytes / t / 1e12,
+        run_lds_frac=w.lds_bytes / t / LDS_PEAK_BPS,
+        host_threshold_s=w.t_thr, host_ensemble_pack_s=w.t_pack,
+        tree_kernel_us=tree_s * 1e6, tree_kernel_launches=kt["tree_launches"],
+        chain_kernel_us=kt["chain_ms"] / kt["chain_launches"] * 1e3,
+        tree_lds_bytes_per_launch=tree_bytes, tree_lds_TBps=tree_bytes / tree_s / 1e12,
+        tree_lds_frac=tree_bytes / tree_s / LDS_PEAK_BPS)
 
 
 def bench_score(P, reps, warmup):
@@ -193,6 +241,7 @@ def main():
     import paper_1805_08166_amd as P
     torch.cuda.set_device(0)
 
+    calibration_copy()
     head, r = bench_sa(P, args.workload, args.steps, args.warmup)
     extra = {}
     if not args.no_extra:
@@ -218,10 +267,12 @@ def main():
         "data": "synthetic (seeded ensemble and configurations; Table 1 shapes)",
         "config": {"workload": r["workload"], "evals_per_step": head.evals,
                    "tree_evals_per_step": head.tree_evals},
-        "roofline": {"bound": "lds", "kernel": "k_sa", "achieved": r["lds_TBps"],
-                     "peak": LDS_PEAK_BPS / 1e12, "unit": "TB/s", "frac": r["lds_frac"],
-                     "traffic": None,
-                     "per_unit": f"{tree_eval_bytes(head.wl['depth'])} B LDS per tree evaluation"},
+        "roofline": {"bound": "lds", "kernel": "k_trees (tree walk of one annealing step)",
+                     "achieved": r["tree_lds_TBps"], "peak": LDS_PEAK_BPS / 1e12, "unit": "TB/s",
+                     "frac": r["tree_lds_frac"], "traffic": committed_traffic(args.workload),
+                     "launch_us": r["tree_kernel_us"],
+                     "per_unit": f"{tree_eval_bytes(head.wl['depth'])} B LDS per tree evaluation, "
+                                 f"{head.n} chains x {head.wl['trees']} trees per launch"},
         "cpu_baseline": cpu,
         "extra": extra,
     }

@@ -195,6 +195,19 @@ at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chai
 at_status at_chains_export(at_chains_t chains, uint64_t* cur_cfg, float* cur_score,
                            at_stream_t stream);
 
+/* Measurement aid.  With profiling enabled, at_sa_run and at_sa_run_traced
+ * attach start/stop events to every launch of the annealing kernels (the
+ * tree kernel, which walks the ensemble, and the chain kernel, which folds,
+ * offers, accepts, proposes and featurises); results are unchanged.  The
+ * events are created on first use and kept with the chains. */
+at_status at_sa_set_profiling(at_chains_t chains, int enable);
+
+/* Device time of the launches of the last profiled run: summed milliseconds
+ * and launch counts of the tree and chain kernels; any output may be NULL.
+ * Waits for the run to finish.  A run without profiling reports zeros. */
+at_status at_sa_kernel_times(at_chains_t chains, double* tree_ms, int64_t* tree_launches, double* chain_ms,
+                             int64_t* chain_launches);
+
 /* Thread-local description of the last non-OK status ("" if none). */
 const char* at_last_error(void);
 

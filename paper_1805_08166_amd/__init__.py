@@ -32,7 +32,8 @@ EXPORTED = [
     "at_space_create", "at_space_info", "at_spaceset_create", "at_space_destroy",
     "at_extract_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_gbt_predict", "at_chains_create", "at_chains_destroy", "at_chains_step",
-    "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_last_error",
+    "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
+    "at_sa_kernel_times", "at_last_error",
 ]
 
 
@@ -64,6 +65,8 @@ def _load():
         "at_sa_run": [vp, vp, vp, i32, vp, vp, vp],
         "at_sa_run_traced": [vp, vp, vp, i32, vp, vp, vp, vp],
         "at_chains_export": [vp, vp, vp, vp],
+        "at_sa_set_profiling": [vp, i32],
+        "at_sa_kernel_times": [vp, vp, vp, vp, vp],
         "at_last_error": [],
     }
     for name, args in sig.items():
@@ -275,6 +278,19 @@ def at_chains_export(chains: Chains, cur_cfg=None, cur_score=None, stream=None):
     _check("at_chains_export", _lib.at_chains_export(
         chains.h, _dev(cur_cfg, torch.int64, "cur_cfg"), _dev(cur_score, torch.float32, "cur_score"),
         _stream(stream)))
+
+
+def at_sa_set_profiling(chains: Chains, enable: bool):
+    _check("at_sa_set_profiling", _lib.at_sa_set_profiling(chains.h, 1 if enable else 0))
+
+
+def at_sa_kernel_times(chains: Chains) -> dict:
+    """Device time of the last profiled run's launches (waits for the run)."""
+    tms, cms = ctypes.c_double(0), ctypes.c_double(0)
+    tn, cn = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check("at_sa_kernel_times", _lib.at_sa_kernel_times(chains.h, ctypes.byref(tms), ctypes.byref(tn),
+                                                         ctypes.byref(cms), ctypes.byref(cn)))
+    return {"tree_ms": tms.value, "tree_launches": tn.value, "chain_ms": cms.value, "chain_launches": cn.value}
 
 
 def entries(t) -> np.ndarray:

@@ -345,7 +345,38 @@ void at_chains_destroy(at_chains_t chains) {
     release(chains->d_meta);
     release(chains->d_fg);
     release(chains->d_v);
+    for (auto& pool : chains->events)
+        for (hipEvent_t e : pool) (void)hipEventDestroy(e);
     delete chains;
+}
+
+at_status at_sa_set_profiling(at_chains_t chains, int enable) {
+    if (!chains) return fail(AT_E_INVALID, "at_sa_set_profiling: NULL chains");
+    chains->profiling = enable != 0;
+    return AT_OK;
+}
+
+at_status at_sa_kernel_times(at_chains_t chains, double* tree_ms, int64_t* tree_launches, double* chain_ms,
+                             int64_t* chain_launches) {
+    if (!chains) return fail(AT_E_INVALID, "at_sa_kernel_times: NULL chains");
+    DeviceGuard g(chains->device);
+    double total[2] = {0.0, 0.0};
+    for (int kind = 0; kind < 2; ++kind) {
+        const std::vector<hipEvent_t>& pool = chains->events[kind];
+        for (size_t i = 0; i + 1 < chains->events_used[kind]; i += 2) {
+            hipError_t e = hipEventSynchronize(pool[i + 1]);
+            if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+            float ms = 0.0f;
+            e = hipEventElapsedTime(&ms, pool[i], pool[i + 1]);
+            if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+            total[kind] += ms;
+        }
+    }
+    if (tree_ms) *tree_ms = total[0];
+    if (tree_launches) *tree_launches = (int64_t)(chains->events_used[0] / 2);
+    if (chain_ms) *chain_ms = total[1];
+    if (chain_launches) *chain_launches = (int64_t)(chains->events_used[1] / 2);
+    return AT_OK;
 }
 
 at_status at_chains_step(at_chains_t chains, uint64_t* step_abs) {

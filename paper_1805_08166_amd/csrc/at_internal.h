@@ -169,6 +169,11 @@ struct at_chains_s {
     at::DeviceBuf d_meta;     // ChainMeta [n_chains]
     at::DeviceBuf d_fg;       // uint32 [Q][n_chains] packed candidate features
     at::DeviceBuf d_v;        // float leaf values, [ceil(T/4)][n_chains][4]
+    // launch timing (measurement aid): start/stop events attached to every
+    // launch of the last run; kind 0 is the tree kernel, 1 the chain kernel
+    bool profiling = false;
+    std::vector<hipEvent_t> events[2];
+    size_t events_used[2] = {0, 0};
 };
 
 namespace at {

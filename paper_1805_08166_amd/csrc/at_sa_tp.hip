@@ -20,6 +20,8 @@
 // float4 per lane per group, coalesced across the wave.
 #include <cstddef>
 
+#include <hip/hip_ext.h>
+
 #include "at_device.h"
 
 namespace at {
@@ -749,28 +751,51 @@ bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TR
     return true;
 }
 
+// Start and stop events for the next launch of one kind, or nulls when the
+// chains are not being profiled.
+hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t& stop) {
+    start = stop = nullptr;
+    if (!ch.profiling) return hipSuccess;
+    std::vector<hipEvent_t>& pool = ch.events[kind];
+    size_t& used = ch.events_used[kind];
+    while (pool.size() < used + 2) {
+        hipEvent_t e;
+        hipError_t err = hipEventCreate(&e);
+        if (err != hipSuccess) return err;
+        pool.push_back(e);
+    }
+    start = pool[used];
+    stop = pool[used + 1];
+    used += 2;
+    return hipSuccess;
+}
+
 template <int DEPTH, int Q, int SLOT_LOG2>
-hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream) {
+hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     const int grid = (a.n_trees + a.tpw - 1) / a.tpw * a.slices;
-    hipLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, a);
+    if (start)
+        hipExtLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, start, stop, 0, a);
+    else
+        hipLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, a);
     return hipGetLastError();
 }
 
 template <int Q, int SLOT_LOG2>
-hipError_t launch_trees_q(const TreeArgs& a, int depth, int nw, hipStream_t stream) {
+hipError_t launch_trees_q(const TreeArgs& a, int depth, int nw, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop) {
     switch (depth) {
-        case 1: return launch_trees_t<1, Q, SLOT_LOG2>(a, nw, stream);
-        case 2: return launch_trees_t<2, Q, SLOT_LOG2>(a, nw, stream);
-        case 3: return launch_trees_t<3, Q, SLOT_LOG2>(a, nw, stream);
-        case 4: return launch_trees_t<4, Q, SLOT_LOG2>(a, nw, stream);
-        case 5: return launch_trees_t<5, Q, SLOT_LOG2>(a, nw, stream);
-        case 6: return launch_trees_t<6, Q, SLOT_LOG2>(a, nw, stream);
-        case 7: return launch_trees_t<7, Q, SLOT_LOG2>(a, nw, stream);
-        case 8: return launch_trees_t<8, Q, SLOT_LOG2>(a, nw, stream);
-        case 9: return launch_trees_t<9, Q, SLOT_LOG2>(a, nw, stream);
-        case 10: return launch_trees_t<10, Q, SLOT_LOG2>(a, nw, stream);
-        case 11: return launch_trees_t<11, Q, SLOT_LOG2>(a, nw, stream);
-        case 12: return launch_trees_t<12, Q, SLOT_LOG2>(a, nw, stream);
+        case 1: return launch_trees_t<1, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 2: return launch_trees_t<2, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 3: return launch_trees_t<3, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 4: return launch_trees_t<4, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 5: return launch_trees_t<5, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 6: return launch_trees_t<6, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 7: return launch_trees_t<7, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 8: return launch_trees_t<8, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 9: return launch_trees_t<9, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 10: return launch_trees_t<10, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 11: return launch_trees_t<11, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 12: return launch_trees_t<12, Q, SLOT_LOG2>(a, nw, stream, start, stop);
         default: return hipErrorInvalidValue;
     }
 }
@@ -781,9 +806,10 @@ constexpr int GEMM_SLOT_LOG2 = 13, CONV_SLOT_LOG2 = 14;
 static_assert((GEMM_Q * 256) <= (1 << GEMM_SLOT_LOG2) && (GEMM_Q * 256) > (1 << (GEMM_SLOT_LOG2 - 1)), "slot");
 static_assert((CONV_Q * 256) <= (1 << CONV_SLOT_LOG2) && (CONV_Q * 256) > (1 << (CONV_SLOT_LOG2 - 1)), "slot");
 
-hipError_t launch_trees(const TreeArgs& a, int Q, int depth, int nw, hipStream_t stream) {
-    if (Q == GEMM_Q) return launch_trees_q<GEMM_Q, GEMM_SLOT_LOG2>(a, depth, nw, stream);
-    if (Q == CONV_Q) return launch_trees_q<CONV_Q, CONV_SLOT_LOG2>(a, depth, nw, stream);
+hipError_t launch_trees(const TreeArgs& a, int Q, int depth, int nw, hipStream_t stream, hipEvent_t start,
+                        hipEvent_t stop) {
+    if (Q == GEMM_Q) return launch_trees_q<GEMM_Q, GEMM_SLOT_LOG2>(a, depth, nw, stream, start, stop);
+    if (Q == CONV_Q) return launch_trees_q<CONV_Q, CONV_SLOT_LOG2>(a, depth, nw, stream, start, stop);
     return hipErrorInvalidValue;
 }
 
@@ -896,13 +922,24 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
         }
         chain_configured = true;
     }
+    ch.events_used[0] = ch.events_used[1] = 0;
     auto chain_kernel = [&](const ChainArgs& x) -> hipError_t {
         const size_t lds = x.fin == FIN_NONE ? 0 : chain_lds;
-        if (sp.tmpl == AT_TMPL_GEMM)
-            hipLaunchKernelGGL(k_chain<AT_TMPL_GEMM>, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, x);
+        hipEvent_t start, stop;
+        const hipError_t ev = next_events(ch, 1, start, stop);
+        if (ev != hipSuccess) return ev;
+        auto kern = sp.tmpl == AT_TMPL_GEMM ? k_chain<AT_TMPL_GEMM> : k_chain<AT_TMPL_CONV2D_NCHW>;
+        if (start)
+            hipExtLaunchKernelGGL(kern, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, start, stop, 0, x);
         else
-            hipLaunchKernelGGL(k_chain<AT_TMPL_CONV2D_NCHW>, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, x);
+            hipLaunchKernelGGL(kern, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, x);
         return hipGetLastError();
+    };
+    auto trees_kernel = [&]() -> hipError_t {
+        hipEvent_t start, stop;
+        const hipError_t ev = next_events(ch, 0, start, stop);
+        if (ev != hipSuccess) return ev;
+        return launch_trees(ta, Q, e.depth, nw, stream, start, stop);
     };
 
     int pending = FIN_NONE;
@@ -911,7 +948,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
         x.fin = FIN_NONE;
         x.draw = DRAW_INIT;
         if ((err = chain_kernel(x)) != hipSuccess) return err;
-        if ((err = launch_trees(ta, Q, e.depth, nw, stream)) != hipSuccess) return err;
+        if ((err = trees_kernel()) != hipSuccess) return err;
         pending = FIN_INIT;
     }
     for (int s = 0; s < steps; ++s) {
@@ -921,7 +958,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
         x.draw = DRAW_PROPOSE;
         x.draw_step = (uint32_t)(ch.step_abs + (uint64_t)s);
         if ((err = chain_kernel(x)) != hipSuccess) return err;
-        if ((err = launch_trees(ta, Q, e.depth, nw, stream)) != hipSuccess) return err;
+        if ((err = trees_kernel()) != hipSuccess) return err;
         pending = FIN_STEP;
     }
     ChainArgs x = ca;

@@ -69,6 +69,8 @@ def test_argument_errors_before_device_use(P):
     deep = np.zeros((1, (1 << 13) - 1), np.uint8)
     expect_status(P, lambda: P.at_ensemble_create(deep, deep, np.zeros((1, 1 << 13), np.float32), 8), UNSUPPORTED)
     assert "depth" in P.lib().at_last_error().decode()
+    assert P.lib().at_sa_set_profiling(None, 1) == INVALID
+    assert P.lib().at_sa_kernel_times(None, None, None, None, None) == INVALID
 
 
 def bitlen(x):

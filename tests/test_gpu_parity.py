@@ -338,6 +338,26 @@ def test_sa_chain_independence_and_determinism(P):
     assert np.array_equal(tr_p, tr_f[250:290]) and np.array_equal(best_p, best_f[250:290])
 
 
+def test_sa_profiled_run_is_identical_and_counts_launches(P):
+    sp, osp, ens_t, ens = small_setup(P)
+    n, steps, seed, k = 130, 25, 21, 4
+    thr = P.at_sa_thresholds(seed, 0, n, 0, steps)
+    plain = P.at_chains_create(sp, 0, n, k, seed)
+    best_a, tr_a = gpu_sa(P, sp, ens, plain, steps, thr)
+    assert P.at_sa_kernel_times(plain)["tree_launches"] == 0
+    prof = P.at_chains_create(sp, 0, n, k, seed)
+    P.at_sa_set_profiling(prof, True)
+    best_b, tr_b = gpu_sa(P, sp, ens, prof, steps, thr)
+    assert np.array_equal(tr_a, tr_b) and np.array_equal(best_a, best_b)
+    t = P.at_sa_kernel_times(prof)
+    # first run: initial draw + one tree pass, then steps x (chain + trees), then the final chain pass
+    assert t["tree_launches"] == steps + 1 and t["chain_launches"] == steps + 2
+    assert t["tree_ms"] > 0 and t["chain_ms"] > 0
+    best_c, tr_c = gpu_sa(P, sp, ens, prof, 10, P.at_sa_thresholds(seed, 0, n, steps, 10))
+    t = P.at_sa_kernel_times(prof)
+    assert t["tree_launches"] == 10 and t["chain_launches"] == 11
+
+
 @pytest.mark.parametrize("kind", ["zero_steps", "plus_inf", "minus_inf", "zero_temp", "topk1", "topk64", "one_by_one"])
 def test_sa_edge_cases(P, kind):
     shape = (1, 2, 6, 6, 2, 1, 1, 0, 2) if kind == "one_by_one" else (1, 2, 6, 6, 4, 3, 3, 1, 1)
