@@ -53,7 +53,8 @@ def tree_eval_bytes(depth: int) -> int:
     return (2 * depth + 1) * 4
 
 
-TREE_KERNEL_SOURCE = os.path.join(ROOT, "paper_1805_08166_amd", "csrc", "at_sa_tp.hip")
+KERNEL_SOURCES = {"k_trees": os.path.join(ROOT, "paper_1805_08166_amd", "csrc", "at_sa_tp.hip"),
+                  "k_local": os.path.join(ROOT, "paper_1805_08166_amd", "csrc", "at_sa_local.hip")}
 COPY_BYTES = 256 << 20
 
 
@@ -66,10 +67,11 @@ def calibration_copy():
     torch.cuda.synchronize()
 
 
-def committed_traffic(workload: str):
-    """HBM bytes per tree-kernel launch from the committed counter summary,
-    or None when there is none or the kernel source has changed since."""
-    path = os.path.join(ROOT, "profiles", f"k_trees_{workload}_traffic.md")
+def committed_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of the walk kernel from the committed counter
+    summary, or None when there is none or the kernel source has changed
+    since."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -77,7 +79,7 @@ def committed_traffic(workload: str):
     val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not sha or not val:
         return None
-    cur = hashlib.sha256(open(TREE_KERNEL_SOURCE, "rb").read()).hexdigest()
+    cur = hashlib.sha256(open(KERNEL_SOURCES[kernel], "rb").read()).hexdigest()
     return float(val.group(1)) if sha.group(1) == cur else None
 
 
@@ -154,21 +156,29 @@ def bench_sa(P, name, steps, warmup):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     t = float(np.mean(ev))
-    # one profiled run: average launch durations of the two kernels
+    # one profiled run: average launch durations of the kernels.  The walk
+    # kernel is k_local on the chain-local path (one launch per run: the
+    # initial round and every step) and k_trees on the tree-partitioned path
+    # (one launch per scoring round).
     ch = w.make_chains(1)[0]
     P.at_sa_set_profiling(ch, True)
     w.run(ch)
     kt = P.at_sa_kernel_times(ch)
+    local = P.at_chains_last_path(ch) == P.AT_SA_PATH_LOCAL
+    plan = P.at_chains_last_plan(ch) if local else None
     tree_s = kt["tree_ms"] / kt["tree_launches"] * 1e-3
-    tree_bytes = w.n * w.wl["trees"] * tree_eval_bytes(w.wl["depth"])
+    rounds_per_launch = (w.steps + 1) if local else 1
+    tree_bytes = w.n * w.wl["trees"] * rounds_per_launch * tree_eval_bytes(w.wl["depth"])
     return w, dict(
+        path="chain-local" if local else "tree-partitioned", plan=plan,
+        walk_kernel="k_local" if local else "k_trees",
         workload=describe(name), ms_per_run=t * 1e3, ms_min=float(np.min(ev)) * 1e3, wall_s=wall,
         evals_per_s=w.evals / t, tree_evals_per_s=w.tree_evals / t,
         run_lds_bytes=w.lds_bytes, run_lds_TBps=w.lds_bytes / t / 1e12,
         run_lds_frac=w.lds_bytes / t / LDS_PEAK_BPS,
         host_threshold_s=w.t_thr, host_ensemble_pack_s=w.t_pack,
         tree_kernel_us=tree_s * 1e6, tree_kernel_launches=kt["tree_launches"],
-        chain_kernel_us=kt["chain_ms"] / kt["chain_launches"] * 1e3,
+        chain_kernel_us=(kt["chain_ms"] / kt["chain_launches"] * 1e3) if kt["chain_launches"] else None,
         tree_lds_bytes_per_launch=tree_bytes, tree_lds_TBps=tree_bytes / tree_s / 1e12,
         tree_lds_frac=tree_bytes / tree_s / LDS_PEAK_BPS)
 
@@ -267,12 +277,16 @@ def main():
         "data": "synthetic (seeded ensemble and configurations; Table 1 shapes)",
         "config": {"workload": r["workload"], "evals_per_step": head.evals,
                    "tree_evals_per_step": head.tree_evals},
-        "roofline": {"bound": "lds", "kernel": "k_trees (tree walk of one annealing step)",
+        "roofline": {"bound": "lds",
+                     "kernel": (f"{r['walk_kernel']} ({r['path']} path: "
+                                + ("one launch runs every step" if r["path"] == "chain-local"
+                                   else "tree walk of one annealing step") + ")"),
                      "achieved": r["tree_lds_TBps"], "peak": LDS_PEAK_BPS / 1e12, "unit": "TB/s",
-                     "frac": r["tree_lds_frac"], "traffic": committed_traffic(args.workload),
+                     "frac": r["tree_lds_frac"], "traffic": committed_traffic(r["walk_kernel"], args.workload),
                      "launch_us": r["tree_kernel_us"],
                      "per_unit": f"{tree_eval_bytes(head.wl['depth'])} B LDS per tree evaluation, "
-                                 f"{head.n} chains x {head.wl['trees']} trees per launch"},
+                                 f"{head.n} chains x {head.wl['trees']} trees x "
+                                 f"{(head.steps + 1) if r['path'] == 'chain-local' else 1} rounds per launch"},
         "cpu_baseline": cpu,
         "extra": extra,
     }

@@ -177,10 +177,18 @@ at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint
  * at_entry receiving a copy of the best lists after the run (entries with
  * flag 0 are empty).  The ensemble's feature count must match the space's
  * (AT_E_MISMATCH).  steps == 0 only initialises.
+ * Two execution paths compute the same result bit for bit (at_sa_path):
+ * chain-local, one launch per run in which each workgroup keeps a few chains
+ * and streams the ensemble through its LDS every step, and tree-partitioned,
+ * two launches per step in which workgroups hold disjoint tree groups and
+ * exchange features and leaf values through global memory.  By default the
+ * library takes the chain-local path when the whole ensemble stays resident
+ * in one workgroup's LDS, else the tree-partitioned one.
  * Workspace: the first run on a chains handle, and any run with more trees
- * than before, allocates the chains' device workspace (about
- * n_chains * (16 * ceil(n_trees / 4) + 4 * ceil(n_features / 4) + 32)
- * bytes), which synchronises the device; later runs allocate nothing. */
+ * than before, allocates the chains' device workspace (tree-partitioned:
+ * about n_chains * (16 * ceil(n_trees / 4) + 4 * ceil(n_features / 4) + 32)
+ * bytes; chain-local: 16 bytes per chain), which synchronises the device;
+ * later runs allocate nothing. */
 at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
                     const float* thr, at_entry* best, at_stream_t stream);
 
@@ -190,6 +198,30 @@ at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int
 at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
                            const float* thr, at_entry* best, at_entry* trace, at_stream_t stream);
 
+/* Execution path of the annealing runs of a chains handle. */
+typedef enum {
+    AT_SA_PATH_AUTO = 0,   /* chosen per run from the ensemble and chain count */
+    AT_SA_PATH_TREES = 1,  /* tree-partitioned: two kernels per step */
+    AT_SA_PATH_LOCAL = 2   /* chain-local: one persistent kernel per run */
+} at_sa_path;
+
+/* Selects the path of later runs on `chains` (AT_E_INVALID for an unknown
+ * value).  A run asked to take the chain-local path when its plan does not
+ * fit one workgroup's LDS fails with AT_E_UNSUPPORTED.  Either path may
+ * continue chains the other has advanced. */
+at_status at_chains_set_path(at_chains_t chains, int path);
+
+/* The path the last run on `chains` took (AT_SA_PATH_AUTO before any run). */
+at_status at_chains_last_path(at_chains_t chains, int* path);
+
+/* Launch plan of the last chain-local run (measurement aid; zeros when the
+ * last run took the other path): info[0] chains per workgroup, [1] threads
+ * per workgroup, [2] workgroups, [3] trees per chunk, [4] chunks streamed
+ * per step (0: the ensemble stays resident in LDS), [5] 1 when leaves are read from
+ * global memory rather than streamed, [6] dynamic LDS bytes, [7] bytes one
+ * workgroup streams per step. */
+at_status at_chains_last_plan(at_chains_t chains, int64_t info[8]);
+
 /* Copies the chains' current configuration indices (device [n_chains]
  * uint64) and scores (device [n_chains] float); either may be NULL. */
 at_status at_chains_export(at_chains_t chains, uint64_t* cur_cfg, float* cur_score,
@@ -198,8 +230,9 @@ at_status at_chains_export(at_chains_t chains, uint64_t* cur_cfg, float* cur_sco
 /* Measurement aid.  With profiling enabled, at_sa_run and at_sa_run_traced
  * attach start/stop events to every launch of the annealing kernels (the
  * tree kernel, which walks the ensemble, and the chain kernel, which folds,
- * offers, accepts, proposes and featurises); results are unchanged.  The
- * events are created on first use and kept with the chains. */
+ * offers, accepts, proposes and featurises; the chain-local path's single
+ * kernel counts as a tree kernel); results are unchanged.  The events are
+ * created on first use and kept with the chains. */
 at_status at_sa_set_profiling(at_chains_t chains, int enable);
 
 /* Device time of the launches of the last profiled run: summed milliseconds

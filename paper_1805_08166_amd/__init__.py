@@ -33,8 +33,13 @@ EXPORTED = [
     "at_extract_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_gbt_predict", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
-    "at_sa_kernel_times", "at_last_error",
+    "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_last_error",
 ]
+
+# at_sa_path
+AT_SA_PATH_AUTO = 0
+AT_SA_PATH_TREES = 1
+AT_SA_PATH_LOCAL = 2
 
 
 class ATError(RuntimeError):
@@ -67,6 +72,9 @@ def _load():
         "at_chains_export": [vp, vp, vp, vp],
         "at_sa_set_profiling": [vp, i32],
         "at_sa_kernel_times": [vp, vp, vp, vp, vp],
+        "at_chains_set_path": [vp, i32],
+        "at_chains_last_path": [vp, vp],
+        "at_chains_last_plan": [vp, vp],
         "at_last_error": [],
     }
     for name, args in sig.items():
@@ -238,6 +246,25 @@ def at_chains_step(chains: Chains) -> int:
     v = ctypes.c_uint64()
     _check("at_chains_step", _lib.at_chains_step(chains.h, ctypes.byref(v)))
     return v.value
+
+
+def at_chains_set_path(chains: Chains, path: int):
+    _check("at_chains_set_path", _lib.at_chains_set_path(chains.h, int(path)))
+
+
+def at_chains_last_path(chains: Chains) -> int:
+    v = ctypes.c_int()
+    _check("at_chains_last_path", _lib.at_chains_last_path(chains.h, ctypes.byref(v)))
+    return v.value
+
+
+def at_chains_last_plan(chains: Chains) -> dict:
+    """Launch plan of the last chain-local run (zeros after a tree-partitioned one)."""
+    v = np.zeros(8, np.int64)
+    _check("at_chains_last_plan", _lib.at_chains_last_plan(chains.h, _np(v)))
+    keys = ["chains_per_wg", "threads", "workgroups", "trees_per_chunk", "chunks", "gather", "lds_bytes",
+            "stream_bytes_per_step"]
+    return dict(zip(keys, (int(x) for x in v)))
 
 
 def at_sa_thresholds(seed: int, chain0: int, n_chains: int, step_base: int, steps: int) -> np.ndarray:

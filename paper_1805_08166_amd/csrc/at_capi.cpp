@@ -13,6 +13,12 @@ namespace at {
 namespace {
 thread_local std::string g_last_error;
 
+// Bytes one workgroup of the chain-local path may stream per step for the
+// path to be chosen by default.  Measured on MI355X, the chain-local path
+// wins when its ensemble stays resident in LDS (GEMM 512^3: 2.8 ms against
+// 6.4 ms per run) and loses once it streams (conv2d C2: 9.5 against 9.2 ms).
+constexpr double LOCAL_AUTO_BYTES = 0.0;
+
 template <class T>
 at_status upload(DeviceBuf& buf, const T* host, size_t count) {
     buf.bytes = count * sizeof(T);
@@ -254,11 +260,26 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
         for (size_t p = 1; p < NB; ++p) tw[p] = node(2 * p) | (node(2 * p + 1) << 16);
         std::memcpy(tw + NB, &leaf[t * n_leaf], n_leaf * 4);
     }
+    // local forms for the chain-local annealing path (layout in at_internal.h)
+    const size_t ts_full = (size_t)local_tree_stride((int)W16), ts_nodes = (size_t)local_tree_stride((int)NB);
+    std::vector<uint32_t> local_full, local_nodes;
+    try {
+        local_full.assign((size_t)n_trees * ts_full + 4, 0u);
+        local_nodes.assign((size_t)n_trees * ts_nodes + 4, 0u);
+    } catch (...) {
+        return fail(AT_E_OOM, "at_ensemble_create: host allocation");
+    }
+    for (size_t t = 0; t < (size_t)n_trees; ++t) {
+        std::memcpy(local_full.data() + t * ts_full, words16.data() + t * W16, W16 * 4);
+        std::memcpy(local_nodes.data() + t * ts_nodes, words16.data() + t * W16, NB * 4);
+    }
     at_ensemble_s* e = new (std::nothrow) at_ensemble_s();
     if (!e) return fail(AT_E_OOM, "at_ensemble_create: host allocation");
     e->device = current_device();
     at_status st = upload(e->d_words, words.data(), words.size());
     if (st == AT_OK) st = upload(e->d_words16, words16.data(), words16.size());
+    if (st == AT_OK) st = upload(e->d_local_full, local_full.data(), local_full.size());
+    if (st == AT_OK) st = upload(e->d_local_nodes, local_nodes.data(), local_nodes.size());
     if (st != AT_OK) {
         at_ensemble_destroy(e);
         return st;
@@ -269,6 +290,8 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     e->desc.words_per_tree = (int32_t)W;
     e->desc.words = static_cast<const uint32_t*>(e->d_words.p);
     e->desc.words16 = static_cast<const uint32_t*>(e->d_words16.p);
+    e->desc.local_full = static_cast<const uint32_t*>(e->d_local_full.p);
+    e->desc.local_nodes = static_cast<const uint32_t*>(e->d_local_nodes.p);
     *out = e;
     return AT_OK;
 }
@@ -278,6 +301,8 @@ void at_ensemble_destroy(at_ensemble_t ens) {
     DeviceGuard g(ens->device);
     release(ens->d_words);
     release(ens->d_words16);
+    release(ens->d_local_full);
+    release(ens->d_local_nodes);
     delete ens;
 }
 
@@ -379,6 +404,26 @@ at_status at_sa_kernel_times(at_chains_t chains, double* tree_ms, int64_t* tree_
     return AT_OK;
 }
 
+at_status at_chains_set_path(at_chains_t chains, int path) {
+    if (!chains) return fail(AT_E_INVALID, "at_chains_set_path: NULL chains");
+    if (path != AT_SA_PATH_AUTO && path != AT_SA_PATH_TREES && path != AT_SA_PATH_LOCAL)
+        return fail(AT_E_INVALID, "at_chains_set_path: unknown path");
+    chains->path = path;
+    return AT_OK;
+}
+
+at_status at_chains_last_path(at_chains_t chains, int* path) {
+    if (!chains || !path) return fail(AT_E_INVALID, "at_chains_last_path: NULL argument");
+    *path = chains->last_path;
+    return AT_OK;
+}
+
+at_status at_chains_last_plan(at_chains_t chains, int64_t info[8]) {
+    if (!chains || !info) return fail(AT_E_INVALID, "at_chains_last_plan: NULL argument");
+    for (int i = 0; i < 8; ++i) info[i] = chains->last_plan[i];
+    return AT_OK;
+}
+
 at_status at_chains_step(at_chains_t chains, uint64_t* step_abs) {
     if (!chains || !step_abs) return fail(AT_E_INVALID, "at_chains_step: NULL argument");
     *step_abs = chains->step_abs;
@@ -418,8 +463,22 @@ static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t ch
         return fail(AT_E_UNSUPPORTED, "at_sa_run: step counter must fit 32 bits");
     DeviceGuard g(chains->device);
     const bool init = !chains->initialised;
-    hipError_t e = launch_sa_tp(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
+    // path: chain-local when its plan fits and one workgroup streams at most
+    // LOCAL_AUTO_BYTES per step, else tree-partitioned
+    LocalPlan pl;
+    const bool local_fits = chains->n_chains > 0 && plan_local(*space, ens->desc, *chains, pl);
+    int path = chains->path;
+    if (path == AT_SA_PATH_AUTO) path = (local_fits && pl.round_bytes <= LOCAL_AUTO_BYTES) ? AT_SA_PATH_LOCAL : AT_SA_PATH_TREES;
+    if (path == AT_SA_PATH_LOCAL && chains->n_chains > 0 && !local_fits)
+        return fail(AT_E_UNSUPPORTED, "at_sa_run: the chain-local plan does not fit one workgroup's LDS");
+    hipError_t e = path == AT_SA_PATH_LOCAL
+                       ? launch_sa_local(*space, ens->desc, *chains, pl, steps, init, thr, best, trace, (hipStream_t)stream)
+                       : launch_sa_tp(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "at_sa_run");
+    chains->last_path = path;
+    const int64_t plan[8] = {pl.cpb, pl.threads, pl.grid, pl.ct, pl.resident ? 0 : pl.n_chunks, pl.gather,
+                             (int64_t)pl.lds_bytes, (int64_t)pl.round_bytes};
+    for (int i = 0; i < 8; ++i) chains->last_plan[i] = path == AT_SA_PATH_LOCAL ? plan[i] : 0;
     chains->initialised = true;
     chains->step_abs += (uint64_t)steps;
     return AT_OK;

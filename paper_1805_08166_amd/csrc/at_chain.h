@@ -1,0 +1,141 @@
+// Chain bookkeeping shared by the annealing kernels: knob vectors packed as
+// u16, the space of a chain in a space set, and insertion into a chain's
+// best list (Section 3.3: every scored candidate is offered; entries are
+// ordered by score descending, then configuration index ascending, with
+// distinct indices).
+#pragma once
+
+#include "at_device.h"
+
+namespace at {
+namespace dev {
+
+__device__ __forceinline__ int space_of(const int64_t* offsets, int n_spaces, int64_t c) {
+    int w = 0;
+    while (w + 1 < n_spaces && offsets[w + 1] <= c) ++w;
+    return w;
+}
+
+__device__ __forceinline__ void load_knobs(const uint16_t* p, int64_t c, uint32_t (&kv)[MAX_KNOBS]) {
+    const uint4 w = reinterpret_cast<const uint4*>(p)[c];
+    const uint32_t pw[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = (pw[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+}
+
+__device__ __forceinline__ void store_knobs(uint16_t* p, int64_t c, const uint32_t (&kv)[MAX_KNOBS]) {
+    uint4 w;
+    w.x = kv[0] | (kv[1] << 16);
+    w.y = kv[2] | (kv[3] << 16);
+    w.z = kv[4] | (kv[5] << 16);
+    w.w = kv[6] | (kv[7] << 16);
+    reinterpret_cast<uint4*>(p)[c] = w;
+}
+
+__device__ __forceinline__ bool precedes(float sa, uint64_t ca, float sb, uint64_t cb) {
+    return sa > sb || (sa == sb && ca < cb);
+}
+
+// Per-chain record shared between the chain's owner lane and its group of
+// 16 lanes through LDS.
+struct ChainRec {
+    uint64_t cfg;
+    float score;
+    uint32_t count;
+    float kth_score;
+    uint32_t qual;
+    uint64_t kth_cfg;
+    uint32_t nx[MAX_KNOBS / 2];   // proposed knob values, packed in pairs
+};
+
+// Offers (cfg, sc) to the best list of one chain held in LDS, with the 16
+// lanes r = 0..15 of its group (entries are ordered by score descending then
+// index ascending, distinct indices, at most k <= 64).  Lane r looks after
+// entries r, r+16, r+32, r+48.  A wave ballot gives whether the index is
+// already listed and how many entries precede the new one (its position);
+// the entries from that position on then move down by one.  All lanes of
+// the wave must call this (the ballots are wave-wide); gm selects the
+// group's 16 bits of a ballot mask and `active` the lanes of a group whose
+// chain offers.
+__device__ __forceinline__ void group_offer(at_entry* list, ChainRec& rec, int k, int r, uint64_t gm, bool active) {
+    const uint64_t cfg = rec.cfg;
+    const float sc = rec.score;
+    const int count = active ? (int)rec.count : 0;
+    at_entry old[4], prev[4];
+    bool dup = false;
+    uint32_t pre = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = r + 16 * u;
+        if (active && i < count) {
+            old[u] = list[i];
+            dup |= old[u].cfg == cfg;
+            pre |= precedes(old[u].score, old[u].cfg, sc, cfg) ? (1u << u) : 0u;
+        }
+        if (active && i > 0 && i <= count && i < k) prev[u] = list[i - 1];
+    }
+    const bool any_dup = (__ballot(dup) & gm) != 0;
+    int pos = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) pos += __popcll(__ballot((pre >> u) & 1u) & gm);
+    if (!active || any_dup) return;
+    // new list: entries before pos stay, the new entry goes to pos, later
+    // entries move down one place, the last one drops out when the list is full
+    const int n_new = count < k ? count + 1 : k;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = r + 16 * u;
+        if (i >= pos && i < n_new) {
+            at_entry e;
+            if (i == pos) {
+                e.cfg = cfg;
+                e.score = sc;
+                e.flag = 1u;
+            } else {
+                e = prev[u];
+            }
+            list[i] = e;
+            if (i == n_new - 1) {
+                rec.count = (uint32_t)n_new;
+                rec.kth_score = e.score;
+                rec.kth_cfg = e.cfg;
+            }
+        }
+    }
+}
+
+// One level of four trees: for each tree, right = (node & 0xff) <= x4, node
+// becomes the right or left half of its children pair pr, p becomes 2p +
+// right (the comparison's carry), then the next feature address
+// (node & mask) | fb and pair address nb + 4p.  The compiler does not form
+// the carry and the half-word select from plain code.  A VALU write of VCC
+// is read two or more instructions later (gfx950 wait states): the first
+// compare is followed by s_nop 1, the others by the previous tree's address
+// instructions.
+// Operands: 0-3 node, 4-7 p, 8-11 feature address, 12-15 pair address,
+// 16-19 x4, 20-23 pr, 24 mask, 25 fb, 26-29 nb.
+#define AT_WALK4_ASM                                                                                       \
+    "v_cmp_le_u32_sdwa vcc, %0, %16 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32_sdwa %0, %20, %20, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %4, vcc, %4, %4, vcc\n\t"                                                               \
+    "v_cmp_le_u32_sdwa vcc, %1, %17 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %8, %0, %24, %25\n\t"                                                                    \
+    "v_lshl_add_u32 %12, %4, 2, %26\n\t"                                                                   \
+    "v_cndmask_b32_sdwa %1, %21, %21, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %5, vcc, %5, %5, vcc\n\t"                                                               \
+    "v_cmp_le_u32_sdwa vcc, %2, %18 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %9, %1, %24, %25\n\t"                                                                    \
+    "v_lshl_add_u32 %13, %5, 2, %27\n\t"                                                                   \
+    "v_cndmask_b32_sdwa %2, %22, %22, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %6, vcc, %6, %6, vcc\n\t"                                                               \
+    "v_cmp_le_u32_sdwa vcc, %3, %19 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %10, %2, %24, %25\n\t"                                                                   \
+    "v_lshl_add_u32 %14, %6, 2, %28\n\t"                                                                   \
+    "v_cndmask_b32_sdwa %3, %23, %23, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
+    "v_addc_co_u32 %7, vcc, %7, %7, vcc\n\t"                                                               \
+    "v_and_or_b32 %11, %3, %24, %25\n\t"                                                                   \
+    "v_lshl_add_u32 %15, %7, 2, %29"
+
+}  // namespace dev
+}  // namespace at

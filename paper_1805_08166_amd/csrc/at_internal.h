@@ -64,6 +64,12 @@ struct EnsembleDesc {
     int32_t words_per_tree;
     const uint32_t* words;
     const uint32_t* words16;
+    // Local forms for the chain-local annealing path: the compact form's
+    // trees re-laid at an odd word stride (the smallest >= the tree's words
+    // that is 1 mod 32), whole trees (local_full) or node blocks only
+    // (local_nodes); zero padded, plus 16 bytes of slack at the end.
+    const uint32_t* local_full;
+    const uint32_t* local_nodes;
 };
 
 // Largest threshold the compact form keeps; annealing features never exceed
@@ -147,6 +153,8 @@ struct at_ensemble_s {
     at::EnsembleDesc desc{};
     at::DeviceBuf d_words;
     at::DeviceBuf d_words16;
+    at::DeviceBuf d_local_full;
+    at::DeviceBuf d_local_nodes;
 };
 
 struct at_chains_s {
@@ -174,6 +182,10 @@ struct at_chains_s {
     bool profiling = false;
     std::vector<hipEvent_t> events[2];
     size_t events_used[2] = {0, 0};
+    // annealing path: requested (at_sa_path) and taken by the last run
+    int path = AT_SA_PATH_AUTO;
+    int last_path = AT_SA_PATH_AUTO;
+    int64_t last_plan[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 };
 
 namespace at {
@@ -196,6 +208,32 @@ hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, 
 hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
                         bool init, const float* thr, at_entry* best, at_entry* trace,
                         hipStream_t stream);
+// Chain-local annealing path (at_sa_local.hip): launch geometry and the
+// byte offsets of its dynamic LDS blocks.
+struct LocalPlan {
+    int cpb = 0;              // chains per workgroup
+    int threads = 0;
+    int grid = 0;
+    int gather = 0;           // leaves read from global memory
+    int ts = 0;               // tree stride of the local form used (words)
+    int ct = 0;               // trees per chunk
+    int n_chunks = 0;         // chunks walked per step
+    int resident = 0;         // 1: every tree stays in LDS, loaded once
+    uint32_t ring_bytes = 0;
+    uint32_t off_ring = 0, off_lv = 0, off_lists = 0, off_rec = 0, off_frow = 0, off_desc = 0;
+    int lv_stride = 0;
+    size_t lds_bytes = 0;
+    double round_bytes = 0.0; // bytes streamed per round by one workgroup
+};
+int local_tree_stride(int words);
+bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& ch, LocalPlan& pl);
+hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, const LocalPlan& pl,
+                           int steps, bool init, const float* thr, at_entry* best, at_entry* trace,
+                           hipStream_t stream);
+// Start and stop events for the next launch of one kind (0: the walk
+// kernel, 1: the chain kernel), or nulls when the chains are not profiled.
+hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t& stop);
+
 hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score,
                          hipStream_t stream);
 

@@ -22,7 +22,7 @@
 
 #include <hip/hip_ext.h>
 
-#include "at_device.h"
+#include "at_chain.h"
 
 namespace at {
 namespace {
@@ -68,28 +68,6 @@ struct ChainArgs {
     uint32_t draw_step;       // absolute step of the proposal
     at_entry* best;           // copy of the best lists (last launch), or null
 };
-
-__device__ __forceinline__ int space_of(const ChainArgs& a, int64_t c) {
-    int w = 0;
-    while (w + 1 < a.n_spaces && a.offsets[w + 1] <= c) ++w;
-    return w;
-}
-
-__device__ __forceinline__ void load_knobs(const uint16_t* p, int64_t c, uint32_t (&kv)[MAX_KNOBS]) {
-    const uint4 w = reinterpret_cast<const uint4*>(p)[c];
-    const uint32_t pw[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = (pw[j >> 1] >> (16 * (j & 1))) & 0xffffu;
-}
-
-__device__ __forceinline__ void store_knobs(uint16_t* p, int64_t c, const uint32_t (&kv)[MAX_KNOBS]) {
-    uint4 w;
-    w.x = kv[0] | (kv[1] << 16);
-    w.y = kv[2] | (kv[3] << 16);
-    w.z = kv[4] | (kv[5] << 16);
-    w.w = kv[6] | (kv[7] << 16);
-    reinterpret_cast<uint4*>(p)[c] = w;
-}
 
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
 // 6:4, lgkmcnt 11:8): wait for vmcnt <= n only, or for lgkmcnt 0 only.
@@ -177,78 +155,6 @@ __device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int64_
     return s;
 }
 
-__device__ __forceinline__ bool precedes(float sa, uint64_t ca, float sb, uint64_t cb) {
-    return sa > sb || (sa == sb && ca < cb);
-}
-
-// Per-chain record shared between the chain's owner lane and its group of
-// 16 lanes through LDS.
-struct ChainRec {
-    uint64_t cfg;
-    float score;
-    uint32_t count;
-    float kth_score;
-    uint32_t qual;
-    uint64_t kth_cfg;
-    uint32_t nx[MAX_KNOBS / 2];   // proposed knob values, packed in pairs
-};
-
-// Offers (cfg, sc) to the best list of one chain held in LDS, with the 16
-// lanes r = 0..15 of its group (entries are ordered by score descending then
-// index ascending, distinct indices, at most k <= 64).  Lane r looks after
-// entries r, r+16, r+32, r+48.  A wave ballot gives whether the index is
-// already listed and how many entries precede the new one (its position);
-// the entries from that position on then move down by one.  All lanes of
-// the wave must call this (the ballots are wave-wide); gm selects the
-// group's 16 bits of a ballot mask and `active` the lanes of a group whose
-// chain offers.
-__device__ __forceinline__ void group_offer(at_entry* list, ChainRec& rec, int k, int r, uint64_t gm, bool active) {
-    const uint64_t cfg = rec.cfg;
-    const float sc = rec.score;
-    const int count = active ? (int)rec.count : 0;
-    at_entry old[4], prev[4];
-    bool dup = false;
-    uint32_t pre = 0;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int i = r + 16 * u;
-        if (active && i < count) {
-            old[u] = list[i];
-            dup |= old[u].cfg == cfg;
-            pre |= precedes(old[u].score, old[u].cfg, sc, cfg) ? (1u << u) : 0u;
-        }
-        if (active && i > 0 && i <= count && i < k) prev[u] = list[i - 1];
-    }
-    const bool any_dup = (__ballot(dup) & gm) != 0;
-    int pos = 0;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) pos += __popcll(__ballot((pre >> u) & 1u) & gm);
-    if (!active || any_dup) return;
-    // new list: entries before pos stay, the new entry goes to pos, later
-    // entries move down one place, the last one drops out when the list is full
-    const int n_new = count < k ? count + 1 : k;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int i = r + 16 * u;
-        if (i >= pos && i < n_new) {
-            at_entry e;
-            if (i == pos) {
-                e.cfg = cfg;
-                e.score = sc;
-                e.flag = 1u;
-            } else {
-                e = prev[u];
-            }
-            list[i] = e;
-            if (i == n_new - 1) {
-                rec.count = (uint32_t)n_new;
-                rec.kth_score = e.score;
-                rec.kth_cfg = e.cfg;
-            }
-        }
-    }
-}
-
 template <int TMPL>
 __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     using N = Nest<TMPL>;
@@ -276,7 +182,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     // lane reads its own space from global memory.
     __shared__ SpaceDesc s_desc;
     __shared__ uint64_t s_fac[FAC_MAX];
-    const int w_lo = space_of(a, c0), w_hi = space_of(a, c0 + nc - 1);
+    const int w_lo = space_of(a.offsets, a.n_spaces, c0), w_hi = space_of(a.offsets, a.n_spaces, c0 + nc - 1);
     int fac_lo = 0, fac_n = 0;
     if (w_lo == w_hi) {
         const SpaceDesc& g = a.descs[w_lo];
@@ -295,8 +201,8 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     }
     const uint64_t* facp = staged ? s_fac : a.factors;
     // owner lanes: their chain's space; group lanes: the space of chain gj
-    const SpaceDesc* sdp = staged ? &s_desc : a.descs + space_of(a, c);
-    const SpaceDesc* gsdp = staged ? &s_desc : a.descs + space_of(a, c0 + (gvalid ? gj : 0));
+    const SpaceDesc* sdp = staged ? &s_desc : a.descs + space_of(a.offsets, a.n_spaces, c);
+    const SpaceDesc* gsdp = staged ? &s_desc : a.descs + space_of(a.offsets, a.n_spaces, c0 + (gvalid ? gj : 0));
 
     // per-chain state, fetched before the fold so the loads overlap it
     uint32_t cur[MAX_KNOBS], cd[MAX_KNOBS];
@@ -503,39 +409,6 @@ struct TreeArgs {
     // LDS dword offsets of tree i's node block (low half) and leaf block (high half)
     uint32_t toff[TREES_MAX];
 };
-
-// One level of four trees: for each tree, right = (node & 0xff) <= x4, node
-// becomes the right or left half of its children pair pr, p becomes 2p +
-// right (the comparison's carry), then the next feature address
-// (node & mask) | fb and pair address nb + 4p.  The compiler does not form
-// the carry and the half-word select from plain code.  A VALU write of VCC
-// is read two or more instructions later (gfx950 wait states): the first
-// compare is followed by s_nop 1, the others by the previous tree's address
-// instructions.
-// Operands: 0-3 node, 4-7 p, 8-11 feature address, 12-15 pair address,
-// 16-19 x4, 20-23 pr, 24 mask, 25 fb, 26-29 nb.
-#define AT_WALK4_ASM                                                                                       \
-    "v_cmp_le_u32_sdwa vcc, %0, %16 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
-    "s_nop 1\n\t"                                                                                          \
-    "v_cndmask_b32_sdwa %0, %20, %20, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
-    "v_addc_co_u32 %4, vcc, %4, %4, vcc\n\t"                                                               \
-    "v_cmp_le_u32_sdwa vcc, %1, %17 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
-    "v_and_or_b32 %8, %0, %24, %25\n\t"                                                                    \
-    "v_lshl_add_u32 %12, %4, 2, %26\n\t"                                                                   \
-    "v_cndmask_b32_sdwa %1, %21, %21, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
-    "v_addc_co_u32 %5, vcc, %5, %5, vcc\n\t"                                                               \
-    "v_cmp_le_u32_sdwa vcc, %2, %18 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
-    "v_and_or_b32 %9, %1, %24, %25\n\t"                                                                    \
-    "v_lshl_add_u32 %13, %5, 2, %27\n\t"                                                                   \
-    "v_cndmask_b32_sdwa %2, %22, %22, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
-    "v_addc_co_u32 %6, vcc, %6, %6, vcc\n\t"                                                               \
-    "v_cmp_le_u32_sdwa vcc, %3, %19 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
-    "v_and_or_b32 %10, %2, %24, %25\n\t"                                                                   \
-    "v_lshl_add_u32 %14, %6, 2, %28\n\t"                                                                   \
-    "v_cndmask_b32_sdwa %3, %23, %23, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t" \
-    "v_addc_co_u32 %7, vcc, %7, %7, vcc\n\t"                                                               \
-    "v_and_or_b32 %11, %3, %24, %25\n\t"                                                                   \
-    "v_lshl_add_u32 %15, %7, 2, %29"
 
 // Walks G trees for this lane's chain: nb/lb are the LDS byte offsets of the
 // trees' node and leaf blocks, mask the node bits of a tile address.  Node
@@ -751,25 +624,6 @@ bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TR
     return true;
 }
 
-// Start and stop events for the next launch of one kind, or nulls when the
-// chains are not being profiled.
-hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t& stop) {
-    start = stop = nullptr;
-    if (!ch.profiling) return hipSuccess;
-    std::vector<hipEvent_t>& pool = ch.events[kind];
-    size_t& used = ch.events_used[kind];
-    while (pool.size() < used + 2) {
-        hipEvent_t e;
-        hipError_t err = hipEventCreate(&e);
-        if (err != hipSuccess) return err;
-        pool.push_back(e);
-    }
-    start = pool[used];
-    stop = pool[used + 1];
-    used += 2;
-    return hipSuccess;
-}
-
 template <int DEPTH, int Q, int SLOT_LOG2>
 hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     const int grid = (a.n_trees + a.tpw - 1) / a.tpw * a.slices;
@@ -831,6 +685,25 @@ hipError_t ensure(DeviceBuf& b, size_t bytes) {
 }
 
 }  // namespace
+
+// Start and stop events for the next launch of one kind, or nulls when the
+// chains are not being profiled.
+hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t& stop) {
+    start = stop = nullptr;
+    if (!ch.profiling) return hipSuccess;
+    std::vector<hipEvent_t>& pool = ch.events[kind];
+    size_t& used = ch.events_used[kind];
+    while (pool.size() < used + 2) {
+        hipEvent_t e;
+        hipError_t err = hipEventCreate(&e);
+        if (err != hipSuccess) return err;
+        pool.push_back(e);
+    }
+    start = pool[used];
+    stop = pool[used + 1];
+    used += 2;
+    return hipSuccess;
+}
 
 hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps, bool init,
                         const float* thr, at_entry* best, at_entry* trace, hipStream_t stream) {

@@ -181,6 +181,21 @@ def test_predict_batched_scoring_workload_full_size(P):
 # --------------------------------------------------------------------------
 # annealing
 # --------------------------------------------------------------------------
+PATHS = {"trees": 1, "local": 2}
+
+
+@pytest.fixture(params=sorted(PATHS))
+def path(request):
+    return request.param
+
+
+def mk_chains(P, sp, chain0, n, k, seed, path):
+    ch = P.at_chains_create(sp, chain0, n, k, seed)
+    P.at_chains_set_path(ch, PATHS[path])
+    ch.path_name = path
+    return ch
+
+
 def gpu_sa(P, sp, ens, chains, steps, thr, traced=True):
     import torch
     d_thr = torch.from_numpy(np.ascontiguousarray(thr, np.float32)).to(DEV)
@@ -192,6 +207,9 @@ def gpu_sa(P, sp, ens, chains, steps, thr, traced=True):
         tr = None
         P.at_sa_run(sp, ens, chains, steps, d_thr, best)
     torch.cuda.synchronize()
+    want = getattr(chains, "path_name", None)
+    if want is not None and chains.n_chains > 0:
+        assert P.at_chains_last_path(chains) == PATHS[want], "the run took the other path"
     return P.entries(best), (P.entries(tr) if traced else None)
 
 
@@ -231,11 +249,11 @@ def sa_case(P, name, n_gpu, n_oracle, steps=None, oracle_rows=None):
     return spaces, ospaces, (fid, thr, leaf), ens, seed, k, steps
 
 
-def test_sa_gemm_workload_full(P):
+def test_sa_gemm_workload_full(P, path):
     say("sa gemm512 64x500 full")
     spaces, ospaces, ens_t, ens, seed, k, steps = sa_case(P, "gemm512_sa", 64, 64)
     n = 64
-    ch = P.at_chains_create(spaces[0], 0, n, k, seed)
+    ch = mk_chains(P, spaces[0], 0, n, k, seed, path)
     thr_g = P.at_sa_thresholds(seed, 0, n, 0, steps)
     best, tr = gpu_sa(P, spaces[0], ens, ch, steps, thr_g)
     cur = export(P, ch)
@@ -244,11 +262,11 @@ def test_sa_gemm_workload_full(P):
     assert_same_run(best, tr, och, otr, cur=cur)
 
 
-def test_sa_conv_c2_workload_full_gpu_sliced_oracle(P):
+def test_sa_conv_c2_workload_full_gpu_sliced_oracle(P, path):
     say("sa conv C2 1024x500, oracle on 2 slices")
     spaces, ospaces, ens_t, ens, seed, k, steps = sa_case(P, "conv_c2_sa", 1024, 0)
     n = 1024
-    ch = P.at_chains_create(spaces[0], 0, n, k, seed)
+    ch = mk_chains(P, spaces[0], 0, n, k, seed, path)
     best, tr = gpu_sa(P, spaces[0], ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     cur = export(P, ch)
     for lo, hi in [(0, 96), (1000, 1024)]:
@@ -257,18 +275,18 @@ def test_sa_conv_c2_workload_full_gpu_sliced_oracle(P):
         assert_same_run(best, tr, och, otr, rows=slice(lo, hi), cur=cur)
 
 
-def test_sa_conv_c12_deep_ensemble_short(P):
+def test_sa_conv_c12_deep_ensemble_short(P, path):
     say("sa conv C12 2000 trees depth 10, 300 chains x 12 steps")
     spaces, ospaces, ens_t, ens, seed, k, _ = sa_case(P, "conv_c12_sa", 300, 300)
     n, steps = 300, 12
-    ch = P.at_chains_create(spaces[0], 0, n, k, seed)
+    ch = mk_chains(P, spaces[0], 0, n, k, seed, path)
     best, tr = gpu_sa(P, spaces[0], ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     och = oracle.Chains(ospaces, [0, n], seed=seed, chain0=0, topk=k)
     otr = och.run(ens_t, steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
     assert_same_run(best, tr, och, otr, cur=export(P, ch))
 
 
-def test_sa_twelve_workload_set_short(P):
+def test_sa_twelve_workload_set_short(P, path):
     say("sa 12-workload set, 40 chains each x 60 steps")
     wl = W.WORKLOADS["resnet18_12conv_sa"]
     spaces = [P.at_space_create(t, s) for t, s in wl["spaces"]]
@@ -278,14 +296,14 @@ def test_sa_twelve_workload_set_short(P):
     off = W.chain_offsets(12, 40)
     sset = P.at_spaceset_create(spaces, off)
     n, steps, seed, k = int(off[-1]), 60, wl["sa_seed"], wl["topk"]
-    ch = P.at_chains_create(sset, 0, n, k, seed)
+    ch = mk_chains(P, sset, 0, n, k, seed, path)
     best, tr = gpu_sa(P, sset, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     och = oracle.Chains(ospaces, off, seed=seed, chain0=0, topk=k)
     otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
     assert_same_run(best, tr, och, otr, cur=export(P, ch))
 
 
-def test_sa_ragged_set_offsets(P):
+def test_sa_ragged_set_offsets(P, path):
     shapes = [(1, 2, 4, 4, 2, 3, 3, 1, 1), (1, 2, 6, 6, 2, 1, 1, 0, 2), (1, 1, 8, 8, 2, 7, 7, 3, 2)]
     spaces = [P.at_space_create(W.CONV2D, s) for s in shapes]
     ospaces = [oracle.Space(W.CONV2D, s) for s in shapes]
@@ -294,7 +312,7 @@ def test_sa_ragged_set_offsets(P):
     ens = P.at_ensemble_create(fid, thr, leaf, 176)
     sset = P.at_spaceset_create(spaces, off)
     n, steps, seed, k = 301, 50, 21, 4
-    ch = P.at_chains_create(sset, 7, n, k, seed)
+    ch = mk_chains(P, sset, 7, n, k, seed, path)
     best, tr = gpu_sa(P, sset, ens, ch, steps, P.at_sa_thresholds(seed, 7, n, 0, steps))
     och = oracle.Chains(ospaces, off, seed=seed, chain0=7, topk=k)
     otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 7, n, 0, steps), trace=True)
@@ -309,13 +327,13 @@ def small_setup(P, n=70, topk=6, trees=25, depth=6, shape=(1, 2, 6, 6, 4, 3, 3, 
     return sp, osp, (fid, thr, leaf), ens
 
 
-def test_sa_persistence_split_equals_full(P):
+def test_sa_persistence_split_equals_full(P, path):
     sp, osp, ens_t, ens = small_setup(P)
     n, steps, seed, k = 70, 80, 5, 6
     thr = P.at_sa_thresholds(seed, 0, n, 0, steps)
-    a = P.at_chains_create(sp, 0, n, k, seed)
+    a = mk_chains(P, sp, 0, n, k, seed, path)
     best_a, tr_a = gpu_sa(P, sp, ens, a, steps, thr)
-    b = P.at_chains_create(sp, 0, n, k, seed)
+    b = mk_chains(P, sp, 0, n, k, seed, path)
     _, tr_b1 = gpu_sa(P, sp, ens, b, 30, thr[:, :30].copy())
     assert P.at_chains_step(b) == 30
     best_b, tr_b2 = gpu_sa(P, sp, ens, b, 50, thr[:, 30:].copy())
@@ -324,16 +342,16 @@ def test_sa_persistence_split_equals_full(P):
     assert P.at_chains_step(a) == P.at_chains_step(b) == 80
 
 
-def test_sa_chain_independence_and_determinism(P):
+def test_sa_chain_independence_and_determinism(P, path):
     sp, osp, ens_t, ens = small_setup(P)
     n, steps, seed, k = 300, 40, 9, 5
     thr = P.at_sa_thresholds(seed, 0, n, 0, steps)
-    full = P.at_chains_create(sp, 0, n, k, seed)
+    full = mk_chains(P, sp, 0, n, k, seed, path)
     best_f, tr_f = gpu_sa(P, sp, ens, full, steps, thr)
-    again = P.at_chains_create(sp, 0, n, k, seed)
+    again = mk_chains(P, sp, 0, n, k, seed, path)
     best_g, tr_g = gpu_sa(P, sp, ens, again, steps, thr)
     assert np.array_equal(tr_f, tr_g) and np.array_equal(best_f, best_g)
-    part = P.at_chains_create(sp, 250, 40, k, seed)
+    part = mk_chains(P, sp, 250, 40, k, seed, path)
     best_p, tr_p = gpu_sa(P, sp, ens, part, steps, thr[250:290].copy())
     assert np.array_equal(tr_p, tr_f[250:290]) and np.array_equal(best_p, best_f[250:290])
 
@@ -342,10 +360,10 @@ def test_sa_profiled_run_is_identical_and_counts_launches(P):
     sp, osp, ens_t, ens = small_setup(P)
     n, steps, seed, k = 130, 25, 21, 4
     thr = P.at_sa_thresholds(seed, 0, n, 0, steps)
-    plain = P.at_chains_create(sp, 0, n, k, seed)
+    plain = mk_chains(P, sp, 0, n, k, seed, "trees")
     best_a, tr_a = gpu_sa(P, sp, ens, plain, steps, thr)
     assert P.at_sa_kernel_times(plain)["tree_launches"] == 0
-    prof = P.at_chains_create(sp, 0, n, k, seed)
+    prof = mk_chains(P, sp, 0, n, k, seed, "trees")
     P.at_sa_set_profiling(prof, True)
     best_b, tr_b = gpu_sa(P, sp, ens, prof, steps, thr)
     assert np.array_equal(tr_a, tr_b) and np.array_equal(best_a, best_b)
@@ -359,7 +377,7 @@ def test_sa_profiled_run_is_identical_and_counts_launches(P):
 
 
 @pytest.mark.parametrize("kind", ["zero_steps", "plus_inf", "minus_inf", "zero_temp", "topk1", "topk64", "one_by_one"])
-def test_sa_edge_cases(P, kind):
+def test_sa_edge_cases(P, path, kind):
     shape = (1, 2, 6, 6, 2, 1, 1, 0, 2) if kind == "one_by_one" else (1, 2, 6, 6, 4, 3, 3, 1, 1)
     sp, osp, ens_t, ens = small_setup(P, shape=shape)
     n, steps, seed = 65, 30, 13
@@ -376,7 +394,7 @@ def test_sa_edge_cases(P, kind):
         thr_g = P.at_sa_thresholds(seed, 0, n, 0, max(steps, 1))[:, :steps].copy()
     thr_o = thr_g.copy() if kind in ("plus_inf", "minus_inf", "zero_temp") else \
         oracle.thresholds(seed, 0, n, 0, max(steps, 1))[:, :steps].copy()
-    ch = P.at_chains_create(sp, 0, n, k, seed)
+    ch = mk_chains(P, sp, 0, n, k, seed, path)
     best, tr = gpu_sa(P, sp, ens, ch, steps, thr_g, traced=steps > 0)
     och = oracle.Chains([osp], [0, n], seed=seed, chain0=0, topk=k)
     otr = och.run(ens_t, steps, thr_o, trace=True)
@@ -396,3 +414,69 @@ def test_sa_rejects_mismatched_ensemble(P):
     with pytest.raises(P.ATError) as ei:
         P.at_sa_run(sp, ens, ch, 3, thr_d, best)
     assert ei.value.status == -6
+
+
+def test_sa_local_profiled_run_is_one_launch(P):
+    sp, osp, ens_t, ens = small_setup(P)
+    n, steps, seed, k = 130, 25, 21, 4
+    thr = P.at_sa_thresholds(seed, 0, n, 0, steps)
+    plain = mk_chains(P, sp, 0, n, k, seed, "local")
+    best_a, tr_a = gpu_sa(P, sp, ens, plain, steps, thr)
+    prof = mk_chains(P, sp, 0, n, k, seed, "local")
+    P.at_sa_set_profiling(prof, True)
+    best_b, tr_b = gpu_sa(P, sp, ens, prof, steps, thr)
+    assert np.array_equal(tr_a, tr_b) and np.array_equal(best_a, best_b)
+    t = P.at_sa_kernel_times(prof)
+    assert t["tree_launches"] == 1 and t["chain_launches"] == 0 and t["tree_ms"] > 0
+
+
+def test_sa_paths_agree_and_interleave(P):
+    """The two paths give the same trajectories; a run on one path continues
+    chains the other has advanced."""
+    sp, osp, ens_t, ens = small_setup(P, trees=90, depth=7)
+    n, steps, seed, k = 200, 60, 31, 8
+    thr = P.at_sa_thresholds(seed, 0, n, 0, steps)
+    ref = mk_chains(P, sp, 0, n, k, seed, "trees")
+    best_r, tr_r = gpu_sa(P, sp, ens, ref, steps, thr)
+    mix = mk_chains(P, sp, 0, n, k, seed, "local")
+    _, tr_1 = gpu_sa(P, sp, ens, mix, 20, thr[:, :20].copy())
+    P.at_chains_set_path(mix, PATHS["trees"])
+    mix.path_name = "trees"
+    _, tr_2 = gpu_sa(P, sp, ens, mix, 25, thr[:, 20:45].copy())
+    P.at_chains_set_path(mix, PATHS["local"])
+    mix.path_name = "local"
+    best_m, tr_3 = gpu_sa(P, sp, ens, mix, 15, thr[:, 45:].copy())
+    assert np.array_equal(np.concatenate([tr_1, tr_2, tr_3], axis=1), tr_r)
+    assert np.array_equal(best_m, best_r)
+    assert np.array_equal(export(P, mix)[0], export(P, ref)[0])
+
+
+# chain-local plans: resident ensemble, streamed whole trees, streamed node
+# blocks with leaves from global memory; each checked against the oracle
+LOCAL_PLANS = {
+    "resident": dict(n=48, trees=40, depth=6, steps=30),
+    "streamed": dict(n=8192, trees=300, depth=8, steps=6),
+    "gathered": dict(n=64, trees=400, depth=9, steps=20),
+}
+
+
+@pytest.mark.parametrize("mode", sorted(LOCAL_PLANS))
+def test_sa_local_plans_match_oracle(P, mode):
+    cfg = LOCAL_PLANS[mode]
+    say(f"sa local plan {mode}: {cfg}")
+    shape = (1, 16, 14, 14, 32, 3, 3, 1, 1)
+    sp = P.at_space_create(W.CONV2D, shape)
+    osp = oracle.Space(W.CONV2D, shape)
+    fid, thr, leaf = W.make_ensemble(cfg["trees"], cfg["depth"], 176, 404)
+    ens = P.at_ensemble_create(fid, thr, leaf, 176)
+    n, steps, seed, k = cfg["n"], cfg["steps"], 55, 8
+    ch = mk_chains(P, sp, 0, n, k, seed, "local")
+    best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
+    plan = P.at_chains_last_plan(ch)
+    assert (plan["chunks"] == 0) == (mode == "resident")
+    assert plan["gather"] == (1 if mode == "gathered" else 0)
+    rows = slice(0, min(n, 160))
+    m = rows.stop
+    och = oracle.Chains([osp], [0, m], seed=seed, chain0=0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, m, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, rows=rows, cur=export(P, ch))
