@@ -182,8 +182,9 @@ at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint
  * and streams the ensemble through its LDS every step, and tree-partitioned,
  * two launches per step in which workgroups hold disjoint tree groups and
  * exchange features and leaf values through global memory.  By default the
- * library takes the chain-local path when the whole ensemble stays resident
- * in one workgroup's LDS, else the tree-partitioned one.
+ * library takes the chain-local path when one workgroup keeps the whole
+ * ensemble in its LDS or streams at most 768 KB of it per step, else the
+ * tree-partitioned one.
  * Workspace: the first run on a chains handle, and any run with more trees
  * than before, allocates the chains' device workspace (tree-partitioned:
  * about n_chains * (16 * ceil(n_trees / 4) + 4 * ceil(n_features / 4) + 32)

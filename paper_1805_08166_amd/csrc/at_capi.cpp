@@ -14,10 +14,12 @@ namespace {
 thread_local std::string g_last_error;
 
 // Bytes one workgroup of the chain-local path may stream per step for the
-// path to be chosen by default.  Measured on MI355X, the chain-local path
-// wins when its ensemble stays resident in LDS (GEMM 512^3: 2.8 ms against
-// 6.4 ms per run) and loses once it streams (conv2d C2: 9.5 against 9.2 ms).
-constexpr double LOCAL_AUTO_BYTES = 0.0;
+// path to be chosen by default.  Measured on MI355X: the chain-local path
+// wins with its ensemble resident in LDS (GEMM 512^3: 2.5 ms against 6.4 ms
+// per run) and streaming about 0.4 MB per step (conv2d C2: 5.7 against
+// 9.2 ms), and loses at 1.5 MB per step (twelve conv2d workloads: 33 against
+// 20 ms).
+constexpr double LOCAL_AUTO_BYTES = 768.0 * 1024;
 
 template <class T>
 at_status upload(DeviceBuf& buf, const T* host, size_t count) {

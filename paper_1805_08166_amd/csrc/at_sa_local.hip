@@ -64,6 +64,7 @@ struct LocalArgs {
     int ct;                   // trees per chunk, a multiple of 4 and at most 4 per walk slot
     int n_chunks;
     int resident;             // the ring holds every tree (loaded once); else two chunk buffers
+    int walk_waves;           // waves 1 .. walk_waves walk; later waves load
     int gather;               // leaves from global memory (leaf_src) instead of the ring
     const uint32_t* leaf_src; // compact form: leaves of tree t at leaf_src[t * w16 + 2^(d-1) + q]
     int w16;
@@ -71,7 +72,7 @@ struct LocalArgs {
     uint32_t off_ring, ring_bytes;
     uint32_t off_lv;
     int lv_stride;            // floats per chain row of leaf values: two chunk slots (one when resident)
-    uint32_t off_lists, off_rec, off_frow, off_desc;
+    uint32_t off_lists, off_rec, off_frow, off_any, off_desc;
 };
 
 // Leaf indices of four trees for this lane: nb holds the LDS byte offsets
@@ -114,13 +115,14 @@ __device__ __forceinline__ void walk4_local(const uint8_t* __restrict__ L, const
 }
 
 // Issues the direct-to-LDS loads of trees [t0, t0 + nt) of the local form
-// into LDS at dst (one wave, 16 bytes per lane and instruction).
-__device__ __forceinline__ void load_trees(const LocalArgs& a, uint8_t* dst, int t0, int nt, int lane) {
+// into LDS at dst: thread li of nl (whole waves) moves 16-byte units
+// li, li + nl, ...
+__device__ __forceinline__ void load_trees(const LocalArgs& a, uint8_t* dst, int t0, int nt, int li, int nl) {
     const int n16 = (nt * a.ts * 4 + 15) >> 4;
     const uint4* src = reinterpret_cast<const uint4*>(a.tw + (size_t)t0 * a.ts);
     uint4* d = reinterpret_cast<uint4*>(dst);
-    for (int base = 0; base < n16; base += 64) {
-        const int i = base + lane;
+    for (int base = li - (li & 63); base < n16; base += nl) {
+        const int i = base + (li & 63);
         if (i < n16) __builtin_amdgcn_global_load_lds(src + i, d + base, 16, 0, 0);
     }
 }
@@ -128,6 +130,66 @@ __device__ __forceinline__ void load_trees(const LocalArgs& a, uint8_t* dst, int
 // Workgroup barrier that orders LDS accesses only: each wave's own LDS
 // operations complete before it arrives; global loads stay in flight.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Adds the leaf values row[0 .. nt) to s in order, eight float4 reads ahead
+// of the adds (row 16-byte aligned; nt a multiple of 4 except in a last,
+// partial chunk).
+__device__ __forceinline__ float fold_row(float s, const float* __restrict__ row, int nt) {
+    const float4* r4 = reinterpret_cast<const float4*>(row);
+    const int n4 = nt >> 2;
+    int i = 0;
+    if (n4 >= 8) {
+        float4 cur[8], nxt[8];
+#pragma unroll
+        for (int g = 0; g < 8; ++g) cur[g] = r4[g];
+        for (; i + 16 <= n4; i += 8) {
+#pragma unroll
+            for (int g = 0; g < 8; ++g) nxt[g] = r4[i + 8 + g];
+#pragma unroll
+            for (int g = 0; g < 8; ++g) {
+                s = s + cur[g].x;
+                s = s + cur[g].y;
+                s = s + cur[g].z;
+                s = s + cur[g].w;
+            }
+#pragma unroll
+            for (int g = 0; g < 8; ++g) cur[g] = nxt[g];
+        }
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+            s = s + cur[g].x;
+            s = s + cur[g].y;
+            s = s + cur[g].z;
+            s = s + cur[g].w;
+        }
+        i += 8;
+    }
+    for (; i < n4; ++i) {
+        const float4 v = r4[i];
+        s = s + v.x;
+        s = s + v.y;
+        s = s + v.z;
+        s = s + v.w;
+    }
+    for (int t = n4 * 4; t < nt; ++t) s = s + row[t];
+    return s;
+}
+
+// The knob a step changes and the value it draws among the knob's other
+// values, before the shift past the current value (block (chain, step, 0, 0)).
+// Neither depends on the chain's state, so they are drawn ahead of time.
+__device__ __forceinline__ void draw_move(const SpaceDesc& sd, uint32_t k0, uint32_t k1, uint32_t chain,
+                                          uint32_t step, int& jm, uint32_t& v, uint64_t& radix) {
+    const U4 rr = philox(k0, k1, U4{chain, step, 0u, 0u});
+    jm = -1;
+    v = 0u;
+    radix = 0;
+    if (sd.n_mut > 0) {
+        jm = sd.mut[uniform_below(rr.x, (uint32_t)sd.n_mut)];
+        v = uniform_below(rr.y, sd.knob_size[jm] - 1u);
+        radix = sd.radix[jm];
+    }
+}
 
 template <int TMPL, int DEPTH>
 __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
@@ -144,6 +206,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     at_entry* lists = reinterpret_cast<at_entry*>(lds + a.off_lists);
     ChainRec* rec = reinterpret_cast<ChainRec*>(lds + a.off_rec);
     uint8_t* frow = lds + a.off_frow;
+    uint32_t* s_any = reinterpret_cast<uint32_t*>(lds + a.off_any);   // [2]: some chain qualifies
     SpaceDesc& s_desc = *reinterpret_cast<SpaceDesc*>(lds + a.off_desc);
     uint64_t* s_fac = reinterpret_cast<uint64_t*>(lds + a.off_desc + sizeof(SpaceDesc));
 
@@ -159,6 +222,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     const uint64_t gmask = 0xffffull << (16 * (gj & 3));
     const bool gvalid = gj < nc;
     const int gjc = gvalid ? gj : 0;
+    // wave roles: 0 folds and keeps the books; 1 .. nww walk; the rest load
+    const int nww = a.walk_waves;
+    const bool walker = wave >= 1 && wave <= nww;
+    const bool loader = wave > nww;
+    const int n_load_waves = nthreads / 64 - 1 - nww;
 
     // space tables: staged in LDS when every chain of the workgroup uses one space
     const int w_lo = space_of(a.offsets, a.n_spaces, c0), w_hi = space_of(a.offsets, a.n_spaces, c0 + nc - 1);
@@ -178,9 +246,16 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             ld[i] = (i >= SO && i < SO + MAX_AXES) ? gd[i] - (uint32_t)fac_lo : gd[i];
         for (int i = tid; i < fac_n; i += nthreads) s_fac[i] = a.factors[fac_lo + i];
     }
-    const uint64_t* facp = staged ? s_fac : a.factors;
-    const SpaceDesc* sdp = staged ? &s_desc : a.descs + space_of(a.offsets, a.n_spaces, c);
-    const SpaceDesc* gsdp = staged ? &s_desc : a.descs + space_of(a.offsets, a.n_spaces, c0 + gjc);
+    // space of the owner's chain and of the group's chain: the staged copy in
+    // LDS or the set's tables in global memory.  Each use branches on
+    // `staged` (uniform in the workgroup) so that either branch reads one
+    // address space directly.
+    const SpaceDesc* sdp_g = a.descs + space_of(a.offsets, a.n_spaces, c);
+    const SpaceDesc* gsdp_g = a.descs + space_of(a.offsets, a.n_spaces, c0 + gjc);
+    auto with_space = [&](auto&& f) {
+        if (staged) f(s_desc);
+        else f(*sdp_g);
+    };
 
     // chain state: knobs and score in the owner lanes, best lists and their
     // bookkeeping in LDS
@@ -212,65 +287,77 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             lists[e] = a.top[c0 * k + e];
         }
     }
-
-    // the staged tables, initial lists and records are in place
-    lds_barrier();
+    if (tid < 2) s_any[tid] = 0u;
     const int rounds = (a.init ? 1 : 0) + a.steps;
     const bool resident = a.resident != 0;
     const int nck = a.n_chunks;
     const int total_chunks = rounds * nck;
-    // the loader wave starts the first chunk (the whole ensemble when resident)
-    if (wave == 1 && rounds > 0) {
-        if (resident) load_trees(a, ring, 0, a.T, lane);
-        else load_trees(a, ring, 0, a.ct < a.T ? a.ct : a.T, lane);
+    const int lag = a.gather ? 2 : 1;   // chunks between a walk and the fold of its leaf values
+    // the first chunk (every tree when resident) is loaded by all waves but 0
+    if (wave >= 1 && rounds > 0) {
+        load_trees(a, ring, 0, resident ? a.T : (a.ct < a.T ? a.ct : a.T), tid - 64, nthreads - 64);
+        __builtin_amdgcn_s_waitcnt(0);
     }
+    // the staged tables, initial lists and records are in place
+    lds_barrier();
 
-    // walk-lane geometry: chain jw, tree slot u of S (four trees per lane and chunk)
-    const int wt = tid - 128;                     // walk thread (waves 2..)
+    // walker geometry: chain jw, tree slot u; a chunk of nt trees gives slot
+    // u the trees u, u + S', u + 2S', u + 3S' with S' = ceil(nt / 4)
+    const int wi = tid - 64;
     const int jw = lane % cpb;
-    const int S = (nthreads - 128) / cpb;
-    const int u = (wt >= 0 ? wt : 0) / cpb;
+    const int u = (walker ? wi : 0) / cpb;
     const uint32_t fb = (uint32_t)lane * 4u;
     const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-    const uint64_t gchain = a.chain0 + (uint64_t)c;
-    // threshold of the owner's next step, loaded one round ahead
+    const uint32_t gchain = (uint32_t)(a.chain0 + (uint64_t)c);
+    // the owner's next threshold and move, ready one round ahead
     float thr_next = (owner && a.steps > 0) ? a.thr[c * a.steps] : 0.0f;
+    int mv_j = -1;
+    uint32_t mv_v = 0u;
+    uint64_t mv_radix = 0;     // weight of the moved knob in the configuration index
+    uint64_t cur_cfg = 0;      // index of the current configuration
+    if (owner && !a.init)
+        with_space([&](const SpaceDesc& sd) {
+#pragma unroll
+            for (int j = 0; j < MAX_KNOBS; ++j)
+                if (j < sd.n_knobs) cur_cfg += (uint64_t)cur[j] * sd.radix[j];
+        });
+    if (owner && a.steps > 0)
+        with_space([&](const SpaceDesc& sd) { draw_move(sd, k0, k1, gchain, a.step0, mv_j, mv_v, mv_radix); });
 
     for (int r = 0; r < rounds; ++r) {
         const bool is_init = a.init && r == 0;
         const int s = r - (a.init ? 1 : 0);
         // (1) candidate: the initial draw (block (chain, 0, 1, j / 4)) or one
-        // knob moved to another value (block (chain, step, 0, 0))
+        // knob moved to a uniformly chosen other value
         uint32_t cd[MAX_KNOBS];
         float thr_v = 0.0f;
+        uint64_t cfg = 0;
         if (owner) {
-            const SpaceDesc& sd = *sdp;
             if (is_init) {
-                U4 rr{0, 0, 0, 0};
+                with_space([&](const SpaceDesc& sd) {
+                    U4 rr{0, 0, 0, 0};
 #pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j) {
-                    if ((j & 3) == 0) rr = philox(k0, k1, U4{(uint32_t)gchain, 0u, 1u, (uint32_t)(j >> 2)});
-                    const uint32_t word = (j & 3) == 0 ? rr.x : (j & 3) == 1 ? rr.y : (j & 3) == 2 ? rr.z : rr.w;
-                    cd[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
-                }
+                    for (int j = 0; j < MAX_KNOBS; ++j) {
+                        if ((j & 3) == 0) rr = philox(k0, k1, U4{gchain, 0u, 1u, (uint32_t)(j >> 2)});
+                        const uint32_t word = (j & 3) == 0 ? rr.x : (j & 3) == 1 ? rr.y : (j & 3) == 2 ? rr.z : rr.w;
+                        cd[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
+                        if (j < sd.n_knobs) cfg += (uint64_t)cd[j] * sd.radix[j];
+                    }
+                });
             } else {
                 thr_v = thr_next;
                 if (s + 1 < a.steps) thr_next = a.thr[c * a.steps + s + 1];
-                const U4 rr = philox(k0, k1, U4{(uint32_t)gchain, a.step0 + (uint32_t)s, 0u, 0u});
+                uint32_t old = 0;
 #pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j) cd[j] = cur[j];
-                if (sd.n_mut > 0) {
-                    const int jm = sd.mut[uniform_below(rr.x, (uint32_t)sd.n_mut)];
-                    uint32_t old = 0, size = 2;
-#pragma unroll
-                    for (int j = 0; j < MAX_KNOBS; ++j)
-                        if (j == jm) { old = cur[j]; size = sd.knob_size[j]; }
-                    uint32_t nv = uniform_below(rr.y, size - 1u);
-                    if (nv >= old) nv += 1u;
-#pragma unroll
-                    for (int j = 0; j < MAX_KNOBS; ++j)
-                        if (j == jm) cd[j] = nv;
+                for (int j = 0; j < MAX_KNOBS; ++j) {
+                    old = (j == mv_j) ? cur[j] : old;
+                    cd[j] = (j == mv_j) ? mv_v + (mv_v >= cur[j] ? 1u : 0u) : cur[j];
                 }
+                // the index moves by (new - old) times the knob's weight
+                const uint32_t nv = mv_v + (mv_v >= old ? 1u : 0u);
+                cfg = mv_j < 0 ? cur_cfg
+                               : (nv >= old ? cur_cfg + (uint64_t)(nv - old) * mv_radix
+                                            : cur_cfg - (uint64_t)(old - nv) * mv_radix);
             }
 #pragma unroll
             for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = cd[2 * j] | (cd[2 * j + 1] << 16);
@@ -278,134 +365,123 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         lds_barrier();
         // (2) features: lane gr of group gj evaluates loop gr of chain gj
         if (gvalid && gr < N::L) {
-            const SpaceDesc& sd = *gsdp;
             uint32_t nx[MAX_KNOBS];
 #pragma unroll
             for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (rec[gj].nx[j >> 1] >> (16 * (j & 1))) & 0xffffu;
-            uint32_t fac[6][4];
-            gather_factors<TMPL>(sd, facp, nx, fac);
-            uint32_t f[11];
-            loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f);
+            auto feats = [&](const SpaceDesc& sd, const uint64_t* facp) {
+                uint32_t fac[6][4];
+                gather_factors<TMPL>(sd, facp, nx, fac);
+                uint32_t f[11];
+                loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f);
 #pragma unroll
-            for (int i = 0; i < 11; ++i) frow[gj * RS + gr * 11 + i] = (uint8_t)f[i];
+                for (int i = 0; i < 11; ++i) frow[gj * RS + gr * 11 + i] = (uint8_t)f[i];
+            };
+            if (staged) feats(s_desc, s_fac);
+            else feats(*gsdp_g, a.factors);
         }
         lds_barrier();
         // (3) the tile: column l holds chain l % cpb (the last chain stands
         // in for missing ones), bytes 4x+3
+        // (features are at most 31, so 4x+3 stays within each byte; bytes past
+        // the last feature are never read)
         for (int i = tid; i < Q * 64; i += nthreads) {
             const int q = i >> 6;
-            int j = (i & 63) % cpb;
+            int j = i & (cpb - 1);
             j = j < nc ? j : nc - 1;
-            uint32_t w = 0;
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const int f = 4 * q + b;
-                if (f < N::F) w |= (4u * frow[j * RS + f] + 3u) << (8 * b);
-            }
-            tile[i] = w;
+            const uint32_t w = *reinterpret_cast<const uint32_t*>(frow + j * RS + 4 * q);
+            tile[i] = (w << 2) | 0x03030303u;
         }
-        // (4) chunk pipeline.  Iteration it: the loader brings the next chunk;
-        // walkers walk chunk it, write the leaf values of chunk it - 1 (held
-        // in registers since the last iteration) and fetch those of chunk it;
-        // the fold wave adds chunk it - 2.
+        // (4) chunk pipeline.  Iteration it: loaders bring chunk it + 1;
+        // walkers walk chunk it and write its leaf values (leaves gathered
+        // from global memory are written one iteration later); wave 0 folds
+        // chunk it - lag.
         float sc = 0.0f;
         uint32_t vprev[4] = {0u, 0u, 0u, 0u};
         int tprev[4] = {-1, -1, -1, -1};
-        for (int it = 0; it <= nck; ++it) {
+        for (int it = 0; it < nck + lag; ++it) {
             const int gc = r * nck + it;
-            if (wave == 1 && it < nck) __builtin_amdgcn_s_waitcnt(0);   // chunk it has landed
+            if (loader && it < nck) __builtin_amdgcn_s_waitcnt(0);   // chunk it has landed
             lds_barrier();
-            if (wave == 1) {
+            if (loader) {
                 if (!resident && it < nck && gc + 1 < total_chunks) {
                     const int x = (it + 1) % nck;
                     const int t0 = x * a.ct;
                     load_trees(a, ring + (size_t)((gc + 1) & 1) * a.ring_bytes, t0,
-                               (a.T - t0 < a.ct ? a.T - t0 : a.ct), lane);
+                               (a.T - t0 < a.ct ? a.T - t0 : a.ct), tid - 64 * (1 + nww), 64 * n_load_waves);
                 }
-            } else if (wave >= 2) {
-                uint32_t q[4];
-                int ti[4] = {-1, -1, -1, -1};
+            } else if (walker) {
                 const int t0 = it * a.ct;
                 const int nt = it < nck ? (a.T - t0 < a.ct ? a.T - t0 : a.ct) : 0;
-                uint32_t nb[4];
-                if (nt > 0) {
-                    // chunk it: resident trees sit at their own place, streamed
-                    // ones in buffer gc & 1
+                const int sp4 = (nt + 3) >> 2;
+                int ti[4] = {-1, -1, -1, -1};
+                uint32_t nb[4], q[4];
+                const bool walks = u < sp4;
+                if (walks) {
+                    // resident trees sit at their own place, streamed ones in buffer gc & 1
                     const uint32_t rb = a.off_ring + (resident ? (uint32_t)t0 * (uint32_t)a.ts * 4u
                                                                : (uint32_t)(gc & 1) * a.ring_bytes);
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const int tl = u + g * S;
+                        const int tl = u + g * sp4;
                         ti[g] = tl < nt ? tl : -1;
-                        nb[g] = rb + (uint32_t)(tl < nt ? tl : 0) * (uint32_t)a.ts * 4u;
+                        nb[g] = rb + (uint32_t)(tl < nt ? tl : u) * (uint32_t)a.ts * 4u;
                     }
                     walk4_local<DEPTH>(lds, nb, fb, q);
                 }
-                if (it > 0 && jw < nc) {
-                    float* lvk = lv + ((it - 1) & 1) * a.ct + jw * a.lv_stride;
-#pragma unroll
-                    for (int g = 0; g < 4; ++g)
-                        if (tprev[g] >= 0) lvk[tprev[g]] = __uint_as_float(vprev[g]);
-                }
-                if (nt > 0) {
-                    if (a.gather) {
-#pragma unroll
-                        for (int g = 0; g < 4; ++g) {
-                            const int tt = ti[g] >= 0 ? ti[g] : 0;
-                            vprev[g] = a.leaf_src[(size_t)(t0 + tt) * a.w16 + (NBB / 4) + q[g]];
-                        }
-                    } else {
+                if (a.gather) {
+                    // the leaf values gathered last iteration, then this chunk's
+                    if (it > 0 && jw < nc) {
+                        float* lvk = lv + ((it - 1) & 1) * a.ct + jw * a.lv_stride;
 #pragma unroll
                         for (int g = 0; g < 4; ++g)
-                            vprev[g] = *reinterpret_cast<const uint32_t*>(lds + nb[g] + NBB + 4u * q[g]);
+                            if (tprev[g] >= 0) lvk[tprev[g]] = __uint_as_float(vprev[g]);
+                    }
+                    if (walks) {
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int tt = ti[g] >= 0 ? ti[g] : u;
+                            vprev[g] = a.leaf_src[(size_t)(t0 + tt) * a.w16 + (NBB / 4) + q[g]];
+                        }
+                    }
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) tprev[g] = walks ? ti[g] : -1;
+                } else if (walks && jw < nc) {
+                    float* lvk = lv + (it & 1) * a.ct + jw * a.lv_stride;
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const uint32_t v = *reinterpret_cast<const uint32_t*>(lds + nb[g] + NBB + 4u * q[g]);
+                        if (ti[g] >= 0) lvk[ti[g]] = __uint_as_float(v);
                     }
                 }
-#pragma unroll
-                for (int g = 0; g < 4; ++g) tprev[g] = ti[g];
-            } else if (it >= 2 && lane < nc) {
-                // fold chunk it - 2 (a whole one), in tree order
-                const float* row = lv + lane * a.lv_stride + (it & 1) * a.ct;
-                for (int t = 0; t < a.ct; t += 4) {
-                    const float4 v4 = *reinterpret_cast<const float4*>(row + t);
-                    sc = sc + v4.x;
-                    sc = sc + v4.y;
-                    sc = sc + v4.z;
-                    sc = sc + v4.w;
+            } else {
+                if (it == 0 && owner && s + 1 < a.steps)
+                    with_space([&](const SpaceDesc& sd) {
+                        draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
+                    });
+                const int fc = it - lag;   // chunk to fold
+                if (fc >= 0 && lane < nc) {
+                    const int t0 = fc * a.ct;
+                    const int nt = a.T - t0 < a.ct ? a.T - t0 : a.ct;
+                    sc = fold_row(sc, lv + lane * a.lv_stride + (fc & 1) * a.ct, nt);
                 }
             }
         }
-        // the last chunk's leaf values are in place
-        lds_barrier();
-        if (wave == 0 && lane < nc) {
-            const int last = nck - 1;
-            const float* row = lv + lane * a.lv_stride + (last & 1) * a.ct;
-            const int nt = a.T - last * a.ct;
-            int t = 0;
-            for (; t + 4 <= nt; t += 4) {
-                const float4 v4 = *reinterpret_cast<const float4*>(row + t);
-                sc = sc + v4.x;
-                sc = sc + v4.y;
-                sc = sc + v4.z;
-                sc = sc + v4.w;
-            }
-            for (; t < nt; ++t) sc = sc + row[t];
-        }
-        // (5) offer to the best list, then the Metropolis test
-        uint64_t cfg = 0;
+        // (5) offer to the best list when some chain qualifies, then the
+        // Metropolis test
         if (owner) {
-            const SpaceDesc& sd = *sdp;
-#pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j)
-                if (j < sd.n_knobs) cfg += (uint64_t)cd[j] * sd.radix[j];
             ChainRec& R = rec[tid];
             const bool qual = is_init || (int)R.count < k || precedes(sc, cfg, R.kth_score, R.kth_cfg);
             R.cfg = cfg;
             R.score = sc;
             R.qual = qual ? 1u : 0u;
+            if (qual) atomicOr(&s_any[r & 1], 1u);
         }
+        if (tid == 0) s_any[(r + 1) & 1] = 0u;
         lds_barrier();
-        if (gj < cpb) group_offer(lists + gjc * k, rec[gjc], k, gr, gmask, gvalid && rec[gjc].qual != 0);
-        lds_barrier();
+        if (s_any[r & 1]) {
+            if (gj < cpb) group_offer(lists + gjc * k, rec[gjc], k, gr, gmask, gvalid && rec[gjc].qual != 0);
+            lds_barrier();
+        }
         if (owner) {
             bool acc = true;
             if (!is_init) {
@@ -422,6 +498,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
 #pragma unroll
                 for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
                 cur_s = sc;
+                cur_cfg = cfg;
             }
         }
     }
@@ -479,10 +556,12 @@ hipError_t launch_local_t(const LocalArgs& a, int depth, int grid, int threads, 
 int local_tree_stride(int words) { return words + ((1 - words) % 32 + 32) % 32; }
 
 // Plan of the chain-local path for a run, or false when it does not fit.
-// Workgroups of 512 threads: wave 0 folds and keeps the books, wave 1 loads
-// trees, waves 2-7 walk.  Chains per workgroup: the smallest divisor of 64
-// that leaves at most one workgroup per compute unit (at most 32).  A chunk
-// holds at most four trees per walk slot.
+// Workgroups of 512 threads: wave 0 folds and keeps the books, then walker
+// waves (a slot per chain and up to four trees per slot and chunk), then
+// loader waves.  Chains per workgroup: the smallest divisor of 64 that
+// leaves at most one workgroup per compute unit (at most 32).  A streamed
+// chunk leaves at least four loader waves when it can: one wave moves about
+// 8 bytes per clock from L2, a compute unit some 50-60.
 bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& ch, LocalPlan& pl) {
     const int64_t n = ch.n_chains;
     const int Q = (sp.descs[0].n_features + 3) / 4;
@@ -493,9 +572,9 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, ch.device);
     int cpb = 1;
     while (cpb < 32 && (n + cpb - 1) / cpb > n_cu) cpb *= 2;
-    const int threads = 512;
-    const int slots = (threads - 128) / cpb;
-    const int ct_cap = 4 * slots / 4 * 4;
+    const int threads = 512, waves = threads / 64;
+    // trees per chunk that w walker waves cover (four per slot), a multiple of 4
+    auto walk_cap = [&](int w) { return 4 * (w * 64 / cpb) / 4 * 4; };
     int fac_max = 0;
     for (const SpaceDesc& x : sp.descs) {
         int f = 0;
@@ -507,7 +586,7 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     auto al16 = [](size_t x) { return (x + 15) & ~(size_t)15; };
     const size_t tile = (size_t)Q * 256;
     const size_t fixed = al16((size_t)cpb * ch.topk * sizeof(at_entry)) + al16((size_t)cpb * sizeof(ChainRec)) +
-                         al16((size_t)cpb * RS) + al16(sizeof(SpaceDesc) + (size_t)fac_max * 8);
+                         al16((size_t)cpb * RS) + 16 + al16(sizeof(SpaceDesc) + (size_t)fac_max * 8);
     if (tile + fixed >= LOCAL_LDS_BYTES) return false;
     const size_t avail = LOCAL_LDS_BYTES - tile - fixed;
     const int ts_full = local_tree_stride(NB + NL), ts_nodes = local_tree_stride(NB);
@@ -518,9 +597,10 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     pl.grid = (int)((n + cpb - 1) / cpb);
     pl.off_ring = (uint32_t)tile;
     // resident: every tree in LDS, loaded once, walked in chunks of ct
-    const int ct_res = T <= ct_cap ? T : ct_cap;
+    const int cap_all = walk_cap(waves - 1);
+    const int ct_res = T <= cap_all ? T : cap_all;
     const size_t res_bytes = al16((size_t)T * ts_full * 4);
-    if (res_bytes + lv_bytes(ct_res) <= avail) {
+    if (cap_all >= 4 && res_bytes + lv_bytes(ct_res) <= avail) {
         pl.resident = 1;
         pl.gather = 0;
         pl.ts = ts_full;
@@ -539,12 +619,15 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
         const size_t per_tree = 8 * ((size_t)pl.ts + cpb);
         const size_t spare = avail > (size_t)cpb * 16 + 64 ? avail - (size_t)cpb * 16 - 64 : 0;
         int ct_max = (int)(spare / per_tree) / 4 * 4;
-        ct_max = ct_max < ct_cap ? ct_max : ct_cap;
+        const int cap = walk_cap(3) >= 16 ? walk_cap(3) : walk_cap(waves - 2);
+        ct_max = ct_max < cap ? ct_max : cap;
         if (ct_max < 4) return false;
         const int chunks = (T + ct_max - 1) / ct_max;
         pl.ct = ((T + chunks - 1) / chunks + 3) / 4 * 4;
         pl.ring_bytes = (uint32_t)al16((size_t)pl.ct * pl.ts * 4);
     }
+    pl.walk_waves = (pl.ct * cpb + 255) / 256;
+    if (pl.walk_waves > waves - 1) pl.walk_waves = waves - 1;
     pl.n_chunks = (T + pl.ct - 1) / pl.ct;
     pl.lv_stride = 2 * pl.ct + 4;
     size_t off = tile + (pl.resident ? 1 : 2) * (size_t)pl.ring_bytes;
@@ -556,6 +639,8 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     off += al16((size_t)cpb * sizeof(ChainRec));
     pl.off_frow = (uint32_t)off;
     off += al16((size_t)cpb * RS);
+    pl.off_any = (uint32_t)off;
+    off += 16;
     pl.off_desc = (uint32_t)off;
     off += al16(sizeof(SpaceDesc) + (size_t)fac_max * 8);
     pl.lds_bytes = off;
@@ -614,6 +699,8 @@ hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chain
     a.off_lists = pl.off_lists;
     a.off_rec = pl.off_rec;
     a.off_frow = pl.off_frow;
+    a.off_any = pl.off_any;
+    a.walk_waves = pl.walk_waves;
     a.off_desc = pl.off_desc;
     ch.events_used[0] = ch.events_used[1] = 0;
     hipEvent_t start = nullptr, stop = nullptr;
