@@ -55,6 +55,7 @@ def lib():
         L.or_philox.argtypes = [u64, vp, vp]
         L.or_philox.restype = None
         L.or_thresholds.argtypes = [u64, i64, i64, u64, i32, vp]
+        L.or_select_batch.argtypes = [vp, vp, i64, i32, i32, ctypes.c_float, i32, u64, vp]
         L.or_sa_run.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp, vp, u64, i64, i64, i32,
                                 i32, vp, i32, vp, vp, vp, vp, vp, vp]
         _lib = L
@@ -200,3 +201,15 @@ class Chains:
                              _p(self.top), _p(tr) if trace else None)
         _check(st, "sa_run")
         return tr
+
+
+def select_batch(space: Space, cand, pool: int, n_greedy: int, alpha: float, n_random: int, seed: int) -> np.ndarray:
+    """The batch to measure (Algorithm 1, Eq. 3): greedy picks from the top
+    `pool` distinct candidates, then `n_random` uniform configurations.
+    cand: TOP_DTYPE entries (any shape).  Returns n_greedy + n_random entries
+    (valid 1 greedy, 2 random, 0 empty)."""
+    c = np.ascontiguousarray(np.asarray(cand).reshape(-1).astype(TOP_DTYPE, copy=False))
+    out = np.zeros(n_greedy + n_random, dtype=TOP_DTYPE)
+    _check(lib().or_select_batch(space._h, _p(c), len(c), int(pool), int(n_greedy), float(alpha),
+                                 int(n_random), int(seed), _p(out)), "select_batch")
+    return out

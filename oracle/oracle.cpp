@@ -458,6 +458,88 @@ float score_config(const Space& sp, const Ensemble& e, uint64_t cfg) {
     return predict_row(e, row.data(), nullptr);
 }
 
+// ---------------------------------------------------------------------------
+// Picking the batch to measure (Algorithm 1 after the annealing; Section 3.3,
+// Eq. 3).  Q is the set of distinct configurations the chains keep.  From
+// the top `pool` of Q (the paper's top lambda*b, ordered by score, higher
+// first, then by index) a greedy submodular maximisation of
+//     L(S) = sum_{s in S} score(s) + alpha * sum_j |{ s_j : s in S }|
+// (Eq. 3 with score = -f_hat) picks n_greedy configurations one at a time:
+// each pick maximises the marginal gain L(S + {s}) - L(S), which is score(s)
+// plus alpha times the number of knobs j whose value s_j no pick in S has.
+// Readings: the gain is evaluated in fp32 as score + alpha * count (one
+// product, one sum); ties go to the earlier configuration in pool order.
+// Then epsilon-greedy: n_random configurations drawn uniformly among those of
+// S_e not yet selected; draw i uses Philox block (i, 0, 5, 0) under `seed`,
+// u = r1 * 2^32 + r0, and takes the floor(u * remaining / 2^64)-th
+// unselected configuration in index order.
+// ---------------------------------------------------------------------------
+// Writes n_greedy + n_random entries: greedy picks (flag 1) in pick order,
+// then random picks (flag 2, score 0); slots left empty have flag 0.
+void select_batch(const Space& sp, const TopEntry* cand, int64_t n_cand, int pool, int n_greedy, float alpha,
+                  int n_random, uint64_t seed, TopEntry* out) {
+    // Q: distinct valid configurations
+    std::vector<TopEntry> q;
+    for (int64_t i = 0; i < n_cand; ++i)
+        if (cand[i].valid) q.push_back(TopEntry{cand[i].cfg, cand[i].score, 1u});
+    std::sort(q.begin(), q.end(),
+              [](const TopEntry& a, const TopEntry& b) { return precedes(a.score, a.cfg, b.score, b.cfg); });
+    std::vector<TopEntry> distinct;
+    for (const TopEntry& e : q)
+        if (distinct.empty() || distinct.back().cfg != e.cfg) distinct.push_back(e);
+    // the top `pool` of Q
+    if ((int64_t)distinct.size() > pool) distinct.resize(pool);
+    const int m = (int)sp.knobs.size();
+    std::vector<std::vector<int64_t>> vals(distinct.size());
+    for (size_t i = 0; i < distinct.size(); ++i) decode(sp, distinct[i].cfg, vals[i]);
+    // greedy maximisation of L
+    std::vector<std::vector<int64_t>> covered(m);   // knob values already in S
+    std::vector<bool> taken(distinct.size(), false);
+    for (int i = 0; i < n_greedy + n_random; ++i) out[i] = TopEntry{0, 0.0f, 0u};
+    std::vector<uint64_t> selected;
+    int picks = 0;
+    for (int step = 0; step < n_greedy && step < (int)distinct.size(); ++step) {
+        int best = -1;
+        float best_gain = 0.0f;
+        for (size_t i = 0; i < distinct.size(); ++i) {
+            if (taken[i]) continue;
+            int fresh = 0;
+            for (int j = 0; j < m; ++j)
+                if (std::find(covered[j].begin(), covered[j].end(), vals[i][j]) == covered[j].end()) ++fresh;
+            float cov = alpha * (float)fresh;
+            float gain = distinct[i].score + cov;
+            if (best < 0 || gain > best_gain) {
+                best = (int)i;
+                best_gain = gain;
+            }
+        }
+        taken[best] = true;
+        for (int j = 0; j < m; ++j)
+            if (std::find(covered[j].begin(), covered[j].end(), vals[best][j]) == covered[j].end())
+                covered[j].push_back(vals[best][j]);
+        out[picks++] = TopEntry{distinct[best].cfg, distinct[best].score, 1u};
+        selected.push_back(distinct[best].cfg);
+    }
+    // epsilon-greedy: uniform over the configurations not selected yet
+    for (int i = 0; i < n_random; ++i) {
+        std::sort(selected.begin(), selected.end());
+        uint64_t remaining = sp.n_configs - (uint64_t)selected.size();
+        if (remaining == 0) break;
+        uint32_t r[4];
+        philox_block(seed, (uint32_t)i, 0u, 5u, 0u, r);
+        unsigned __int128 u = ((unsigned __int128)r[1] << 32) | r[0];
+        uint64_t k = (uint64_t)((u * remaining) >> 64);
+        // the k-th configuration (0-based, ascending) that is not selected
+        uint64_t cfg = k;
+        for (uint64_t x : selected) {
+            if (x <= cfg) ++cfg;
+            else break;
+        }
+        out[picks++] = TopEntry{cfg, 0.0f, 2u};
+        selected.push_back(cfg);
+    }
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -643,6 +725,15 @@ int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
         }
         for (int j = 0; j < nk; ++j) v[j] = cur[j];
     }
+    return 0;
+}
+
+// Batch selection (see select_batch): cand [n_cand] entries, out
+// [n_greedy + n_random] entries.
+int or_select_batch(void* h, const TopEntry* cand, int64_t n_cand, int pool, int n_greedy, float alpha,
+                    int n_random, uint64_t seed, TopEntry* out) {
+    if (!h || n_cand < 0 || pool < 0 || n_greedy < 0 || n_random < 0) return -1;
+    select_batch(*(Space*)h, cand, n_cand, pool, n_greedy, alpha, n_random, seed, out);
     return 0;
 }
 
