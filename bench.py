@@ -212,6 +212,24 @@ def bench_score(P, reps, warmup):
         predict_hbm_GBps=n * (176 * 4 + 4) / tp / 1e9)
 
 
+def bench_select(P, w, reps=20):
+    """Batch selection after an annealing run (Algorithm 1, Eq. 3) on the
+    run's best lists: the paper's batch b = 64 with epsilon = 0.05 (61
+    greedy picks, 3 random) from the top 2b = 128, alpha = 1."""
+    import torch
+    sp = w.spaces[0]
+    out = torch.zeros((64, 4), dtype=torch.int32, device="cuda")
+    fn = lambda r: P.at_select_batch(sp, w.best, 128, 61, 1.0, 3, 4000 + r, out)
+    for r in range(2):
+        fn(r)
+    torch.cuda.synchronize()
+    t = float(np.median(time_events(fn, reps)))
+    n_cand = w.best.numel() // 4
+    return dict(workload=f"{w.name}: best lists {w.n} x {w.topk}, pool 128, 61 greedy + 3 random, alpha 1",
+                candidates=n_cand, ms=t * 1e3, candidates_per_s=n_cand / t,
+                read_GBps=n_cand * 16 / t / 1e9)
+
+
 def cpu_baseline(name, budget_s):
     """The oracle (single-threaded C++) on the first chains of the workload."""
     import oracle
@@ -255,12 +273,15 @@ def main():
     head, r = bench_sa(P, args.workload, args.steps, args.warmup)
     extra = {}
     if not args.no_extra:
+        extra["select_" + args.workload] = bench_select(P, head)
         extra["conv_c2_score1m"] = bench_score(P, reps=5, warmup=1)
         for name in ["gemm512_sa", "conv_c12_sa", "resnet18_12conv_sa"]:
             if name == args.workload:
                 continue
             reps = 2 if name == "conv_c12_sa" else 3
-            _, extra[name] = bench_sa(P, name, reps, 1)
+            w, extra[name] = bench_sa(P, name, reps, 1)
+            if name == "conv_c12_sa":
+                extra["select_conv_c12_sa"] = bench_select(P, w)
     cpu = cpu_baseline(args.workload, args.cpu_budget)
     line = {
         "metric": METRIC,

@@ -199,6 +199,34 @@ at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int
 at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
                            const float* thr, at_entry* best, at_entry* trace, at_stream_t stream);
 
+/* Picks the batch of configurations to measure next (Algorithm 1 after the
+ * annealing; Section 3.3, Eq. 3, and the epsilon-greedy step).
+ * Q is the set of distinct configurations among the valid entries of cand;
+ * its `pool` best (score descending, then index ascending; the paper's top
+ * lambda*b) form the candidate set.  A greedy maximisation of
+ *   L(S) = sum_{s in S} score(s) + alpha * sum_j |{ s_j : s in S }|
+ * (score = -f_hat; s_j the value of knob j) then picks n_greedy of them one
+ * at a time, each maximising its marginal gain score(s) + alpha * (number of
+ * knobs whose value no earlier pick has), evaluated in fp32 as one product
+ * and one sum, ties going to the earlier candidate in pool order.  Last,
+ * n_random configurations are drawn uniformly among those of the space not
+ * selected yet: draw i takes Philox-4x32-10 block (i, 0, 5, 0) keyed by
+ * seed, u = r1 * 2^32 + r0, and the floor(u * remaining / 2^64)-th
+ * unselected index in ascending order.
+ * cand: device [n_cand] at_entry, for example the best lists written by
+ * at_sa_run ([n_chains][topk]); an index listed more than once must carry
+ * the same score each time (as best lists do).  out: device
+ * [n_greedy + n_random] at_entry: the greedy picks (flag 1) in pick order,
+ * then the random ones (flag 2, score 0); slots left over when the pool or
+ * the space runs out have flag 0.
+ * Limits: 0 <= pool <= 1024, n_greedy + n_random <= 2048, a single space
+ * (not a set) whose knobs have at most 65536 values each; AT_E_INVALID or
+ * AT_E_UNSUPPORTED otherwise.  Enqueued on `stream`; more than 4096
+ * candidates use stream-ordered device scratch (hipMallocAsync) for a
+ * partial reduction. */
+at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
+                          float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream);
+
 /* Execution path of the annealing runs of a chains handle. */
 typedef enum {
     AT_SA_PATH_AUTO = 0,   /* chosen per run from the ensemble and chain count */

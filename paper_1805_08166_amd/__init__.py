@@ -33,7 +33,7 @@ EXPORTED = [
     "at_extract_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_gbt_predict", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
-    "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_last_error",
+    "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_last_error",
 ]
 
 # at_sa_path
@@ -75,6 +75,7 @@ def _load():
         "at_chains_set_path": [vp, i32],
         "at_chains_last_path": [vp, vp],
         "at_chains_last_plan": [vp, vp],
+        "at_select_batch": [vp, vp, i64, i32, i32, ctypes.c_float, i32, u64, vp, vp],
         "at_last_error": [],
     }
     for name, args in sig.items():
@@ -265,6 +266,21 @@ def at_chains_last_plan(chains: Chains) -> dict:
     keys = ["chains_per_wg", "threads", "workgroups", "trees_per_chunk", "chunks", "gather", "lds_bytes",
             "stream_bytes_per_step"]
     return dict(zip(keys, (int(x) for x in v)))
+
+
+def at_select_batch(space: Space, cand, pool: int, n_greedy: int, alpha: float, n_random: int, seed: int, out,
+                    stream=None):
+    """cand: device int32 [..., 4] (at_entry, any leading shape); out: device
+    int32 [n_greedy + n_random, 4] (at_entry)."""
+    import torch
+    n_cand = cand.numel() // 4 if cand is not None else 0
+    if cand is not None and (cand.dtype != torch.int32 or cand.shape[-1] != 4 or not cand.is_contiguous()):
+        raise ValueError("cand must be a contiguous int32 [..., 4] at_entry tensor")
+    if out.shape != (n_greedy + n_random, 4):
+        raise ValueError("out must be [n_greedy + n_random, 4] int32")
+    _check("at_select_batch", _lib.at_select_batch(
+        space.h, _dev(cand, torch.int32, "cand") if n_cand else None, int(n_cand), int(pool), int(n_greedy),
+        float(alpha), int(n_random), int(seed), _dev(out, torch.int32, "out"), _stream(stream)))
 
 
 def at_sa_thresholds(seed: int, chain0: int, n_chains: int, step_base: int, steps: int) -> np.ndarray:

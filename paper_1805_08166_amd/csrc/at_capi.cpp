@@ -406,6 +406,26 @@ at_status at_sa_kernel_times(at_chains_t chains, double* tree_ms, int64_t* tree_
     return AT_OK;
 }
 
+at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
+                          float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream) {
+    if (!space) return fail(AT_E_INVALID, "at_select_batch: NULL space");
+    if (space->n_spaces != 1) return fail(AT_E_INVALID, "at_select_batch: takes a single space, not a set");
+    if (n_cand < 0 || pool < 0 || n_greedy < 0 || n_random < 0) return fail(AT_E_INVALID, "at_select_batch: negative size");
+    if (n_cand > 0 && !cand) return fail(AT_E_INVALID, "at_select_batch: NULL candidates");
+    if (pool > select_pool_max()) return fail(AT_E_UNSUPPORTED, "at_select_batch: pool above 1024");
+    if ((int64_t)n_greedy + n_random > select_pick_max()) return fail(AT_E_UNSUPPORTED, "at_select_batch: more than 2048 picks");
+    if (!std::isfinite(alpha)) return fail(AT_E_INVALID, "at_select_batch: alpha must be finite");
+    const SpaceDesc& d = space->descs[0];
+    for (int j = 0; j < d.n_knobs; ++j)
+        if (d.knob_size[j] > 65536u) return fail(AT_E_UNSUPPORTED, "at_select_batch: a knob has more than 65536 values");
+    if (n_greedy + n_random == 0) return AT_OK;
+    if (!out) return fail(AT_E_INVALID, "at_select_batch: NULL output");
+    if (n_cand > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, "at_select_batch: too many candidates");
+    DeviceGuard g(space->device);
+    return finish_launch(launch_select(*space, cand, n_cand, pool, n_greedy, alpha, n_random, seed, out,
+                                       (hipStream_t)stream), "at_select_batch");
+}
+
 at_status at_chains_set_path(at_chains_t chains, int path) {
     if (!chains) return fail(AT_E_INVALID, "at_chains_set_path: NULL chains");
     if (path != AT_SA_PATH_AUTO && path != AT_SA_PATH_TREES && path != AT_SA_PATH_LOCAL)

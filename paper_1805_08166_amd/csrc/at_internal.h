@@ -235,6 +235,12 @@ hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chain
 // kernel, 1: the chain kernel), or nulls when the chains are not profiled.
 hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t& stop);
 
+// Batch selection (at_select.hip).
+int select_pool_max();
+int select_pick_max();
+hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
+                         float alpha, int n_random, uint64_t seed, at_entry* out, hipStream_t stream);
+
 hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score,
                          hipStream_t stream);
 

@@ -71,6 +71,9 @@ def test_argument_errors_before_device_use(P):
     assert "depth" in P.lib().at_last_error().decode()
     assert P.lib().at_sa_set_profiling(None, 1) == INVALID
     assert P.lib().at_sa_kernel_times(None, None, None, None, None) == INVALID
+    assert P.lib().at_chains_set_path(None, 1) == INVALID
+    assert P.lib().at_chains_last_plan(None, None) == INVALID
+    assert P.lib().at_select_batch(None, None, 0, 4, 2, 1.0, 1, 0, None, None) == INVALID
 
 
 def bitlen(x):

@@ -104,3 +104,28 @@ def make_configs(n: int, n_configs: int, seed: int) -> np.ndarray:
 def chain_offsets(n_spaces: int, chains_per_space: int) -> np.ndarray:
     """Contiguous chain ranges per space: space w owns [w*c, (w+1)*c)."""
     return np.arange(n_spaces + 1, dtype=np.int64) * chains_per_space
+
+
+ENTRY_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("flag", "<u4")])
+
+
+def make_candidates(n_lists: int, per_list: int, n_configs: int, seed: int, dup_frac: float = 0.2,
+                    invalid_frac: float = 0.05) -> np.ndarray:
+    """Synthetic best lists [n_lists, per_list] of (cfg, score, flag) entries
+    for the batch selection: uniformly random configuration indices, a share
+    of them repeated across lists (with the same score, as a deterministic
+    model gives), a share of empty slots, scores float32(N(0, 1))."""
+    rng = np.random.default_rng(seed)
+    n = n_lists * per_list
+    base = rng.integers(0, n_configs, n, dtype=np.uint64)
+    rep = rng.random(n) < dup_frac
+    base[rep] = base[rng.integers(0, n, int(rep.sum()))]
+    uniq, inv = np.unique(base, return_inverse=True)
+    sc = rng.normal(0.0, 1.0, len(uniq)).astype(np.float32)
+    out = np.zeros(n, dtype=ENTRY_DTYPE)
+    out["cfg"] = base
+    out["score"] = sc[inv]
+    out["flag"] = (rng.random(n) >= invalid_frac).astype(np.uint32)
+    out["cfg"][out["flag"] == 0] = 0
+    out["score"][out["flag"] == 0] = 0.0
+    return out.reshape(n_lists, per_list)
