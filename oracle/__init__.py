@@ -55,6 +55,7 @@ def lib():
         L.or_philox.argtypes = [u64, vp, vp]
         L.or_philox.restype = None
         L.or_thresholds.argtypes = [u64, i64, i64, u64, i32, vp]
+        L.or_relation_features.argtypes = [vp, vp, i64, vp]
         L.or_select_batch.argtypes = [vp, vp, i64, i32, i32, ctypes.c_float, i32, u64, vp]
         L.or_sa_run.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp, vp, u64, i64, i64, i32,
                                 i32, vp, i32, vp, vp, vp, vp, vp, vp]
@@ -123,6 +124,17 @@ class Space:
         out = np.zeros(self.n_loops * 12, dtype=np.int64)
         _check(lib().or_loop_quantities(self._h, int(cfg), _p(out)), "loop_quantities")
         return out.reshape(self.n_loops, 12)
+
+    RELATION_THRESHOLDS = 32
+
+    def relation_features(self, cfgs) -> np.ndarray:
+        """Context relation features (Section 4, Appendix A.2): [n, 2, 3, 32]
+        flattened to [n, 192]: per pair (reuse, top-down) and buffer, the
+        largest bitlen over the loops touching fewer than 2^t elements."""
+        c = np.ascontiguousarray(cfgs, dtype=np.uint64)
+        out = np.zeros((len(c), 2 * 3 * self.RELATION_THRESHOLDS), dtype=np.int32)
+        _check(lib().or_relation_features(self._h, _p(c), len(c), _p(out)), "relation_features")
+        return out
 
     def features(self, cfgs) -> np.ndarray:
         c = np.ascontiguousarray(cfgs, dtype=np.uint64)

@@ -377,6 +377,48 @@ void features_of(const Space& sp, uint64_t cfg, int32_t* row) {
 int n_features_of(const Space& sp) { return (int)sp.loops.size() * (2 + 3 * (int)sp.buffers.size()); }
 
 // ---------------------------------------------------------------------------
+// Context relation features (Section 4; Appendix A.2 "Relation Feature").
+// Over the loops of the nest's longest chain (here the whole perfect nest),
+// with Z_ki the i-th context feature of loop k and log2-spaced thresholds
+// beta_t, R_t^(ij) = max over the loops k with Z_kj < beta_t of Z_ki.  The
+// two pairs of the appendix, per buffer b: reuse ratio against touch count,
+// and top-down against touch count.
+// Readings: beta_t = 2^t for t = 1..32; the maximised value is taken in the
+// same bitlen space as the loop features (bitlen of the reuse ratio, bitlen
+// of the top-down product); top-down is the product of the lengths of the
+// loops strictly outside loop k (1 for the outermost); a threshold that no
+// loop meets gives 0.  Row layout: [pair][buffer][t - 1], pair 0 the reuse
+// relation, pair 1 the top-down one.
+// ---------------------------------------------------------------------------
+const int REL_THRESHOLDS = 32;
+
+int n_relation_features_of(const Space& sp) { return 2 * (int)sp.buffers.size() * REL_THRESHOLDS; }
+
+void relation_features_of(const Space& sp, uint64_t cfg, int32_t* row) {
+    std::vector<int64_t> v;
+    decode(sp, cfg, v);
+    std::vector<LoopQ> q;
+    loop_quantities(sp, v, q);
+    const int n_loops = (int)q.size(), n_buf = (int)sp.buffers.size();
+    std::vector<int64_t> top_down(n_loops, 1);
+    for (int k = 1; k < n_loops; ++k) top_down[k] = top_down[k - 1] * q[k - 1].ext;
+    for (int b = 0; b < n_buf; ++b) {
+        for (int t = 1; t <= REL_THRESHOLDS; ++t) {
+            const int64_t beta = (int64_t)1 << t;
+            int32_t r_reuse = 0, r_top = 0;
+            for (int k = 0; k < n_loops; ++k) {
+                if (q[k].touched[b] < beta) {
+                    r_reuse = std::max(r_reuse, bitlen(q[k].reuse[b]));
+                    r_top = std::max(r_top, bitlen(top_down[k]));
+                }
+            }
+            row[(0 * n_buf + b) * REL_THRESHOLDS + (t - 1)] = r_reuse;
+            row[(1 * n_buf + b) * REL_THRESHOLDS + (t - 1)] = r_top;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Gradient-boosted tree ensemble (Section 3.1).  Full depth-d trees in heap
 // order: node n has children 2n+1 (taken when x[fid] < thr) and 2n+2.  The
 // prediction is the fp32 sum of the reached leaves, added one tree after the
@@ -724,6 +766,16 @@ int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
             step_abs[c] += 1;
         }
         for (int j = 0; j < nk; ++j) v[j] = cur[j];
+    }
+    return 0;
+}
+
+int or_relation_features(void* h, const uint64_t* cfgs, int64_t n, int32_t* feats) {
+    const Space& sp = *(Space*)h;
+    int F = n_relation_features_of(sp);
+    for (int64_t i = 0; i < n; ++i) {
+        if (cfgs[i] >= sp.n_configs) return -5;
+        relation_features_of(sp, cfgs[i], feats + i * F);
     }
     return 0;
 }
