@@ -201,6 +201,12 @@ def bench_score(P, reps, warmup):
     te = time_events(lambda r: P.at_extract_features(sp, cfgs, feats), reps)
     tp = time_events(lambda r: P.at_gbt_predict(ens, feats, scores), reps)
     te, tp = float(np.mean(te)), float(np.mean(tp))
+    # context relation features of the same configurations (192 int32 a row)
+    rel = torch.empty((n, P.RELATION_FEATURES), dtype=torch.int32, device="cuda")
+    P.at_extract_relation_features(sp, cfgs, rel)
+    tr = float(np.mean(time_events(lambda r: P.at_extract_relation_features(sp, cfgs, rel), reps)))
+    rel_bytes = n * (8 + P.RELATION_FEATURES * 4)
+    del rel
     feat_bytes = n * (8 + 176 * 4)              # cfg in, feature row out
     score_lds = n * wl["trees"] * tree_eval_bytes(wl["depth"])
     return dict(
@@ -209,7 +215,9 @@ def bench_score(P, reps, warmup):
         extract_hbm_frac=feat_bytes / te / HBM_PEAK_BPS,
         predict_ms=tp * 1e3, scores_per_s=n / tp, tree_evals_per_s=n * wl["trees"] / tp,
         predict_lds_TBps=score_lds / tp / 1e12, predict_lds_frac=score_lds / tp / LDS_PEAK_BPS,
-        predict_hbm_GBps=n * (176 * 4 + 4) / tp / 1e9)
+        predict_hbm_GBps=n * (176 * 4 + 4) / tp / 1e9,
+        relation_ms=tr * 1e3, relation_rows_per_s=n / tr, relation_hbm_GBps=rel_bytes / tr / 1e9,
+        relation_hbm_frac=rel_bytes / tr / HBM_PEAK_BPS)
 
 
 def bench_select(P, w, reps=20):

@@ -199,6 +199,21 @@ at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int
 at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
                            const float* thr, at_entry* best, at_entry* trace, at_stream_t stream);
 
+/* Context relation features (Section 4, "Context Relation Features for
+ * GBT"; Appendix A.2 "Relation Feature") of n configurations: the invariant
+ * representation the paper transfers across workloads.  Over the loops of
+ * the nest (a single chain here), with thresholds beta_t = 2^t, t = 1..32,
+ * per buffer b: R[0][b][t-1] = max over loops touching fewer than 2^t
+ * elements of b of bitlen(reuse ratio), R[1][b][t-1] = max over the same
+ * loops of bitlen(top-down), top-down being the product of the lengths of
+ * the loops outside; 0 when no loop qualifies.
+ * cfgs: device [n] uint64; feats: device [n][192] int32 row-major, buffers
+ * in the loop features' order, 16-byte aligned.  A configuration index
+ * outside [0, n_configs) gives a row of -1 and is counted as in
+ * at_extract_features.  Enqueued on `stream`. */
+at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                       at_stream_t stream);
+
 /* Picks the batch of configurations to measure next (Algorithm 1 after the
  * annealing; Section 3.3, Eq. 3, and the epsilon-greedy step).
  * Q is the set of distinct configurations among the valid entries of cand;

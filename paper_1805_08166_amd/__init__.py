@@ -30,7 +30,7 @@ ENTRY_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("flag", "<u4")])
 
 EXPORTED = [
     "at_space_create", "at_space_info", "at_spaceset_create", "at_space_destroy",
-    "at_extract_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
+    "at_extract_features", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_gbt_predict", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
     "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_last_error",
@@ -59,6 +59,7 @@ def _load():
         "at_spaceset_create": [vp, i32, vp, vp],
         "at_space_destroy": [vp],
         "at_extract_features": [vp, vp, i64, vp, vp],
+        "at_extract_relation_features": [vp, vp, i64, vp, vp],
         "at_space_errors": [vp, vp],
         "at_ensemble_create": [i32, i32, i32, vp, vp, vp, vp],
         "at_ensemble_destroy": [vp],
@@ -195,6 +196,19 @@ def at_extract_features(space: Space, cfgs, feats, stream=None):
     if feats.shape != (n, space.n_features):
         raise ValueError("feats must be [n, n_features]")
     _check("at_extract_features", _lib.at_extract_features(
+        space.h, _dev(cfgs, torch.int64, "cfgs"), n, _dev(feats, torch.int32, "feats"), _stream(stream)))
+
+
+RELATION_FEATURES = 192
+
+
+def at_extract_relation_features(space: Space, cfgs, feats, stream=None):
+    """cfgs: device uint64 [n] (torch.int64 storage); feats: device int32 [n, 192]."""
+    import torch
+    n = cfgs.numel()
+    if feats.shape != (n, RELATION_FEATURES):
+        raise ValueError("feats must be [n, 192]")
+    _check("at_extract_relation_features", _lib.at_extract_relation_features(
         space.h, _dev(cfgs, torch.int64, "cfgs"), n, _dev(feats, torch.int32, "feats"), _stream(stream)))
 
 

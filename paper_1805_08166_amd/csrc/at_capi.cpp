@@ -201,6 +201,20 @@ at_status at_extract_features(at_space_t space, const uint64_t* cfgs, int64_t n,
     return finish_launch(launch_extract(*space, cfgs, n, feats, (hipStream_t)stream), "at_extract_features");
 }
 
+at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                       at_stream_t stream) {
+    if (!space) return fail(AT_E_INVALID, "at_extract_relation_features: NULL space");
+    if (space->n_spaces != 1) return fail(AT_E_INVALID, "at_extract_relation_features: takes a single space, not a set");
+    if (n < 0) return fail(AT_E_INVALID, "at_extract_relation_features: n < 0");
+    if (n == 0) return AT_OK;
+    if (!cfgs || !feats) return fail(AT_E_INVALID, "at_extract_relation_features: NULL buffer");
+    if ((reinterpret_cast<uintptr_t>(feats) & 15u) != 0)
+        return fail(AT_E_INVALID, "at_extract_relation_features: feats must be 16-byte aligned");
+    if (n > ((int64_t)1 << 36)) return fail(AT_E_UNSUPPORTED, "at_extract_relation_features: n too large for one call");
+    DeviceGuard g(space->device);
+    return finish_launch(launch_relation(*space, cfgs, n, feats, (hipStream_t)stream), "at_extract_relation_features");
+}
+
 at_status at_space_errors(at_space_t space, uint64_t* n_out_of_range) {
     if (!space || !n_out_of_range) return fail(AT_E_INVALID, "at_space_errors: NULL argument");
     DeviceGuard g(space->device);

@@ -201,6 +201,8 @@ at_status build_space(int tmpl, const int64_t* shape, int nshape, SpaceDesc& des
 // Kernel launchers (at_kernels.hip).
 hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                           hipStream_t stream);
+hipError_t launch_relation(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                           hipStream_t stream);
 hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
                           uint16_t* leaves, hipStream_t stream);
 hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,

@@ -94,6 +94,102 @@ __global__ __launch_bounds__(WG) void k_extract(SpaceDesc sd, const uint64_t* __
 }
 
 // ==========================================================================
+// Context relation features (Section 4; Appendix A.2), one configuration per
+// lane.  Per buffer b and t = 1..REL_T, over the loops whose sub-nest
+// touches fewer than 2^t elements of b (bitlen(touch) <= t):
+//   R[0][b][t-1] = the largest bitlen(reuse ratio),
+//   R[1][b][t-1] = the largest bitlen(top-down product of the outer lengths),
+// 0 when no loop qualifies.  The loop quantities come from nest_features; the
+// rows go through LDS as bytes (odd dword stride) to coalesced int4 stores.
+// ==========================================================================
+constexpr int REL_T = 32;
+constexpr int REL_F = 2 * 3 * REL_T;        // 192 features per row
+constexpr int REL_RS = REL_F + 4;           // 49 dwords per LDS row
+
+template <int TMPL>
+__global__ __launch_bounds__(WG) void k_relation(SpaceDesc sd, const uint64_t* __restrict__ factors,
+                                                 const uint64_t* __restrict__ cfgs, int64_t n,
+                                                 int32_t* __restrict__ feats, unsigned long long* __restrict__ n_bad) {
+    using N = Nest<TMPL>;
+    __shared__ int8_t rows[WG * REL_RS];
+    const int tid = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * WG;
+    const int64_t row = base + tid;
+    int8_t* my = rows + tid * REL_RS;
+    if (row < n) {
+        const uint64_t cfg = cfgs[row];
+        if (cfg >= sd.n_configs) {
+            for (int f = 0; f < REL_F; ++f) my[f] = -1;
+            atomicAdd(n_bad, 1ull);
+        } else {
+            uint32_t rest = (uint32_t)cfg;
+            uint32_t kv[MAX_KNOBS];
+#pragma unroll
+            for (int j = MAX_KNOBS - 1; j >= 0; --j) {
+                if (j < sd.n_knobs) {
+                    const uint32_t sz = sd.knob_size[j];
+                    const uint32_t q = rest / sz;
+                    kv[j] = rest - q * sz;
+                    rest = q;
+                } else {
+                    kv[j] = 0u;
+                }
+            }
+            uint32_t fac[6][4];
+            gather_factors<TMPL>(sd, factors, kv, fac);
+            constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
+            // per loop: bitlen of the touch count (tc) and of the reuse ratio (ru) per buffer
+            uint32_t tc[N::L][3], ru[N::L][3];
+            nest_features<TMPL>(sd, fac, unroll_max_of(kv[A]), 1u + kv[A + 1], [&](int f, uint32_t v) {
+                const int p = f / 11, c = f - p * 11;
+                if (c >= 2 && (c - 2) % 3 == 0) tc[p][(c - 2) / 3] = v;
+                if (c >= 2 && (c - 2) % 3 == 1) ru[p][(c - 2) / 3] = v;
+            });
+            // bitlen of the top-down product of each loop (outer lengths only)
+            uint32_t td[N::L];
+            uint32_t prod = 1u;
+#pragma unroll
+            for (int p = 0; p < N::L; ++p) {
+                td[p] = bitlen(prod);
+                const uint32_t e = N::axis[p] == FUSED ? fac[4][N::level[p]] * fac[5][N::level[p]]
+                                                       : fac[N::axis[p]][N::level[p]];
+                prod *= e;
+            }
+#pragma unroll
+            for (int b = 0; b < 3; ++b) {
+#pragma unroll
+                for (int t = 1; t <= REL_T; ++t) {
+                    uint32_t r0 = 0u, r1 = 0u;
+#pragma unroll
+                    for (int p = 0; p < N::L; ++p) {
+                        const bool in = tc[p][b] <= (uint32_t)t;
+                        r0 = max(r0, in ? ru[p][b] : 0u);
+                        r1 = max(r1, in ? td[p] : 0u);
+                    }
+                    my[(0 * 3 + b) * REL_T + (t - 1)] = (int8_t)r0;
+                    my[(1 * 3 + b) * REL_T + (t - 1)] = (int8_t)r1;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    const int64_t rows_here = (n - base < WG) ? (n - base) : WG;
+    const int total = (int)rows_here * REL_F;
+    int32_t* out = feats + base * REL_F;
+    for (int g = tid; g < total / 4; g += WG) {
+        const int e = g * 4;
+        const int r = e / REL_F, c = e - r * REL_F;
+        const int w = *reinterpret_cast<const int*>(rows + r * REL_RS + c);
+        int4 v;
+        v.x = (int)(int8_t)(w & 0xff);
+        v.y = (int)(int8_t)((w >> 8) & 0xff);
+        v.z = (int)(int8_t)((w >> 16) & 0xff);
+        v.w = (int)(int8_t)((w >> 24) & 0xff);
+        *reinterpret_cast<int4*>(out + e) = v;
+    }
+}
+
+// ==========================================================================
 // Tree-ensemble traversal shared by scoring and annealing.
 // A workgroup holds the features of its 256 rows (chains or candidates) in
 // an LDS tile and streams the packed trees through LDS in chunks.  Each lane
@@ -213,6 +309,21 @@ hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n,
         hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, false>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs,
                            n, feats, bad);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_relation(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                           hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const SpaceDesc& sd = sp.descs[0];
+    const unsigned grid = (unsigned)((n + WG - 1) / WG);
+    const uint64_t* fac = static_cast<const uint64_t*>(sp.d_factors.p);
+    auto* bad = static_cast<unsigned long long*>(sp.d_errors.p);
+    if (sp.tmpl == AT_TMPL_GEMM)
+        hipLaunchKernelGGL((k_relation<AT_TMPL_GEMM>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs, n, feats, bad);
+    else
+        hipLaunchKernelGGL((k_relation<AT_TMPL_CONV2D_NCHW>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs, n,
+                           feats, bad);
     return hipGetLastError();
 }
 
