@@ -206,6 +206,11 @@ def bench_score(P, reps, warmup):
     P.at_extract_relation_features(sp, cfgs, rel)
     tr = float(np.mean(time_events(lambda r: P.at_extract_relation_features(sp, cfgs, rel), reps)))
     rel_bytes = n * (8 + P.RELATION_FEATURES * 4)
+    # Eq. 4: a 1000-tree global model on the relation features plus the
+    # workload's local model on the loop features
+    glob = P.at_ensemble_create(*W.make_ensemble(wl["trees"], wl["depth"], P.RELATION_FEATURES, wl["ens_seed"] + 50),
+                                P.RELATION_FEATURES)
+    tg = float(np.mean(time_events(lambda r: P.at_gbt_predict_global_local(glob, rel, ens, feats, scores), reps)))
     del rel
     feat_bytes = n * (8 + 176 * 4)              # cfg in, feature row out
     score_lds = n * wl["trees"] * tree_eval_bytes(wl["depth"])
@@ -217,7 +222,9 @@ def bench_score(P, reps, warmup):
         predict_lds_TBps=score_lds / tp / 1e12, predict_lds_frac=score_lds / tp / LDS_PEAK_BPS,
         predict_hbm_GBps=n * (176 * 4 + 4) / tp / 1e9,
         relation_ms=tr * 1e3, relation_rows_per_s=n / tr, relation_hbm_GBps=rel_bytes / tr / 1e9,
-        relation_hbm_frac=rel_bytes / tr / HBM_PEAK_BPS)
+        relation_hbm_frac=rel_bytes / tr / HBM_PEAK_BPS,
+        global_local_ms=tg * 1e3, global_local_scores_per_s=n / tg,
+        global_local_lds_frac=2 * score_lds / tg / LDS_PEAK_BPS)
 
 
 def bench_select(P, w, reps=20):

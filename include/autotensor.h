@@ -139,6 +139,17 @@ void at_ensemble_destroy(at_ensemble_t ens);
 at_status at_gbt_predict(at_ensemble_t ens, const int32_t* feats, int64_t n, float* scores,
                          uint16_t* leaves, at_stream_t stream);
 
+/* Transfer model of Section 4, Eq. 4: f_hat(x) = f_hat_global(x) +
+ * f_hat_local(x).  Each model's prediction is its own fp32 left fold over its
+ * trees (as at_gbt_predict); scores[i] = fp32(global_i + local_i), global
+ * first.  The two models may read different feature rows, for instance the
+ * invariant context relation features for the global model and the loop
+ * features for the local one.  feats_global: device [n][F_global] int32;
+ * feats_local: device [n][F_local] int32; scores: device [n] float.
+ * Enqueued on `stream` (two launches). */
+at_status at_gbt_predict_global_local(at_ensemble_t global, const int32_t* feats_global, at_ensemble_t local,
+                                      const int32_t* feats_local, int64_t n, float* scores, at_stream_t stream);
+
 /* Persistent state of n_chains Markov chains (Section 3.3: chain states
  * persist across model updates): current knob values and score, absolute
  * step counter and a best list of the topk highest-scoring distinct

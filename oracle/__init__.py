@@ -159,6 +159,15 @@ def predict(fid, thr, leaf, feats, want_leaves=False):
     return (scores, leaves) if want_leaves else scores
 
 
+def predict_global_local(global_model, feats_global, local_model, feats_local):
+    """Eq. 4 (Section 4): f_hat = f_hat_global + f_hat_local.  Each model's
+    score is its own fp32 left fold over its trees (predict); the two are
+    added once in fp32, the global one first.  A model is (fid, thr, leaf)."""
+    g = predict(*global_model, feats_global)
+    l = predict(*local_model, feats_local)
+    return (g + l).astype(np.float32)
+
+
 def philox(seed: int, ctr) -> np.ndarray:
     c = np.ascontiguousarray(ctr, dtype=np.uint32)
     out = np.zeros(4, dtype=np.uint32)

@@ -31,7 +31,7 @@ ENTRY_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("flag", "<u4")])
 EXPORTED = [
     "at_space_create", "at_space_info", "at_spaceset_create", "at_space_destroy",
     "at_extract_features", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
-    "at_gbt_predict", "at_chains_create", "at_chains_destroy", "at_chains_step",
+    "at_gbt_predict", "at_gbt_predict_global_local", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
     "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_last_error",
 ]
@@ -64,6 +64,7 @@ def _load():
         "at_ensemble_create": [i32, i32, i32, vp, vp, vp, vp],
         "at_ensemble_destroy": [vp],
         "at_gbt_predict": [vp, vp, i64, vp, vp, vp],
+        "at_gbt_predict_global_local": [vp, vp, vp, vp, i64, vp, vp],
         "at_chains_create": [vp, i64, i64, i32, u64, vp],
         "at_chains_destroy": [vp],
         "at_chains_step": [vp, vp],
@@ -246,6 +247,17 @@ def at_gbt_predict(ens: Ensemble, feats, scores, leaves=None, stream=None):
     _check("at_gbt_predict", _lib.at_gbt_predict(
         ens.h, _dev(feats, torch.int32, "feats"), n, _dev(scores, torch.float32, "scores"),
         _dev(leaves, torch.int16, "leaves"), _stream(stream)))
+
+
+def at_gbt_predict_global_local(glob: Ensemble, feats_global, local: Ensemble, feats_local, scores, stream=None):
+    """Eq. 4: scores = global(feats_global) + local(feats_local), device tensors."""
+    import torch
+    n = scores.numel()
+    if feats_global.shape != (n, glob.n_features) or feats_local.shape != (n, local.n_features):
+        raise ValueError("shape mismatch")
+    _check("at_gbt_predict_global_local", _lib.at_gbt_predict_global_local(
+        glob.h, _dev(feats_global, torch.int32, "feats_global"), local.h, _dev(feats_local, torch.int32, "feats_local"),
+        n, _dev(scores, torch.float32, "scores"), _stream(stream)))
 
 
 def at_chains_create(space: Space, chain0: int, n_chains: int, topk: int, seed: int) -> Chains:

@@ -330,7 +330,22 @@ at_status at_gbt_predict(at_ensemble_t ens, const int32_t* feats, int64_t n, flo
     if (!feats || !scores) return fail(AT_E_INVALID, "at_gbt_predict: NULL buffer");
     if (n > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, "at_gbt_predict: n too large");
     DeviceGuard g(ens->device);
-    return finish_launch(launch_predict(ens->desc, feats, n, scores, leaves, (hipStream_t)stream), "at_gbt_predict");
+    return finish_launch(launch_predict(ens->desc, feats, n, scores, leaves, false, (hipStream_t)stream),
+                         "at_gbt_predict");
+}
+
+at_status at_gbt_predict_global_local(at_ensemble_t global, const int32_t* feats_global, at_ensemble_t local,
+                                      const int32_t* feats_local, int64_t n, float* scores, at_stream_t stream) {
+    if (!global || !local) return fail(AT_E_INVALID, "at_gbt_predict_global_local: NULL ensemble");
+    if (global->device != local->device) return fail(AT_E_INVALID, "at_gbt_predict_global_local: ensembles on different devices");
+    if (n < 0) return fail(AT_E_INVALID, "at_gbt_predict_global_local: n < 0");
+    if (n == 0) return AT_OK;
+    if (!feats_global || !feats_local || !scores) return fail(AT_E_INVALID, "at_gbt_predict_global_local: NULL buffer");
+    if (n > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, "at_gbt_predict_global_local: n too large");
+    DeviceGuard g(global->device);
+    hipError_t e = launch_predict(global->desc, feats_global, n, scores, nullptr, false, (hipStream_t)stream);
+    if (e == hipSuccess) e = launch_predict(local->desc, feats_local, n, scores, nullptr, true, (hipStream_t)stream);
+    return finish_launch(e, "at_gbt_predict_global_local");
 }
 
 at_status at_chains_create(at_space_t space, int64_t chain0, int64_t n_chains, int topk, uint64_t seed,

@@ -203,10 +203,11 @@ hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n,
                           hipStream_t stream);
 hipError_t launch_relation(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                            hipStream_t stream);
+// accumulate: add to scores (fp32, the stored value first) instead of storing
 hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
-                          uint16_t* leaves, hipStream_t stream);
+                          uint16_t* leaves, bool accumulate, hipStream_t stream);
 hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
-                        uint16_t* leaves, hipStream_t stream);
+                        uint16_t* leaves, bool accumulate, hipStream_t stream);
 hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
                         bool init, const float* thr, at_entry* best, at_entry* trace,
                         hipStream_t stream);

@@ -243,7 +243,7 @@ constexpr int CHUNK_BYTES = 32768;
 template <int DEPTH>
 __global__ __launch_bounds__(WG) void k_predict(EnsembleDesc e, const int32_t* __restrict__ feats, int64_t n,
                                                 float* __restrict__ scores, uint16_t* __restrict__ leaves,
-                                                int chunk_trees) {
+                                                int chunk_trees, int accumulate) {
     extern __shared__ uint32_t lds[];
     const int Q = (e.n_features + 3) / 4;
     uint32_t* tile = lds;
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(WG) void k_predict(EnsembleDesc e, const int32_t* _
     }
     uint16_t* lrow = (leaves && row < n) ? leaves + row * e.n_trees : nullptr;
     const float s = score_tile<DEPTH>(e, tile, chunk, chunk_trees, lrow);
-    if (row < n) scores[row] = s;
+    if (row < n) scores[row] = accumulate ? scores[row] + s : s;
 }
 
 __global__ __launch_bounds__(WG) void k_export(const SpaceDesc* descs, const int64_t* offsets, int n_spaces,
@@ -331,7 +331,7 @@ namespace {
 
 template <int DEPTH>
 hipError_t predict_depth(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores, uint16_t* leaves,
-                         hipStream_t stream) {
+                         bool accumulate, hipStream_t stream) {
     const int Q = (e.n_features + 3) / 4;
     const int ct = chunk_trees_for(DEPTH, CHUNK_BYTES);
     const size_t lds = (size_t)Q * WG * 4 + (size_t)ct * (2 << DEPTH) * 4;
@@ -339,31 +339,33 @@ hipError_t predict_depth(const EnsembleDesc& e, const int32_t* feats, int64_t n,
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (err != hipSuccess) return err;
     const unsigned grid = (unsigned)((n + WG - 1) / WG);
-    hipLaunchKernelGGL((k_predict<DEPTH>), dim3(grid), dim3(WG), lds, stream, e, feats, n, scores, leaves, ct);
+    hipLaunchKernelGGL((k_predict<DEPTH>), dim3(grid), dim3(WG), lds, stream, e, feats, n, scores, leaves, ct,
+                       accumulate ? 1 : 0);
     return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
-                          uint16_t* leaves, hipStream_t stream) {
+                          uint16_t* leaves, bool accumulate, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    // conv2d rows (176 features, 16-byte aligned) take the tuned kernel
-    if (e.n_features == 176 && (reinterpret_cast<uintptr_t>(feats) & 15u) == 0)
-        return launch_score(e, feats, n, scores, leaves, stream);
+    // conv2d loop-feature rows (176) and relation-feature rows (192), 16-byte
+    // aligned, take the tuned kernel
+    if ((e.n_features == 176 || e.n_features == 192) && (reinterpret_cast<uintptr_t>(feats) & 15u) == 0)
+        return launch_score(e, feats, n, scores, leaves, accumulate, stream);
     switch (e.depth) {
-        case 1: return predict_depth<1>(e, feats, n, scores, leaves, stream);
-        case 2: return predict_depth<2>(e, feats, n, scores, leaves, stream);
-        case 3: return predict_depth<3>(e, feats, n, scores, leaves, stream);
-        case 4: return predict_depth<4>(e, feats, n, scores, leaves, stream);
-        case 5: return predict_depth<5>(e, feats, n, scores, leaves, stream);
-        case 6: return predict_depth<6>(e, feats, n, scores, leaves, stream);
-        case 7: return predict_depth<7>(e, feats, n, scores, leaves, stream);
-        case 8: return predict_depth<8>(e, feats, n, scores, leaves, stream);
-        case 9: return predict_depth<9>(e, feats, n, scores, leaves, stream);
-        case 10: return predict_depth<10>(e, feats, n, scores, leaves, stream);
-        case 11: return predict_depth<11>(e, feats, n, scores, leaves, stream);
-        case 12: return predict_depth<12>(e, feats, n, scores, leaves, stream);
+        case 1: return predict_depth<1>(e, feats, n, scores, leaves, accumulate, stream);
+        case 2: return predict_depth<2>(e, feats, n, scores, leaves, accumulate, stream);
+        case 3: return predict_depth<3>(e, feats, n, scores, leaves, accumulate, stream);
+        case 4: return predict_depth<4>(e, feats, n, scores, leaves, accumulate, stream);
+        case 5: return predict_depth<5>(e, feats, n, scores, leaves, accumulate, stream);
+        case 6: return predict_depth<6>(e, feats, n, scores, leaves, accumulate, stream);
+        case 7: return predict_depth<7>(e, feats, n, scores, leaves, accumulate, stream);
+        case 8: return predict_depth<8>(e, feats, n, scores, leaves, accumulate, stream);
+        case 9: return predict_depth<9>(e, feats, n, scores, leaves, accumulate, stream);
+        case 10: return predict_depth<10>(e, feats, n, scores, leaves, accumulate, stream);
+        case 11: return predict_depth<11>(e, feats, n, scores, leaves, accumulate, stream);
+        case 12: return predict_depth<12>(e, feats, n, scores, leaves, accumulate, stream);
         default: return hipErrorInvalidValue;
     }
 }

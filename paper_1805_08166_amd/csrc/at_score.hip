@@ -1,4 +1,5 @@
-// Batched ensemble scoring for conv2d feature rows (176 features).
+// Batched ensemble scoring for conv2d feature rows: 176 loop-context
+// features or 192 context relation features (44 or 48 feature quads).
 //
 // One candidate per lane, 256 per workgroup.  LDS holds one chunk of packed
 // tree words (8 KB, 32 KB for depth 12) followed by the workgroup's feature
@@ -15,7 +16,6 @@ namespace {
 using namespace dev;
 
 constexpr int SWG = 256;
-constexpr int SQ = 44;   // feature quads of a conv2d row
 
 template <int DEPTH> struct ScoreShape {
     static constexpr int W = 2 << DEPTH;                       // words per tree
@@ -51,10 +51,14 @@ __device__ __forceinline__ void walk_add_rest(const uint8_t* L, int t, int r, ui
     if constexpr (H > 1) walk_add_rest<DEPTH, H / 2, LEAVES>(L, t, r, fb, acc, lrow, t0);
 }
 
-template <int DEPTH, bool LEAVES>
+// SQ: feature quads of a row (44 or 48); accumulate: add the score to the
+// value already in scores (fp32, that value first) instead of storing it.
+template <int DEPTH, bool LEAVES, int SQ>
 __global__ __launch_bounds__(SWG) void k_score(EnsembleDesc e, const int32_t* __restrict__ feats, int64_t n,
-                                               float* __restrict__ scores, uint16_t* __restrict__ leaves) {
+                                               float* __restrict__ scores, uint16_t* __restrict__ leaves,
+                                               int accumulate) {
     using S = ScoreShape<DEPTH>;
+    constexpr int PK = SQ % 11 == 0 ? 11 : 12;   // quads loaded together
     constexpr uint32_t TB = (uint32_t)S::W * 4u;
     __shared__ uint32_t lds[S::CW + SQ * SWG];
     const uint8_t* L = reinterpret_cast<const uint8_t*>(lds);
@@ -77,12 +81,12 @@ __global__ __launch_bounds__(SWG) void k_score(EnsembleDesc e, const int32_t* __
         const int4* fr = reinterpret_cast<const int4*>(feats + r * (SQ * 4));
         uint32_t packed[SQ];
 #pragma unroll
-        for (int h = 0; h < SQ; h += 11) {
-            int4 v[11];
+        for (int h = 0; h < SQ; h += PK) {
+            int4 v[PK];
 #pragma unroll
-            for (int q = 0; q < 11; ++q) v[q] = fr[h + q];
+            for (int q = 0; q < PK; ++q) v[q] = fr[h + q];
 #pragma unroll
-            for (int q = 0; q < 11; ++q) {
+            for (int q = 0; q < PK; ++q) {
                 const uint32_t b0 = (uint32_t)min(max(v[q].x, 0), 255), b1 = (uint32_t)min(max(v[q].y, 0), 255);
                 const uint32_t b2 = (uint32_t)min(max(v[q].z, 0), 255), b3 = (uint32_t)min(max(v[q].w, 0), 255);
                 packed[h + q] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
@@ -123,38 +127,47 @@ __global__ __launch_bounds__(SWG) void k_score(EnsembleDesc e, const int32_t* __
             if constexpr (S::G > 1) walk_add_rest<DEPTH, S::G / 2, LEAVES>(L, t, nt - t, fb, acc, lrow, t0);
         }
     }
-    if (row < n) scores[row] = acc;
+    if (row < n) scores[row] = accumulate ? scores[row] + acc : acc;
+}
+
+template <int DEPTH, int SQ>
+hipError_t score_q(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores, uint16_t* leaves,
+                   bool accumulate, hipStream_t stream) {
+    const unsigned grid = (unsigned)((n + SWG - 1) / SWG);
+    if (leaves)
+        hipLaunchKernelGGL((k_score<DEPTH, true, SQ>), dim3(grid), dim3(SWG), 0, stream, e, feats, n, scores, leaves,
+                           accumulate ? 1 : 0);
+    else
+        hipLaunchKernelGGL((k_score<DEPTH, false, SQ>), dim3(grid), dim3(SWG), 0, stream, e, feats, n, scores, leaves,
+                           accumulate ? 1 : 0);
+    return hipGetLastError();
 }
 
 template <int DEPTH>
 hipError_t score_depth(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores, uint16_t* leaves,
-                       hipStream_t stream) {
-    const unsigned grid = (unsigned)((n + SWG - 1) / SWG);
-    if (leaves)
-        hipLaunchKernelGGL((k_score<DEPTH, true>), dim3(grid), dim3(SWG), 0, stream, e, feats, n, scores, leaves);
-    else
-        hipLaunchKernelGGL((k_score<DEPTH, false>), dim3(grid), dim3(SWG), 0, stream, e, feats, n, scores, leaves);
-    return hipGetLastError();
+                       bool accumulate, hipStream_t stream) {
+    if (e.n_features == 192) return score_q<DEPTH, 48>(e, feats, n, scores, leaves, accumulate, stream);
+    return score_q<DEPTH, 44>(e, feats, n, scores, leaves, accumulate, stream);
 }
 
 }  // namespace
 
 hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores, uint16_t* leaves,
-                        hipStream_t stream) {
+                        bool accumulate, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     switch (e.depth) {
-        case 1: return score_depth<1>(e, feats, n, scores, leaves, stream);
-        case 2: return score_depth<2>(e, feats, n, scores, leaves, stream);
-        case 3: return score_depth<3>(e, feats, n, scores, leaves, stream);
-        case 4: return score_depth<4>(e, feats, n, scores, leaves, stream);
-        case 5: return score_depth<5>(e, feats, n, scores, leaves, stream);
-        case 6: return score_depth<6>(e, feats, n, scores, leaves, stream);
-        case 7: return score_depth<7>(e, feats, n, scores, leaves, stream);
-        case 8: return score_depth<8>(e, feats, n, scores, leaves, stream);
-        case 9: return score_depth<9>(e, feats, n, scores, leaves, stream);
-        case 10: return score_depth<10>(e, feats, n, scores, leaves, stream);
-        case 11: return score_depth<11>(e, feats, n, scores, leaves, stream);
-        case 12: return score_depth<12>(e, feats, n, scores, leaves, stream);
+        case 1: return score_depth<1>(e, feats, n, scores, leaves, accumulate, stream);
+        case 2: return score_depth<2>(e, feats, n, scores, leaves, accumulate, stream);
+        case 3: return score_depth<3>(e, feats, n, scores, leaves, accumulate, stream);
+        case 4: return score_depth<4>(e, feats, n, scores, leaves, accumulate, stream);
+        case 5: return score_depth<5>(e, feats, n, scores, leaves, accumulate, stream);
+        case 6: return score_depth<6>(e, feats, n, scores, leaves, accumulate, stream);
+        case 7: return score_depth<7>(e, feats, n, scores, leaves, accumulate, stream);
+        case 8: return score_depth<8>(e, feats, n, scores, leaves, accumulate, stream);
+        case 9: return score_depth<9>(e, feats, n, scores, leaves, accumulate, stream);
+        case 10: return score_depth<10>(e, feats, n, scores, leaves, accumulate, stream);
+        case 11: return score_depth<11>(e, feats, n, scores, leaves, accumulate, stream);
+        case 12: return score_depth<12>(e, feats, n, scores, leaves, accumulate, stream);
         default: return hipErrorInvalidValue;
     }
 }

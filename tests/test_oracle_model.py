@@ -149,3 +149,46 @@ def test_thresholds_use_the_step_blocks_third_word():
     # same global chain at T = 1 holds the same value
     big = oracle.thresholds(seed, c0 - 2, 6, base, 9)
     assert (big[2:5, 0] == thr[:, 0]).all()
+
+
+# --------------------------------------------------------------------------
+# Eq. 4: global + local model
+# --------------------------------------------------------------------------
+def single_tree_model(leaves):
+    """Depth-1 stumps on feature 0 with threshold 0: every row (x >= 0)
+    reaches leaf 1, so the prediction is the fold of leaves[t][1]."""
+    T = len(leaves)
+    fid = np.zeros((T, 1), np.uint8)
+    thr = np.zeros((T, 1), np.uint8)
+    leaf = np.zeros((T, 2), np.float32)
+    leaf[:, 1] = leaves
+    return fid, thr, leaf
+
+
+def test_global_local_is_a_sum_of_two_folds():
+    """Each model folds its own trees and the two results are added once:
+    global (1e8, 1) folds to 1e8 (1e8 + 1 rounds back), local (-1e8, 1) to
+    -1e8, so the sum is 0; one fold over the concatenated trees would give 1."""
+    x = np.zeros((3, 4), np.int32)
+    g = single_tree_model([1e8, 1.0])
+    l = single_tree_model([-1e8, 1.0])
+    got = oracle.predict_global_local(g, x, l, x)
+    assert (got == 0.0).all()
+    both = single_tree_model([1e8, 1.0, -1e8, 1.0])
+    assert (oracle.predict(*both, x) == 1.0).all()
+
+
+def test_global_local_special_cases():
+    rng = np.random.default_rng(5)
+    fid, thr, leaf = workloads.make_ensemble(40, 5, 20, 17)
+    feats = rng.integers(0, 33, (300, 20)).astype(np.int32)
+    g = oracle.predict(fid, thr, leaf, feats)
+    zero = (fid, thr, np.zeros_like(leaf))
+    assert np.array_equal(oracle.predict_global_local((fid, thr, leaf), feats, zero, feats), g + np.float32(0.0))
+    neg = (fid, thr, -leaf)
+    assert (oracle.predict_global_local((fid, thr, leaf), feats, neg, feats) == 0.0).all()
+    # different feature sets for the two models
+    fid2, thr2, leaf2 = workloads.make_ensemble(25, 3, 7, 18)
+    f2 = rng.integers(0, 33, (300, 7)).astype(np.int32)
+    want = (g.astype(np.float64) + oracle.predict(fid2, thr2, leaf2, f2)).astype(np.float32)
+    assert np.array_equal(oracle.predict_global_local((fid, thr, leaf), feats, (fid2, thr2, leaf2), f2), want)
