@@ -317,7 +317,7 @@ def main():
                      "kernel": (f"{r['walk_kernel']} ({r['path']} path: "
                                 + ("one launch runs every step" if r["path"] == "chain-local"
                                    else "tree walk of one annealing step") + ")"),
-                     "achieved": r["tree_lds_TBps"], "peak": LDS_PEAK_BPS / 1e12, "unit": "TB/s",
+                     "achieved": r["tree_lds_TBps"] * 1e3, "peak": LDS_PEAK_BPS / 1e9, "unit": "GB/s",
                      "frac": r["tree_lds_frac"], "traffic": committed_traffic(r["walk_kernel"], args.workload),
                      "launch_us": r["tree_kernel_us"],
                      "per_unit": f"{tree_eval_bytes(head.wl['depth'])} B LDS per tree evaluation, "
