@@ -75,17 +75,26 @@ struct LocalArgs {
     uint32_t off_lists, off_rec, off_frow, off_any, off_desc;
 };
 
-// Leaf indices of four trees for this lane: nb holds the LDS byte offsets
+// Leaf indices of four trees for this lane: nb holds the LDS byte addresses
 // of the trees' node blocks (per lane), fb the lane's tile column.  The
 // levels are those of the tree kernel's walk (five vector instructions per
 // level and tree); trees are independent, so their LDS round trips overlap.
+// The reads are issued with absolute LDS addresses from inline asm (the
+// compiler would add the dynamic LDS base to every address) and waited for
+// in the same statement.
 template <int DEPTH>
-__device__ __forceinline__ void walk4_local(const uint8_t* __restrict__ L, const uint32_t (&nb)[4], uint32_t fb,
-                                            uint32_t (&q)[4]) {
+__device__ __forceinline__ void walk4_local(const uint32_t (&nb)[4], uint32_t fb, uint32_t (&q)[4]) {
     uint32_t node[4], p[4], fa[4], pa[4];
+    asm volatile(
+        "ds_read_u16 %0, %4\n\t"
+        "ds_read_u16 %1, %5\n\t"
+        "ds_read_u16 %2, %6\n\t"
+        "ds_read_u16 %3, %7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(node[0]), "=&v"(node[1]), "=&v"(node[2]), "=&v"(node[3])
+        : "v"(nb[0]), "v"(nb[1]), "v"(nb[2]), "v"(nb[3]));
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-        node[g] = *reinterpret_cast<const uint16_t*>(L + nb[g]);
         p[g] = 1u;
         fa[g] = (node[g] & LOCAL_TILE_MASK) | fb;
         pa[g] = nb[g] + 4u;
@@ -93,11 +102,19 @@ __device__ __forceinline__ void walk4_local(const uint8_t* __restrict__ L, const
 #pragma unroll
     for (int l = 0; l + 1 < DEPTH; ++l) {
         uint32_t x4[4], pr[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            x4[g] = L[fa[g]];
-            pr[g] = *reinterpret_cast<const uint32_t*>(L + pa[g]);
-        }
+        asm volatile(
+            "ds_read_u8 %0, %8\n\t"
+            "ds_read_b32 %4, %12\n\t"
+            "ds_read_u8 %1, %9\n\t"
+            "ds_read_b32 %5, %13\n\t"
+            "ds_read_u8 %2, %10\n\t"
+            "ds_read_b32 %6, %14\n\t"
+            "ds_read_u8 %3, %11\n\t"
+            "ds_read_b32 %7, %15\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(x4[0]), "=&v"(x4[1]), "=&v"(x4[2]), "=&v"(x4[3]), "=&v"(pr[0]), "=&v"(pr[1]), "=&v"(pr[2]),
+              "=&v"(pr[3])
+            : "v"(fa[0]), "v"(fa[1]), "v"(fa[2]), "v"(fa[3]), "v"(pa[0]), "v"(pa[1]), "v"(pa[2]), "v"(pa[3]));
         const uint32_t mask = LOCAL_TILE_MASK;
         asm(AT_WALK4_ASM
             : "+v"(node[0]), "+v"(node[1]), "+v"(node[2]), "+v"(node[3]), "+v"(p[0]), "+v"(p[1]), "+v"(p[2]),
@@ -107,11 +124,17 @@ __device__ __forceinline__ void walk4_local(const uint8_t* __restrict__ L, const
               "s"(mask), "v"(fb), "v"(nb[0]), "v"(nb[1]), "v"(nb[2]), "v"(nb[3])
             : "vcc");
     }
+    uint32_t x4[4];
+    asm volatile(
+        "ds_read_u8 %0, %4\n\t"
+        "ds_read_u8 %1, %5\n\t"
+        "ds_read_u8 %2, %6\n\t"
+        "ds_read_u8 %3, %7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(x4[0]), "=&v"(x4[1]), "=&v"(x4[2]), "=&v"(x4[3])
+        : "v"(fa[0]), "v"(fa[1]), "v"(fa[2]), "v"(fa[3]));
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        const uint32_t x4 = L[fa[g]];
-        q[g] = 2u * p[g] + (x4 >= (node[g] & 0xffu) ? 1u : 0u) - (1u << DEPTH);
-    }
+    for (int g = 0; g < 4; ++g) q[g] = 2u * p[g] + (x4[g] >= (node[g] & 0xffu) ? 1u : 0u) - (1u << DEPTH);
 }
 
 // Issues the direct-to-LDS loads of trees [t0, t0 + nt) of the local form
@@ -210,6 +233,10 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     SpaceDesc& s_desc = *reinterpret_cast<SpaceDesc*>(lds + a.off_desc);
     uint64_t* s_fac = reinterpret_cast<uint64_t*>(lds + a.off_desc + sizeof(SpaceDesc));
 
+    // LDS address of the dynamic block (0: the kernel has no static LDS, as
+    // the launcher checks); the walk's and-or of node bits and the lane's
+    // tile column needs the tile at a 16 KB boundary
+    const uint32_t lbase = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)lds;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int nthreads = (int)blockDim.x;
     const int cpb = a.cpb;
@@ -306,7 +333,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     const int wi = tid - 64;
     const int jw = lane % cpb;
     const int u = (walker ? wi : 0) / cpb;
-    const uint32_t fb = (uint32_t)lane * 4u;
+    const uint32_t fb = lbase | (uint32_t)lane * 4u;
     const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
     const uint32_t gchain = (uint32_t)(a.chain0 + (uint64_t)c);
     // the owner's next threshold and move, ready one round ahead
@@ -418,15 +445,15 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                 const bool walks = u < sp4;
                 if (walks) {
                     // resident trees sit at their own place, streamed ones in buffer gc & 1
-                    const uint32_t rb = a.off_ring + (resident ? (uint32_t)t0 * (uint32_t)a.ts * 4u
-                                                               : (uint32_t)(gc & 1) * a.ring_bytes);
+                    const uint32_t rb = lbase + a.off_ring + (resident ? (uint32_t)t0 * (uint32_t)a.ts * 4u
+                                                                       : (uint32_t)(gc & 1) * a.ring_bytes);
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         const int tl = u + g * sp4;
                         ti[g] = tl < nt ? tl : -1;
                         nb[g] = rb + (uint32_t)(tl < nt ? tl : u) * (uint32_t)a.ts * 4u;
                     }
-                    walk4_local<DEPTH>(lds, nb, fb, q);
+                    walk4_local<DEPTH>(nb, fb, q);
                 }
                 if (a.gather) {
                     // the leaf values gathered last iteration, then this chunk's
@@ -449,7 +476,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                     float* lvk = lv + (it & 1) * a.ct + jw * a.lv_stride;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const uint32_t v = *reinterpret_cast<const uint32_t*>(lds + nb[g] + NBB + 4u * q[g]);
+                        const uint32_t v = *reinterpret_cast<const uint32_t*>(lds + (nb[g] - lbase) + NBB + 4u * q[g]);
                         if (ti[g] >= 0) lvk[ti[g]] = __uint_as_float(v);
                     }
                 }
@@ -535,7 +562,13 @@ hipError_t launch_local_t(const LocalArgs& a, int depth, int grid, int threads, 
     }
     static bool configured[13] = {};
     if (!configured[depth]) {
-        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)LOCAL_LDS_BYTES);
+        // the walk addresses the tile with an and-or, which needs the
+        // dynamic LDS block at address 0: no static LDS in the kernel
+        hipFuncAttributes fa;
+        hipError_t e = hipFuncGetAttributes(&fa, fn);
+        if (e != hipSuccess) return e;
+        if (fa.sharedSizeBytes != 0) return hipErrorInvalidKernelFile;
+        e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)LOCAL_LDS_BYTES);
         if (e != hipSuccess) return e;
         configured[depth] = true;
     }
