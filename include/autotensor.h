@@ -272,9 +272,11 @@ at_status at_chains_last_path(at_chains_t chains, int* path);
 /* Launch plan of the last chain-local run (measurement aid; zeros when the
  * last run took the other path): info[0] chains per workgroup, [1] threads
  * per workgroup, [2] workgroups, [3] trees per chunk, [4] chunks streamed
- * per step (0: the ensemble stays resident in LDS), [5] 1 when leaves are read from
- * global memory rather than streamed, [6] dynamic LDS bytes, [7] bytes one
- * workgroup streams per step. */
+ * per step (0: nothing is streamed), [5] how leaves are reached: 0 from LDS
+ * (whole trees resident or streamed), 1 streamed node blocks with leaves
+ * read from global memory, 2 tree tops resident in LDS with the last level
+ * and its leaves read from global memory, [6] dynamic LDS bytes, [7] bytes
+ * one workgroup reads per step from outside its LDS. */
 at_status at_chains_last_plan(at_chains_t chains, int64_t info[8]);
 
 /* Copies the chains' current configuration indices (device [n_chains]

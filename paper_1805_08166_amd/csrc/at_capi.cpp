@@ -289,6 +289,28 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
         std::memcpy(local_full.data() + t * ts_full, words16.data() + t * W16, W16 * 4);
         std::memcpy(local_nodes.data() + t * ts_nodes, words16.data() + t * W16, NB * 4);
     }
+    // split form: tops (levels 0 .. d-2) and last-level records
+    const size_t top_words = depth >= 2 ? NB / 2 : 1;
+    const size_t ts_top = (size_t)local_tree_stride((int)top_words);
+    std::vector<uint32_t> local_top;
+    std::vector<uint32_t> tail;
+    try {
+        local_top.assign((size_t)n_trees * ts_top + 4, 0u);
+        tail.assign((size_t)n_trees * NB * 4, 0u);
+    } catch (...) {
+        return fail(AT_E_OOM, "at_ensemble_create: host allocation");
+    }
+    for (size_t t = 0; t < (size_t)n_trees && depth >= 2; ++t) {
+        std::memcpy(local_top.data() + t * ts_top, words16.data() + t * W16, top_words * 4);
+        for (size_t j = 0; j < NB; ++j) {
+            // last-level node m = 2^(d-1) + j (1-based heap); leaves 2m, 2m+1
+            const size_t m = NB + j;
+            uint32_t* r = tail.data() + (t * NB + j) * 4;
+            r[0] = node16(fid[t * n_int + m - 1], thr[t * n_int + m - 1]);
+            std::memcpy(&r[1], &leaf[t * n_leaf + 2 * m - n_leaf], 4);
+            std::memcpy(&r[2], &leaf[t * n_leaf + 2 * m + 1 - n_leaf], 4);
+        }
+    }
     at_ensemble_s* e = new (std::nothrow) at_ensemble_s();
     if (!e) return fail(AT_E_OOM, "at_ensemble_create: host allocation");
     e->device = current_device();
@@ -296,6 +318,8 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     if (st == AT_OK) st = upload(e->d_words16, words16.data(), words16.size());
     if (st == AT_OK) st = upload(e->d_local_full, local_full.data(), local_full.size());
     if (st == AT_OK) st = upload(e->d_local_nodes, local_nodes.data(), local_nodes.size());
+    if (st == AT_OK) st = upload(e->d_local_top, local_top.data(), local_top.size());
+    if (st == AT_OK) st = upload(e->d_tail, tail.data(), tail.size());
     if (st != AT_OK) {
         at_ensemble_destroy(e);
         return st;
@@ -308,6 +332,8 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     e->desc.words16 = static_cast<const uint32_t*>(e->d_words16.p);
     e->desc.local_full = static_cast<const uint32_t*>(e->d_local_full.p);
     e->desc.local_nodes = static_cast<const uint32_t*>(e->d_local_nodes.p);
+    e->desc.local_top = static_cast<const uint32_t*>(e->d_local_top.p);
+    e->desc.tail = static_cast<const uint4*>(e->d_tail.p);
     *out = e;
     return AT_OK;
 }
@@ -319,6 +345,8 @@ void at_ensemble_destroy(at_ensemble_t ens) {
     release(ens->d_words16);
     release(ens->d_local_full);
     release(ens->d_local_nodes);
+    release(ens->d_local_top);
+    release(ens->d_tail);
     delete ens;
 }
 
@@ -527,8 +555,8 @@ static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t ch
                        : launch_sa_tp(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "at_sa_run");
     chains->last_path = path;
-    const int64_t plan[8] = {pl.cpb, pl.threads, pl.grid, pl.ct, pl.resident ? 0 : pl.n_chunks, pl.gather,
-                             (int64_t)pl.lds_bytes, (int64_t)pl.round_bytes};
+    const int64_t plan[8] = {pl.cpb, pl.threads, pl.grid, pl.ct, (pl.resident || pl.tail) ? 0 : pl.n_chunks,
+                             pl.tail ? 2 : pl.gather, (int64_t)pl.lds_bytes, (int64_t)pl.round_bytes};
     for (int i = 0; i < 8; ++i) chains->last_plan[i] = path == AT_SA_PATH_LOCAL ? plan[i] : 0;
     chains->initialised = true;
     chains->step_abs += (uint64_t)steps;

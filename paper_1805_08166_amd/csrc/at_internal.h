@@ -70,6 +70,13 @@ struct EnsembleDesc {
     // (local_nodes); zero padded, plus 16 bytes of slack at the end.
     const uint32_t* local_full;
     const uint32_t* local_nodes;
+    // Split form for walks whose top levels stay in LDS: local_top holds the
+    // first 2^(d-2) words of each compact node block (levels 0 .. d-2) at an
+    // odd word stride; tail holds per tree and last-level node m (2^(d-1)
+    // of them) a 16-byte record {node m's 16-bit node, its left leaf, its
+    // right leaf, 0}.  Depth 2 and above.
+    const uint32_t* local_top;
+    const uint4* tail;
 };
 
 // Largest threshold the compact form keeps; annealing features never exceed
@@ -155,6 +162,8 @@ struct at_ensemble_s {
     at::DeviceBuf d_words16;
     at::DeviceBuf d_local_full;
     at::DeviceBuf d_local_nodes;
+    at::DeviceBuf d_local_top;
+    at::DeviceBuf d_tail;
 };
 
 struct at_chains_s {
@@ -222,6 +231,7 @@ struct LocalPlan {
     int ct = 0;               // trees per chunk
     int n_chunks = 0;         // chunks walked per step
     int resident = 0;         // 1: every tree stays in LDS, loaded once
+    int tail = 0;             // 1: tree tops resident in LDS, last level and leaves gathered
     uint32_t ring_bytes = 0;
     int walk_waves = 0;       // waves 1 .. walk_waves walk, later ones load
     uint32_t off_ring = 0, off_lv = 0, off_lists = 0, off_rec = 0, off_frow = 0, off_any = 0, off_desc = 0;

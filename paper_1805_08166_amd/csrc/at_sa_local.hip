@@ -65,6 +65,8 @@ struct LocalArgs {
     int n_chunks;
     int resident;             // the ring holds every tree (loaded once); else two chunk buffers
     int walk_waves;           // waves 1 .. walk_waves walk; later waves load
+    int tail;                 // tops resident (local_top), last level and leaves from the tail records
+    const uint4* tail_rec;    // [T][2^(d-1)] records {node, left leaf, right leaf, 0}
     int gather;               // leaves from global memory (leaf_src) instead of the ring
     const uint32_t* leaf_src; // compact form: leaves of tree t at leaf_src[t * w16 + 2^(d-1) + q]
     int w16;
@@ -316,7 +318,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     }
     if (tid < 2) s_any[tid] = 0u;
     const int rounds = (a.init ? 1 : 0) + a.steps;
-    const bool resident = a.resident != 0;
+    const bool resident = a.resident != 0 || a.tail != 0;
     const int nck = a.n_chunks;
     const int total_chunks = rounds * nck;
     const int lag = a.gather ? 2 : 1;   // chunks between a walk and the fold of its leaf values
@@ -418,11 +420,52 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             const uint32_t w = *reinterpret_cast<const uint32_t*>(frow + j * RS + 4 * q);
             tile[i] = (w << 2) | 0x03030303u;
         }
+        float sc = 0.0f;
+        if (a.tail) {
+            // (4') every tree of every chain in one pass: the resident top
+            // levels from LDS, then the last level and its leaf from the
+            // tree's 16-byte tail record; thread t takes chain t % cpb and
+            // trees u, u + S, u + 2S, u + 3S (S = threads / cpb)
+            if (owner && s + 1 < a.steps)
+                with_space([&](const SpaceDesc& sd) {
+                    draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
+                });
+            lds_barrier();
+            const int S = nthreads / cpb;
+            const int ua = tid / cpb;
+            const int ja = tid & (cpb - 1);
+            const uint32_t fba = lbase | (uint32_t)lane * 4u;
+            for (int base = 0; base < a.T; base += 4 * S) {
+                uint32_t nb[4], q[4];
+                int ti[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int t = base + ua + g * S;
+                    ti[g] = t < a.T ? t : -1;
+                    nb[g] = lbase + a.off_ring + (uint32_t)(t < a.T ? t : 0) * (uint32_t)a.ts * 4u;
+                }
+                walk4_local<(DEPTH >= 2 ? DEPTH - 1 : 1)>(nb, fba, q);
+                uint4 rec4[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int t = ti[g] >= 0 ? ti[g] : 0;
+                    rec4[g] = a.tail_rec[((size_t)t << (DEPTH - 1)) + q[g]];
+                }
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const uint32_t node = rec4[g].x;
+                    const uint32_t x4 = lds[((node & LOCAL_TILE_MASK) | fba) - lbase];
+                    const uint32_t v = x4 >= (node & 0xffu) ? rec4[g].z : rec4[g].y;
+                    if (ti[g] >= 0 && ja < nc) lv[ja * a.lv_stride + ti[g]] = __uint_as_float(v);
+                }
+            }
+            lds_barrier();
+            if (wave == 0 && lane < nc) sc = fold_row(sc, lv + lane * a.lv_stride, a.T);
+        } else {
         // (4) chunk pipeline.  Iteration it: loaders bring chunk it + 1;
         // walkers walk chunk it and write its leaf values (leaves gathered
         // from global memory are written one iteration later); wave 0 folds
         // chunk it - lag.
-        float sc = 0.0f;
         uint32_t vprev[4] = {0u, 0u, 0u, 0u};
         int tprev[4] = {-1, -1, -1, -1};
         for (int it = 0; it < nck + lag; ++it) {
@@ -492,6 +535,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                     sc = fold_row(sc, lv + lane * a.lv_stride + (fc & 1) * a.ct, nt);
                 }
             }
+        }
         }
         // (5) offer to the best list when some chain qualifies, then the
         // Metropolis test
@@ -633,12 +677,26 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     const int cap_all = walk_cap(waves - 1);
     const int ct_res = T <= cap_all ? T : cap_all;
     const size_t res_bytes = al16((size_t)T * ts_full * 4);
+    // tail: the tree tops (levels 0 .. d-2) resident, every tree walked in
+    // one pass with the last level and leaf read from the tail records;
+    // needs one row of leaf values per chain for all trees
+    const int ts_top = local_tree_stride(d >= 2 ? NB / 2 : 1);
+    const size_t top_bytes = al16((size_t)T * ts_top * 4);
+    const int T4 = (T + 3) / 4 * 4;
+    const size_t lv_all = al16((size_t)cpb * ((size_t)T4 + 4) * 4);
     if (cap_all >= 4 && res_bytes + lv_bytes(ct_res) <= avail) {
         pl.resident = 1;
         pl.gather = 0;
         pl.ts = ts_full;
         pl.ct = ct_res;
         pl.ring_bytes = (uint32_t)res_bytes;
+    } else if (d >= 2 && top_bytes + lv_all <= avail) {
+        pl.tail = 1;
+        pl.resident = 0;
+        pl.gather = 0;
+        pl.ts = ts_top;
+        pl.ct = T;
+        pl.ring_bytes = (uint32_t)top_bytes;
     } else {
         // streamed in chunks through two buffers.  Leaves are gathered from
         // global memory when that moves fewer bytes per round than streaming
@@ -662,10 +720,10 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     pl.walk_waves = (pl.ct * cpb + 255) / 256;
     if (pl.walk_waves > waves - 1) pl.walk_waves = waves - 1;
     pl.n_chunks = (T + pl.ct - 1) / pl.ct;
-    pl.lv_stride = 2 * pl.ct + 4;
-    size_t off = tile + (pl.resident ? 1 : 2) * (size_t)pl.ring_bytes;
+    pl.lv_stride = pl.tail ? T4 + 4 : 2 * pl.ct + 4;
+    size_t off = tile + ((pl.resident || pl.tail) ? 1 : 2) * (size_t)pl.ring_bytes;
     pl.off_lv = (uint32_t)off;
-    off += lv_bytes(pl.ct);
+    off += pl.tail ? lv_all : lv_bytes(pl.ct);
     pl.off_lists = (uint32_t)off;
     off += al16((size_t)cpb * ch.topk * sizeof(at_entry));
     pl.off_rec = (uint32_t)off;
@@ -678,7 +736,9 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     off += al16(sizeof(SpaceDesc) + (size_t)fac_max * 8);
     pl.lds_bytes = off;
     // streamed bytes per round and workgroup, for the path choice
-    pl.round_bytes = pl.resident ? 0.0 : (double)T * pl.ts * 4 + (pl.gather ? (double)cpb * T * 64 : 0.0);
+    pl.round_bytes = pl.resident ? 0.0
+                   : pl.tail ? (double)cpb * T * 64
+                             : (double)T * pl.ts * 4 + (pl.gather ? (double)cpb * T * 64 : 0.0);
     return pl.lds_bytes <= LOCAL_LDS_BYTES;
 }
 
@@ -716,12 +776,14 @@ hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chain
     a.thr = thr;
     a.trace = trace;
     a.best = best;
-    a.tw = pl.gather ? e.local_nodes : e.local_full;
+    a.tw = pl.tail ? e.local_top : (pl.gather ? e.local_nodes : e.local_full);
     a.ts = pl.ts;
     a.T = e.n_trees;
     a.ct = pl.ct;
     a.n_chunks = pl.n_chunks;
     a.resident = pl.resident;
+    a.tail = pl.tail;
+    a.tail_rec = e.tail;
     a.gather = pl.gather;
     a.leaf_src = e.words16;
     a.w16 = 3 << (e.depth - 1);

@@ -452,11 +452,14 @@ def test_sa_paths_agree_and_interleave(P):
 
 
 # chain-local plans: resident ensemble, streamed whole trees, streamed node
-# blocks with leaves from global memory; each checked against the oracle
+# blocks with leaves from global memory, resident tree tops with the last
+# level from global memory; each checked against the oracle
 LOCAL_PLANS = {
     "resident": dict(n=48, trees=40, depth=6, steps=30),
-    "streamed": dict(n=8192, trees=300, depth=8, steps=6),
+    "streamed": dict(n=8192, trees=1000, depth=8, steps=4),
     "gathered": dict(n=64, trees=400, depth=9, steps=20),
+    "tail": dict(n=300, trees=300, depth=8, steps=25),
+    "tail_depth2": dict(n=1024, trees=2000, depth=2, steps=15),
 }
 
 
@@ -473,8 +476,8 @@ def test_sa_local_plans_match_oracle(P, mode):
     ch = mk_chains(P, sp, 0, n, k, seed, "local")
     best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     plan = P.at_chains_last_plan(ch)
-    assert (plan["chunks"] == 0) == (mode == "resident")
-    assert plan["gather"] == (1 if mode == "gathered" else 0)
+    assert (plan["chunks"] == 0) == (mode in ("resident", "tail", "tail_depth2"))
+    assert plan["gather"] == {"gathered": 1, "tail": 2, "tail_depth2": 2}.get(mode, 0)
     rows = slice(0, min(n, 160))
     m = rows.stop
     och = oracle.Chains([osp], [0, m], seed=seed, chain0=0, topk=k)
