@@ -394,6 +394,8 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int TREES_MAX = 16;          // trees per workgroup
 constexpr int TREE_WAVES_MAX = 16;
+// the last 16 bytes of the tree kernel's LDS hold its block counter
+constexpr uint32_t TREE_LDS_FREE = (uint32_t)MAX_LDS_BYTES - 16u;
 
 struct TreeArgs {
     const uint32_t* words16;   // compact ensemble
@@ -468,21 +470,133 @@ __device__ __forceinline__ void walk16(const uint8_t* __restrict__ L, const uint
     }
 }
 
+// Reads of one level for four trees: the feature byte of each tree's node
+// and the word holding its pair of children.  Operand numbers are those of
+// AT_WALK4_ASM (8-11 feature address, 12-15 pair address, 16-19 x4, 20-23
+// pr).
+#define AT_ISSUE4_ASM                                                                                      \
+    "ds_read_u8 %16, %8\n\t"                                                                               \
+    "ds_read_b32 %20, %12\n\t"                                                                             \
+    "ds_read_u8 %17, %9\n\t"                                                                               \
+    "ds_read_b32 %21, %13\n\t"                                                                             \
+    "ds_read_u8 %18, %10\n\t"                                                                              \
+    "ds_read_b32 %22, %14\n\t"                                                                             \
+    "ds_read_u8 %19, %11\n\t"                                                                              \
+    "ds_read_b32 %23, %15"
+
+// walk16 for eight trees and DEPTH >= 2 as two software-pipelined groups of
+// four (A = trees 0-3, B = trees 4-7).  Each group's step waits for its own
+// reads (LDS answers in issue order, so lgkmcnt(8) leaves just the other
+// group's eight in flight), computes the level, and at once issues the reads
+// of its next level; the other group's reads are served meanwhile.  The
+// reads live across asm statements, so the registers that receive them are
+// handed from one statement to the next as in-out operands and nothing else
+// touches them in between.  The last internal level reads the feature byte
+// together with the 8-byte pair of leaves (leaves 2(p - 2^(DEPTH-1)) and
+// +1), so the leaf needs no further round trip.  The asm takes offsets into
+// L as LDS addresses: L is the kernel's only LDS object, so it starts at
+// LDS address 0 (the launcher checks that the kernel's static LDS is that
+// array alone).
+template <int DEPTH>
+__device__ __forceinline__ void walk8_roll(const uint8_t* __restrict__ L, const uint32_t (&nb)[8],
+                                           const uint32_t (&lb)[8], uint32_t fb, uint32_t mask,
+                                           uint32_t (&out)[8]) {
+    static_assert(DEPTH >= 2, "two or more levels");
+    uint32_t node[8], p[8], fa[8], pa[8], x4[8], pr[8];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        node[g] = *reinterpret_cast<const uint16_t*>(L + nb[g]);
+        p[g] = 1u;
+        fa[g] = (node[g] & mask) | fb;
+        pa[g] = nb[g] + 4u;
+    }
+#pragma unroll
+    for (int h = 0; h < 8; h += 4)
+        asm volatile(AT_ISSUE4_ASM
+                     : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
+                       "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "+v"(fa[h]), "+v"(fa[h + 1]),
+                       "+v"(fa[h + 2]), "+v"(fa[h + 3]), "+v"(pa[h]), "+v"(pa[h + 1]), "+v"(pa[h + 2]),
+                       "+v"(pa[h + 3]), "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]),
+                       "=&v"(pr[h]), "=&v"(pr[h + 1]), "=&v"(pr[h + 2]), "=&v"(pr[h + 3])
+                     :
+                     : "memory");
+#pragma unroll
+    for (int l = 0; l + 2 < DEPTH; ++l) {
+#pragma unroll
+        for (int h = 0; h < 8; h += 4)
+            asm volatile("s_waitcnt lgkmcnt(8)\n\t" AT_WALK4_ASM "\n\t" AT_ISSUE4_ASM
+                         : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
+                           "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "=&v"(fa[h]), "=&v"(fa[h + 1]),
+                           "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]), "=&v"(pa[h + 2]),
+                           "=&v"(pa[h + 3]), "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]),
+                           "+v"(pr[h]), "+v"(pr[h + 1]), "+v"(pr[h + 2]), "+v"(pr[h + 3])
+                         : "s"(mask), "v"(fb), "s"(nb[h]), "s"(nb[h + 1]), "s"(nb[h + 2]), "s"(nb[h + 3])
+                         : "vcc");
+    }
+    // last pair level, then the feature byte and leaf pair of the last
+    // internal node
+    uint64_t lp[8];
+#pragma unroll
+    for (int h = 0; h < 8; h += 4) {
+        asm volatile("s_waitcnt lgkmcnt(8)\n\t" AT_WALK4_ASM
+                     : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
+                       "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "=&v"(fa[h]), "=&v"(fa[h + 1]),
+                       "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]), "=&v"(pa[h + 2]),
+                       "=&v"(pa[h + 3])
+                     : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"(pr[h]), "v"(pr[h + 1]),
+                       "v"(pr[h + 2]), "v"(pr[h + 3]), "s"(mask), "v"(fb), "s"(nb[h]), "s"(nb[h + 1]),
+                       "s"(nb[h + 2]), "s"(nb[h + 3])
+                     : "vcc");
+        uint32_t la[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) la[g] = lb[h + g] - (8u << (DEPTH - 1)) + 8u * p[h + g];
+        asm volatile(
+            "ds_read_u8 %0, %8\n\t"
+            "ds_read_b64 %4, %12\n\t"
+            "ds_read_u8 %1, %9\n\t"
+            "ds_read_b64 %5, %13\n\t"
+            "ds_read_u8 %2, %10\n\t"
+            "ds_read_b64 %6, %14\n\t"
+            "ds_read_u8 %3, %11\n\t"
+            "ds_read_b64 %7, %15"
+            : "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]), "=&v"(lp[h]), "=&v"(lp[h + 1]),
+              "=&v"(lp[h + 2]), "=&v"(lp[h + 3])
+            : "v"(fa[h]), "v"(fa[h + 1]), "v"(fa[h + 2]), "v"(fa[h + 3]), "v"(la[0]), "v"(la[1]), "v"(la[2]),
+              "v"(la[3]));
+    }
+    asm volatile("s_waitcnt lgkmcnt(8)"
+                 : "+v"(x4[0]), "+v"(x4[1]), "+v"(x4[2]), "+v"(x4[3]), "+v"(lp[0]), "+v"(lp[1]), "+v"(lp[2]),
+                   "+v"(lp[3]));
+#pragma unroll
+    for (int g = 0; g < 4; ++g) out[g] = x4[g] >= (node[g] & 0xffu) ? (uint32_t)(lp[g] >> 32) : (uint32_t)lp[g];
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(x4[4]), "+v"(x4[5]), "+v"(x4[6]), "+v"(x4[7]), "+v"(lp[4]), "+v"(lp[5]), "+v"(lp[6]),
+                   "+v"(lp[7]));
+#pragma unroll
+    for (int g = 4; g < 8; ++g) out[g] = x4[g] >= (node[g] & 0xffu) ? (uint32_t)(lp[g] >> 32) : (uint32_t)lp[g];
+}
+
 // Walks local trees t .. t+G-1 and stores their leaf values to V (groups of
 // four trees of one chain are 16 consecutive bytes, stored as one vector
 // when aligned).
 template <int DEPTH, int G>
-__device__ __forceinline__ void walk_group(const uint8_t* __restrict__ L, const TreeArgs& a, int t, int t_global,
-                                           uint32_t fb, int64_t c, bool active) {
-    uint32_t nb[G], lb[G], v[G];
+__device__ __forceinline__ void walk_vals(const uint8_t* __restrict__ L, const TreeArgs& a, int t, uint32_t fb,
+                                          uint32_t (&v)[G]) {
+    uint32_t nb[G], lb[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         const uint32_t o = a.toff[t + g];
         nb[g] = (o & 0xffffu) * 4u;
         lb[g] = (o >> 16) * 4u;
     }
-    walk16<DEPTH, G>(L, nb, lb, fb, a.mask, v);
-    if (!active) return;
+    if constexpr (G == 8 && DEPTH >= 2)
+        walk8_roll<DEPTH>(L, nb, lb, fb, a.mask, v);
+    else
+        walk16<DEPTH, G>(L, nb, lb, fb, a.mask, v);
+}
+
+template <int G>
+__device__ __forceinline__ void store_vals(const TreeArgs& a, int t_global, int64_t c, const uint32_t (&v)[G]) {
     float* dst = a.V + ((((int64_t)(t_global >> 2) * a.n + c) << 2) + (t_global & 3));
     if (G >= 4 && (t_global & 3) == 0) {
 #pragma unroll
@@ -501,6 +615,14 @@ __device__ __forceinline__ void walk_group(const uint8_t* __restrict__ L, const 
     }
 }
 
+template <int DEPTH, int G>
+__device__ __forceinline__ void walk_group(const uint8_t* __restrict__ L, const TreeArgs& a, int t, int t_global,
+                                           uint32_t fb, int64_t c, bool active) {
+    uint32_t v[G];
+    walk_vals<DEPTH, G>(L, a, t, fb, v);
+    if (active) store_vals<G>(a, t_global, c, v);
+}
+
 // r (< 2H) remaining trees from local tree t, in groups of H, H/2, ..., 1.
 template <int DEPTH, int H>
 __device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const TreeArgs& a, int t, int t_global, int r,
@@ -516,7 +638,9 @@ __device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const T
 
 // Workgroup b walks trees [g*tpw, g*tpw + tpw) for chain blocks (64 chains
 // each) [cs*slice_blocks, (cs+1)*slice_blocks), with g = b / slices and
-// cs = b % slices; its waves take the blocks in turn.
+// cs = b % slices.  Wave w starts with block w of the slice and then takes
+// the next unclaimed block from a counter in LDS, so waves that share a
+// SIMD with fewer others take more blocks.
 template <int DEPTH, int Q, int SLOT_LOG2>
 __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     constexpr uint32_t SLOT = 1u << SLOT_LOG2;
@@ -560,9 +684,11 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
             }
         }
     }
-    __syncthreads();
-    const int wave = tid >> 6, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int nw = (int)(blockDim.x >> 6);
+    uint32_t* counter = lds + TREE_LDS_FREE / 4;
+    if (tid == 0) *counter = (uint32_t)nw;
+    __syncthreads();
     const int64_t n = a.n;
     const int64_t blocks = (n + 63) >> 6;
     const int64_t b_end0 = (int64_t)(cs + 1) * a.slice_blocks;
@@ -574,10 +700,21 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     // 4k + i/16, which land on tile dwords 256k + 4i .. +3 = quad * 64 + chain
     const uint32_t* fsrc = a.Fg + (int64_t)(lane >> 4) * a.fg_stride + 4 * (lane & 15);
     static_assert(Q % 4 == 0, "whole quad groups");
-    for (int64_t b = (int64_t)cs * a.slice_blocks + wave; b < b_end; b += nw) {
+    const int64_t b_first = (int64_t)cs * a.slice_blocks;
+    auto claim_next = [&]() -> uint32_t {
+        uint32_t r = 0;
+        if (lane == 0) r = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        return r;
+    };
+    // b: the block walked now; nb: the next one, claimed a block ahead so
+    // that the claim's answer is never waited for
+    int64_t b = b_first + wave, nb = b_end;
+    if (b < b_end) nb = b_first + (int64_t)__builtin_amdgcn_readfirstlane(claim_next());
+    while (b < b_end) {
         // every earlier read of this wave's tile has returned before the
         // tile is overwritten (s_waitcnt lgkmcnt(0))
         __builtin_amdgcn_s_waitcnt(0xc07f);
+        const uint32_t claim = nb < b_end ? claim_next() : 0u;
 #pragma unroll
         for (int k = 0; k < Q / 4; ++k)
             __builtin_amdgcn_global_load_lds(fsrc + (int64_t)(4 * k) * a.fg_stride + b * 64, tile + 256 * k, 16, 0, 0);
@@ -587,6 +724,8 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
         int t = 0;
         for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
         walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
+        b = nb;
+        if (b < b_end) nb = b_first + (int64_t)__builtin_amdgcn_readfirstlane(claim);
     }
 }
 
@@ -600,8 +739,8 @@ bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TR
     int ng = 0;
     for (int w = 0; w < nw; ++w) {
         const uint32_t lo = (uint32_t)w * slot + tile;
-        const uint32_t hi = (w + 1 < nw) ? (uint32_t)(w + 1) * slot : (uint32_t)MAX_LDS_BYTES;
-        if (lo > (uint32_t)MAX_LDS_BYTES) return false;
+        const uint32_t hi = (w + 1 < nw) ? (uint32_t)(w + 1) * slot : TREE_LDS_FREE;
+        if (lo > TREE_LDS_FREE) return false;
         gaps[ng++] = Gap{lo, hi};
     }
     const uint32_t nbytes = 4u << (depth - 1), lbytes = 4u << depth;
@@ -627,6 +766,16 @@ bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TR
 template <int DEPTH, int Q, int SLOT_LOG2>
 hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     const int grid = (a.n_trees + a.tpw - 1) / a.tpw * a.slices;
+    static bool checked = false;
+    if (!checked) {
+        // the walk's asm takes offsets into the kernel's LDS array as LDS
+        // addresses: the array must be the kernel's only LDS object
+        hipFuncAttributes fa;
+        hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(&k_trees<DEPTH, Q, SLOT_LOG2>));
+        if (e != hipSuccess) return e;
+        if (fa.sharedSizeBytes != MAX_LDS_BYTES) return hipErrorInvalidKernelFile;
+        checked = true;
+    }
     if (start)
         hipExtLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, start, stop, 0, a);
     else
