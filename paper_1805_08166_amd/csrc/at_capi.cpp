@@ -276,6 +276,27 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
         for (size_t p = 1; p < NB; ++p) tw[p] = node(2 * p) | (node(2 * p + 1) << 16);
         std::memcpy(tw + NB, &leaf[t * n_leaf], n_leaf * 4);
     }
+    // pointer form for the tree-partitioned annealing path (layout in at_internal.h)
+    const size_t W32 = 4 * NB;
+    std::vector<uint32_t> words32;
+    try {
+        words32.assign((size_t)n_trees * W32, 0u);
+    } catch (...) {
+        return fail(AT_E_OOM, "at_ensemble_create: host allocation");
+    }
+    for (size_t t = 0; t < (size_t)n_trees; ++t) {
+        uint32_t* tw = words32.data() + t * W32;
+        auto node = [&](size_t m) {
+            const uint32_t rel = m < NB ? (uint32_t)(2 * m) : (uint32_t)(2 * (m - NB));
+            return node16(fid[t * n_int + m - 1], thr[t * n_int + m - 1]) | (rel << 16);
+        };
+        tw[0] = node(1);
+        for (size_t p = 1; p < NB; ++p) {
+            tw[2 * p] = node(2 * p);
+            tw[2 * p + 1] = node(2 * p + 1);
+        }
+        std::memcpy(tw + 2 * NB, &leaf[t * n_leaf], n_leaf * 4);
+    }
     // local forms for the chain-local annealing path (layout in at_internal.h)
     const size_t ts_full = (size_t)local_tree_stride((int)W16), ts_nodes = (size_t)local_tree_stride((int)NB);
     std::vector<uint32_t> local_full, local_nodes;
@@ -316,6 +337,7 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     e->device = current_device();
     at_status st = upload(e->d_words, words.data(), words.size());
     if (st == AT_OK) st = upload(e->d_words16, words16.data(), words16.size());
+    if (st == AT_OK) st = upload(e->d_words32, words32.data(), words32.size());
     if (st == AT_OK) st = upload(e->d_local_full, local_full.data(), local_full.size());
     if (st == AT_OK) st = upload(e->d_local_nodes, local_nodes.data(), local_nodes.size());
     if (st == AT_OK) st = upload(e->d_local_top, local_top.data(), local_top.size());
@@ -330,6 +352,7 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     e->desc.words_per_tree = (int32_t)W;
     e->desc.words = static_cast<const uint32_t*>(e->d_words.p);
     e->desc.words16 = static_cast<const uint32_t*>(e->d_words16.p);
+    e->desc.words32 = static_cast<const uint32_t*>(e->d_words32.p);
     e->desc.local_full = static_cast<const uint32_t*>(e->d_local_full.p);
     e->desc.local_nodes = static_cast<const uint32_t*>(e->d_local_nodes.p);
     e->desc.local_top = static_cast<const uint32_t*>(e->d_local_top.p);
@@ -343,6 +366,7 @@ void at_ensemble_destroy(at_ensemble_t ens) {
     DeviceGuard g(ens->device);
     release(ens->d_words);
     release(ens->d_words16);
+    release(ens->d_words32);
     release(ens->d_local_full);
     release(ens->d_local_nodes);
     release(ens->d_local_top);

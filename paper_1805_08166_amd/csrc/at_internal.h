@@ -77,6 +77,17 @@ struct EnsembleDesc {
     // right leaf, 0}.  Depth 2 and above.
     const uint32_t* local_top;
     const uint4* tail;
+    // Pointer form for the tree-partitioned annealing path.  Tree t occupies
+    // words32 [t*W32, (t+1)*W32) with W32 = 2^(d+1): a node block of 2^(d-1)
+    // 8-byte slots (slot 0 holds the root in its low word, slot p >= 1 holds
+    // internal nodes 2p and 2p+1), then a leaf block of 2^(d-1) slots (slot j
+    // holds leaves 2j and 2j+1).  A 32-bit node is its 16-bit compact node in
+    // the low half and, in the high half, the word offset of its children's
+    // slot: 2m in the node block for node m < 2^(d-1), 2(m - 2^(d-1)) in the
+    // leaf block otherwise.  A kernel that copies the blocks to LDS adds the
+    // word address of the target block to the high half, which then holds
+    // the LDS address of the children divided by 4.
+    const uint32_t* words32;
 };
 
 // Largest threshold the compact form keeps; annealing features never exceed
@@ -160,6 +171,7 @@ struct at_ensemble_s {
     at::EnsembleDesc desc{};
     at::DeviceBuf d_words;
     at::DeviceBuf d_words16;
+    at::DeviceBuf d_words32;
     at::DeviceBuf d_local_full;
     at::DeviceBuf d_local_nodes;
     at::DeviceBuf d_local_top;

@@ -7,7 +7,7 @@
 //            candidate (one knob changed, Philox block (chain, step, 0, 0)),
 //            evaluates its loop-context features and writes them as packed
 //            bytes 4x+3, quad-major (dword q of chain c at Fg[q * n + c]).
-//   k_trees  workgroup w holds the compact form of trees [w*tpw, (w+1)*tpw)
+//   k_trees  workgroup w holds the pointer form of trees [w*tpw, (w+1)*tpw)
 //            in LDS; each of its waves walks them for 64 chains at a time
 //            through its own LDS feature tile, writing the reached leaf
 //            values to V.
@@ -381,12 +381,12 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tree kernel.  A workgroup holds the compact form of its trees in LDS and
+// Tree kernel.  A workgroup holds the pointer form of its trees in LDS and
 // walks them for every chain.  Each wave owns a feature tile of 64 chains in
 // a slot of SLOT bytes at wave * SLOT: byte (f & 3) of dword (f >> 2) * 64 +
 // lane holds 4x+3 for feature value x, so lanes read distinct banks whatever
 // features they ask for, and the tile byte address of feature f is
-// (node & mask) | (wave * SLOT + 4 * lane) for a 16-bit node of that feature,
+// (node & mask) | (wave * SLOT + 4 * lane) for a node of that feature,
 // mask = 3 | (SLOT - 1) & ~0xff.
 // With 4x+3 in the tile, x >= thr is (4x+3) >= (low byte of the node) for
 // x, thr <= 63.  Tiles are private to their wave, so the walk loop needs no
@@ -398,7 +398,7 @@ constexpr int TREE_WAVES_MAX = 16;
 constexpr uint32_t TREE_LDS_FREE = (uint32_t)MAX_LDS_BYTES - 16u;
 
 struct TreeArgs {
-    const uint32_t* words16;   // compact ensemble
+    const uint32_t* words32;   // pointer form of the ensemble
     int n_trees;
     int tpw;                   // trees per workgroup
     const uint32_t* Fg;        // [Q][fg_stride] packed features (4x+3 per byte)
@@ -412,187 +412,224 @@ struct TreeArgs {
     uint32_t toff[TREES_MAX];
 };
 
-// Walks G trees for this lane's chain: nb/lb are the LDS byte offsets of the
-// trees' node and leaf blocks, mask the node bits of a tile address.  Node
-// p (1-based heap) has its children in word p of the node block; the chosen
-// child of the last internal level is leaf 2p + right - 2^DEPTH.  A level
-// costs five vector instructions per tree when G is a multiple of four.
+// Tree walks over the pointer form.  A node is 32 bits: its compact node in
+// the low half and its children's LDS address / 4 in the high half, so the
+// children's slot is at node >> 14 (bits 14-15 of a compact node are zero).
+// A level reads the node's feature byte from the tile and its children's
+// 8-byte slot, then keeps the right child when (node & 0xff) <= x4.  After
+// DEPTH levels the kept word is the leaf value.  nb[g] is the LDS address
+// of tree g's node block (the root is its first word).
+
+// Plain walk of G trees (any DEPTH).
 template <int DEPTH, int G>
-__device__ __forceinline__ void walk16(const uint8_t* __restrict__ L, const uint32_t (&nb)[G],
-                                       const uint32_t (&lb)[G], uint32_t fb, uint32_t mask, uint32_t (&out)[G]) {
-    uint32_t node[G], p[G], fa[G], pa[G];
+__device__ __forceinline__ void walk_plain(const uint8_t* __restrict__ L, const uint32_t (&nb)[G], uint32_t fb,
+                                           uint32_t mask, uint32_t (&out)[G]) {
+    uint32_t node[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-        node[g] = *reinterpret_cast<const uint16_t*>(L + nb[g]);
-        p[g] = 1u;
-        fa[g] = (node[g] & mask) | fb;
-        pa[g] = nb[g] + 4u;
+    for (int g = 0; g < G; ++g) node[g] = *reinterpret_cast<const uint32_t*>(L + nb[g]);
+#pragma unroll
+    for (int l = 0; l < DEPTH; ++l) {
+        uint32_t x4[G];
+        uint64_t pr[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            x4[g] = L[(node[g] & mask) | fb];
+            pr[g] = *reinterpret_cast<const uint64_t*>(L + (node[g] >> 14));
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) node[g] = x4[g] >= (node[g] & 0xffu) ? (uint32_t)(pr[g] >> 32) : (uint32_t)pr[g];
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) out[g] = node[g];
+}
+
+// One level of four trees: right = (node & 0xff) <= x4 (the compiler does
+// not form the byte compare from plain code), node = right ? hi : lo, then
+// the next feature address (node & mask) | fb and slot address node >> 14.
+// A VALU write of VCC is read two or more instructions later (gfx950 wait
+// states): the first compare is followed by s_nop 1, the others by the
+// previous tree's address instructions.
+// Operands: 0-3 node, 4-7 feature address, 8-11 slot address, 12-15 x4,
+// 16-19 lo, 20-23 hi, 24 mask, 25 fb.
+#define AT_PLEVEL4_ASM                                                                                     \
+    "v_cmp_le_u32_sdwa vcc, %0, %12 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32 %0, %16, %20, vcc\n\t"                                                                   \
+    "v_cmp_le_u32_sdwa vcc, %1, %13 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %4, %0, %24, %25\n\t"                                                                    \
+    "v_lshrrev_b32 %8, 14, %0\n\t"                                                                         \
+    "v_cndmask_b32 %1, %17, %21, vcc\n\t"                                                                   \
+    "v_cmp_le_u32_sdwa vcc, %2, %14 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %5, %1, %24, %25\n\t"                                                                    \
+    "v_lshrrev_b32 %9, 14, %1\n\t"                                                                         \
+    "v_cndmask_b32 %2, %18, %22, vcc\n\t"                                                                   \
+    "v_cmp_le_u32_sdwa vcc, %3, %15 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                    \
+    "v_and_or_b32 %6, %2, %24, %25\n\t"                                                                    \
+    "v_lshrrev_b32 %10, 14, %2\n\t"                                                                        \
+    "v_cndmask_b32 %3, %19, %23, vcc\n\t"                                                                   \
+    "v_and_or_b32 %7, %3, %24, %25\n\t"                                                                    \
+    "v_lshrrev_b32 %11, 14, %3"
+
+// The last level of four trees: the kept word is the leaf value.
+// Operands: 0-3 node, 4-7 x4, 8-11 lo, 12-15 hi.
+#define AT_PLAST4_ASM                                                                                      \
+    "v_cmp_le_u32_sdwa vcc, %0, %4 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                     \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32 %0, %8, %12, vcc\n\t"                                                                    \
+    "v_cmp_le_u32_sdwa vcc, %1, %5 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                     \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32 %1, %9, %13, vcc\n\t"                                                                    \
+    "v_cmp_le_u32_sdwa vcc, %2, %6 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                     \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32 %2, %10, %14, vcc\n\t"                                                                   \
+    "v_cmp_le_u32_sdwa vcc, %3, %7 src0_sel:BYTE_0 src1_sel:DWORD\n\t"                                     \
+    "s_nop 1\n\t"                                                                                          \
+    "v_cndmask_b32 %3, %11, %15, vcc"
+
+// Reads of one level for four trees: feature byte and children's slot.
+// Operands: 0-3 x4, 4-7 slot (64-bit), 8-11 feature address, 12-15 slot
+// address.
+#define AT_PISSUE4_ASM                                                                                     \
+    "ds_read_u8 %0, %8\n\t"                                                                                \
+    "ds_read_b64 %4, %12\n\t"                                                                              \
+    "ds_read_u8 %1, %9\n\t"                                                                                \
+    "ds_read_b64 %5, %13\n\t"                                                                              \
+    "ds_read_u8 %2, %10\n\t"                                                                               \
+    "ds_read_b64 %6, %14\n\t"                                                                              \
+    "ds_read_u8 %3, %11\n\t"                                                                               \
+    "ds_read_b64 %7, %15"
+
+// Eight trees as two software-pipelined groups of four (A = trees 0-3, B =
+// 4-7).  A group's step waits for its own reads (LDS answers in issue
+// order, so lgkmcnt(8) leaves just the other group's eight in flight),
+// computes the level and at once issues the reads of its next level; the
+// other group's reads are served meanwhile.  Reads live across asm
+// statements: the wait is a statement of its own that takes the receiving
+// registers as in-out operands, so whatever the compiler does with them
+// comes after the wait.  The asm takes offsets into L as LDS addresses: L
+// is the kernel's only LDS object, so it starts at LDS address 0 (the
+// launcher checks that the kernel's static LDS is that array alone).
+template <int DEPTH, bool ROOTS>
+__device__ __forceinline__ void walk8_roll(const uint8_t* __restrict__ L, const uint32_t (&nb)[8], uint32_t fb,
+                                           uint32_t mask, const uint32_t (&rnode)[8], const uint32_t (&rlo)[8],
+                                           const uint32_t (&rhi)[8], uint32_t (&out)[8]) {
+    uint32_t node[8], fa[8], pa[8], x4[8];
+    uint64_t pr[8];
+    int l0 = 0;
+    if constexpr (ROOTS) {
+        // roots and their children's slots are given: level 0 needs only
+        // the feature bytes
+        static_assert(DEPTH >= 2, "a level below the root");
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+            node[g] = rnode[g];
+            fa[g] = (rnode[g] & mask) | fb;
+        }
+#pragma unroll
+        for (int h = 0; h < 8; h += 4)
+            asm volatile("ds_read_u8 %0, %4\n\t"
+                         "ds_read_u8 %1, %5\n\t"
+                         "ds_read_u8 %2, %6\n\t"
+                         "ds_read_u8 %3, %7"
+                         : "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3])
+                         : "v"(fa[h]), "v"(fa[h + 1]), "v"(fa[h + 2]), "v"(fa[h + 3])
+                         : "memory");
+#pragma unroll
+        for (int h = 0; h < 8; h += 4) {
+            // group A waits for its four reads (group B's four are behind
+            // them), group B for its four (group A's next eight are behind)
+            if (h == 0)
+                asm volatile("s_waitcnt lgkmcnt(4)" : "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]));
+            else
+                asm volatile("s_waitcnt lgkmcnt(8)" : "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]));
+            asm volatile(AT_PLEVEL4_ASM
+                         : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "=&v"(fa[h]),
+                           "=&v"(fa[h + 1]), "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]),
+                           "=&v"(pa[h + 2]), "=&v"(pa[h + 3])
+                         : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"(rlo[h]), "v"(rlo[h + 1]),
+                           "v"(rlo[h + 2]), "v"(rlo[h + 3]), "v"(rhi[h]), "v"(rhi[h + 1]), "v"(rhi[h + 2]),
+                           "v"(rhi[h + 3]), "s"(mask), "v"(fb)
+                         : "vcc");
+            asm volatile(AT_PISSUE4_ASM
+                         : "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]), "=&v"(pr[h]),
+                           "=&v"(pr[h + 1]), "=&v"(pr[h + 2]), "=&v"(pr[h + 3])
+                         : "v"(fa[h]), "v"(fa[h + 1]), "v"(fa[h + 2]), "v"(fa[h + 3]), "v"(pa[h]), "v"(pa[h + 1]),
+                           "v"(pa[h + 2]), "v"(pa[h + 3]));
+        }
+        l0 = 1;
+    } else {
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+            node[g] = *reinterpret_cast<const uint32_t*>(L + nb[g]);
+            fa[g] = (node[g] & mask) | fb;
+            pa[g] = node[g] >> 14;
+        }
+#pragma unroll
+        for (int h = 0; h < 8; h += 4)
+            asm volatile(AT_PISSUE4_ASM
+                         : "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]), "=&v"(pr[h]),
+                           "=&v"(pr[h + 1]), "=&v"(pr[h + 2]), "=&v"(pr[h + 3])
+                         : "v"(fa[h]), "v"(fa[h + 1]), "v"(fa[h + 2]), "v"(fa[h + 3]), "v"(pa[h]), "v"(pa[h + 1]),
+                           "v"(pa[h + 2]), "v"(pa[h + 3])
+                         : "memory");
     }
 #pragma unroll
     for (int l = 0; l + 1 < DEPTH; ++l) {
-        uint32_t x4[G], pr[G];
+        if (l < l0) continue;
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            x4[g] = L[fa[g]];
-            pr[g] = *reinterpret_cast<const uint32_t*>(L + pa[g]);
-        }
-        if constexpr (G % 4 == 0) {
-#pragma unroll
-            for (int h = 0; h < G; h += 4) {
-                asm(AT_WALK4_ASM
-                    : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
-                      "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "=&v"(fa[h]), "=&v"(fa[h + 1]),
-                      "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]), "=&v"(pa[h + 2]),
-                      "=&v"(pa[h + 3])
-                    : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"(pr[h]), "v"(pr[h + 1]),
-                      "v"(pr[h + 2]), "v"(pr[h + 3]), "s"(mask), "v"(fb), "s"(nb[h]), "s"(nb[h + 1]),
-                      "s"(nb[h + 2]), "s"(nb[h + 3])
-                    : "vcc");
-            }
-        } else {
-            // plain code for groups of one or two trees (high bits of node
-            // are left as they fall; only its low half is used)
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                const bool right = x4[g] >= (node[g] & 0xffu);
-                node[g] = right ? (pr[g] >> 16) : pr[g];
-                p[g] = 2u * p[g] + (right ? 1u : 0u);
-                fa[g] = (node[g] & mask) | fb;
-                pa[g] = nb[g] + 4u * p[g];
-            }
-        }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        const uint32_t x4 = L[fa[g]];
-        const uint32_t q = 2u * p[g] + (x4 >= (node[g] & 0xffu) ? 1u : 0u);
-        out[g] = *reinterpret_cast<const uint32_t*>(L + lb[g] + 4u * (q - (1u << DEPTH)));
-    }
-}
-
-// Reads of one level for four trees: the feature byte of each tree's node
-// and the word holding its pair of children.  Operand numbers are those of
-// AT_WALK4_ASM (8-11 feature address, 12-15 pair address, 16-19 x4, 20-23
-// pr).
-#define AT_ISSUE4_ASM                                                                                      \
-    "ds_read_u8 %16, %8\n\t"                                                                               \
-    "ds_read_b32 %20, %12\n\t"                                                                             \
-    "ds_read_u8 %17, %9\n\t"                                                                               \
-    "ds_read_b32 %21, %13\n\t"                                                                             \
-    "ds_read_u8 %18, %10\n\t"                                                                              \
-    "ds_read_b32 %22, %14\n\t"                                                                             \
-    "ds_read_u8 %19, %11\n\t"                                                                              \
-    "ds_read_b32 %23, %15"
-
-// walk16 for eight trees and DEPTH >= 2 as two software-pipelined groups of
-// four (A = trees 0-3, B = trees 4-7).  Each group's step waits for its own
-// reads (LDS answers in issue order, so lgkmcnt(8) leaves just the other
-// group's eight in flight), computes the level, and at once issues the reads
-// of its next level; the other group's reads are served meanwhile.  The
-// reads live across asm statements, so the registers that receive them are
-// handed from one statement to the next as in-out operands and nothing else
-// touches them in between.  The last internal level reads the feature byte
-// together with the 8-byte pair of leaves (leaves 2(p - 2^(DEPTH-1)) and
-// +1), so the leaf needs no further round trip.  The asm takes offsets into
-// L as LDS addresses: L is the kernel's only LDS object, so it starts at
-// LDS address 0 (the launcher checks that the kernel's static LDS is that
-// array alone).
-template <int DEPTH>
-__device__ __forceinline__ void walk8_roll(const uint8_t* __restrict__ L, const uint32_t (&nb)[8],
-                                           const uint32_t (&lb)[8], uint32_t fb, uint32_t mask,
-                                           uint32_t (&out)[8]) {
-    static_assert(DEPTH >= 2, "two or more levels");
-    uint32_t node[8], p[8], fa[8], pa[8], x4[8], pr[8];
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-        node[g] = *reinterpret_cast<const uint16_t*>(L + nb[g]);
-        p[g] = 1u;
-        fa[g] = (node[g] & mask) | fb;
-        pa[g] = nb[g] + 4u;
-    }
-#pragma unroll
-    for (int h = 0; h < 8; h += 4)
-        asm volatile(AT_ISSUE4_ASM
-                     : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
-                       "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "+v"(fa[h]), "+v"(fa[h + 1]),
-                       "+v"(fa[h + 2]), "+v"(fa[h + 3]), "+v"(pa[h]), "+v"(pa[h + 1]), "+v"(pa[h + 2]),
-                       "+v"(pa[h + 3]), "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]),
-                       "=&v"(pr[h]), "=&v"(pr[h + 1]), "=&v"(pr[h + 2]), "=&v"(pr[h + 3])
-                     :
-                     : "memory");
-#pragma unroll
-    for (int l = 0; l + 2 < DEPTH; ++l) {
-#pragma unroll
-        for (int h = 0; h < 8; h += 4)
-            asm volatile("s_waitcnt lgkmcnt(8)\n\t" AT_WALK4_ASM "\n\t" AT_ISSUE4_ASM
-                         : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
-                           "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "=&v"(fa[h]), "=&v"(fa[h + 1]),
-                           "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]), "=&v"(pa[h + 2]),
-                           "=&v"(pa[h + 3]), "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]),
-                           "+v"(pr[h]), "+v"(pr[h + 1]), "+v"(pr[h + 2]), "+v"(pr[h + 3])
-                         : "s"(mask), "v"(fb), "s"(nb[h]), "s"(nb[h + 1]), "s"(nb[h + 2]), "s"(nb[h + 3])
+        for (int h = 0; h < 8; h += 4) {
+            asm volatile("s_waitcnt lgkmcnt(8)"
+                         : "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]), "+v"(pr[h]),
+                           "+v"(pr[h + 1]), "+v"(pr[h + 2]), "+v"(pr[h + 3]));
+            asm volatile(AT_PLEVEL4_ASM
+                         : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "=&v"(fa[h]),
+                           "=&v"(fa[h + 1]), "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]),
+                           "=&v"(pa[h + 2]), "=&v"(pa[h + 3])
+                         : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"((uint32_t)pr[h]),
+                           "v"((uint32_t)pr[h + 1]), "v"((uint32_t)pr[h + 2]), "v"((uint32_t)pr[h + 3]),
+                           "v"((uint32_t)(pr[h] >> 32)), "v"((uint32_t)(pr[h + 1] >> 32)),
+                           "v"((uint32_t)(pr[h + 2] >> 32)), "v"((uint32_t)(pr[h + 3] >> 32)), "s"(mask), "v"(fb)
                          : "vcc");
+            asm volatile(AT_PISSUE4_ASM
+                         : "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]), "=&v"(pr[h]),
+                           "=&v"(pr[h + 1]), "=&v"(pr[h + 2]), "=&v"(pr[h + 3])
+                         : "v"(fa[h]), "v"(fa[h + 1]), "v"(fa[h + 2]), "v"(fa[h + 3]), "v"(pa[h]), "v"(pa[h + 1]),
+                           "v"(pa[h + 2]), "v"(pa[h + 3]));
+        }
     }
-    // last pair level, then the feature byte and leaf pair of the last
-    // internal node
-    uint64_t lp[8];
 #pragma unroll
     for (int h = 0; h < 8; h += 4) {
-        asm volatile("s_waitcnt lgkmcnt(8)\n\t" AT_WALK4_ASM
-                     : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3]), "+v"(p[h]),
-                       "+v"(p[h + 1]), "+v"(p[h + 2]), "+v"(p[h + 3]), "=&v"(fa[h]), "=&v"(fa[h + 1]),
-                       "=&v"(fa[h + 2]), "=&v"(fa[h + 3]), "=&v"(pa[h]), "=&v"(pa[h + 1]), "=&v"(pa[h + 2]),
-                       "=&v"(pa[h + 3])
-                     : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"(pr[h]), "v"(pr[h + 1]),
-                       "v"(pr[h + 2]), "v"(pr[h + 3]), "s"(mask), "v"(fb), "s"(nb[h]), "s"(nb[h + 1]),
-                       "s"(nb[h + 2]), "s"(nb[h + 3])
+        if (h == 0)
+            asm volatile("s_waitcnt lgkmcnt(8)"
+                         : "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]), "+v"(pr[h]),
+                           "+v"(pr[h + 1]), "+v"(pr[h + 2]), "+v"(pr[h + 3]));
+        else
+            asm volatile("s_waitcnt lgkmcnt(0)"
+                         : "+v"(x4[h]), "+v"(x4[h + 1]), "+v"(x4[h + 2]), "+v"(x4[h + 3]), "+v"(pr[h]),
+                           "+v"(pr[h + 1]), "+v"(pr[h + 2]), "+v"(pr[h + 3]));
+        asm volatile(AT_PLAST4_ASM
+                     : "+v"(node[h]), "+v"(node[h + 1]), "+v"(node[h + 2]), "+v"(node[h + 3])
+                     : "v"(x4[h]), "v"(x4[h + 1]), "v"(x4[h + 2]), "v"(x4[h + 3]), "v"((uint32_t)pr[h]),
+                       "v"((uint32_t)pr[h + 1]), "v"((uint32_t)pr[h + 2]), "v"((uint32_t)pr[h + 3]),
+                       "v"((uint32_t)(pr[h] >> 32)), "v"((uint32_t)(pr[h + 1] >> 32)),
+                       "v"((uint32_t)(pr[h + 2] >> 32)), "v"((uint32_t)(pr[h + 3] >> 32))
                      : "vcc");
-        uint32_t la[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) la[g] = lb[h + g] - (8u << (DEPTH - 1)) + 8u * p[h + g];
-        asm volatile(
-            "ds_read_u8 %0, %8\n\t"
-            "ds_read_b64 %4, %12\n\t"
-            "ds_read_u8 %1, %9\n\t"
-            "ds_read_b64 %5, %13\n\t"
-            "ds_read_u8 %2, %10\n\t"
-            "ds_read_b64 %6, %14\n\t"
-            "ds_read_u8 %3, %11\n\t"
-            "ds_read_b64 %7, %15"
-            : "=&v"(x4[h]), "=&v"(x4[h + 1]), "=&v"(x4[h + 2]), "=&v"(x4[h + 3]), "=&v"(lp[h]), "=&v"(lp[h + 1]),
-              "=&v"(lp[h + 2]), "=&v"(lp[h + 3])
-            : "v"(fa[h]), "v"(fa[h + 1]), "v"(fa[h + 2]), "v"(fa[h + 3]), "v"(la[0]), "v"(la[1]), "v"(la[2]),
-              "v"(la[3]));
     }
-    asm volatile("s_waitcnt lgkmcnt(8)"
-                 : "+v"(x4[0]), "+v"(x4[1]), "+v"(x4[2]), "+v"(x4[3]), "+v"(lp[0]), "+v"(lp[1]), "+v"(lp[2]),
-                   "+v"(lp[3]));
 #pragma unroll
-    for (int g = 0; g < 4; ++g) out[g] = x4[g] >= (node[g] & 0xffu) ? (uint32_t)(lp[g] >> 32) : (uint32_t)lp[g];
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(x4[4]), "+v"(x4[5]), "+v"(x4[6]), "+v"(x4[7]), "+v"(lp[4]), "+v"(lp[5]), "+v"(lp[6]),
-                   "+v"(lp[7]));
-#pragma unroll
-    for (int g = 4; g < 8; ++g) out[g] = x4[g] >= (node[g] & 0xffu) ? (uint32_t)(lp[g] >> 32) : (uint32_t)lp[g];
+    for (int g = 0; g < 8; ++g) out[g] = node[g];
 }
 
-// Walks local trees t .. t+G-1 and stores their leaf values to V (groups of
-// four trees of one chain are 16 consecutive bytes, stored as one vector
-// when aligned).
 template <int DEPTH, int G>
 __device__ __forceinline__ void walk_vals(const uint8_t* __restrict__ L, const TreeArgs& a, int t, uint32_t fb,
                                           uint32_t (&v)[G]) {
-    uint32_t nb[G], lb[G];
+    uint32_t nb[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-        const uint32_t o = a.toff[t + g];
-        nb[g] = (o & 0xffffu) * 4u;
-        lb[g] = (o >> 16) * 4u;
-    }
-    if constexpr (G == 8 && DEPTH >= 2)
-        walk8_roll<DEPTH>(L, nb, lb, fb, a.mask, v);
-    else
-        walk16<DEPTH, G>(L, nb, lb, fb, a.mask, v);
+    for (int g = 0; g < G; ++g) nb[g] = (a.toff[t + g] & 0xffffu) * 4u;
+    if constexpr (G == 8) {
+        const uint32_t none[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        walk8_roll<DEPTH, false>(L, nb, fb, a.mask, none, none, none, v);
+    } else
+        walk_plain<DEPTH, G>(L, nb, fb, a.mask, v);
 }
 
 template <int G>
@@ -644,7 +681,7 @@ __device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const T
 template <int DEPTH, int Q, int SLOT_LOG2>
 __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     constexpr uint32_t SLOT = 1u << SLOT_LOG2;
-    constexpr int NB = 1 << (DEPTH - 1), NL = 1 << DEPTH, W16 = NB + NL;
+    constexpr int NB = 1 << (DEPTH - 1);
     constexpr int G = 8;
     __shared__ uint32_t lds[MAX_LDS_BYTES / 4];
     const uint8_t* L = reinterpret_cast<const uint8_t*>(lds);
@@ -652,14 +689,17 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     const int grp = blockIdx.x / a.slices, cs = blockIdx.x - grp * a.slices;
     const int t0 = grp * a.tpw;
     const int nt = (a.n_trees - t0 < a.tpw) ? (a.n_trees - t0) : a.tpw;
-    // trees into LDS: per round, one piece of every tree is loaded before
-    // any store.  Loads and stores are unconditional so that the loads stay
-    // in flight together: slots past the last tree and lanes past the last
-    // piece repeat the last tree's or piece's store (same value, same place).
-    if constexpr (DEPTH >= 3) {
-        // blocks are whole 16-byte pieces at 16-byte aligned offsets
-        constexpr int NB4 = NB / 4, W4 = W16 / 4;
-        const uint4* src = reinterpret_cast<const uint4*>(a.words16 + (size_t)t0 * W16);
+    // trees into LDS, relocating node pointers: a node-block slot p holds
+    // nodes whose children sit in the leaf block when p >= NB / 2 (the last
+    // internal level; for DEPTH 1 the root), else in the node block.  Per
+    // round, one piece of every tree is loaded before any store.  Loads and
+    // stores are unconditional so that the loads stay in flight together:
+    // slots past the last tree and lanes past the last piece repeat the last
+    // tree's or piece's store (same value, same place).
+    if constexpr (DEPTH >= 2) {
+        // blocks are whole 16-byte pieces (two slots) at 16-byte aligned offsets
+        constexpr int B4 = NB / 2, W4 = 2 * B4;
+        const uint4* src = reinterpret_cast<const uint4*>(a.words32 + (size_t)t0 * 4 * NB);
         for (int base = 0; base < W4; base += (int)blockDim.x) {
             const int i = base + tid < W4 ? base + tid : W4 - 1;
             uint4 v[TREES_MAX];
@@ -668,20 +708,32 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
 #pragma unroll
             for (int t = 0; t < TREES_MAX; ++t) {
                 const uint32_t o = a.toff[t < nt ? t : nt - 1];
-                const uint32_t d = i < NB4 ? (o & 0xffffu) + 4u * (uint32_t)i : (o >> 16) + 4u * (uint32_t)(i - NB4);
+                const uint32_t nw4 = o & 0xffffu, lw4 = o >> 16;
+                uint32_t d;
+                if (i < B4) {
+                    // slots 2i and 2i + 1 of the node block
+                    const uint32_t r0 = ((2 * i >= NB / 2) ? lw4 : nw4) << 16;
+                    const uint32_t r1 = ((2 * i + 1 >= NB / 2) ? lw4 : nw4) << 16;
+                    v[t].x += r0;
+                    v[t].y += r0;
+                    v[t].z += r1;
+                    v[t].w += r1;
+                    d = nw4 + 4u * (uint32_t)i;
+                } else {
+                    d = lw4 + 4u * (uint32_t)(i - B4);
+                }
                 *reinterpret_cast<uint4*>(lds + d) = v[t];
             }
         }
     } else {
-        const uint32_t* src = a.words16 + (size_t)t0 * W16;
-        for (int i = tid; i < W16; i += (int)blockDim.x) {
-#pragma unroll
-            for (int t = 0; t < TREES_MAX; ++t) {
-                if (t < nt) {
-                    const uint32_t o = a.toff[t];
-                    lds[i < NB ? (o & 0xffffu) + (uint32_t)i : (o >> 16) + (uint32_t)(i - NB)] = src[t * W16 + i];
-                }
-            }
+        // one node slot (the root, whose children are leaves) and one leaf slot
+        const uint32_t* src = a.words32 + (size_t)t0 * 4;
+        if (tid < 4 * nt) {
+            const int t = tid >> 2, w = tid & 3;
+            const uint32_t o = a.toff[t];
+            uint32_t v = src[tid];
+            if (w < 2) v += (o >> 16) << 16;
+            lds[w < 2 ? (o & 0xffffu) + (uint32_t)w : (o >> 16) + (uint32_t)(w - 2)] = v;
         }
     }
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -700,6 +752,20 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     // 4k + i/16, which land on tile dwords 256k + 4i .. +3 = quad * 64 + chain
     const uint32_t* fsrc = a.Fg + (int64_t)(lane >> 4) * a.fg_stride + 4 * (lane & 15);
     static_assert(Q % 4 == 0, "whole quad groups");
+    // the roots of the first eight trees and their children's slots: the
+    // same for every chain, read once
+    constexpr bool ROOTS = DEPTH >= 2;
+    uint32_t rnode[G], rlo[G], rhi[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        rnode[g] = rlo[g] = rhi[g] = 0u;
+        if (ROOTS && g < nt) {
+            rnode[g] = *reinterpret_cast<const uint32_t*>(L + (a.toff[g] & 0xffffu) * 4u);
+            const uint64_t pr = *reinterpret_cast<const uint64_t*>(L + (rnode[g] >> 14));
+            rlo[g] = (uint32_t)pr;
+            rhi[g] = (uint32_t)(pr >> 32);
+        }
+    }
     const int64_t b_first = (int64_t)cs * a.slice_blocks;
     auto claim_next = [&]() -> uint32_t {
         uint32_t r = 0;
@@ -722,6 +788,14 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
         const int64_t c = b * 64 + lane;
         const bool active = c < n;
         int t = 0;
+        if (ROOTS && nt >= G) {
+            uint32_t nbr[G], v[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) nbr[g] = 0u;
+            walk8_roll<(ROOTS ? DEPTH : 2), true>(L, nbr, fb, a.mask, rnode, rlo, rhi, v);
+            if (active) store_vals<G>(a, t0, c, v);
+            t = G;
+        }
         for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
         walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
         b = nb;
@@ -743,7 +817,8 @@ bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TR
         if (lo > TREE_LDS_FREE) return false;
         gaps[ng++] = Gap{lo, hi};
     }
-    const uint32_t nbytes = 4u << (depth - 1), lbytes = 4u << depth;
+    // node and leaf blocks: 2^(depth-1) slots of 8 bytes each
+    const uint32_t nbytes = 4u << depth, lbytes = 4u << depth;
     uint32_t noff[TREES_MAX], loff[TREES_MAX];
     auto place = [&](uint32_t bytes, uint32_t& off) {
         for (int i = 0; i < ng; ++i) {
@@ -890,7 +965,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     ca.trace = trace;
 
     TreeArgs ta{};
-    ta.words16 = e.words16;
+    ta.words32 = e.words32;
     ta.n_trees = e.n_trees;
     ta.Fg = ca.Fg;
     ta.fg_stride = fg_stride;
