@@ -74,29 +74,42 @@ struct ChainArgs {
 constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 constexpr int WAIT_LGKM0 = (15) | (3 << 14) | (7 << 4);
 
-// Score of the pending candidates of chains c0 .. c0+nc-1: lane j < nc adds
+// Score of the pending candidates of chains c0 .. c0+nc-1 (the first passes
+// issued by fold_prime): lane j < nc adds
 // its chain's leaf values in tree order (fp32, from +0.0f).  All 64 lanes of
 // the calling wave move the values into a ring of FOLD_R LDS buffers: pass p
 // (groups p*FOLD_P ..) goes to buffer p % FOLD_R, instruction i of a pass
 // moves groups 4i .. 4i+3 of the 16 chains (lane l: group 4i + l/16, chain
 // c0 + l%16), so buffer entry g * 16 + j holds group g of chain c0 + j.
 // FOLD_R - 1 passes stay in flight while one is folded.
+// Issues the moves of pass p into its ring buffer (all 64 lanes).
+__device__ __forceinline__ void fold_issue(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
+                                           float4* ring, int lane, int p) {
+    const int groups = (T + 3) >> 2;
+    const int j = lane & (CPW - 1);
+    const int64_t cj = c0 + (j < nc ? j : nc - 1);
+    float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
+#pragma unroll
+    for (int ins = 0; ins < FOLD_P / 4; ++ins) {
+        const int g = p * FOLD_P + ins * 4 + (lane >> 4);
+        const int gc = g < groups ? g : groups - 1;
+        __builtin_amdgcn_global_load_lds(V4 + (int64_t)gc * n + cj, buf + ins * 64, 16, 0, 0);
+    }
+}
+
+// The first FOLD_R - 1 passes, issued before fold_ring (as early as the
+// kernel can, so that they overlap its set-up).
+__device__ __forceinline__ void fold_prime(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
+                                           float4* ring, int lane) {
+    const int npass = (((T + 3) >> 2) + FOLD_P - 1) / FOLD_P;
+    for (int p = 0; p < FOLD_R - 1 && p < npass; ++p) fold_issue(V4, n, T, c0, nc, ring, lane, p);
+}
+
 __device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
                                            float4* ring, int lane) {
     const int groups = (T + 3) >> 2;
     const int npass = (groups + FOLD_P - 1) / FOLD_P;
-    const int j = lane & (CPW - 1);
-    const int64_t cj = c0 + (j < nc ? j : nc - 1);
-    auto issue = [&](int p) {
-        float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
-#pragma unroll
-        for (int ins = 0; ins < FOLD_P / 4; ++ins) {
-            const int g = p * FOLD_P + ins * 4 + (lane >> 4);
-            const int gc = g < groups ? g : groups - 1;
-            __builtin_amdgcn_global_load_lds(V4 + (int64_t)gc * n + cj, buf + ins * 64, 16, 0, 0);
-        }
-    };
-    for (int p = 0; p < FOLD_R - 1 && p < npass; ++p) issue(p);
+    auto issue = [&](int p) { fold_issue(V4, n, T, c0, nc, ring, lane, p); };
     float s = 0.0f;
     for (int p = 0; p < npass; ++p) {
         if (p + FOLD_R - 1 < npass) {
@@ -164,7 +177,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     // dynamic LDS: the fold ring, then the chains' best lists [CPW][topk]
     extern __shared__ float4 ring[];
     __shared__ ChainRec rec[CPW];
-    __shared__ uint8_t frow[CPW][RS];
+    __shared__ __attribute__((aligned(16))) uint8_t frow[CPW][RS];
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int64_t c0 = (int64_t)blockIdx.x * CPW;
@@ -176,6 +189,8 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     const int gj = tid >> 4, gr = tid & 15;
     const uint64_t gmask = 0xffffull << (16 * (gj & 3));
     const bool gvalid = gj < nc;
+    // leaf values of the pending candidates start streaming in at once
+    if (a.fin != FIN_NONE && wave == 0) fold_prime(reinterpret_cast<const float4*>(a.V), a.n, a.T, c0, nc, ring, tid);
 
     // The workgroup's space: when all its chains share one space whose split
     // tables fit, the descriptor and tables are staged in LDS; otherwise each
@@ -368,14 +383,13 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     __syncthreads();
     // packed rows out (4x+3 per byte, the tree kernel's tile encoding),
     // consecutive lanes on consecutive chains
-    for (int idx = tid; idx < nc * Q; idx += CHAIN_WG) {
-        const int q = idx / nc, j = idx - q * nc;
-        uint32_t w = 0;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int f = 4 * q + b;
-            if (f < N::F) w |= (4u * frow[j][f] + 3u) << (8 * b);
-        }
+    // (a feature value x <= 63 makes (x << 2) | 3 stay within its byte)
+    constexpr uint32_t LAST = (N::F & 3) ? (1u << (8 * (N::F & 3))) - 1u : 0xffffffffu;
+    for (int idx = tid; idx < CPW * Q; idx += CHAIN_WG) {
+        const int q = idx >> 4, j = idx & (CPW - 1);
+        if (j >= nc) continue;
+        uint32_t w = (*reinterpret_cast<const uint32_t*>(&frow[j][4 * q]) << 2) | 0x03030303u;
+        if (q == Q - 1) w &= LAST;
         a.Fg[(int64_t)q * a.fg_stride + c0 + j] = w;
     }
 }
