@@ -46,6 +46,12 @@ struct ChainRec {
     uint32_t qual;
     uint64_t kth_cfg;
     uint32_t nx[MAX_KNOBS / 2];   // proposed knob values, packed in pairs
+    // chain-local path, ahead of time: the next candidate if this one is
+    // rejected (nx holds the one if it is accepted), and which of the two
+    // feature rows the next round uses (0: accepted, 1: rejected)
+    uint32_t nxb[MAX_KNOBS / 2];
+    uint32_t sel;
+    uint64_t cfga, cfgb;          // configuration indices of nx and nxb
 };
 
 // Offers (cfg, sc) to the best list of one chain held in LDS, with the 16

@@ -75,6 +75,7 @@ struct LocalArgs {
     uint32_t off_lv;
     int lv_stride;            // floats per chain row of leaf values: two chunk slots (one when resident)
     uint32_t off_lists, off_rec, off_frow, off_any, off_desc;
+    uint32_t frow_stride;     // tail: bytes between the two feature-row buffers
 };
 
 // Leaf indices of four trees for this lane: nb holds the LDS byte addresses
@@ -156,45 +157,48 @@ __device__ __forceinline__ void load_trees(const LocalArgs& a, uint8_t* dst, int
 // operations complete before it arrives; global loads stay in flight.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Adds the leaf values row[0 .. nt) to s in order, eight float4 reads ahead
-// of the adds (row 16-byte aligned; nt a multiple of 4 except in a last,
-// partial chunk).
+// Adds the leaf values row[0 .. nt) to s in order (row 16-byte aligned).
+// Two sets of eight float4 registers alternate, so the reads of one block
+// of 32 values are in flight while the previous block is added (no copies
+// between the sets, which would make the adds wait for the reads).
+__device__ __forceinline__ void add4(float& s, const float4& v) {
+    s = s + v.x;
+    s = s + v.y;
+    s = s + v.z;
+    s = s + v.w;
+}
+
 __device__ __forceinline__ float fold_row(float s, const float* __restrict__ row, int nt) {
     const float4* r4 = reinterpret_cast<const float4*>(row);
     const int n4 = nt >> 2;
-    int i = 0;
-    if (n4 >= 8) {
-        float4 cur[8], nxt[8];
+    if (n4 > 0) {
+        // reads past the last float4 re-read it (clamped) and are not added
+        const int last = n4 - 1;
+        float4 A[8], B[8];
 #pragma unroll
-        for (int g = 0; g < 8; ++g) cur[g] = r4[g];
-        for (; i + 16 <= n4; i += 8) {
+        for (int g = 0; g < 8; ++g) A[g] = r4[g < last ? g : last];
+        int i = 0;
+        for (; i + 16 <= n4; i += 16) {
 #pragma unroll
-            for (int g = 0; g < 8; ++g) nxt[g] = r4[i + 8 + g];
+            for (int g = 0; g < 8; ++g) B[g] = r4[i + 8 + g];
 #pragma unroll
-            for (int g = 0; g < 8; ++g) {
-                s = s + cur[g].x;
-                s = s + cur[g].y;
-                s = s + cur[g].z;
-                s = s + cur[g].w;
-            }
+            for (int g = 0; g < 8; ++g) add4(s, A[g]);
 #pragma unroll
-            for (int g = 0; g < 8; ++g) cur[g] = nxt[g];
+            for (int g = 0; g < 8; ++g) A[g] = r4[i + 16 + g < last ? i + 16 + g : last];
+#pragma unroll
+            for (int g = 0; g < 8; ++g) add4(s, B[g]);
         }
+        // A holds float4 i .. i + 7; fewer than 16 remain
 #pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            s = s + cur[g].x;
-            s = s + cur[g].y;
-            s = s + cur[g].z;
-            s = s + cur[g].w;
+        for (int g = 0; g < 8; ++g)
+            if (i + g < n4) add4(s, A[g]);
+        if (i + 8 < n4) {
+#pragma unroll
+            for (int g = 0; g < 8; ++g) B[g] = r4[i + 8 + g < last ? i + 8 + g : last];
+#pragma unroll
+            for (int g = 0; g < 8; ++g)
+                if (i + 8 + g < n4) add4(s, B[g]);
         }
-        i += 8;
-    }
-    for (; i < n4; ++i) {
-        const float4 v = r4[i];
-        s = s + v.x;
-        s = s + v.y;
-        s = s + v.z;
-        s = s + v.w;
     }
     for (int t = n4 * 4; t < nt; ++t) s = s + row[t];
     return s;
@@ -214,6 +218,22 @@ __device__ __forceinline__ void draw_move(const SpaceDesc& sd, uint32_t k0, uint
         v = uniform_below(rr.y, sd.knob_size[jm] - 1u);
         radix = sd.radix[jm];
     }
+}
+
+// base with knob jm moved to the drawn value v shifted past base's value
+// (jm < 0: no knob can move), and the configuration index of the result.
+__device__ __forceinline__ void apply_move(const uint32_t (&base)[MAX_KNOBS], uint64_t base_cfg, int jm, uint32_t v,
+                                           uint64_t radix, uint32_t (&out)[MAX_KNOBS], uint64_t& cfg) {
+    uint32_t old = 0;
+#pragma unroll
+    for (int j = 0; j < MAX_KNOBS; ++j) {
+        old = (j == jm) ? base[j] : old;
+        out[j] = (j == jm) ? v + (v >= base[j] ? 1u : 0u) : base[j];
+    }
+    // the index moves by (new - old) times the knob's weight
+    const uint32_t nv = v + (v >= old ? 1u : 0u);
+    cfg = jm < 0 ? base_cfg
+                 : (nv >= old ? base_cfg + (uint64_t)(nv - old) * radix : base_cfg - (uint64_t)(old - nv) * radix);
 }
 
 template <int TMPL, int DEPTH>
@@ -275,12 +295,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             ld[i] = (i >= SO && i < SO + MAX_AXES) ? gd[i] - (uint32_t)fac_lo : gd[i];
         for (int i = tid; i < fac_n; i += nthreads) s_fac[i] = a.factors[fac_lo + i];
     }
-    // space of the owner's chain and of the group's chain: the staged copy in
-    // LDS or the set's tables in global memory.  Each use branches on
+    // space of the owner's chain: the staged copy in LDS or the set's tables
+    // in global memory.  Each use branches on
     // `staged` (uniform in the workgroup) so that either branch reads one
     // address space directly.
     const SpaceDesc* sdp_g = a.descs + space_of(a.offsets, a.n_spaces, c);
-    const SpaceDesc* gsdp_g = a.descs + space_of(a.offsets, a.n_spaces, c0 + gjc);
     auto with_space = [&](auto&& f) {
         if (staged) f(s_desc);
         else f(*sdp_g);
@@ -353,15 +372,45 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     if (owner && a.steps > 0)
         with_space([&](const SpaceDesc& sd) { draw_move(sd, k0, k1, gchain, a.step0, mv_j, mv_v, mv_radix); });
 
+    // Loop gr's features of chain j's configuration nx into row dst.
+    auto eval_loop = [&](const uint32_t (&nx)[MAX_KNOBS], int j, int gr_, uint8_t* dst) {
+        auto feats = [&](const SpaceDesc& sd, const uint64_t* facp) {
+            uint32_t fac[6][4];
+            gather_factors<TMPL>(sd, facp, nx, fac);
+            uint32_t f[11];
+            loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr_, f);
+#pragma unroll
+            for (int i = 0; i < 11; ++i) dst[gr_ * 11 + i] = (uint8_t)f[i];
+        };
+        if (staged) feats(s_desc, s_fac);
+        else feats(a.descs[space_of(a.offsets, a.n_spaces, c0 + j)], a.factors);
+    };
+    auto unpack = [](const uint32_t (&w)[MAX_KNOBS / 2], uint32_t (&nx)[MAX_KNOBS]) {
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (w[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+    };
+    // tail mode works a round ahead: while a round's scores are folded, the
+    // other waves evaluate the next round's candidate both for an accepted
+    // and for a rejected current one (feature rows 0 and 1), so a round
+    // starts from ready rows.  Owners keep both candidates (na, nb).
+    const int cpb_log2 = __builtin_ctz((unsigned)cpb);
+    uint32_t cd[MAX_KNOBS];
+    uint64_t cfg = 0;
+#pragma unroll
+    for (int j = 0; j < MAX_KNOBS; ++j) cd[j] = 0u;
     for (int r = 0; r < rounds; ++r) {
         const bool is_init = a.init && r == 0;
         const int s = r - (a.init ? 1 : 0);
+        const bool ahead = a.tail && r > 0;   // this round's candidate and rows are ready
+        const bool more = r + 1 < rounds;
         // (1) candidate: the initial draw (block (chain, 0, 1, j / 4)) or one
         // knob moved to a uniformly chosen other value
-        uint32_t cd[MAX_KNOBS];
         float thr_v = 0.0f;
-        uint64_t cfg = 0;
-        if (owner) {
+        if (owner && ahead) {
+            thr_v = thr_next;
+            if (s + 1 < a.steps) thr_next = a.thr[c * a.steps + s + 1];
+        } else if (owner) {
+            cfg = 0;
             if (is_init) {
                 with_space([&](const SpaceDesc& sd) {
                     U4 rr{0, 0, 0, 0};
@@ -376,49 +425,43 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             } else {
                 thr_v = thr_next;
                 if (s + 1 < a.steps) thr_next = a.thr[c * a.steps + s + 1];
-                uint32_t old = 0;
-#pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j) {
-                    old = (j == mv_j) ? cur[j] : old;
-                    cd[j] = (j == mv_j) ? mv_v + (mv_v >= cur[j] ? 1u : 0u) : cur[j];
-                }
-                // the index moves by (new - old) times the knob's weight
-                const uint32_t nv = mv_v + (mv_v >= old ? 1u : 0u);
-                cfg = mv_j < 0 ? cur_cfg
-                               : (nv >= old ? cur_cfg + (uint64_t)(nv - old) * mv_radix
-                                            : cur_cfg - (uint64_t)(old - nv) * mv_radix);
+                apply_move(cur, cur_cfg, mv_j, mv_v, mv_radix, cd, cfg);
             }
 #pragma unroll
             for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = cd[2 * j] | (cd[2 * j + 1] << 16);
         }
-        lds_barrier();
-        // (2) features: lane gr of group gj evaluates loop gr of chain gj
-        if (gvalid && gr < N::L) {
-            uint32_t nx[MAX_KNOBS];
-#pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (rec[gj].nx[j >> 1] >> (16 * (j & 1))) & 0xffffu;
-            auto feats = [&](const SpaceDesc& sd, const uint64_t* facp) {
-                uint32_t fac[6][4];
-                gather_factors<TMPL>(sd, facp, nx, fac);
-                uint32_t f[11];
-                loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f);
-#pragma unroll
-                for (int i = 0; i < 11; ++i) frow[gj * RS + gr * 11 + i] = (uint8_t)f[i];
-            };
-            if (staged) feats(s_desc, s_fac);
-            else feats(*gsdp_g, a.factors);
+        if (!ahead) {
+            lds_barrier();
+            // (2) features: lane gr of group gj evaluates loop gr of chain gj
+            if (gvalid && gr < N::L) {
+                uint32_t nx[MAX_KNOBS];
+                unpack(rec[gj].nx, nx);
+                eval_loop(nx, gj, gr, frow + gj * RS);
+            }
+            lds_barrier();
         }
-        lds_barrier();
         // (3) the tile: column l holds chain l % cpb (the last chain stands
         // in for missing ones), bytes 4x+3
         // (features are at most 31, so 4x+3 stays within each byte; bytes past
         // the last feature are never read)
-        for (int i = tid; i < Q * 64; i += nthreads) {
-            const int q = i >> 6;
-            int j = i & (cpb - 1);
+        {
+            // thread tid fills tile words tid, tid + 512, ...: always chain
+            // j = tid % cpb (cpb divides 512)
+            constexpr int TU = (Q * 64 + LOCAL_WG_MAX - 1) / LOCAL_WG_MAX;
+            int j = tid & (cpb - 1);
             j = j < nc ? j : nc - 1;
-            const uint32_t w = *reinterpret_cast<const uint32_t*>(frow + j * RS + 4 * q);
-            tile[i] = (w << 2) | 0x03030303u;
+            const uint8_t* row = frow + (ahead ? rec[j].sel * a.frow_stride : 0u) + j * RS;
+            uint32_t w[TU];
+#pragma unroll
+            for (int u = 0; u < TU; ++u) {
+                const int i = tid + u * LOCAL_WG_MAX;
+                if (i < Q * 64) w[u] = *reinterpret_cast<const uint32_t*>(row + 4 * (i >> 6));
+            }
+#pragma unroll
+            for (int u = 0; u < TU; ++u) {
+                const int i = tid + u * LOCAL_WG_MAX;
+                if (i < Q * 64) tile[i] = (w[u] << 2) | 0x03030303u;
+            }
         }
         float sc = 0.0f;
         if (a.tail) {
@@ -426,10 +469,25 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             // levels from LDS, then the last level and its leaf from the
             // tree's 16-byte tail record; thread t takes chain t % cpb and
             // trees u, u + S, u + 2S, u + 3S (S = threads / cpb)
-            if (owner && s + 1 < a.steps)
+            if (owner && more) {
                 with_space([&](const SpaceDesc& sd) {
                     draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
                 });
+                // the next candidate after an accept (from cd) and after a
+                // reject (from cur; after the initial draw, which is always
+                // accepted, also from cd), kept in the chain's record
+                uint32_t nx[MAX_KNOBS];
+                uint64_t ncfg;
+                apply_move(cd, cfg, mv_j, mv_v, mv_radix, nx, ncfg);
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = nx[2 * j] | (nx[2 * j + 1] << 16);
+                rec[tid].cfga = ncfg;
+                if (is_init) apply_move(cd, cfg, mv_j, mv_v, mv_radix, nx, ncfg);
+                else apply_move(cur, cur_cfg, mv_j, mv_v, mv_radix, nx, ncfg);
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nxb[j] = nx[2 * j] | (nx[2 * j + 1] << 16);
+                rec[tid].cfgb = ncfg;
+            }
             lds_barrier();
             const int S = nthreads / cpb;
             const int ua = tid / cpb;
@@ -460,7 +518,20 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                 }
             }
             lds_barrier();
-            if (wave == 0 && lane < nc) sc = fold_row(sc, lv + lane * a.lv_stride, a.T);
+            if (wave == 0) {
+                if (lane < nc) sc = fold_row(sc, lv + lane * a.lv_stride, a.T);
+            } else if (more) {
+                // the next round's feature rows: item (v * cpb + j) * 16 + gr
+                // is loop gr of chain j's candidate for outcome v
+                for (int it = tid - 64; it < 32 * cpb; it += nthreads - 64) {
+                    const int gr2 = it & 15, j = (it >> 4) & (cpb - 1), v = (it >> 4) >> cpb_log2;
+                    if (j < nc && gr2 < N::L) {
+                        uint32_t nx[MAX_KNOBS];
+                        unpack(v ? rec[j].nxb : rec[j].nx, nx);
+                        eval_loop(nx, j, gr2, frow + v * a.frow_stride + j * RS);
+                    }
+                }
+            }
         } else {
         // (4) chunk pipeline.  Iteration it: loaders bring chunk it + 1;
         // walkers walk chunk it and write its leaf values (leaves gathered
@@ -545,6 +616,8 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             R.cfg = cfg;
             R.score = sc;
             R.qual = qual ? 1u : 0u;
+            // the next round's rows (read after the barrier below)
+            R.sel = (is_init || (sc - cur_s) >= thr_v) ? 0u : 1u;
             if (qual) atomicOr(&s_any[r & 1], 1u);
         }
         if (tid == 0) s_any[(r + 1) & 1] = 0u;
@@ -570,6 +643,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                 for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
                 cur_s = sc;
                 cur_cfg = cfg;
+            }
+            if (a.tail && more) {
+                const ChainRec& R = rec[tid];
+                unpack(acc ? R.nx : R.nxb, cd);
+                cfg = acc ? R.cfga : R.cfgb;
             }
         }
     }
@@ -690,7 +768,7 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
         pl.ts = ts_full;
         pl.ct = ct_res;
         pl.ring_bytes = (uint32_t)res_bytes;
-    } else if (d >= 2 && top_bytes + lv_all <= avail) {
+    } else if (d >= 2 && top_bytes + lv_all + al16((size_t)cpb * RS) <= avail) {
         pl.tail = 1;
         pl.resident = 0;
         pl.gather = 0;
@@ -729,7 +807,10 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     pl.off_rec = (uint32_t)off;
     off += al16((size_t)cpb * sizeof(ChainRec));
     pl.off_frow = (uint32_t)off;
-    off += al16((size_t)cpb * RS);
+    // tail: two buffers, the next round's rows for an accepted and for a
+    // rejected candidate
+    pl.frow_stride = pl.tail ? (uint32_t)al16((size_t)cpb * RS) : 0u;
+    off += al16((size_t)cpb * RS) + pl.frow_stride;
     pl.off_any = (uint32_t)off;
     off += 16;
     pl.off_desc = (uint32_t)off;
@@ -794,6 +875,7 @@ hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chain
     a.off_lists = pl.off_lists;
     a.off_rec = pl.off_rec;
     a.off_frow = pl.off_frow;
+    a.frow_stride = pl.frow_stride;
     a.off_any = pl.off_any;
     a.walk_waves = pl.walk_waves;
     a.off_desc = pl.off_desc;
