@@ -52,6 +52,7 @@ struct ChainRec {
     uint32_t nxb[MAX_KNOBS / 2];
     uint32_t sel;
     uint64_t cfga, cfgb;          // configuration indices of nx and nxb
+    float thr;                    // the next round's Metropolis threshold
 };
 
 // Offers (cfg, sc) to the best list of one chain held in LDS, with the 16

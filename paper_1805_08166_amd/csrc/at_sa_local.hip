@@ -157,10 +157,11 @@ __device__ __forceinline__ void load_trees(const LocalArgs& a, uint8_t* dst, int
 // operations complete before it arrives; global loads stay in flight.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Adds the leaf values row[0 .. nt) to s in order (row 16-byte aligned).
-// Two sets of eight float4 registers alternate, so the reads of one block
-// of 32 values are in flight while the previous block is added (no copies
-// between the sets, which would make the adds wait for the reads).
+// Adds the leaf values row[0 .. nt) to s in order (row 16-byte aligned):
+// blocks of sixteen float4 reads in flight, then their 64 adds; the rest in
+// batches of 8, 4, 2 and 1 float4.  Nothing is carried from one block to
+// the next but s, so the compiler has no registers to shuffle between
+// blocks, and every branch is uniform (no selects in the chain of adds).
 __device__ __forceinline__ void add4(float& s, const float4& v) {
     s = s + v.x;
     s = s + v.y;
@@ -168,38 +169,33 @@ __device__ __forceinline__ void add4(float& s, const float4& v) {
     s = s + v.w;
 }
 
+template <int B>
+__device__ __forceinline__ void fold_block(float& s, const float4* __restrict__ r4) {
+    float4 R[B];
+#pragma unroll
+    for (int g = 0; g < B; ++g) R[g] = r4[g];
+#pragma unroll
+    for (int g = 0; g < B; ++g) add4(s, R[g]);
+}
+
 __device__ __forceinline__ float fold_row(float s, const float* __restrict__ row, int nt) {
     const float4* r4 = reinterpret_cast<const float4*>(row);
     const int n4 = nt >> 2;
-    if (n4 > 0) {
-        // reads past the last float4 re-read it (clamped) and are not added
-        const int last = n4 - 1;
-        float4 A[8], B[8];
-#pragma unroll
-        for (int g = 0; g < 8; ++g) A[g] = r4[g < last ? g : last];
-        int i = 0;
-        for (; i + 16 <= n4; i += 16) {
-#pragma unroll
-            for (int g = 0; g < 8; ++g) B[g] = r4[i + 8 + g];
-#pragma unroll
-            for (int g = 0; g < 8; ++g) add4(s, A[g]);
-#pragma unroll
-            for (int g = 0; g < 8; ++g) A[g] = r4[i + 16 + g < last ? i + 16 + g : last];
-#pragma unroll
-            for (int g = 0; g < 8; ++g) add4(s, B[g]);
-        }
-        // A holds float4 i .. i + 7; fewer than 16 remain
-#pragma unroll
-        for (int g = 0; g < 8; ++g)
-            if (i + g < n4) add4(s, A[g]);
-        if (i + 8 < n4) {
-#pragma unroll
-            for (int g = 0; g < 8; ++g) B[g] = r4[i + 8 + g < last ? i + 8 + g : last];
-#pragma unroll
-            for (int g = 0; g < 8; ++g)
-                if (i + 8 + g < n4) add4(s, B[g]);
-        }
+    int i = 0;
+    for (; i + 16 <= n4; i += 16) fold_block<16>(s, r4 + i);
+    if (n4 - i >= 8) {
+        fold_block<8>(s, r4 + i);
+        i += 8;
     }
+    if (n4 - i >= 4) {
+        fold_block<4>(s, r4 + i);
+        i += 4;
+    }
+    if (n4 - i >= 2) {
+        fold_block<2>(s, r4 + i);
+        i += 2;
+    }
+    if (n4 - i >= 1) fold_block<1>(s, r4 + i);
     for (int t = n4 * 4; t < nt; ++t) s = s + row[t];
     return s;
 }
@@ -357,7 +353,9 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     const uint32_t fb = lbase | (uint32_t)lane * 4u;
     const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
     const uint32_t gchain = (uint32_t)(a.chain0 + (uint64_t)c);
-    // the owner's next threshold and move, ready one round ahead
+    // the owner's next threshold and move, ready one round ahead (in tail
+    // mode the threshold of each round after the first is brought into the
+    // chain's record by the last wave during the previous fold)
     float thr_next = (owner && a.steps > 0) ? a.thr[c * a.steps] : 0.0f;
     int mv_j = -1;
     uint32_t mv_v = 0u;
@@ -407,8 +405,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         // knob moved to a uniformly chosen other value
         float thr_v = 0.0f;
         if (owner && ahead) {
-            thr_v = thr_next;
-            if (s + 1 < a.steps) thr_next = a.thr[c * a.steps + s + 1];
+            thr_v = rec[tid].thr;
         } else if (owner) {
             cfg = 0;
             if (is_init) {
@@ -521,6 +518,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             if (wave == 0) {
                 if (lane < nc) sc = fold_row(sc, lv + lane * a.lv_stride, a.T);
             } else if (more) {
+                if (wave == nthreads / 64 - 1 && lane < nc) rec[lane].thr = a.thr[(c0 + lane) * a.steps + s + 1];
                 // the next round's feature rows: item (v * cpb + j) * 16 + gr
                 // is loop gr of chain j's candidate for outcome v
                 for (int it = tid - 64; it < 32 * cpb; it += nthreads - 64) {
