@@ -53,6 +53,13 @@ struct ChainRec {
     uint32_t sel;
     uint64_t cfga, cfgb;          // configuration indices of nx and nxb
     float thr;                    // the next round's Metropolis threshold
+    // drawn moves by step parity (knob, value, knob weight) and the scored
+    // candidates waiting for their offer, by round parity
+    int32_t mvj[2];
+    uint32_t mvv[2];
+    uint64_t mvr[2];
+    uint64_t pcfg[2];
+    float pscore[2];
 };
 
 // Offers (cfg, sc) to the best list of one chain held in LDS, with the 16

@@ -369,6 +369,47 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         });
     if (owner && a.steps > 0)
         with_space([&](const SpaceDesc& sd) { draw_move(sd, k0, k1, gchain, a.step0, mv_j, mv_v, mv_radix); });
+    // Tail mode with at most four chains per workgroup takes the owners'
+    // side work off the path from one fold to the next: a helper wave draws
+    // the moves two steps ahead, and a round's candidates are offered to the
+    // best lists by another wave during the next round's fold (the offers of
+    // a chain stay in round order).  Roles during a fold: wave 0 folds,
+    // waves 1-2 evaluate the next candidates, wave 3 offers, wave 4 draws,
+    // the last wave brings the next thresholds.
+    const bool fast = a.tail && cpb <= 4 && nthreads == LOCAL_WG_MAX;
+    auto draw_into = [&](int j, int st) {
+        // move of step st for chain j into its record (slot st & 1)
+        int jm;
+        uint32_t v;
+        uint64_t radix;
+        const uint32_t gch = (uint32_t)(a.chain0 + (uint64_t)(c0 + j));
+        if (staged) draw_move(s_desc, k0, k1, gch, a.step0 + (uint32_t)st, jm, v, radix);
+        else draw_move(a.descs[space_of(a.offsets, a.n_spaces, c0 + j)], k0, k1, gch, a.step0 + (uint32_t)st, jm, v,
+                       radix);
+        rec[j].mvj[st & 1] = jm;
+        rec[j].mvv[st & 1] = v;
+        rec[j].mvr[st & 1] = radix;
+    };
+    // offer of round rr's candidates (waiting in the records) by the 16-lane
+    // groups of one wave: group g takes chain g
+    auto offer_pending = [&](int rr) {
+        const int g = lane >> 4, gl = lane & 15;
+        const int jc = g < nc ? g : 0;
+        ChainRec& R = rec[jc];
+        const uint64_t pc = R.pcfg[rr & 1];
+        const float ps = R.pscore[rr & 1];
+        const bool first = a.init && rr == 0;
+        const bool q = g < nc && (first || (int)R.count < k || precedes(ps, pc, R.kth_score, R.kth_cfg));
+        if (gl == 0 && g < nc) {
+            R.cfg = pc;
+            R.score = ps;
+        }
+        group_offer(lists + jc * k, R, k, gl, 0xffffull << (16 * g), q);
+    };
+    if (fast && owner) {
+        const int s1 = (a.init ? -1 : 0) + 1;
+        if (s1 < a.steps) draw_into(tid, s1);
+    }
 
     // Loop gr's features of chain j's configuration nx into row dst.
     auto eval_loop = [&](const uint32_t (&nx)[MAX_KNOBS], int j, int gr_, uint8_t* dst) {
@@ -467,9 +508,16 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             // tree's 16-byte tail record; thread t takes chain t % cpb and
             // trees u, u + S, u + 2S, u + 3S (S = threads / cpb)
             if (owner && more) {
-                with_space([&](const SpaceDesc& sd) {
-                    draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
-                });
+                if (fast) {
+                    const int sl = (s + 1) & 1;
+                    mv_j = rec[tid].mvj[sl];
+                    mv_v = rec[tid].mvv[sl];
+                    mv_radix = rec[tid].mvr[sl];
+                } else {
+                    with_space([&](const SpaceDesc& sd) {
+                        draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
+                    });
+                }
                 // the next candidate after an accept (from cd) and after a
                 // reject (from cur; after the initial draw, which is always
                 // accepted, also from cd), kept in the chain's record
@@ -517,7 +565,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             lds_barrier();
             if (wave == 0) {
                 if (lane < nc) sc = fold_row(sc, lv + lane * a.lv_stride, a.T);
-            } else if (more) {
+            } else {
+                if (fast && wave == 3 && r > 0) offer_pending(r - 1);
+                if (fast && wave == 4 && lane < nc && s + 2 < a.steps) draw_into(lane, s + 2);
+            }
+            if (wave > 0 && more) {
                 if (wave == nthreads / 64 - 1 && lane < nc) rec[lane].thr = a.thr[(c0 + lane) * a.steps + s + 1];
                 // the next round's feature rows: item (v * cpb + j) * 16 + gr
                 // is loop gr of chain j's candidate for outcome v
@@ -608,6 +660,34 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         }
         // (5) offer to the best list when some chain qualifies, then the
         // Metropolis test
+        if (fast) {
+            if (owner) {
+                const bool acc = is_init || (sc - cur_s) >= thr_v;
+                if (!is_init && a.trace) {
+                    at_entry tr;
+                    tr.cfg = cfg;
+                    tr.score = sc;
+                    tr.flag = acc ? 1u : 0u;
+                    a.trace[c * a.steps + s] = tr;
+                }
+                ChainRec& R = rec[tid];
+                R.pcfg[r & 1] = cfg;
+                R.pscore[r & 1] = sc;
+                R.sel = acc ? 0u : 1u;
+                if (acc) {
+#pragma unroll
+                    for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
+                    cur_s = sc;
+                    cur_cfg = cfg;
+                }
+                if (more) {
+                    unpack(acc ? R.nx : R.nxb, cd);
+                    cfg = acc ? R.cfga : R.cfgb;
+                }
+            }
+            lds_barrier();
+            continue;
+        }
         if (owner) {
             ChainRec& R = rec[tid];
             const bool qual = is_init || (int)R.count < k || precedes(sc, cfg, R.kth_score, R.kth_cfg);
@@ -650,6 +730,8 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         }
     }
 
+    // the last round's offer (the loop ended on a barrier)
+    if (fast && rounds > 0 && wave == 3) offer_pending(rounds - 1);
     // write the chain state and the best lists back
     __syncthreads();
     if (owner) {

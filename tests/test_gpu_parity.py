@@ -460,6 +460,8 @@ LOCAL_PLANS = {
     "gathered": dict(n=64, trees=400, depth=9, steps=20),
     "tail": dict(n=300, trees=300, depth=8, steps=25),
     "tail_depth2": dict(n=1024, trees=2000, depth=2, steps=15),
+    # sixteen chains per workgroup: the tail walk without helper waves
+    "tail_wide": dict(n=4096, trees=300, depth=8, steps=10),
 }
 
 
@@ -476,8 +478,10 @@ def test_sa_local_plans_match_oracle(P, mode):
     ch = mk_chains(P, sp, 0, n, k, seed, "local")
     best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     plan = P.at_chains_last_plan(ch)
-    assert (plan["chunks"] == 0) == (mode in ("resident", "tail", "tail_depth2"))
-    assert plan["gather"] == {"gathered": 1, "tail": 2, "tail_depth2": 2}.get(mode, 0)
+    assert (plan["chunks"] == 0) == (mode in ("resident", "tail", "tail_depth2", "tail_wide"))
+    assert plan["gather"] == {"gathered": 1, "tail": 2, "tail_depth2": 2, "tail_wide": 2}.get(mode, 0)
+    if mode.startswith("tail"):
+        assert (plan["chains_per_wg"] > 4) == (mode == "tail_wide")
     rows = slice(0, min(n, 160))
     m = rows.stop
     och = oracle.Chains([osp], [0, m], seed=seed, chain0=0, topk=k)
