@@ -482,22 +482,27 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         // in for missing ones), bytes 4x+3
         // (features are at most 31, so 4x+3 stays within each byte; bytes past
         // the last feature are never read)
-        {
-            // thread tid fills tile words tid, tid + 512, ...: always chain
-            // j = tid % cpb (cpb divides 512)
-            constexpr int TU = (Q * 64 + LOCAL_WG_MAX - 1) / LOCAL_WG_MAX;
-            int j = tid & (cpb - 1);
+        if (!a.tail || wave > 0) {
+            // In tail mode waves 1.. fill the tile while the owners in wave 0
+            // prepare the next candidates; else every wave does.  Thread t of
+            // the fill fills tile words t, t + NF, ...: always chain t % cpb
+            // (cpb divides NF, 448 or 512).
+            constexpr int NF_MIN = LOCAL_WG_MAX - 64;
+            constexpr int TU = (Q * 64 + NF_MIN - 1) / NF_MIN;
+            const int nf = a.tail ? nthreads - 64 : nthreads;
+            const int t = a.tail ? tid - 64 : tid;
+            int j = t & (cpb - 1);
             j = j < nc ? j : nc - 1;
             const uint8_t* row = frow + (ahead ? rec[j].sel * a.frow_stride : 0u) + j * RS;
             uint32_t w[TU];
 #pragma unroll
             for (int u = 0; u < TU; ++u) {
-                const int i = tid + u * LOCAL_WG_MAX;
+                const int i = t + u * nf;
                 if (i < Q * 64) w[u] = *reinterpret_cast<const uint32_t*>(row + 4 * (i >> 6));
             }
 #pragma unroll
             for (int u = 0; u < TU; ++u) {
-                const int i = tid + u * LOCAL_WG_MAX;
+                const int i = t + u * nf;
                 if (i < Q * 64) tile[i] = (w[u] << 2) | 0x03030303u;
             }
         }
@@ -908,6 +913,8 @@ hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chain
                            hipStream_t stream) {
     const int64_t n = ch.n_chains;
     if (n == 0) return hipSuccess;
+    // the kernel's tile fill and its wave roles assume full workgroups
+    if (pl.threads != LOCAL_WG_MAX) return hipErrorInvalidConfiguration;
     hipError_t err;
     if (!ch.d_meta.p) {
         err = hipMalloc(&ch.d_meta.p, (size_t)n * sizeof(ChainMeta));

@@ -462,6 +462,8 @@ LOCAL_PLANS = {
     "tail_depth2": dict(n=1024, trees=2000, depth=2, steps=15),
     # sixteen chains per workgroup: the tail walk without helper waves
     "tail_wide": dict(n=4096, trees=300, depth=8, steps=10),
+    # four chains per workgroup, the last workgroup holding one
+    "tail_ragged": dict(n=1021, trees=300, depth=8, steps=12),
 }
 
 
@@ -478,12 +480,13 @@ def test_sa_local_plans_match_oracle(P, mode):
     ch = mk_chains(P, sp, 0, n, k, seed, "local")
     best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     plan = P.at_chains_last_plan(ch)
-    assert (plan["chunks"] == 0) == (mode in ("resident", "tail", "tail_depth2", "tail_wide"))
-    assert plan["gather"] == {"gathered": 1, "tail": 2, "tail_depth2": 2, "tail_wide": 2}.get(mode, 0)
+    assert (plan["chunks"] == 0) == (mode in ("resident", "tail", "tail_depth2", "tail_wide", "tail_ragged"))
+    assert plan["gather"] == (2 if mode.startswith("tail") else {"gathered": 1}.get(mode, 0))
     if mode.startswith("tail"):
         assert (plan["chains_per_wg"] > 4) == (mode == "tail_wide")
-    rows = slice(0, min(n, 160))
-    m = rows.stop
-    och = oracle.Chains([osp], [0, m], seed=seed, chain0=0, topk=k)
-    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, m, 0, steps), trace=True)
-    assert_same_run(best, tr, och, otr, rows=rows, cur=export(P, ch))
+    # the first 160 chains, or the last 160 when the last workgroup is short
+    r0 = n - 160 if mode == "tail_ragged" else 0
+    m = min(n - r0, 160)
+    och = oracle.Chains([osp], [0, m], seed=seed, chain0=r0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, r0, m, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, rows=slice(r0, r0 + m), cur=export(P, ch))
