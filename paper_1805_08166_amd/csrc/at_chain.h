@@ -10,6 +10,10 @@
 namespace at {
 namespace dev {
 
+// Workgroup barrier that orders LDS accesses only: each wave's own LDS
+// operations complete before it arrives; global loads stay in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 __device__ __forceinline__ int space_of(const int64_t* offsets, int n_spaces, int64_t c) {
     int w = 0;
     while (w + 1 < n_spaces && offsets[w + 1] <= c) ++w;

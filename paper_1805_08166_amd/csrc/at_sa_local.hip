@@ -153,9 +153,6 @@ __device__ __forceinline__ void load_trees(const LocalArgs& a, uint8_t* dst, int
     }
 }
 
-// Workgroup barrier that orders LDS accesses only: each wave's own LDS
-// operations complete before it arrives; global loads stay in flight.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Adds the leaf values row[0 .. nt) to s in order (row 16-byte aligned):
 // blocks of sixteen float4 reads in flight, then their 64 adds; the rest in

@@ -15,9 +15,11 @@
 // than an in-kernel grid barrier here because the cross-XCD data (features
 // and leaf values) must be written back from the per-XCD L2 caches anyway.
 //
-// V is laid out in groups of four trees: the values of trees 4g..4g+3 for
-// chain c are the 16 bytes at V[(g * n + c) * 4], so the fold reads one
-// float4 per lane per group, coalesced across the wave.
+// V is laid out by blocks of 16 chains, then groups of four trees: the
+// values of trees 4g..4g+3 for chain c are the 16 bytes at float
+// ((c / 16) * G + g) * 64 + (c % 16) * 4 with G = ceil(T / 4) groups, so a
+// chain kernel workgroup (16 chains) reads one contiguous stretch of V and
+// the fold reads one float4 per lane per group.
 #include <cstddef>
 
 #include <hip/hip_ext.h>
@@ -29,8 +31,14 @@ namespace {
 
 using namespace dev;
 
+// Float index of tree t's leaf value for chain c in V (groups: ceil(T / 4)).
+__device__ __forceinline__ int64_t v_index(int64_t c, int t, int groups) {
+    return ((((c >> 4) * groups + (t >> 2)) << 6) + ((c & 15) << 2) + (t & 3));
+}
+
 constexpr int CHAIN_WG = 256;           // wave 0 runs the chains, all four waves move data
 constexpr int CPW = 16;                 // chains per chain-kernel workgroup
+static_assert(CPW == 16, "a chain-kernel workgroup reads one 16-chain block of V");
 constexpr int FOLD_P = 32;              // 4-tree groups per fold pass: 32 x 16 chains x 16 B = 8 KB
 constexpr int FOLD_R = 6;               // passes in the LDS ring (five in flight while one is folded)
 constexpr size_t RING_BYTES = (size_t)FOLD_R * FOLD_P * CPW * 16;
@@ -69,99 +77,108 @@ struct ChainArgs {
     at_entry* best;           // copy of the best lists (last launch), or null
 };
 
-// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
-// 6:4, lgkmcnt 11:8): wait for vmcnt <= n only, or for lgkmcnt 0 only.
-constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-constexpr int WAIT_LGKM0 = (15) | (3 << 14) | (7 << 4);
 
-// Score of the pending candidates of chains c0 .. c0+nc-1 (the first passes
-// issued by fold_prime): lane j < nc adds
-// its chain's leaf values in tree order (fp32, from +0.0f).  All 64 lanes of
-// the calling wave move the values into a ring of FOLD_R LDS buffers: pass p
-// (groups p*FOLD_P ..) goes to buffer p % FOLD_R, instruction i of a pass
-// moves groups 4i .. 4i+3 of the 16 chains (lane l: group 4i + l/16, chain
-// c0 + l%16), so buffer entry g * 16 + j holds group g of chain c0 + j.
-// FOLD_R - 1 passes stay in flight while one is folded.
-// Issues the moves of pass p into its ring buffer (all 64 lanes).
-__device__ __forceinline__ void fold_issue(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
-                                           float4* ring, int lane, int p) {
+// Score of the pending candidates of chains c0 .. c0+nc-1: lane j < nc of
+// wave 0 adds its chain's leaf values in tree order (fp32, from +0.0f).  All
+// four waves move the values into a ring of FOLD_R LDS buffers, each wave two
+// of a pass's eight direct-to-LDS instructions (one wave alone issues them
+// too slowly to keep the fold fed): pass p (groups p*FOLD_P ..) goes to
+// buffer p % FOLD_R, instruction i of a pass moves groups 4i .. 4i+3 of the
+// 16 chains (lane l: group 4i + l/16, chain c0 + l%16), so buffer entry
+// g * 16 + j holds group g of chain c0 + j.  FOLD_R - 1 passes stay in flight
+// while one is folded; a workgroup barrier per pass tells wave 0 that the
+// pass has landed and the other waves that the buffer they refill is free.
+constexpr int FOLD_SHARE = FOLD_P / 4 / (CHAIN_WG / 64);   // instructions per wave and pass
+static_assert(FOLD_SHARE * (CHAIN_WG / 64) * 4 == FOLD_P, "the waves share a pass evenly");
+
+__device__ __forceinline__ void fold_issue(const float4* __restrict__ V4, int T, int64_t c0, int nc, float4* ring,
+                                           int tid, int p) {
+    const int lane = tid & 63, wave = tid >> 6;
     const int groups = (T + 3) >> 2;
     const int j = lane & (CPW - 1);
     const int64_t cj = c0 + (j < nc ? j : nc - 1);
     float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
 #pragma unroll
-    for (int ins = 0; ins < FOLD_P / 4; ++ins) {
+    for (int q = 0; q < FOLD_SHARE; ++q) {
+        const int ins = wave * FOLD_SHARE + q;
         const int g = p * FOLD_P + ins * 4 + (lane >> 4);
         const int gc = g < groups ? g : groups - 1;
-        __builtin_amdgcn_global_load_lds(V4 + (int64_t)gc * n + cj, buf + ins * 64, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(V4 + (((cj >> 4) * groups + gc) << 4) + (cj & 15), buf + ins * 64, 16, 0, 0);
     }
 }
 
-// The first FOLD_R - 1 passes, issued before fold_ring (as early as the
-// kernel can, so that they overlap its set-up).
-__device__ __forceinline__ void fold_prime(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
-                                           float4* ring, int lane) {
+// The first FOLD_R - 1 passes, issued at kernel entry so that they overlap
+// the set-up.
+__device__ __forceinline__ void fold_prime(const float4* __restrict__ V4, int T, int64_t c0, int nc, float4* ring,
+                                           int tid) {
     const int npass = (((T + 3) >> 2) + FOLD_P - 1) / FOLD_P;
-    for (int p = 0; p < FOLD_R - 1 && p < npass; ++p) fold_issue(V4, n, T, c0, nc, ring, lane, p);
+    for (int p = 0; p < FOLD_R - 1 && p < npass; ++p) fold_issue(V4, T, c0, nc, ring, tid, p);
 }
 
-__device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int64_t n, int T, int64_t c0, int nc,
-                                           float4* ring, int lane) {
+// Wait for this wave's moves up to pass p (later = its passes issued after
+// p), then meet the other waves.
+#define AT_VM_BARRIER(K) asm volatile("s_waitcnt vmcnt(" #K ")\n\ts_barrier" ::: "memory")
+__device__ __forceinline__ void pass_barrier(int later) {
+    static_assert(FOLD_SHARE == 2 && FOLD_R == 6, "the waits below count two moves per pass, at most four passes");
+    switch (later) {
+        case 0: AT_VM_BARRIER(0); break;
+        case 1: AT_VM_BARRIER(2); break;
+        case 2: AT_VM_BARRIER(4); break;
+        case 3: AT_VM_BARRIER(6); break;
+        default: AT_VM_BARRIER(8); break;
+    }
+}
+
+// cnt float4 from src (stride CPW float4) added in order: blocks of sixteen
+// reads, then their adds.
+template <int B>
+__device__ __forceinline__ void fold_strided(float& s, const float4* __restrict__ src) {
+    float4 R[B];
+#pragma unroll
+    for (int g = 0; g < B; ++g) R[g] = src[g * CPW];
+#pragma unroll
+    for (int g = 0; g < B; ++g) {
+        s = s + R[g].x;
+        s = s + R[g].y;
+        s = s + R[g].z;
+        s = s + R[g].w;
+    }
+}
+
+// Every wave of the workgroup calls this (it holds workgroup barriers); the
+// score is valid in lanes j < nc of wave 0.
+__device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int T, int64_t c0, int nc, float4* ring,
+                                           int tid) {
+    const int lane = tid & 63, wave = tid >> 6;
     const int groups = (T + 3) >> 2;
     const int npass = (groups + FOLD_P - 1) / FOLD_P;
-    auto issue = [&](int p) { fold_issue(V4, n, T, c0, nc, ring, lane, p); };
     float s = 0.0f;
     for (int p = 0; p < npass; ++p) {
-        if (p + FOLD_R - 1 < npass) {
-            // the fold of pass p - 1 has read the buffer that pass p + R - 1 takes
-            __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
-            issue(p + FOLD_R - 1);
-            __builtin_amdgcn_s_waitcnt(wait_vm(FOLD_P / 4 * (FOLD_R - 1)));
-        } else {
-            __builtin_amdgcn_s_waitcnt(wait_vm(0));
-        }
-        if (lane < nc) {
+        const int issued = p + FOLD_R - 2 < npass - 1 ? p + FOLD_R - 2 : npass - 1;
+        pass_barrier(issued - p);
+        // the buffer pass p + R - 1 takes was folded before the barrier
+        if (p + FOLD_R - 1 < npass) fold_issue(V4, T, c0, nc, ring, tid, p + FOLD_R - 1);
+        if (wave == 0 && lane < nc) {
             const float4* src = ring + (p % FOLD_R) * (FOLD_P * CPW) + lane;
             const int ng = groups - p * FOLD_P < FOLD_P ? groups - p * FOLD_P : FOLD_P;
             const int r = (p == npass - 1) ? (T & 3) : 0;   // trees in a last, partial group
-            const int full = r ? ng - 1 : ng;
-            if (full == FOLD_P) {
-                // whole pass: the next eight groups are read while eight are added
-                float4 cur[8], nxt[8];
-#pragma unroll
-                for (int g = 0; g < 8; ++g) cur[g] = src[g * CPW];
-#pragma unroll
-                for (int b = 0; b < FOLD_P / 8; ++b) {
-                    if (b + 1 < FOLD_P / 8) {
-#pragma unroll
-                        for (int g = 0; g < 8; ++g) nxt[g] = src[(8 * (b + 1) + g) * CPW];
-                    }
-#pragma unroll
-                    for (int g = 0; g < 8; ++g) {
-                        s = s + cur[g].x;
-                        s = s + cur[g].y;
-                        s = s + cur[g].z;
-                        s = s + cur[g].w;
-                    }
-                    if (b + 1 < FOLD_P / 8) {
-#pragma unroll
-                        for (int g = 0; g < 8; ++g) cur[g] = nxt[g];
-                    }
-                }
-            } else {
-                for (int g = 0; g < full; ++g) {
-                    const float4 q = src[g * CPW];
-                    s = s + q.x;
-                    s = s + q.y;
-                    s = s + q.z;
-                    s = s + q.w;
-                }
-                if (r) {
-                    const float4 q = src[full * CPW];
-                    s = s + q.x;
-                    if (r > 1) s = s + q.y;
-                    if (r > 2) s = s + q.z;
-                }
+            int full = r ? ng - 1 : ng;
+            int g = 0;
+            for (; g + 16 <= full; g += 16) fold_strided<16>(s, src + g * CPW);
+            if (full - g >= 8) {
+                fold_strided<8>(s, src + g * CPW);
+                g += 8;
+            }
+            if (full - g >= 4) {
+                fold_strided<4>(s, src + g * CPW);
+                g += 4;
+            }
+            for (; g < full; ++g) fold_strided<1>(s, src + g * CPW);
+            if (r) {
+                const float4 q = src[full * CPW];
+                s = s + q.x;
+                if (r > 1) s = s + q.y;
+                if (r > 2) s = s + q.z;
             }
         }
     }
@@ -189,8 +206,6 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     const int gj = tid >> 4, gr = tid & 15;
     const uint64_t gmask = 0xffffull << (16 * (gj & 3));
     const bool gvalid = gj < nc;
-    // leaf values of the pending candidates start streaming in at once
-    if (a.fin != FIN_NONE && wave == 0) fold_prime(reinterpret_cast<const float4*>(a.V), a.n, a.T, c0, nc, ring, tid);
 
     // The workgroup's space: when all its chains share one space whose split
     // tables fit, the descriptor and tables are staged in LDS; otherwise each
@@ -235,15 +250,19 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             thr_v = a.thr[c * a.steps + a.fin_step];
         }
     }
-    __syncthreads();   // publishes the staged space tables
+    // the leaf values of the pending candidates start streaming in (after
+    // the table staging, whose loads would otherwise queue behind them)
+    if (a.fin != FIN_NONE) fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+    // publishes the staged space tables; the first passes of the fold stay
+    // in flight
+    lds_barrier();
 
     if (a.fin != FIN_NONE) {
-        // score of the pending candidate (wave 0); meanwhile waves 1-3 bring
-        // the chains' best lists into LDS (an initial list is empty)
+        // score of the pending candidate (wave 0, fed by every wave); waves
+        // 1-3 first bring the chains' best lists into LDS (an initial list
+        // is empty)
         at_entry* lists = reinterpret_cast<at_entry*>(ring + RING_BYTES / 16);
-        float s = 0.0f;
         if (wave == 0) {
-            s = fold_ring(reinterpret_cast<const float4*>(a.V), a.n, a.T, c0, nc, ring, tid);
         } else if (a.fin == FIN_STEP) {
             const at_entry* src = a.top + c0 * k;
             const int total = nc * k;
@@ -260,6 +279,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
                 lists[e] = z;
             }
         }
+        const float s = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
         __builtin_amdgcn_s_waitcnt(0);
 
         // best lists: the chain's group of 16 lanes inserts the candidate
@@ -648,11 +668,12 @@ __device__ __forceinline__ void walk_vals(const uint8_t* __restrict__ L, const T
 
 template <int G>
 __device__ __forceinline__ void store_vals(const TreeArgs& a, int t_global, int64_t c, const uint32_t (&v)[G]) {
-    float* dst = a.V + ((((int64_t)(t_global >> 2) * a.n + c) << 2) + (t_global & 3));
+    const int groups = (a.n_trees + 3) >> 2;
+    float* dst = a.V + v_index(c, t_global, groups);
     if (G >= 4 && (t_global & 3) == 0) {
 #pragma unroll
         for (int h = 0; h + 4 <= G; h += 4)
-            *reinterpret_cast<float4*>(dst + (int64_t)(h >> 2) * a.n * 4) =
+            *reinterpret_cast<float4*>(dst + 16 * h) =
                 make_float4(__uint_as_float(v[h]), __uint_as_float(v[(h + 1) % G]), __uint_as_float(v[(h + 2) % G]),
                             __uint_as_float(v[(h + 3) % G]));
     } else if (G == 2 && (t_global & 1) == 0) {
@@ -661,7 +682,7 @@ __device__ __forceinline__ void store_vals(const TreeArgs& a, int t_global, int6
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             const int tg = t_global + g;
-            a.V[(((int64_t)(tg >> 2) * a.n + c) << 2) + (tg & 3)] = __uint_as_float(v[g]);
+            a.V[v_index(c, tg, groups)] = __uint_as_float(v[g]);
         }
     }
 }
@@ -954,7 +975,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     if ((err = ensure(ch.d_meta, (size_t)n * sizeof(ChainMeta))) != hipSuccess) return err;
     const int64_t fg_stride = (n + 63) / 64 * 64;
     if ((err = ensure(ch.d_fg, (size_t)Q * fg_stride * 4)) != hipSuccess) return err;
-    if ((err = ensure(ch.d_v, (size_t)groups * n * 16)) != hipSuccess) return err;
+    if ((err = ensure(ch.d_v, (size_t)groups * ((n + 15) / 16 * 16) * 16)) != hipSuccess) return err;
 
     ChainArgs ca{};
     ca.descs = static_cast<const SpaceDesc*>(sp.d_descs.p);
