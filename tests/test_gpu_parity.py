@@ -319,6 +319,27 @@ def test_sa_ragged_set_offsets(P, path):
     assert_same_run(best, tr, och, otr, cur=export(P, ch))
 
 
+def test_sa_ragged_set_tail_mode(P):
+    # workgroups of two chains straddle the space boundaries (chains 4-5 and
+    # 300), so the chain-local tail mode reads each chain's own space tables
+    shapes = [(1, 2, 4, 4, 2, 3, 3, 1, 1), (1, 2, 6, 6, 2, 1, 1, 0, 2), (1, 1, 8, 8, 2, 7, 7, 3, 2)]
+    say("sa ragged set, chain-local tail mode")
+    spaces = [P.at_space_create(W.CONV2D, s) for s in shapes]
+    ospaces = [oracle.Space(W.CONV2D, s) for s in shapes]
+    off = np.array([0, 5, 300, 301], np.int64)
+    fid, thr, leaf = W.make_ensemble(300, 8, 176, 8)
+    ens = P.at_ensemble_create(fid, thr, leaf, 176)
+    sset = P.at_spaceset_create(spaces, off)
+    n, steps, seed, k = 301, 20, 21, 4
+    ch = mk_chains(P, sset, 7, n, k, seed, "local")
+    best, tr = gpu_sa(P, sset, ens, ch, steps, P.at_sa_thresholds(seed, 7, n, 0, steps))
+    plan = P.at_chains_last_plan(ch)
+    assert plan["gather"] == 2 and plan["chains_per_wg"] == 2
+    och = oracle.Chains(ospaces, off, seed=seed, chain0=7, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 7, n, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
+
+
 def small_setup(P, n=70, topk=6, trees=25, depth=6, shape=(1, 2, 6, 6, 4, 3, 3, 1, 1)):
     sp = P.at_space_create(W.CONV2D, shape)
     osp = oracle.Space(W.CONV2D, shape)
