@@ -247,7 +247,7 @@ struct LocalPlan {
     uint32_t ring_bytes = 0;
     int walk_waves = 0;       // waves 1 .. walk_waves walk, later ones load
     uint32_t off_ring = 0, off_lv = 0, off_lists = 0, off_rec = 0, off_frow = 0, off_any = 0, off_desc = 0;
-    uint32_t frow_stride = 0; // tail: bytes between the two feature-row buffers
+    uint32_t frow_stride = 0; // single-pass modes: bytes between the two feature-row buffers
     int lv_stride = 0;
     size_t lds_bytes = 0;
     double round_bytes = 0.0; // bytes streamed per round by one workgroup

@@ -75,7 +75,7 @@ struct LocalArgs {
     uint32_t off_lv;
     int lv_stride;            // floats per chain row of leaf values: two chunk slots (one when resident)
     uint32_t off_lists, off_rec, off_frow, off_any, off_desc;
-    uint32_t frow_stride;     // tail: bytes between the two feature-row buffers
+    uint32_t frow_stride;     // single-pass modes: bytes between the two feature-row buffers
 };
 
 // Leaf indices of four trees for this lane: nb holds the LDS byte addresses
@@ -373,7 +373,10 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     // a chain stay in round order).  Roles during a fold: wave 0 folds,
     // waves 1-2 evaluate the next candidates, wave 3 offers, wave 4 draws,
     // the last wave brings the next thresholds.
-    const bool fast = a.tail && cpb <= 4 && nthreads == LOCAL_WG_MAX;
+    // single pass: every tree walked in one pass per round (tail mode, or
+    // resident trees in one chunk); such runs work a round ahead
+    const bool single = a.tail || (a.resident && a.n_chunks == 1);
+    const bool fast = single && cpb <= 4 && nthreads == LOCAL_WG_MAX;
     auto draw_into = [&](int j, int st) {
         // move of step st for chain j into its record (slot st & 1)
         int jm;
@@ -437,7 +440,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     for (int r = 0; r < rounds; ++r) {
         const bool is_init = a.init && r == 0;
         const int s = r - (a.init ? 1 : 0);
-        const bool ahead = a.tail && r > 0;   // this round's candidate and rows are ready
+        const bool ahead = single && r > 0;   // this round's candidate and rows are ready
         const bool more = r + 1 < rounds;
         // (1) candidate: the initial draw (block (chain, 0, 1, j / 4)) or one
         // knob moved to a uniformly chosen other value
@@ -479,15 +482,15 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         // in for missing ones), bytes 4x+3
         // (features are at most 31, so 4x+3 stays within each byte; bytes past
         // the last feature are never read)
-        if (!a.tail || wave > 0) {
+        if (!single || wave > 0) {
             // In tail mode waves 1.. fill the tile while the owners in wave 0
             // prepare the next candidates; else every wave does.  Thread t of
             // the fill fills tile words t, t + NF, ...: always chain t % cpb
             // (cpb divides NF, 448 or 512).
             constexpr int NF_MIN = LOCAL_WG_MAX - 64;
             constexpr int TU = (Q * 64 + NF_MIN - 1) / NF_MIN;
-            const int nf = a.tail ? nthreads - 64 : nthreads;
-            const int t = a.tail ? tid - 64 : tid;
+            const int nf = single ? nthreads - 64 : nthreads;
+            const int t = single ? tid - 64 : tid;
             int j = t & (cpb - 1);
             j = j < nc ? j : nc - 1;
             const uint8_t* row = frow + (ahead ? rec[j].sel * a.frow_stride : 0u) + j * RS;
@@ -504,11 +507,13 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             }
         }
         float sc = 0.0f;
-        if (a.tail) {
-            // (4') every tree of every chain in one pass: the resident top
-            // levels from LDS, then the last level and its leaf from the
-            // tree's 16-byte tail record; thread t takes chain t % cpb and
-            // trees u, u + S, u + 2S, u + 3S (S = threads / cpb)
+        if (single) {
+            // (4') every tree of every chain in one pass: in tail mode the
+            // resident top levels from LDS, then the last level and its leaf
+            // from the tree's 16-byte tail record; else the whole tree from
+            // LDS.  Thread t takes chain t % cpb and, with S = min(ceil(T /
+            // 4), threads / cpb) slots, slot u = t / cpb < S takes trees u,
+            // u + S, u + 2S, u + 3S per pass.
             if (owner && more) {
                 if (fast) {
                     const int sl = (s + 1) & 1;
@@ -536,32 +541,52 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                 rec[tid].cfgb = ncfg;
             }
             lds_barrier();
-            const int S = nthreads / cpb;
+            // (tail mode keeps every slot busy: its last-level gathers, not
+            // the walks, set the pace)
+            const int want = (a.T + 3) >> 2, have = nthreads / cpb;
+            const int S = (a.tail || want > have) ? have : want;
             const int ua = tid / cpb;
             const int ja = tid & (cpb - 1);
             const uint32_t fba = lbase | (uint32_t)lane * 4u;
-            for (int base = 0; base < a.T; base += 4 * S) {
-                uint32_t nb[4], q[4];
-                int ti[4];
+            auto trees_of = [&](int base, int (&ti)[4], uint32_t (&nb)[4]) {
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const int t = base + ua + g * S;
                     ti[g] = t < a.T ? t : -1;
                     nb[g] = lbase + a.off_ring + (uint32_t)(t < a.T ? t : 0) * (uint32_t)a.ts * 4u;
                 }
-                walk4_local<(DEPTH >= 2 ? DEPTH - 1 : 1)>(nb, fba, q);
-                uint4 rec4[4];
+            };
+            if (a.tail) {
+                for (int base = 0; base < a.T; base += 4 * S) {
+                    uint32_t nb[4], q[4];
+                    int ti[4];
+                    trees_of(base, ti, nb);
+                    walk4_local<(DEPTH >= 2 ? DEPTH - 1 : 1)>(nb, fba, q);
+                    uint4 rec4[4];
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int t = ti[g] >= 0 ? ti[g] : 0;
-                    rec4[g] = a.tail_rec[((size_t)t << (DEPTH - 1)) + q[g]];
+                    for (int g = 0; g < 4; ++g) {
+                        const int t = ti[g] >= 0 ? ti[g] : 0;
+                        rec4[g] = a.tail_rec[((size_t)t << (DEPTH - 1)) + q[g]];
+                    }
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const uint32_t node = rec4[g].x;
+                        const uint32_t x4 = lds[((node & LOCAL_TILE_MASK) | fba) - lbase];
+                        const uint32_t v = x4 >= (node & 0xffu) ? rec4[g].z : rec4[g].y;
+                        if (ti[g] >= 0 && ja < nc) lv[ja * a.lv_stride + ti[g]] = __uint_as_float(v);
+                    }
                 }
+            } else if (ua < S) {
+                for (int base = 0; base < a.T; base += 4 * S) {
+                    uint32_t nb[4], q[4];
+                    int ti[4];
+                    trees_of(base, ti, nb);
+                    walk4_local<DEPTH>(nb, fba, q);
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const uint32_t node = rec4[g].x;
-                    const uint32_t x4 = lds[((node & LOCAL_TILE_MASK) | fba) - lbase];
-                    const uint32_t v = x4 >= (node & 0xffu) ? rec4[g].z : rec4[g].y;
-                    if (ti[g] >= 0 && ja < nc) lv[ja * a.lv_stride + ti[g]] = __uint_as_float(v);
+                    for (int g = 0; g < 4; ++g) {
+                        const uint32_t v = *reinterpret_cast<const uint32_t*>(lds + (nb[g] - lbase) + NBB + 4u * q[g]);
+                        if (ti[g] >= 0 && ja < nc) lv[ja * a.lv_stride + ti[g]] = __uint_as_float(v);
+                    }
                 }
             }
             lds_barrier();
@@ -724,7 +749,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                 cur_s = sc;
                 cur_cfg = cfg;
             }
-            if (a.tail && more) {
+            if (single && more) {
                 const ChainRec& R = rec[tid];
                 unpack(acc ? R.nx : R.nxb, cd);
                 cfg = acc ? R.cfga : R.cfgb;
@@ -844,7 +869,8 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     const size_t top_bytes = al16((size_t)T * ts_top * 4);
     const int T4 = (T + 3) / 4 * 4;
     const size_t lv_all = al16((size_t)cpb * ((size_t)T4 + 4) * 4);
-    if (cap_all >= 4 && res_bytes + lv_bytes(ct_res) <= avail) {
+    // (one chunk of resident trees also needs a second feature-row buffer)
+    if (cap_all >= 4 && res_bytes + lv_bytes(ct_res) + (ct_res == T ? al16((size_t)cpb * RS) : 0) <= avail) {
         pl.resident = 1;
         pl.gather = 0;
         pl.ts = ts_full;
@@ -889,9 +915,9 @@ bool plan_local(const at_space_s& sp, const EnsembleDesc& e, const at_chains_s& 
     pl.off_rec = (uint32_t)off;
     off += al16((size_t)cpb * sizeof(ChainRec));
     pl.off_frow = (uint32_t)off;
-    // tail: two buffers, the next round's rows for an accepted and for a
-    // rejected candidate
-    pl.frow_stride = pl.tail ? (uint32_t)al16((size_t)cpb * RS) : 0u;
+    // single-pass modes (tail, one resident chunk): two buffers, the next
+    // round's rows for an accepted and for a rejected candidate
+    pl.frow_stride = (pl.tail || (pl.resident && pl.n_chunks == 1)) ? (uint32_t)al16((size_t)cpb * RS) : 0u;
     off += al16((size_t)cpb * RS) + pl.frow_stride;
     pl.off_any = (uint32_t)off;
     off += 16;
