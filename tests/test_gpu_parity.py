@@ -477,6 +477,8 @@ def test_sa_paths_agree_and_interleave(P):
 # level from global memory; each checked against the oracle
 LOCAL_PLANS = {
     "resident": dict(n=48, trees=40, depth=6, steps=30),
+    # sixteen chains per workgroup: one resident chunk without helper waves
+    "resident_wide": dict(n=4096, trees=40, depth=6, steps=10),
     "streamed": dict(n=8192, trees=1000, depth=8, steps=4),
     "gathered": dict(n=64, trees=400, depth=9, steps=20),
     "tail": dict(n=300, trees=300, depth=8, steps=25),
@@ -501,10 +503,10 @@ def test_sa_local_plans_match_oracle(P, mode):
     ch = mk_chains(P, sp, 0, n, k, seed, "local")
     best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
     plan = P.at_chains_last_plan(ch)
-    assert (plan["chunks"] == 0) == (mode in ("resident", "tail", "tail_depth2", "tail_wide", "tail_ragged"))
+    assert (plan["chunks"] == 0) == (mode.startswith("resident") or mode.startswith("tail"))
     assert plan["gather"] == (2 if mode.startswith("tail") else {"gathered": 1}.get(mode, 0))
-    if mode.startswith("tail"):
-        assert (plan["chains_per_wg"] > 4) == (mode == "tail_wide")
+    if mode.startswith("tail") or mode.startswith("resident"):
+        assert (plan["chains_per_wg"] > 4) == mode.endswith("_wide")
     # the first 160 chains, or the last 160 when the last workgroup is short
     r0 = n - 160 if mode == "tail_ragged" else 0
     m = min(n - r0, 160)
