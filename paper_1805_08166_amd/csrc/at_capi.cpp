@@ -453,6 +453,7 @@ void at_chains_destroy(at_chains_t chains) {
     release(chains->d_meta);
     release(chains->d_fg);
     release(chains->d_v);
+    release(chains->d_tw);
     for (auto& pool : chains->events)
         for (hipEvent_t e : pool) (void)hipEventDestroy(e);
     delete chains;

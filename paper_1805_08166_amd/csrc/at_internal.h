@@ -198,6 +198,7 @@ struct at_chains_s {
     at::DeviceBuf d_meta;     // ChainMeta [n_chains]
     at::DeviceBuf d_fg;       // uint32 [Q][n_chains] packed candidate features
     at::DeviceBuf d_v;        // float leaf values, [ceil(T/4)][n_chains][4]
+    at::DeviceBuf d_tw;       // uint32 pointer-form trees relocated for the tree kernel's LDS plan
     // launch timing (measurement aid): start/stop events attached to every
     // launch of the last run; kind 0 is the tree kernel, 1 the chain kernel
     bool profiling = false;

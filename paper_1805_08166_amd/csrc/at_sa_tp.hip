@@ -103,7 +103,8 @@ __device__ __forceinline__ void fold_issue(const float4* __restrict__ V4, int T,
         const int ins = wave * FOLD_SHARE + q;
         const int g = p * FOLD_P + ins * 4 + (lane >> 4);
         const int gc = g < groups ? g : groups - 1;
-        __builtin_amdgcn_global_load_lds(V4 + (((cj >> 4) * groups + gc) << 4) + (cj & 15), buf + ins * 64, 16, 0, 0);
+        // non-temporal (cache policy 2): V is read once
+        __builtin_amdgcn_global_load_lds(V4 + (((cj >> 4) * groups + gc) << 4) + (cj & 15), buf + ins * 64, 16, 0, 2);
     }
 }
 
@@ -432,7 +433,7 @@ constexpr int TREE_WAVES_MAX = 16;
 constexpr uint32_t TREE_LDS_FREE = (uint32_t)MAX_LDS_BYTES - 16u;
 
 struct TreeArgs {
-    const uint32_t* words32;   // pointer form of the ensemble
+    const uint32_t* words32;   // pointer form relocated for toff (k_reloc)
     int n_trees;
     int tpw;                   // trees per workgroup
     const uint32_t* Fg;        // [Q][fg_stride] packed features (4x+3 per byte)
@@ -666,16 +667,20 @@ __device__ __forceinline__ void walk_vals(const uint8_t* __restrict__ L, const T
         walk_plain<DEPTH, G>(L, nb, fb, a.mask, v);
 }
 
+// Leaf values go to V with non-temporal stores: each is read once, by the
+// chain kernel, and the L2 is better spent on features and trees.
 template <int G>
 __device__ __forceinline__ void store_vals(const TreeArgs& a, int t_global, int64_t c, const uint32_t (&v)[G]) {
     const int groups = (a.n_trees + 3) >> 2;
     float* dst = a.V + v_index(c, t_global, groups);
     if (G >= 4 && (t_global & 3) == 0) {
 #pragma unroll
-        for (int h = 0; h + 4 <= G; h += 4)
-            *reinterpret_cast<float4*>(dst + 16 * h) =
-                make_float4(__uint_as_float(v[h]), __uint_as_float(v[(h + 1) % G]), __uint_as_float(v[(h + 2) % G]),
-                            __uint_as_float(v[(h + 3) % G]));
+        for (int h = 0; h + 4 <= G; h += 4) {
+            typedef float f4v __attribute__((ext_vector_type(4)));
+            const f4v x = {__uint_as_float(v[h]), __uint_as_float(v[(h + 1) % G]), __uint_as_float(v[(h + 2) % G]),
+                           __uint_as_float(v[(h + 3) % G])};
+            __builtin_nontemporal_store(x, reinterpret_cast<f4v*>(dst + 16 * h));
+        }
     } else if (G == 2 && (t_global & 1) == 0) {
         *reinterpret_cast<float2*>(dst) = make_float2(__uint_as_float(v[0]), __uint_as_float(v[1 % G]));
     } else {
@@ -716,7 +721,6 @@ __device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const T
 template <int DEPTH, int Q, int SLOT_LOG2>
 __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     constexpr uint32_t SLOT = 1u << SLOT_LOG2;
-    constexpr int NB = 1 << (DEPTH - 1);
     constexpr int G = 8;
     __shared__ uint32_t lds[MAX_LDS_BYTES / 4];
     const uint8_t* L = reinterpret_cast<const uint8_t*>(lds);
@@ -724,58 +728,9 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     const int grp = blockIdx.x / a.slices, cs = blockIdx.x - grp * a.slices;
     const int t0 = grp * a.tpw;
     const int nt = (a.n_trees - t0 < a.tpw) ? (a.n_trees - t0) : a.tpw;
-    // trees into LDS, relocating node pointers: a node-block slot p holds
-    // nodes whose children sit in the leaf block when p >= NB / 2 (the last
-    // internal level; for DEPTH 1 the root), else in the node block.  Per
-    // round, one piece of every tree is loaded before any store.  Loads and
-    // stores are unconditional so that the loads stay in flight together:
-    // slots past the last tree and lanes past the last piece repeat the last
-    // tree's or piece's store (same value, same place).
-    if constexpr (DEPTH >= 2) {
-        // blocks are whole 16-byte pieces (two slots) at 16-byte aligned offsets
-        constexpr int B4 = NB / 2, W4 = 2 * B4;
-        const uint4* src = reinterpret_cast<const uint4*>(a.words32 + (size_t)t0 * 4 * NB);
-        for (int base = 0; base < W4; base += (int)blockDim.x) {
-            const int i = base + tid < W4 ? base + tid : W4 - 1;
-            uint4 v[TREES_MAX];
-#pragma unroll
-            for (int t = 0; t < TREES_MAX; ++t) v[t] = src[(t < nt ? t : nt - 1) * W4 + i];
-#pragma unroll
-            for (int t = 0; t < TREES_MAX; ++t) {
-                const uint32_t o = a.toff[t < nt ? t : nt - 1];
-                const uint32_t nw4 = o & 0xffffu, lw4 = o >> 16;
-                uint32_t d;
-                if (i < B4) {
-                    // slots 2i and 2i + 1 of the node block
-                    const uint32_t r0 = ((2 * i >= NB / 2) ? lw4 : nw4) << 16;
-                    const uint32_t r1 = ((2 * i + 1 >= NB / 2) ? lw4 : nw4) << 16;
-                    v[t].x += r0;
-                    v[t].y += r0;
-                    v[t].z += r1;
-                    v[t].w += r1;
-                    d = nw4 + 4u * (uint32_t)i;
-                } else {
-                    d = lw4 + 4u * (uint32_t)(i - B4);
-                }
-                *reinterpret_cast<uint4*>(lds + d) = v[t];
-            }
-        }
-    } else {
-        // one node slot (the root, whose children are leaves) and one leaf slot
-        const uint32_t* src = a.words32 + (size_t)t0 * 4;
-        if (tid < 4 * nt) {
-            const int t = tid >> 2, w = tid & 3;
-            const uint32_t o = a.toff[t];
-            uint32_t v = src[tid];
-            if (w < 2) v += (o >> 16) << 16;
-            lds[w < 2 ? (o & 0xffffu) + (uint32_t)w : (o >> 16) + (uint32_t)(w - 2)] = v;
-        }
-    }
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int nw = (int)(blockDim.x >> 6);
     uint32_t* counter = lds + TREE_LDS_FREE / 4;
-    if (tid == 0) *counter = (uint32_t)nw;
-    __syncthreads();
     const int64_t n = a.n;
     const int64_t blocks = (n + 63) >> 6;
     const int64_t b_end0 = (int64_t)(cs + 1) * a.slice_blocks;
@@ -787,6 +742,45 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     // 4k + i/16, which land on tile dwords 256k + 4i .. +3 = quad * 64 + chain
     const uint32_t* fsrc = a.Fg + (int64_t)(lane >> 4) * a.fg_stride + 4 * (lane & 15);
     static_assert(Q % 4 == 0, "whole quad groups");
+    auto fill = [&](int64_t blk) {
+#pragma unroll
+        for (int k = 0; k < Q / 4; ++k)
+            __builtin_amdgcn_global_load_lds(fsrc + (int64_t)(4 * k) * a.fg_stride + blk * 64, tile + 256 * k, 16, 0, 0);
+    };
+    const int64_t b_first = (int64_t)cs * a.slice_blocks;
+    const int64_t nblk = b_end - b_first;
+    int64_t r = wave, nr = nblk;
+    // the first block's tile is in flight while the trees are copied
+    if (r < nblk) fill(b_first + r);
+    // Trees, already relocated for this LDS plan (a.words32 holds per tree
+    // its node block, whose node words carry the LDS addresses of their
+    // children, then its leaf block), go block by block straight into LDS:
+    // unit u is piece p (PIECE bytes) of block k (node, leaf) of local tree t.
+    {
+        constexpr uint32_t BB = 4u << DEPTH;                // bytes per block
+        constexpr uint32_t SZ = BB >= 16u ? 16u : 4u;       // bytes per lane
+        constexpr uint32_t PIECE = 64u * SZ;
+        constexpr int PPB = (int)((BB + PIECE - 1u) / PIECE);
+        const int units = nt * 2 * PPB;
+        for (int u = wave; u < units; u += nw) {
+            const int t = u / (2 * PPB), r = u - t * (2 * PPB), k = r / PPB, p = r - k * PPB;
+            const uint32_t o = a.toff[t];
+            const uint32_t dw = (k ? (o >> 16) : (o & 0xffffu)) + (uint32_t)p * (PIECE / 4u);
+            const uint32_t* s = a.words32 + ((size_t)(t0 + t) * 2 + (size_t)k) * (BB / 4u) +
+                                (size_t)p * (PIECE / 4u) + (size_t)lane * (SZ / 4u);
+            // lanes past the end of a block smaller than one piece stay idle
+            if ((uint32_t)lane * SZ < BB - (uint32_t)p * PIECE) {
+                if constexpr (SZ == 16u)
+                    __builtin_amdgcn_global_load_lds(s, lds + dw, 16, 0, 0);
+                else
+                    __builtin_amdgcn_global_load_lds(s, lds + dw, 4, 0, 0);
+            }
+        }
+    }
+    if (tid == 0) *counter = (uint32_t)nw;
+    // every wave's copies and its first tile have landed before any wave reads
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
     // the roots of the first eight trees and their children's slots: the
     // same for every chain, read once
     constexpr bool ROOTS = DEPTH >= 2;
@@ -801,25 +795,26 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
             rhi[g] = (uint32_t)(pr >> 32);
         }
     }
-    const int64_t b_first = (int64_t)cs * a.slice_blocks;
     auto claim_next = [&]() -> uint32_t {
         uint32_t r = 0;
         if (lane == 0) r = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         return r;
     };
-    // b: the block walked now; nb: the next one, claimed a block ahead so
+    // r: the block walked now; nr: the next one, claimed a block ahead so
     // that the claim's answer is never waited for
-    int64_t b = b_first + wave, nb = b_end;
-    if (b < b_end) nb = b_first + (int64_t)__builtin_amdgcn_readfirstlane(claim_next());
-    while (b < b_end) {
+    if (r < nblk) nr = (int64_t)__builtin_amdgcn_readfirstlane(claim_next());
+    bool first = true;
+    while (r < nblk) {
         // every earlier read of this wave's tile has returned before the
         // tile is overwritten (s_waitcnt lgkmcnt(0))
-        __builtin_amdgcn_s_waitcnt(0xc07f);
-        const uint32_t claim = nb < b_end ? claim_next() : 0u;
-#pragma unroll
-        for (int k = 0; k < Q / 4; ++k)
-            __builtin_amdgcn_global_load_lds(fsrc + (int64_t)(4 * k) * a.fg_stride + b * 64, tile + 256 * k, 16, 0, 0);
-        __builtin_amdgcn_s_waitcnt(0);
+        if (!first) __builtin_amdgcn_s_waitcnt(0xc07f);
+        const uint32_t claim = nr < nblk ? claim_next() : 0u;
+        const int64_t b = b_first + r;
+        if (!first) {
+            fill(b);
+            __builtin_amdgcn_s_waitcnt(0);
+        }
+        first = false;
         const int64_t c = b * 64 + lane;
         const bool active = c < n;
         int t = 0;
@@ -833,9 +828,30 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
         }
         for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
         walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
-        b = nb;
-        if (b < b_end) nb = b_first + (int64_t)__builtin_amdgcn_readfirstlane(claim);
+        r = nr;
+        if (r < nblk) nr = (int64_t)__builtin_amdgcn_readfirstlane(claim);
     }
+}
+
+// The pointer form relocated for one LDS plan: every node-block word of tree
+// t gets, in its high half, the LDS word address of the block its children's
+// slot lies in (local tree t % tpw; the leaf block for slots p >= NB / 2,
+// whose nodes are on the last internal level, and for the root when DEPTH is
+// 1); leaf words are copied.  Runs once per annealing run, so that the tree
+// kernel copies its trees into LDS unchanged.
+__global__ void k_reloc(const uint32_t* __restrict__ src, uint32_t* __restrict__ dst, int64_t words, int depth,
+                        TreeArgs a) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= words) return;
+    const uint32_t nb = 1u << (depth - 1);
+    const int64_t t = i >> (depth + 1);
+    const uint32_t j = (uint32_t)(i & ((2 << depth) - 1));
+    uint32_t v = src[i];
+    if (j < 2u * nb) {
+        const uint32_t o = a.toff[t % a.tpw];
+        v += ((j >> 1) >= nb / 2u ? (o >> 16) : (o & 0xffffu)) << 16;
+    }
+    dst[i] = v;
 }
 
 // LDS plan of a tree workgroup: nw feature tiles, one per SLOT, and the
@@ -1041,6 +1057,14 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     }
     if (nw == 0) return hipErrorInvalidConfiguration;
     ta.mask = (((uint32_t)slot - 1u) & ~0xffu) | 3u;
+    {
+        const int64_t words = (int64_t)e.n_trees << (e.depth + 1);
+        if ((err = ensure(ch.d_tw, (size_t)words * 4)) != hipSuccess) return err;
+        hipLaunchKernelGGL(k_reloc, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream, e.words32,
+                           static_cast<uint32_t*>(ch.d_tw.p), words, e.depth, ta);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+        ta.words32 = static_cast<const uint32_t*>(ch.d_tw.p);
+    }
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
     const size_t chain_lds = RING_BYTES + (size_t)CPW * ch.topk * sizeof(at_entry);

@@ -348,6 +348,20 @@ def small_setup(P, n=70, topk=6, trees=25, depth=6, shape=(1, 2, 6, 6, 4, 3, 3, 
     return sp, osp, (fid, thr, leaf), ens
 
 
+@pytest.mark.parametrize("depth,trees", [(1, 21), (2, 35), (3, 19), (11, 6), (12, 5)])
+def test_sa_tree_path_depths(P, depth, trees):
+    # the tree kernel's LDS copy at block sizes from 8 bytes (depth 1) to
+    # 16 KB (depth 12), with a partial last tree group
+    say(f"sa tree path depth {depth}, {trees} trees")
+    sp, osp, ens_t, ens = small_setup(P, trees=trees, depth=depth)
+    n, steps, seed, k = 150, 15, 17, 4
+    ch = mk_chains(P, sp, 0, n, k, seed, "trees")
+    best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
+    och = oracle.Chains([osp], [0, n], seed=seed, chain0=0, topk=k)
+    otr = och.run(ens_t, steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
+
+
 def test_sa_persistence_split_equals_full(P, path):
     sp, osp, ens_t, ens = small_setup(P)
     n, steps, seed, k = 70, 80, 5, 6
