@@ -151,6 +151,31 @@ def test_predict_matches_oracle_with_leaf_indices(P, depth, trees, F):
     assert np.array_equal(bits(s), bits(ws))
 
 
+@pytest.mark.parametrize("depth,trees,F,thr_hi", [(1, 530, 176, 64), (2, 259, 192, 64), (5, 70, 176, 64),
+                                                   (7, 19, 192, 64), (8, 15, 176, 64), (8, 13, 192, 64),
+                                                   (8, 11, 176, 256), (6, 9, 192, 256)])
+def test_predict_wide_thresholds_and_clamped_features(P, depth, trees, F, thr_hi):
+    # thresholds up to 63 or 255 and features up to 300 (clamped to 255 on
+    # the device, where x >= thr keeps its value); tree counts leave a
+    # partial last chunk of the scoring kernel's tree stream
+    import torch
+    say(f"predict depth {depth} trees {trees} F {F} thresholds < {thr_hi}")
+    rng = np.random.default_rng(7 * depth + trees)
+    n_int = (1 << depth) - 1
+    fid = rng.integers(0, F, size=(trees, n_int)).astype(np.uint8)
+    thr = rng.integers(0, thr_hi, size=(trees, n_int)).astype(np.uint8)
+    leaf = (rng.standard_normal((trees, 1 << depth)) * 0.05).astype(np.float32)
+    ens = P.at_ensemble_create(fid, thr, leaf, F)
+    n = 1037
+    x = rng.integers(0, 301, size=(n, F)).astype(np.int32)
+    xd = torch.from_numpy(x).to(DEV)
+    s, _ = gpu_predict(P, ens, xd)
+    s_l, lv = gpu_predict(P, ens, xd, leaves=True)
+    ws, wl = oracle.predict(fid, thr, leaf, x, want_leaves=True)
+    assert np.array_equal(bits(s), bits(ws))
+    assert np.array_equal(bits(s_l), bits(ws)) and np.array_equal(lv, wl)
+
+
 def test_predict_fold_order(P):
     import torch
     fid = np.zeros((3, 1), np.uint8)
