@@ -64,6 +64,15 @@ struct ChainRec {
     uint64_t mvr[2];
     uint64_t pcfg[2];
     float pscore[2];
+    // chain-local fast rounds, by round parity: the round's two candidates
+    // (outcome 0 after an accept, 1 after a reject; knobs packed in pairs,
+    // index), the outcome that holds the round's candidate, and the current
+    // configuration the round starts from
+    uint32_t snx[2][2][MAX_KNOBS / 2];
+    uint64_t scfg[2][2];
+    uint32_t ssel[2];
+    uint32_t curk[2][MAX_KNOBS / 2];
+    uint64_t curcfg[2];
 };
 
 // Offers (cfg, sc) to the best list of one chain held in LDS, with the 16

@@ -37,6 +37,11 @@ constexpr uint32_t LOCAL_TILE_MASK = 0x3f03u;  // node bits of a tile byte addre
 // dynamic LDS per workgroup: the compute unit's 160 KB less 1 KB kept for
 // any static LDS the compiler places
 constexpr size_t LOCAL_LDS_BYTES = 163840 - 1024;
+// Fast rounds of ensembles with at least this many trees have the next
+// candidates made by the waves that evaluate them, during the fold (a fold
+// of that many leaves outlasts the moves and the features); smaller ones
+// have the owners make them before the walk.
+constexpr int LOCAL_SPEC_T_MIN = 384;
 
 struct LocalArgs {
     const SpaceDesc* descs;
@@ -229,7 +234,11 @@ __device__ __forceinline__ void apply_move(const uint32_t (&base)[MAX_KNOBS], ui
                  : (nv >= old ? base_cfg + (uint64_t)(nv - old) * radix : base_cfg - (uint64_t)(old - nv) * radix);
 }
 
-template <int TMPL, int DEPTH>
+// FAST instances run the single-pass plans with at most four chains per
+// workgroup and full workgroups (the launcher picks them); the others run
+// every other plan.  Compiling the two apart keeps each one's uniform state
+// within the scalar registers.
+template <int TMPL, int DEPTH, bool FAST>
 __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     using N = Nest<TMPL>;
     constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
@@ -375,8 +384,9 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     // the last wave brings the next thresholds.
     // single pass: every tree walked in one pass per round (tail mode, or
     // resident trees in one chunk); such runs work a round ahead
-    const bool single = a.tail || (a.resident && a.n_chunks == 1);
-    const bool fast = single && cpb <= 4 && nthreads == LOCAL_WG_MAX;
+    const bool single = FAST || a.tail || (a.resident && a.n_chunks == 1);
+    const bool fast = FAST;
+    const bool spec = fast && a.T >= LOCAL_SPEC_T_MIN;
     auto draw_into = [&](int j, int st) {
         // move of step st for chain j into its record (slot st & 1)
         int jm;
@@ -409,6 +419,13 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     if (fast && owner) {
         const int s1 = (a.init ? -1 : 0) + 1;
         if (s1 < a.steps) draw_into(tid, s1);
+        // round 0 starts from the loaded configuration; its candidate is
+        // outcome 0
+        ChainRec& R = rec[tid];
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS / 2; ++j) R.curk[0][j] = cur[2 * j] | (cur[2 * j + 1] << 16);
+        R.curcfg[0] = cur_cfg;
+        R.ssel[0] = 0u;
     }
 
     // Loop gr's features of chain j's configuration nx into row dst.
@@ -447,6 +464,16 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         float thr_v = 0.0f;
         if (owner && ahead) {
             thr_v = rec[tid].thr;
+            if (fast) {
+                // the candidate evaluated for this round's outcome
+                const ChainRec& R = rec[tid];
+                const uint32_t os = R.ssel[r & 1] & 1u;
+                uint32_t w[MAX_KNOBS / 2];
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS / 2; ++j) w[j] = R.snx[r & 1][os][j];
+                unpack(w, cd);
+                cfg = R.scfg[r & 1][os];
+            }
         } else if (owner) {
             cfg = 0;
             if (is_init) {
@@ -467,6 +494,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             }
 #pragma unroll
             for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = cd[2 * j] | (cd[2 * j + 1] << 16);
+            if (fast) {
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].snx[r & 1][0][j] = rec[tid].nx[j];
+                rec[tid].scfg[r & 1][0] = cfg;
+            }
         }
         if (!ahead) {
             lds_barrier();
@@ -493,17 +525,31 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             const int t = single ? tid - 64 : tid;
             int j = t & (cpb - 1);
             j = j < nc ? j : nc - 1;
-            const uint8_t* row = frow + (ahead ? rec[j].sel * a.frow_stride : 0u) + j * RS;
             uint32_t w[TU];
+            if (fast) {
+                // 448 fill threads: the words of every pass but the last exist
+                const uint8_t* row = frow + (ahead ? (rec[j].ssel[r & 1] & 1u) * a.frow_stride : 0u) + j * RS;
+                constexpr bool LAST = (TU - 1) * NF_MIN + NF_MIN > Q * 64;   // the last pass is partial
+                const bool last_ok = !LAST || t + (TU - 1) * NF_MIN < Q * 64;
 #pragma unroll
-            for (int u = 0; u < TU; ++u) {
-                const int i = t + u * nf;
-                if (i < Q * 64) w[u] = *reinterpret_cast<const uint32_t*>(row + 4 * (i >> 6));
-            }
+                for (int u = 0; u < TU; ++u)
+                    if (u + 1 < TU || last_ok)
+                        w[u] = *reinterpret_cast<const uint32_t*>(row + 4 * ((t + u * NF_MIN) >> 6));
 #pragma unroll
-            for (int u = 0; u < TU; ++u) {
-                const int i = t + u * nf;
-                if (i < Q * 64) tile[i] = (w[u] << 2) | 0x03030303u;
+                for (int u = 0; u < TU; ++u)
+                    if (u + 1 < TU || last_ok) tile[t + u * NF_MIN] = (w[u] << 2) | 0x03030303u;
+            } else {
+                const uint8_t* row = frow + (ahead ? rec[j].sel * a.frow_stride : 0u) + j * RS;
+#pragma unroll
+                for (int u = 0; u < TU; ++u) {
+                    const int i = t + u * nf;
+                    if (i < Q * 64) w[u] = *reinterpret_cast<const uint32_t*>(row + 4 * (i >> 6));
+                }
+#pragma unroll
+                for (int u = 0; u < TU; ++u) {
+                    const int i = t + u * nf;
+                    if (i < Q * 64) tile[i] = (w[u] << 2) | 0x03030303u;
+                }
             }
         }
         float sc = 0.0f;
@@ -514,17 +560,25 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             // LDS.  Thread t takes chain t % cpb and, with S = min(ceil(T /
             // 4), threads / cpb) slots, slot u = t / cpb < S takes trees u,
             // u + S, u + 2S, u + 3S per pass.
-            if (owner && more) {
-                if (fast) {
-                    const int sl = (s + 1) & 1;
-                    mv_j = rec[tid].mvj[sl];
-                    mv_v = rec[tid].mvv[sl];
-                    mv_radix = rec[tid].mvr[sl];
-                } else {
-                    with_space([&](const SpaceDesc& sd) {
-                        draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
-                    });
+            if (owner && more && fast && !spec) {
+                // the next round's two candidates, kept by round parity
+                const int sl = (s + 1) & 1;
+                ChainRec& R = rec[tid];
+                uint32_t nx[MAX_KNOBS];
+                uint64_t ncfg;
+#pragma unroll
+                for (int v = 0; v < 2; ++v) {
+                    if (v == 0 || is_init) apply_move(cd, cfg, R.mvj[sl], R.mvv[sl], R.mvr[sl], nx, ncfg);
+                    else apply_move(cur, cur_cfg, R.mvj[sl], R.mvv[sl], R.mvr[sl], nx, ncfg);
+#pragma unroll
+                    for (int j = 0; j < MAX_KNOBS / 2; ++j) R.snx[(r + 1) & 1][v][j] = nx[2 * j] | (nx[2 * j + 1] << 16);
+                    R.scfg[(r + 1) & 1][v] = ncfg;
                 }
+            }
+            if (owner && more && !fast) {
+                with_space([&](const SpaceDesc& sd) {
+                    draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
+                });
                 // the next candidate after an accept (from cd) and after a
                 // reject (from cur; after the initial draw, which is always
                 // accepted, also from cd), kept in the chain's record
@@ -604,7 +658,42 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                     const int gr2 = it & 15, j = (it >> 4) & (cpb - 1), v = (it >> 4) >> cpb_log2;
                     if (j < nc && gr2 < N::L) {
                         uint32_t nx[MAX_KNOBS];
-                        unpack(v ? rec[j].nxb : rec[j].nx, nx);
+                        if (fast && !spec) {
+                            uint32_t w[MAX_KNOBS / 2];
+#pragma unroll
+                            for (int q = 0; q < MAX_KNOBS / 2; ++q) w[q] = rec[j].snx[(r + 1) & 1][v][q];
+                            unpack(w, nx);
+                        } else if (spec) {
+                            // the candidate itself: step s + 1's move applied to
+                            // this round's candidate (v = 0; also v = 1 after
+                            // the initial draw, which is always accepted) or to
+                            // the configuration the round started from (v = 1)
+                            ChainRec& R = rec[j];
+                            const int sl = (s + 1) & 1;
+                            const uint32_t os = R.ssel[r & 1] & 1u;
+                            uint32_t w[MAX_KNOBS / 2], base[MAX_KNOBS];
+                            uint64_t bcfg;
+                            if (v == 0 || is_init) {
+#pragma unroll
+                                for (int q = 0; q < MAX_KNOBS / 2; ++q) w[q] = R.snx[r & 1][os][q];
+                                bcfg = R.scfg[r & 1][os];
+                            } else {
+#pragma unroll
+                                for (int q = 0; q < MAX_KNOBS / 2; ++q) w[q] = R.curk[r & 1][q];
+                                bcfg = R.curcfg[r & 1];
+                            }
+                            unpack(w, base);
+                            uint64_t ncfg;
+                            apply_move(base, bcfg, R.mvj[sl], R.mvv[sl], R.mvr[sl], nx, ncfg);
+                            if (gr2 == 0) {
+#pragma unroll
+                                for (int q = 0; q < MAX_KNOBS / 2; ++q)
+                                    R.snx[(r + 1) & 1][v][q] = nx[2 * q] | (nx[2 * q + 1] << 16);
+                                R.scfg[(r + 1) & 1][v] = ncfg;
+                            }
+                        } else {
+                            unpack(v ? rec[j].nxb : rec[j].nx, nx);
+                        }
                         eval_loop(nx, j, gr2, frow + v * a.frow_stride + j * RS);
                     }
                 }
@@ -700,17 +789,18 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                 ChainRec& R = rec[tid];
                 R.pcfg[r & 1] = cfg;
                 R.pscore[r & 1] = sc;
-                R.sel = acc ? 0u : 1u;
+                // the next round takes the candidate of this outcome and
+                // starts from the configuration published here
+                R.ssel[(r + 1) & 1] = acc ? 0u : 1u;
                 if (acc) {
 #pragma unroll
                     for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
                     cur_s = sc;
                     cur_cfg = cfg;
                 }
-                if (more) {
-                    unpack(acc ? R.nx : R.nxb, cd);
-                    cfg = acc ? R.cfga : R.cfgb;
-                }
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS / 2; ++j) R.curk[(r + 1) & 1][j] = cur[2 * j] | (cur[2 * j + 1] << 16);
+                R.curcfg[(r + 1) & 1] = cur_cfg;
             }
             lds_barrier();
             continue;
@@ -777,13 +867,13 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     }
 }
 
-template <int TMPL>
+template <int TMPL, bool FAST>
 hipError_t launch_local_t(const LocalArgs& a, int depth, int grid, int threads, size_t lds, hipStream_t stream,
                           hipEvent_t start, hipEvent_t stop) {
     const void* fn = nullptr;
     switch (depth) {
 #define AT_LOCAL_CASE(D) \
-    case D: fn = reinterpret_cast<const void*>(&k_local<TMPL, D>); break;
+    case D: fn = reinterpret_cast<const void*>(&k_local<TMPL, D, FAST>); break;
         AT_LOCAL_CASE(1) AT_LOCAL_CASE(2) AT_LOCAL_CASE(3) AT_LOCAL_CASE(4) AT_LOCAL_CASE(5) AT_LOCAL_CASE(6)
         AT_LOCAL_CASE(7) AT_LOCAL_CASE(8) AT_LOCAL_CASE(9) AT_LOCAL_CASE(10) AT_LOCAL_CASE(11) AT_LOCAL_CASE(12)
 #undef AT_LOCAL_CASE
@@ -992,9 +1082,16 @@ hipError_t launch_sa_local(const at_space_s& sp, const EnsembleDesc& e, at_chain
     ch.events_used[0] = ch.events_used[1] = 0;
     hipEvent_t start = nullptr, stop = nullptr;
     if ((err = next_events(ch, 0, start, stop)) != hipSuccess) return err;
+    const bool fast = (pl.tail || (pl.resident && pl.n_chunks == 1)) && pl.cpb <= 4 && pl.threads == LOCAL_WG_MAX;
     if (sp.tmpl == AT_TMPL_GEMM)
-        return launch_local_t<AT_TMPL_GEMM>(a, e.depth, pl.grid, pl.threads, pl.lds_bytes, stream, start, stop);
-    return launch_local_t<AT_TMPL_CONV2D_NCHW>(a, e.depth, pl.grid, pl.threads, pl.lds_bytes, stream, start, stop);
+        return fast ? launch_local_t<AT_TMPL_GEMM, true>(a, e.depth, pl.grid, pl.threads, pl.lds_bytes, stream, start,
+                                                         stop)
+                    : launch_local_t<AT_TMPL_GEMM, false>(a, e.depth, pl.grid, pl.threads, pl.lds_bytes, stream, start,
+                                                          stop);
+    return fast ? launch_local_t<AT_TMPL_CONV2D_NCHW, true>(a, e.depth, pl.grid, pl.threads, pl.lds_bytes, stream,
+                                                            start, stop)
+                : launch_local_t<AT_TMPL_CONV2D_NCHW, false>(a, e.depth, pl.grid, pl.threads, pl.lds_bytes, stream,
+                                                             start, stop);
 }
 
 }  // namespace at

@@ -526,6 +526,8 @@ LOCAL_PLANS = {
     "tail_wide": dict(n=4096, trees=300, depth=8, steps=10),
     # four chains per workgroup, the last workgroup holding one
     "tail_ragged": dict(n=1021, trees=300, depth=8, steps=12),
+    # at least 384 trees: the evaluating waves also make the next candidates
+    "tail_ragged_long": dict(n=1021, trees=400, depth=8, steps=12),
 }
 
 
@@ -547,7 +549,7 @@ def test_sa_local_plans_match_oracle(P, mode):
     if mode.startswith("tail") or mode.startswith("resident"):
         assert (plan["chains_per_wg"] > 4) == mode.endswith("_wide")
     # the first 160 chains, or the last 160 when the last workgroup is short
-    r0 = n - 160 if mode == "tail_ragged" else 0
+    r0 = n - 160 if mode.startswith("tail_ragged") else 0
     m = min(n - r0, 160)
     och = oracle.Chains([osp], [0, m], seed=seed, chain0=r0, topk=k)
     otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, r0, m, 0, steps), trace=True)
