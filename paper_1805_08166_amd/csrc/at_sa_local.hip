@@ -37,11 +37,6 @@ constexpr uint32_t LOCAL_TILE_MASK = 0x3f03u;  // node bits of a tile byte addre
 // dynamic LDS per workgroup: the compute unit's 160 KB less 1 KB kept for
 // any static LDS the compiler places
 constexpr size_t LOCAL_LDS_BYTES = 163840 - 1024;
-// Fast rounds of ensembles with at least this many trees have the next
-// candidates made by the waves that evaluate them, during the fold (a fold
-// of that many leaves outlasts the moves and the features); smaller ones
-// have the owners make them before the walk.
-constexpr int LOCAL_SPEC_T_MIN = 384;
 
 struct LocalArgs {
     const SpaceDesc* descs;
@@ -375,18 +370,21 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         });
     if (owner && a.steps > 0)
         with_space([&](const SpaceDesc& sd) { draw_move(sd, k0, k1, gchain, a.step0, mv_j, mv_v, mv_radix); });
-    // Tail mode with at most four chains per workgroup takes the owners'
-    // side work off the path from one fold to the next: a helper wave draws
-    // the moves two steps ahead, and a round's candidates are offered to the
-    // best lists by another wave during the next round's fold (the offers of
-    // a chain stay in round order).  Roles during a fold: wave 0 folds,
-    // waves 1-2 evaluate the next candidates, wave 3 offers, wave 4 draws,
-    // the last wave brings the next thresholds.
+    // Fast plans (single pass, at most four chains per workgroup) take the
+    // owners' side work off the path from one fold to the next: a helper
+    // wave draws the moves two steps ahead, and a round's candidates are
+    // offered to the best lists by another wave during the next round's fold
+    // (the offers of a chain stay in round order).  Roles during a fold:
+    // wave 0 folds, waves 1-2 make and evaluate the next candidates, wave 3
+    // offers, wave 4 draws, the last wave brings the next thresholds.  The
+    // chain's record carries, by round parity, the two candidates made for
+    // the round, which of them is the round's (the previous accept's
+    // outcome) and the configuration the round starts from, so that no
+    // reader in one round meets a writer of the same round.
     // single pass: every tree walked in one pass per round (tail mode, or
     // resident trees in one chunk); such runs work a round ahead
     const bool single = FAST || a.tail || (a.resident && a.n_chunks == 1);
     const bool fast = FAST;
-    const bool spec = fast && a.T >= LOCAL_SPEC_T_MIN;
     auto draw_into = [&](int j, int st) {
         // move of step st for chain j into its record (slot st & 1)
         int jm;
@@ -445,10 +443,10 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
 #pragma unroll
         for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (w[j >> 1] >> (16 * (j & 1))) & 0xffffu;
     };
-    // tail mode works a round ahead: while a round's scores are folded, the
-    // other waves evaluate the next round's candidate both for an accepted
-    // and for a rejected current one (feature rows 0 and 1), so a round
-    // starts from ready rows.  Owners keep both candidates (na, nb).
+    // single-pass plans work a round ahead: while a round's scores are
+    // folded, the other waves evaluate the next round's candidate both for
+    // an accepted and for a rejected current one (feature rows 0 and 1), so
+    // a round starts from ready rows.
     const int cpb_log2 = __builtin_ctz((unsigned)cpb);
     uint32_t cd[MAX_KNOBS];
     uint64_t cfg = 0;
@@ -560,21 +558,6 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             // LDS.  Thread t takes chain t % cpb and, with S = min(ceil(T /
             // 4), threads / cpb) slots, slot u = t / cpb < S takes trees u,
             // u + S, u + 2S, u + 3S per pass.
-            if (owner && more && fast && !spec) {
-                // the next round's two candidates, kept by round parity
-                const int sl = (s + 1) & 1;
-                ChainRec& R = rec[tid];
-                uint32_t nx[MAX_KNOBS];
-                uint64_t ncfg;
-#pragma unroll
-                for (int v = 0; v < 2; ++v) {
-                    if (v == 0 || is_init) apply_move(cd, cfg, R.mvj[sl], R.mvv[sl], R.mvr[sl], nx, ncfg);
-                    else apply_move(cur, cur_cfg, R.mvj[sl], R.mvv[sl], R.mvr[sl], nx, ncfg);
-#pragma unroll
-                    for (int j = 0; j < MAX_KNOBS / 2; ++j) R.snx[(r + 1) & 1][v][j] = nx[2 * j] | (nx[2 * j + 1] << 16);
-                    R.scfg[(r + 1) & 1][v] = ncfg;
-                }
-            }
             if (owner && more && !fast) {
                 with_space([&](const SpaceDesc& sd) {
                     draw_move(sd, k0, k1, gchain, a.step0 + (uint32_t)(s + 1), mv_j, mv_v, mv_radix);
@@ -658,12 +641,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                     const int gr2 = it & 15, j = (it >> 4) & (cpb - 1), v = (it >> 4) >> cpb_log2;
                     if (j < nc && gr2 < N::L) {
                         uint32_t nx[MAX_KNOBS];
-                        if (fast && !spec) {
-                            uint32_t w[MAX_KNOBS / 2];
-#pragma unroll
-                            for (int q = 0; q < MAX_KNOBS / 2; ++q) w[q] = rec[j].snx[(r + 1) & 1][v][q];
-                            unpack(w, nx);
-                        } else if (spec) {
+                        if (fast) {
                             // the candidate itself: step s + 1's move applied to
                             // this round's candidate (v = 0; also v = 1 after
                             // the initial draw, which is always accepted) or to
