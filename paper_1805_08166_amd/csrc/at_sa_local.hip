@@ -755,8 +755,13 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         // (5) offer to the best list when some chain qualifies, then the
         // Metropolis test
         if (fast) {
-            if (owner) {
-                const bool acc = is_init || (sc - cur_s) >= thr_v;
+            // only the outcome is needed before the barrier (the next round's
+            // tile copy reads it); in tail mode the rest of the owner's books
+            // follow it, beside the other waves' copy (in the resident mode
+            // wave 0 walks first, so they stay ahead of it)
+            const bool acc = owner && (is_init || (sc - cur_s) >= thr_v);
+            if (owner) rec[tid].ssel[(r + 1) & 1] = acc ? 0u : 1u;
+            auto books = [&]() {
                 if (!is_init && a.trace) {
                     at_entry tr;
                     tr.cfg = cfg;
@@ -764,12 +769,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
                     tr.flag = acc ? 1u : 0u;
                     a.trace[c * a.steps + s] = tr;
                 }
+                // the candidate waits for its offer (wave 3, next round); the
+                // next round starts from the configuration published here
                 ChainRec& R = rec[tid];
                 R.pcfg[r & 1] = cfg;
                 R.pscore[r & 1] = sc;
-                // the next round takes the candidate of this outcome and
-                // starts from the configuration published here
-                R.ssel[(r + 1) & 1] = acc ? 0u : 1u;
                 if (acc) {
 #pragma unroll
                     for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
@@ -779,8 +783,10 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
 #pragma unroll
                 for (int j = 0; j < MAX_KNOBS / 2; ++j) R.curk[(r + 1) & 1][j] = cur[2 * j] | (cur[2 * j + 1] << 16);
                 R.curcfg[(r + 1) & 1] = cur_cfg;
-            }
+            };
+            if (owner && !a.tail) books();
             lds_barrier();
+            if (owner && a.tail) books();
             continue;
         }
         if (owner) {
@@ -825,8 +831,11 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
         }
     }
 
-    // the last round's offer (the loop ended on a barrier)
-    if (fast && rounds > 0 && wave == 3) offer_pending(rounds - 1);
+    // the last round's offer, once the owners have recorded its candidates
+    if (fast && rounds > 0) {
+        lds_barrier();
+        if (wave == 3) offer_pending(rounds - 1);
+    }
     // write the chain state and the best lists back
     __syncthreads();
     if (owner) {
