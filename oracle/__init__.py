@@ -52,6 +52,7 @@ def lib():
         L.or_loop_quantities.argtypes = [vp, u64, vp]
         L.or_features.argtypes = [vp, vp, i64, vp]
         L.or_predict.argtypes = [i32, i32, i32, vp, vp, vp, vp, i64, vp, vp]
+        L.or_predict_nodes.argtypes = [i32, vp, vp, vp, vp, vp, vp, i32, vp, i64, vp]
         L.or_philox.argtypes = [u64, vp, vp]
         L.or_philox.restype = None
         L.or_thresholds.argtypes = [u64, i64, i64, u64, i32, vp]
@@ -157,6 +158,24 @@ def predict(fid, thr, leaf, feats, want_leaves=False):
     _check(lib().or_predict(T, depth, F, _p(fid), _p(thr), _p(leaf), _p(feats), n, _p(scores),
                             _p(leaves) if want_leaves else None), "predict")
     return (scores, leaves) if want_leaves else scores
+
+
+def predict_nodes(trees, feats):
+    """fp32 scores of trees in node-list form (left fold in tree order).
+    trees: dict of offsets [T+1], left, right, feature (int32), threshold,
+    value (float32), as written by trained gradient-boosting libraries."""
+    off = np.ascontiguousarray(trees["offsets"], dtype=np.int32)
+    left = np.ascontiguousarray(trees["left"], dtype=np.int32)
+    right = np.ascontiguousarray(trees["right"], dtype=np.int32)
+    feat = np.ascontiguousarray(trees["feature"], dtype=np.int32)
+    th = np.ascontiguousarray(trees["threshold"], dtype=np.float32)
+    val = np.ascontiguousarray(trees["value"], dtype=np.float32)
+    feats = np.ascontiguousarray(feats, dtype=np.int32)
+    n, F = feats.shape
+    scores = np.zeros(n, dtype=np.float32)
+    _check(lib().or_predict_nodes(len(off) - 1, _p(off), _p(left), _p(right), _p(feat), _p(th), _p(val), F,
+                                  _p(feats), n, _p(scores)), "predict_nodes")
+    return scores
 
 
 def predict_global_local(global_model, feats_global, local_model, feats_local):

@@ -688,6 +688,40 @@ int or_predict(int n_trees, int depth, int n_features, const uint8_t* fid, const
     return 0;
 }
 
+// Trees in node-list form, as a trained gradient-boosting library writes
+// them out (Section 3.1: the model is such an ensemble; its trees need not be
+// full nor share one depth).  Tree t owns nodes offsets[t] .. offsets[t+1]-1,
+// its root first; child indices count from the tree's first node.  A node
+// with left >= 0 is a split: the walk takes left when x[feature] <
+// threshold, the two compared as doubles, else right.  A node with left < 0
+// is a leaf worth value.  A row's score is the fp32 sum of its reached
+// leaves, added in tree order from +0.0f, exactly as predict_row.  Returns -1
+// for a child or feature out of range or a walk longer than its tree.
+int or_predict_nodes(int n_trees, const int32_t* offsets, const int32_t* left, const int32_t* right,
+                     const int32_t* feature, const float* threshold, const float* value, int n_features,
+                     const int32_t* feats, int64_t n, float* scores) {
+    if (n_trees < 1 || n_features < 1) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        const int32_t* x = feats + i * n_features;
+        float s = 0.0f;
+        for (int t = 0; t < n_trees; ++t) {
+            const int32_t base = offsets[t], size = offsets[t + 1] - offsets[t];
+            if (size < 1) return -1;
+            int32_t node = 0;
+            for (int32_t steps = 0; left[base + node] >= 0; ++steps) {
+                if (steps >= size) return -1;
+                const int32_t j = base + node;
+                if (feature[j] < 0 || feature[j] >= n_features) return -1;
+                node = (double)x[feature[j]] < (double)threshold[j] ? left[j] : right[j];
+                if (node < 0 || node >= size) return -1;
+            }
+            s = s + value[base + node];
+        }
+        scores[i] = s;
+    }
+    return 0;
+}
+
 void or_philox(uint64_t seed, const uint32_t* ctr, uint32_t* out) {
     philox_block(seed, ctr[0], ctr[1], ctr[2], ctr[3], out);
 }

@@ -95,6 +95,54 @@ def make_ensemble(n_trees: int, depth: int, n_features: int, seed: int):
     return fid.astype(np.uint8), thr.astype(np.uint8), leaf
 
 
+def make_node_trees(n_trees: int, max_depth: int, n_features: int, seed: int, p_leaf: float = 0.25,
+                    shuffle: bool = True) -> dict:
+    """Synthetic trees of varying shape in node-list form, as a trained
+    gradient-boosting library writes them: tree t owns nodes offsets[t] ..
+    offsets[t+1]-1, its root first, children indexed from the tree's first
+    node; left < 0 marks a leaf.  A node below the root becomes a leaf with
+    probability p_leaf, and every node at max_depth is one.  Split features
+    are uniform over [0, n_features); thresholds are float32, mostly integers
+    and half-integers in [0, 33), a few negative or above 255; leaf values are
+    fp32(N(0,1) * 0.05).  shuffle permutes each tree's non-root nodes."""
+    rng = np.random.default_rng(seed)
+    offs, L, R, Fe, Th, V = [0], [], [], [], [], []
+    for _ in range(n_trees):
+        # breadth-first growth: (level) per node, children filled in later
+        lev, left, right = [0], [-1], [-1]
+        i = 0
+        while i < len(lev):
+            if lev[i] < max_depth and (i == 0 or rng.random() >= p_leaf):
+                left[i], right[i] = len(lev), len(lev) + 1
+                lev += [lev[i] + 1, lev[i] + 1]
+                left += [-1, -1]
+                right += [-1, -1]
+            i += 1
+        m = len(lev)
+        perm = np.arange(m)
+        if shuffle and m > 2:
+            perm[1:] = 1 + rng.permutation(m - 1)
+        pos = np.empty(m, np.int64)
+        pos[perm] = np.arange(m)            # node i is written at pos[i]
+        l2, r2 = np.full(m, -1, np.int64), np.full(m, -1, np.int64)
+        for i_ in range(m):
+            if left[i_] >= 0:
+                l2[pos[i_]], r2[pos[i_]] = pos[left[i_]], pos[right[i_]]
+        kind = rng.random(m)
+        th = rng.integers(0, 33, size=m).astype(np.float64) + np.where(kind < 0.5, 0.0, 0.5)
+        th = np.where(kind > 0.97, rng.uniform(-40.0, -0.25, size=m), th)
+        th = np.where((kind > 0.94) & (kind <= 0.97), rng.uniform(255.5, 1e6, size=m), th)
+        L.append(l2)
+        R.append(r2)
+        Fe.append(np.where(l2 >= 0, rng.integers(0, n_features, size=m), 0))
+        Th.append(np.where(l2 >= 0, th, 0.0))
+        V.append(np.where(l2 < 0, rng.standard_normal(size=m) * 0.05, 0.0))
+        offs.append(offs[-1] + m)
+    return {"offsets": np.asarray(offs, np.int32), "left": np.concatenate(L).astype(np.int32),
+            "right": np.concatenate(R).astype(np.int32), "feature": np.concatenate(Fe).astype(np.int32),
+            "threshold": np.concatenate(Th).astype(np.float32), "value": np.concatenate(V).astype(np.float32)}
+
+
 def make_configs(n: int, n_configs: int, seed: int) -> np.ndarray:
     """n configuration indices drawn uniformly from [0, n_configs) (uint64)."""
     rng = np.random.default_rng(seed)
