@@ -131,6 +131,46 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
                              const uint8_t* thr, const float* leaf, at_ensemble_t* out);
 void at_ensemble_destroy(at_ensemble_t ens);
 
+/* Trained trees of any shape (Section 3.1: the cost model is a gradient-
+ * boosted tree ensemble as a boosting library trains it; such trees are
+ * neither full nor of one depth), given as node lists on the host: tree t
+ * owns nodes tree_offsets[t] .. tree_offsets[t+1]-1 of the arrays, its root
+ * first, and child indices count from the tree's first node.  Node i is a
+ * split when left[i] >= 0: a row with x[feature[i]] < threshold[i] goes to
+ * left[i], any other to right[i].  Node i is a leaf worth value[i] when
+ * left[i] < 0 (right, feature and threshold are then ignored).
+ *
+ * at_trees_depth: checks that the lists form binary trees (every child in
+ * range, every node reached at most once from its root; AT_E_INVALID
+ * otherwise) and writes the level of the deepest leaf (0 for a tree that is
+ * a single leaf) to *depth.
+ *
+ * at_trees_pad: writes the full-tree tables of at_ensemble_create at the given
+ * depth (the deepest leaf's or more, 1 .. 12): fid, thr [n_trees][2^depth-1],
+ * leaf [n_trees][2^depth], caller-owned host arrays.  A leaf above the last
+ * level becomes a split on feature 0 with threshold 255 whose subtrees both
+ * end in copies of the leaf, so every row reaches the leaf's value.  A
+ * threshold t becomes ceil(t) clamped to [0, 255] (0 for t <= 0, 255 above
+ * 255): x < t and x < ceil(t) agree for every integer x, so each row reaches
+ * the same leaf value as in the lists whenever its features lie in
+ * [0, 254] (loop features and relation features do).  Leaf indices that
+ * at_gbt_predict reports are those of the padded trees.  Errors:
+ * AT_E_INVALID for bad lists, a split feature outside [0, n_features), a
+ * NaN threshold or a leaf below `depth`; AT_E_UNSUPPORTED for depth or
+ * n_features out of range.
+ *
+ * at_ensemble_import: at_trees_pad at the deepest leaf's depth (at least 1),
+ * then at_ensemble_create.  AT_E_UNSUPPORTED when a leaf lies below level 12.
+ * Synchronous. */
+at_status at_trees_depth(int n_trees, const int32_t* tree_offsets, const int32_t* left, const int32_t* right,
+                         int* depth);
+at_status at_trees_pad(int n_trees, const int32_t* tree_offsets, const int32_t* left, const int32_t* right,
+                       const int32_t* feature, const float* threshold, const float* value, int n_features, int depth,
+                       uint8_t* fid, uint8_t* thr, float* leaf);
+at_status at_ensemble_import(int n_trees, const int32_t* tree_offsets, const int32_t* left, const int32_t* right,
+                             const int32_t* feature, const float* threshold, const float* value, int n_features,
+                             at_ensemble_t* out);
+
 /* Scores of n feature rows: the fp32 sum of each tree's reached leaf,
  * added in tree order starting from +0.0f (higher is better).
  * feats: device [n][n_features] int32 with values in [0, 255] (values

@@ -31,6 +31,7 @@ ENTRY_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("flag", "<u4")])
 EXPORTED = [
     "at_space_create", "at_space_info", "at_spaceset_create", "at_space_destroy",
     "at_extract_features", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
+    "at_trees_depth", "at_trees_pad", "at_ensemble_import",
     "at_gbt_predict", "at_gbt_predict_global_local", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
     "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_last_error",
@@ -63,6 +64,9 @@ def _load():
         "at_space_errors": [vp, vp],
         "at_ensemble_create": [i32, i32, i32, vp, vp, vp, vp],
         "at_ensemble_destroy": [vp],
+        "at_trees_depth": [i32, vp, vp, vp, vp],
+        "at_trees_pad": [i32, vp, vp, vp, vp, vp, vp, i32, i32, vp, vp, vp],
+        "at_ensemble_import": [i32, vp, vp, vp, vp, vp, vp, i32, vp],
         "at_gbt_predict": [vp, vp, i64, vp, vp, vp],
         "at_gbt_predict_global_local": [vp, vp, vp, vp, i64, vp, vp],
         "at_chains_create": [vp, i64, i64, i32, u64, vp],
@@ -233,6 +237,52 @@ def at_ensemble_create(fid, thr, leaf, n_features: int) -> Ensemble:
                                                          ctypes.byref(h)))
     e = Ensemble(h)
     e.n_trees, e.depth, e.n_features = T, depth, int(n_features)
+    return e
+
+
+def _node_lists(trees):
+    keys = ("offsets", "left", "right", "feature", "threshold", "value")
+    dt = (np.int32,) * 4 + (np.float32,) * 2
+    arr = [np.ascontiguousarray(trees[k], dtype=d) for k, d in zip(keys, dt)]
+    m = len(arr[1])
+    if len(arr[0]) < 2 or any(len(a) != m for a in arr[1:]) or arr[0][0] < 0 or arr[0][-1] > m:
+        raise ValueError("inconsistent node lists")
+    return arr
+
+
+def at_trees_depth(trees) -> int:
+    """Level of the deepest leaf of node-list trees (dict of offsets, left,
+    right, feature, threshold, value; host arrays)."""
+    off, left, right, _, _, _ = _node_lists(trees)
+    d = ctypes.c_int()
+    _check("at_trees_depth", _lib.at_trees_depth(len(off) - 1, _np(off), _np(left), _np(right), ctypes.byref(d)))
+    return d.value
+
+
+def at_trees_pad(trees, n_features: int, depth: int):
+    """Full-tree tables (fid, thr uint8 [T, 2^d-1], leaf float32 [T, 2^d]) of
+    node-list trees, padded to `depth`."""
+    off, left, right, feat, th, val = _node_lists(trees)
+    T = len(off) - 1
+    dd = depth if 1 <= depth <= 12 else 1      # the library rejects other depths
+    fid = np.zeros((T, (1 << dd) - 1), np.uint8)
+    thr = np.zeros((T, (1 << dd) - 1), np.uint8)
+    leaf = np.zeros((T, 1 << dd), np.float32)
+    _check("at_trees_pad", _lib.at_trees_pad(T, _np(off), _np(left), _np(right), _np(feat), _np(th), _np(val),
+                                             int(n_features), int(depth), _np(fid), _np(thr), _np(leaf)))
+    return fid, thr, leaf
+
+
+def at_ensemble_import(trees, n_features: int) -> Ensemble:
+    """Ensemble from node-list trees of any shape, padded on the host to the
+    deepest leaf's depth."""
+    off, left, right, feat, th, val = _node_lists(trees)
+    T = len(off) - 1
+    h = ctypes.c_void_p()
+    _check("at_ensemble_import", _lib.at_ensemble_import(T, _np(off), _np(left), _np(right), _np(feat), _np(th),
+                                                         _np(val), int(n_features), ctypes.byref(h)))
+    e = Ensemble(h)
+    e.n_trees, e.depth, e.n_features = T, max(1, at_trees_depth(trees)), int(n_features)
     return e
 
 

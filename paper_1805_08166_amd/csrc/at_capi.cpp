@@ -361,6 +361,140 @@ at_status at_ensemble_create(int n_trees, int depth, int n_features, const uint8
     return AT_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Trained trees of any shape: node lists padded to full heap trees.  A leaf
+// above the last level becomes a split that always goes left (feature 0,
+// threshold 255, while features stay below 255) over two subtrees that both
+// end in copies of the leaf, so every row still reaches the leaf's value.
+// Float thresholds become integers: for an integer x, x < t holds exactly
+// when x < ceil(t).
+// ---------------------------------------------------------------------------
+namespace {
+
+// Checks the lists of tree t (a binary tree rooted at its first node: every
+// child in range, each node reached once) and returns its deepest leaf's
+// level in *depth.
+at_status tree_shape(int t, const int32_t* offsets, const int32_t* left, const int32_t* right, int* depth) {
+    const int64_t base = offsets[t], m = (int64_t)offsets[t + 1] - offsets[t];
+    if (base < 0 || m < 1) return fail(AT_E_INVALID, "trees: tree " + std::to_string(t) + " has no nodes");
+    std::vector<uint8_t> seen((size_t)m, 0);
+    std::vector<std::pair<int32_t, int>> stack{{0, 0}};
+    int deepest = 0;
+    seen[0] = 1;
+    while (!stack.empty()) {
+        const auto [i, lev] = stack.back();
+        stack.pop_back();
+        const int32_t l = left[base + i], r = right[base + i];
+        if (l < 0) {
+            deepest = lev > deepest ? lev : deepest;
+            continue;
+        }
+        for (const int32_t ch : {l, r}) {
+            if (ch < 0 || ch >= m || seen[ch])
+                return fail(AT_E_INVALID, "trees: tree " + std::to_string(t) + " node " + std::to_string(i) +
+                                              " has a child out of range or reached twice");
+            seen[ch] = 1;
+            stack.push_back({ch, lev + 1});
+        }
+    }
+    *depth = deepest;
+    return AT_OK;
+}
+
+uint8_t int_threshold(float t) {
+    if (!(t > 0.0f)) return 0;              // x < t never holds for x >= 0
+    if (t > 255.0f) return 255;
+    return (uint8_t)std::ceil(t);
+}
+
+// Heap node h of a depth-D tree from list node i of tree t at level lev.
+void pad_node(const int32_t* left, const int32_t* right, const int32_t* feature, const float* threshold,
+              const float* value, int64_t base, int32_t i, size_t h, int lev, int D, uint8_t* fid, uint8_t* thr,
+              float* leaf) {
+    const size_t n_int = ((size_t)1 << D) - 1;
+    if (lev == D) {
+        leaf[h - n_int] = value[base + i];
+        return;
+    }
+    const bool split = left[base + i] >= 0;
+    fid[h] = split ? (uint8_t)feature[base + i] : 0;
+    thr[h] = split ? int_threshold(threshold[base + i]) : 255;
+    pad_node(left, right, feature, threshold, value, base, split ? left[base + i] : i, 2 * h + 1, lev + 1, D, fid,
+             thr, leaf);
+    pad_node(left, right, feature, threshold, value, base, split ? right[base + i] : i, 2 * h + 2, lev + 1, D, fid,
+             thr, leaf);
+}
+
+}  // namespace
+
+at_status at_trees_depth(int n_trees, const int32_t* tree_offsets, const int32_t* left, const int32_t* right,
+                         int* depth) {
+    if (!depth) return fail(AT_E_INVALID, "at_trees_depth: depth is NULL");
+    *depth = -1;
+    if (n_trees < 1 || n_trees > 65535) return fail(AT_E_INVALID, "at_trees_depth: n_trees out of [1, 65535]");
+    if (!tree_offsets || !left || !right) return fail(AT_E_INVALID, "at_trees_depth: NULL list");
+    int deepest = 0;
+    for (int t = 0; t < n_trees; ++t) {
+        int d = 0;
+        const at_status st = tree_shape(t, tree_offsets, left, right, &d);
+        if (st != AT_OK) return st;
+        deepest = d > deepest ? d : deepest;
+    }
+    *depth = deepest;
+    return AT_OK;
+}
+
+at_status at_trees_pad(int n_trees, const int32_t* tree_offsets, const int32_t* left, const int32_t* right,
+                       const int32_t* feature, const float* threshold, const float* value, int n_features, int depth,
+                       uint8_t* fid, uint8_t* thr, float* leaf) {
+    if (!feature || !threshold || !value || !fid || !thr || !leaf)
+        return fail(AT_E_INVALID, "at_trees_pad: NULL array");
+    if (n_features < 1 || n_features > 256) return fail(AT_E_UNSUPPORTED, "at_trees_pad: n_features out of [1, 256]");
+    if (depth < 1 || depth > 12) return fail(AT_E_UNSUPPORTED, "at_trees_pad: depth out of [1, 12]");
+    int need = 0;
+    at_status st = at_trees_depth(n_trees, tree_offsets, left, right, &need);
+    if (st != AT_OK) return st;
+    if (need > depth) return fail(AT_E_INVALID, "at_trees_pad: a leaf lies below the requested depth");
+    for (int t = 0; t < n_trees; ++t)
+        for (int64_t j = tree_offsets[t]; j < tree_offsets[t + 1]; ++j) {
+            if (left[j] < 0) continue;
+            if (feature[j] < 0 || feature[j] >= n_features)
+                return fail(AT_E_INVALID, "at_trees_pad: split feature out of [0, n_features)");
+            if (std::isnan(threshold[j])) return fail(AT_E_INVALID, "at_trees_pad: NaN threshold");
+        }
+    const size_t n_int = ((size_t)1 << depth) - 1, n_leaf = (size_t)1 << depth;
+    for (int t = 0; t < n_trees; ++t)
+        pad_node(left, right, feature, threshold, value, tree_offsets[t], 0, 0, 0, depth, fid + t * n_int,
+                 thr + t * n_int, leaf + t * n_leaf);
+    return AT_OK;
+}
+
+at_status at_ensemble_import(int n_trees, const int32_t* tree_offsets, const int32_t* left, const int32_t* right,
+                             const int32_t* feature, const float* threshold, const float* value, int n_features,
+                             at_ensemble_t* out) {
+    if (!out) return fail(AT_E_INVALID, "at_ensemble_import: out is NULL");
+    *out = nullptr;
+    int depth = 0;
+    at_status st = at_trees_depth(n_trees, tree_offsets, left, right, &depth);
+    if (st != AT_OK) return st;
+    depth = depth < 1 ? 1 : depth;
+    if (depth > 12) return fail(AT_E_UNSUPPORTED, "at_ensemble_import: a leaf lies deeper than level 12");
+    const size_t n_int = ((size_t)1 << depth) - 1, n_leaf = (size_t)1 << depth;
+    std::vector<uint8_t> fid, thr;
+    std::vector<float> leaf;
+    try {
+        fid.assign((size_t)n_trees * n_int, 0);
+        thr.assign((size_t)n_trees * n_int, 0);
+        leaf.assign((size_t)n_trees * n_leaf, 0.0f);
+    } catch (...) {
+        return fail(AT_E_OOM, "at_ensemble_import: host allocation");
+    }
+    st = at_trees_pad(n_trees, tree_offsets, left, right, feature, threshold, value, n_features, depth, fid.data(),
+                      thr.data(), leaf.data());
+    if (st != AT_OK) return st;
+    return at_ensemble_create(n_trees, depth, n_features, fid.data(), thr.data(), leaf.data(), out);
+}
+
 void at_ensemble_destroy(at_ensemble_t ens) {
     if (!ens) return;
     DeviceGuard g(ens->device);

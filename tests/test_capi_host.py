@@ -94,3 +94,111 @@ def test_quotient_bitlen_identity():
         a = int(rng.integers(1, 2 ** 31))
         b = int(rng.integers(1, a + 1))
         assert fast(a, b) == bitlen(a // b)
+
+
+# --------------------------------------------------------------------------
+# trained trees of any shape: the library's host-side padding to full trees
+# --------------------------------------------------------------------------
+def heap_walk(fid, thr, leaf, x):
+    """Scores of full heap trees (node h: x[fid] < thr -> 2h+1, else 2h+2),
+    an fp32 left fold in tree order."""
+    T, n_int = fid.shape
+    depth = (n_int + 1).bit_length() - 1
+    out = np.zeros(len(x), np.float32)
+    for i, row in enumerate(x):
+        s = np.float32(0)
+        for t in range(T):
+            h = 0
+            for _ in range(depth):
+                h = 2 * h + 1 if row[fid[t, h]] < thr[t, h] else 2 * h + 2
+            s = np.float32(s + leaf[t, h - n_int])
+        out[i] = s
+    return out
+
+
+def tree_levels(trees):
+    deepest = 0
+    for t in range(len(trees["offsets"]) - 1):
+        o = trees["offsets"][t]
+        stack = [(0, 0)]
+        while stack:
+            i, lev = stack.pop()
+            if trees["left"][o + i] < 0:
+                deepest = max(deepest, lev)
+            else:
+                stack += [(trees["left"][o + i], lev + 1), (trees["right"][o + i], lev + 1)]
+    return deepest
+
+
+@pytest.mark.parametrize("max_depth,T,F,extra", [(3, 30, 7, 0), (6, 40, 110, 0), (5, 25, 176, 2), (1, 9, 4, 0)])
+def test_padded_trees_reach_the_oracle_scores(P, max_depth, T, F, extra):
+    import workloads as W
+    trees = W.make_node_trees(T, max_depth, F, seed=50 + max_depth)
+    d = P.at_trees_depth(trees)
+    assert d == tree_levels(trees)
+    fid, thr, leaf = P.at_trees_pad(trees, F, max(1, d) + extra)
+    rng = np.random.default_rng(max_depth)
+    x = rng.integers(0, 40, size=(200, F)).astype(np.int32)
+    x[:4] = [0, 254, 33, 1][:4] if F == 1 else np.array([0, 254, 33, 1])[:, None]
+    want = oracle.predict_nodes(trees, x)
+    assert np.array_equal(heap_walk(fid, thr, leaf, x).view(np.uint32), want.view(np.uint32))
+
+
+def test_padding_of_the_worked_example(P):
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "trained_trees_worked_example.json")) as f:
+        g = json.load(f)
+    assert P.at_trees_depth(g["trees"]) == 3
+    fid, thr, leaf = P.at_trees_pad(g["trees"], g["n_features"], 3)
+    # tree A (one leaf) is eight copies of 0.5 under always-left splits
+    assert (leaf[0] == 0.5).all() and (thr[0] == 255).all()
+    # tree B's stump: threshold 3.5 becomes 4; each side copied below
+    assert fid[1, 0] == 2 and thr[1, 0] == 4
+    assert leaf[1].tolist() == [-0.25] * 4 + [0.125] * 4
+    assert heap_walk(fid, thr, leaf, np.asarray(g["rows"])).tolist() == g["scores"]
+
+
+def test_xgboost_dump_parses_to_the_worked_example(P):
+    import json
+    from paper_1805_08166_amd.xgboost_dump import trees_from_xgboost_dump
+    with open(os.path.join(ROOT, "tests", "golden", "trained_trees_worked_example.json")) as f:
+        g = json.load(f)
+    trees = trees_from_xgboost_dump(g["xgboost_dump"])
+    assert trees["offsets"].tolist() == [0, 1, 4, 11]
+    assert P.at_trees_depth(trees) == 3
+    fid, thr, leaf = P.at_trees_pad(trees, g["n_features"], 3)
+    assert heap_walk(fid, thr, leaf, np.asarray(g["rows"])).tolist() == g["scores"]
+    with pytest.raises(ValueError):
+        trees_from_xgboost_dump(['{"nodeid": 0, "split": "f1", "split_condition": 1, "yes": 1, "no": 2, '
+                                 '"children": [{"nodeid": 1, "leaf": 0.5}]}'])
+
+
+def test_tree_list_errors(P):
+    INVALID, UNSUPPORTED = -1, -2
+    ok = {"offsets": [0, 3], "left": [1, -1, -1], "right": [2, -1, -1], "feature": [1, 0, 0],
+          "threshold": [1.5, 0, 0], "value": [0, 1.0, 2.0]}
+
+    def bad(**kw):
+        t = dict(ok)
+        t.update(kw)
+        return t
+
+    assert P.at_trees_depth(ok) == 1
+    expect_status(P, lambda: P.at_trees_depth(bad(right=[3, -1, -1])), INVALID)       # child out of range
+    expect_status(P, lambda: P.at_trees_depth(bad(right=[1, -1, -1])), INVALID)       # node reached twice
+    expect_status(P, lambda: P.at_trees_depth(bad(left=[1, 0, -1], right=[2, 2, -1])), INVALID)  # cycle
+    expect_status(P, lambda: P.at_trees_depth(bad(offsets=[0, 0, 3])), INVALID)      # empty tree
+    expect_status(P, lambda: P.at_trees_pad(bad(feature=[2, 0, 0]), 2, 1), INVALID)   # feature out of range
+    expect_status(P, lambda: P.at_trees_pad(bad(threshold=[float("nan"), 0, 0]), 2, 1), INVALID)
+    expect_status(P, lambda: P.at_trees_pad(ok, 2, 13), UNSUPPORTED)
+    deep = {"offsets": [0, 5], "left": [1, 3, -1, -1, -1], "right": [2, 4, -1, -1, -1], "feature": [0] * 5,
+            "threshold": [1.0] * 5, "value": [0.0] * 5}
+    expect_status(P, lambda: P.at_trees_pad(deep, 2, 1), INVALID)                      # leaf below depth
+    # a left spine of 13 splits, each with a leaf on its right: deeper than
+    # any supported ensemble
+    left = [i + 1 if i < 13 else -1 for i in range(14)] + [-1] * 13
+    right = [14 + i if i < 13 else -1 for i in range(14)] + [-1] * 13
+    chain = {"offsets": [0, 27], "left": left, "right": right, "feature": [0] * 27, "threshold": [1.0] * 27,
+             "value": [0.0] * 27}
+    assert P.at_trees_depth(chain) == 13
+    expect_status(P, lambda: P.at_ensemble_import(chain, 2), UNSUPPORTED)
