@@ -51,6 +51,7 @@ def lib():
         L.or_encode.argtypes = [vp, vp, vp]
         L.or_loop_quantities.argtypes = [vp, u64, vp]
         L.or_features.argtypes = [vp, vp, i64, vp]
+        L.or_features_full.argtypes = [vp, vp, i64, vp]
         L.or_predict.argtypes = [i32, i32, i32, vp, vp, vp, vp, i64, vp, vp]
         L.or_predict_nodes.argtypes = [i32, vp, vp, vp, vp, vp, vp, i32, vp, i64, vp]
         L.or_philox.argtypes = [u64, vp, vp]
@@ -94,6 +95,8 @@ class Space:
         self.knob_sizes = sizes[: nk.value].copy()
         self.n_loops = nl.value
         self.n_features = nf.value
+        # full Appendix A.2 rows add top-down and bottom-up: 4 + 3 per buffer (3) per loop
+        self.n_features_full = self.n_loops * 13
         self.n_configs = nc.value
 
     def __del__(self):
@@ -135,6 +138,15 @@ class Space:
         c = np.ascontiguousarray(cfgs, dtype=np.uint64)
         out = np.zeros((len(c), 2 * 3 * self.RELATION_THRESHOLDS), dtype=np.int32)
         _check(lib().or_relation_features(self._h, _p(c), len(c), _p(out)), "relation_features")
+        return out
+
+    def features_full(self, cfgs) -> np.ndarray:
+        """Rows with the top-down and bottom-up columns of Appendix A.2:
+        per loop bitlen(length), annotation, bitlen(top-down),
+        bitlen(bottom-up), then per buffer touch, reuse, stride bitlens."""
+        c = np.ascontiguousarray(cfgs, dtype=np.uint64)
+        out = np.zeros((len(c), self.n_features_full), dtype=np.int32)
+        _check(lib().or_features_full(self._h, _p(c), len(c), _p(out)), "features_full")
         return out
 
     def features(self, cfgs) -> np.ndarray:

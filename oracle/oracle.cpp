@@ -376,6 +376,35 @@ void features_of(const Space& sp, uint64_t cfg, int32_t* row) {
 
 int n_features_of(const Space& sp) { return (int)sp.loops.size() * (2 + 3 * (int)sp.buffers.size()); }
 
+// Feature row with the top-down and bottom-up columns of Appendix A.2: per
+// loop, outer to inner: bitlen(length), annotation id, bitlen(top-down),
+// bitlen(bottom-up), then for each buffer bitlen(touch count), bitlen(reuse
+// ratio), bitlen(stride).  Top-down is the product of the lengths of the
+// loops strictly outside the loop (1 for the outermost), bottom-up that of
+// the loop and the loops inside it.
+void features_full_of(const Space& sp, uint64_t cfg, int32_t* row) {
+    std::vector<int64_t> v;
+    decode(sp, cfg, v);
+    std::vector<LoopQ> q;
+    loop_quantities(sp, v, q);
+    int64_t top_down = 1;
+    int k = 0;
+    for (const LoopQ& o : q) {
+        row[k++] = bitlen(o.ext);
+        row[k++] = (int32_t)o.ann;
+        row[k++] = bitlen(top_down);
+        row[k++] = bitlen(o.bottom_up);
+        for (size_t b = 0; b < o.touched.size(); ++b) {
+            row[k++] = bitlen(o.touched[b]);
+            row[k++] = bitlen(o.reuse[b]);
+            row[k++] = bitlen(o.stride[b]);
+        }
+        top_down *= o.ext;
+    }
+}
+
+int n_features_full_of(const Space& sp) { return (int)sp.loops.size() * (4 + 3 * (int)sp.buffers.size()); }
+
 // ---------------------------------------------------------------------------
 // Context relation features (Section 4; Appendix A.2 "Relation Feature").
 // Over the loops of the nest's longest chain (here the whole perfect nest),
@@ -672,6 +701,16 @@ int or_features(void* h, const uint64_t* cfgs, int64_t n, int32_t* feats) {
     for (int64_t i = 0; i < n; ++i) {
         if (cfgs[i] >= sp.n_configs) return -5;
         features_of(sp, cfgs[i], feats + i * F);
+    }
+    return 0;
+}
+
+int or_features_full(void* h, const uint64_t* cfgs, int64_t n, int32_t* feats) {
+    const Space& sp = *(Space*)h;
+    int F = n_features_full_of(sp);
+    for (int64_t i = 0; i < n; ++i) {
+        if (cfgs[i] >= sp.n_configs) return -5;
+        features_full_of(sp, cfgs[i], feats + i * F);
     }
     return 0;
 }
