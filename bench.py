@@ -212,6 +212,12 @@ def bench_score(P, reps, warmup):
                                 P.RELATION_FEATURES)
     tg = float(np.mean(time_events(lambda r: P.at_gbt_predict_global_local(glob, rel, ens, feats, scores), reps)))
     del rel
+    # full Appendix A.2 rows (208 int32: top-down and bottom-up added)
+    full = torch.empty((n, 13 * sp.n_loops), dtype=torch.int32, device="cuda")
+    P.at_extract_features_full(sp, cfgs, full)
+    tf = float(np.mean(time_events(lambda r: P.at_extract_features_full(sp, cfgs, full), reps)))
+    full_bytes = n * (8 + 13 * sp.n_loops * 4)
+    del full
     feat_bytes = n * (8 + 176 * 4)              # cfg in, feature row out
     score_lds = n * wl["trees"] * tree_eval_bytes(wl["depth"])
     return dict(
@@ -223,6 +229,8 @@ def bench_score(P, reps, warmup):
         predict_hbm_GBps=n * (176 * 4 + 4) / tp / 1e9,
         relation_ms=tr * 1e3, relation_rows_per_s=n / tr, relation_hbm_GBps=rel_bytes / tr / 1e9,
         relation_hbm_frac=rel_bytes / tr / HBM_PEAK_BPS,
+        full_extract_ms=tf * 1e3, full_rows_per_s=n / tf, full_extract_hbm_GBps=full_bytes / tf / 1e9,
+        full_extract_hbm_frac=full_bytes / tf / HBM_PEAK_BPS,
         global_local_ms=tg * 1e3, global_local_scores_per_s=n / tg,
         global_local_lds_frac=2 * score_lds / tg / LDS_PEAK_BPS)
 

@@ -116,6 +116,19 @@ void at_space_destroy(at_space_t space);
 at_status at_extract_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
                               at_stream_t stream);
 
+/* Full feature rows of Appendix A.2: per loop (outer to inner)
+ * bitlen(length), annotation id, bitlen(top-down), bitlen(bottom-up), then
+ * for each buffer bitlen(touch count), bitlen(reuse ratio), bitlen(stride):
+ * 13 int32 per loop, n_loops * 13 per row (GEMM 130, conv2d 208).  Top-down
+ * is the product of the lengths of the loops strictly outside the loop (1
+ * for the outermost), bottom-up that of the loop and the loops inside it;
+ * the other columns are those of at_extract_features.  cfgs: device [n]
+ * uint64; feats: device [n][n_loops * 13] int32.  A single space only.
+ * Out-of-range indices fill their row with -1 and are counted as for
+ * at_extract_features.  n == 0 is a no-op. */
+at_status at_extract_features_full(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                   at_stream_t stream);
+
 /* Number of out-of-range configuration indices seen by at_extract_features
  * since the last call (synchronises the device; resets the counter). */
 at_status at_space_errors(at_space_t space, uint64_t* n_out_of_range);

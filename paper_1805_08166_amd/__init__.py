@@ -30,7 +30,7 @@ ENTRY_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("flag", "<u4")])
 
 EXPORTED = [
     "at_space_create", "at_space_info", "at_spaceset_create", "at_space_destroy",
-    "at_extract_features", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
+    "at_extract_features", "at_extract_features_full", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_trees_depth", "at_trees_pad", "at_ensemble_import",
     "at_gbt_predict", "at_gbt_predict_global_local", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
@@ -61,6 +61,7 @@ def _load():
         "at_space_destroy": [vp],
         "at_extract_features": [vp, vp, i64, vp, vp],
         "at_extract_relation_features": [vp, vp, i64, vp, vp],
+        "at_extract_features_full": [vp, vp, i64, vp, vp],
         "at_space_errors": [vp, vp],
         "at_ensemble_create": [i32, i32, i32, vp, vp, vp, vp],
         "at_ensemble_destroy": [vp],
@@ -201,6 +202,19 @@ def at_extract_features(space: Space, cfgs, feats, stream=None):
     if feats.shape != (n, space.n_features):
         raise ValueError("feats must be [n, n_features]")
     _check("at_extract_features", _lib.at_extract_features(
+        space.h, _dev(cfgs, torch.int64, "cfgs"), n, _dev(feats, torch.int32, "feats"), _stream(stream)))
+
+
+def at_extract_features_full(space: Space, cfgs, feats, stream=None):
+    """Full Appendix A.2 rows (13 per loop: loop-context columns with
+    bitlen(top-down) and bitlen(bottom-up) after the annotation).
+    cfgs: device uint64 [n] (torch.int64 storage); feats: device int32
+    [n, 13 * n_loops]."""
+    import torch
+    n = cfgs.numel()
+    if feats.shape != (n, 13 * space.n_loops):
+        raise ValueError("feats must be [n, 13 * n_loops]")
+    _check("at_extract_features_full", _lib.at_extract_features_full(
         space.h, _dev(cfgs, torch.int64, "cfgs"), n, _dev(feats, torch.int32, "feats"), _stream(stream)))
 
 

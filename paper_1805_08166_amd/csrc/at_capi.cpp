@@ -201,6 +201,18 @@ at_status at_extract_features(at_space_t space, const uint64_t* cfgs, int64_t n,
     return finish_launch(launch_extract(*space, cfgs, n, feats, (hipStream_t)stream), "at_extract_features");
 }
 
+at_status at_extract_features_full(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                   at_stream_t stream) {
+    if (!space) return fail(AT_E_INVALID, "at_extract_features_full: NULL space");
+    if (space->n_spaces != 1) return fail(AT_E_INVALID, "at_extract_features_full: takes a single space, not a set");
+    if (n < 0) return fail(AT_E_INVALID, "at_extract_features_full: n < 0");
+    if (n == 0) return AT_OK;
+    if (!cfgs || !feats) return fail(AT_E_INVALID, "at_extract_features_full: NULL buffer");
+    if (n > ((int64_t)1 << 36)) return fail(AT_E_UNSUPPORTED, "at_extract_features_full: n too large for one call");
+    DeviceGuard g(space->device);
+    return finish_launch(launch_extract_full(*space, cfgs, n, feats, (hipStream_t)stream), "at_extract_features_full");
+}
+
 at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
                                        at_stream_t stream) {
     if (!space) return fail(AT_E_INVALID, "at_extract_relation_features: NULL space");

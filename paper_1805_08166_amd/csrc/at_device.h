@@ -79,13 +79,26 @@ __device__ __forceinline__ void unpack_split(uint64_t w, uint32_t (&f)[4]) {
 // products: range[a] is the extent of axis a covered by the sub-nest, and a
 // loop's stride in buffer b is b's weight of the loop's axis times the range
 // of that axis strictly inside the loop.  emit(f, value) receives feature f.
-template <int TMPL, class Emit>
+// PER = 13 gives the full rows of Appendix A.2: bitlen(top-down) and
+// bitlen(bottom-up) follow the annotation.  Top-down is the nest's iteration
+// count (the product of every factor, below 2^31 for any space) divided by
+// bottom-up, the quotient's bitlen taken without a division.
+template <int TMPL, int PER = 11, class Emit>
 __device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4],
                                               uint32_t unroll_max, uint32_t unroll_id, Emit&& emit) {
+    static_assert(PER == 11 || PER == 13, "loop-context rows or full rows");
     using N = Nest<TMPL>;
+    constexpr int B0 = PER == 13 ? 4 : 2;   // first buffer column
     uint32_t range[6] = {1u, 1u, 1u, 1u, 1u, 1u};
     uint32_t bottom_up = 1u;
     const uint32_t S = (uint32_t)sd.stride;
+    uint32_t total = 1u;
+    if constexpr (PER == 13) {
+#pragma unroll
+        for (int a = 0; a < 6; ++a)
+#pragma unroll
+            for (int l = 0; l < 4; ++l) total *= fac[a][l];
+    }
 #pragma unroll
     for (int p = N::L - 1; p >= 0; --p) {
         uint32_t ext, strd[3];
@@ -111,13 +124,17 @@ __device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_
         N::touched(range, S, t);
         uint32_t ann = N::bind[p] ? (uint32_t)N::bind[p]
                                   : ((unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u);
-        emit(p * 11 + 0, bitlen(ext));
-        emit(p * 11 + 1, ann);
+        emit(p * PER + 0, bitlen(ext));
+        emit(p * PER + 1, ann);
+        if constexpr (PER == 13) {
+            emit(p * PER + 2, bitlen_quot(total, bottom_up));
+            emit(p * PER + 3, bitlen(bottom_up));
+        }
 #pragma unroll
         for (int b = 0; b < 3; ++b) {
-            emit(p * 11 + 2 + 3 * b, bitlen(t[b]));
-            emit(p * 11 + 3 + 3 * b, bitlen_quot(bottom_up, t[b]));
-            emit(p * 11 + 4 + 3 * b, bitlen(strd[b]));
+            emit(p * PER + B0 + 3 * b, bitlen(t[b]));
+            emit(p * PER + B0 + 1 + 3 * b, bitlen_quot(bottom_up, t[b]));
+            emit(p * PER + B0 + 2 + 3 * b, bitlen(strd[b]));
         }
     }
 }

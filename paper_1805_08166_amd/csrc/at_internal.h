@@ -223,6 +223,8 @@ at_status build_space(int tmpl, const int64_t* shape, int nshape, SpaceDesc& des
 // Kernel launchers (at_kernels.hip).
 hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                           hipStream_t stream);
+hipError_t launch_extract_full(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                               hipStream_t stream);
 hipError_t launch_relation(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                            hipStream_t stream);
 // accumulate: add to scores (fp32, the stored value first) instead of storing

@@ -23,19 +23,21 @@ using namespace dev;
 // consecutive lanes covering consecutive 16-byte pieces of the block, so the
 // HBM stores are fully coalesced.
 // ==========================================================================
-template <int TMPL>
+// PER columns per loop: 11 (loop-context rows) or 13 (full Appendix A.2 rows
+// with top-down and bottom-up)
+template <int TMPL, int PER = 11>
 struct RowLayout {
-    static constexpr int F = Nest<TMPL>::F;
+    static constexpr int F = Nest<TMPL>::L * PER;
     static constexpr int RS = ((F + 3) / 4 % 2 == 1) ? ((F + 3) / 4) * 4 : ((F + 3) / 4 + 1) * 4;
 };
 
-template <int TMPL, bool VEC>
+template <int TMPL, bool VEC, int PER = 11>
 __global__ __launch_bounds__(WG) void k_extract(SpaceDesc sd, const uint64_t* __restrict__ factors,
                                                 const uint64_t* __restrict__ cfgs, int64_t n,
                                                 int32_t* __restrict__ feats,
                                                 unsigned long long* __restrict__ n_bad) {
-    constexpr int F = RowLayout<TMPL>::F;
-    constexpr int RS = RowLayout<TMPL>::RS;
+    constexpr int F = RowLayout<TMPL, PER>::F;
+    constexpr int RS = RowLayout<TMPL, PER>::RS;
     __shared__ int8_t rows[WG * RS];
     const int tid = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * WG;
@@ -64,8 +66,8 @@ __global__ __launch_bounds__(WG) void k_extract(SpaceDesc sd, const uint64_t* __
             uint32_t fac[6][4];
             gather_factors<TMPL>(sd, factors, kv, fac);
             constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
-            nest_features<TMPL>(sd, fac, unroll_max_of(kv[A]), 1u + kv[A + 1],
-                                [&](int f, uint32_t v) { my[f] = (int8_t)v; });
+            nest_features<TMPL, PER>(sd, fac, unroll_max_of(kv[A]), 1u + kv[A + 1],
+                                     [&](int f, uint32_t v) { my[f] = (int8_t)v; });
         }
     }
     __syncthreads();
@@ -308,6 +310,28 @@ hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n,
     } else {
         hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, false>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs,
                            n, feats, bad);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_extract_full(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                               hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const SpaceDesc& sd = sp.descs[0];
+    const unsigned grid = (unsigned)((n + WG - 1) / WG);
+    const uint64_t* fac = static_cast<const uint64_t*>(sp.d_factors.p);
+    auto* bad = static_cast<unsigned long long*>(sp.d_errors.p);
+    const bool aligned = (reinterpret_cast<uintptr_t>(feats) & 15u) == 0;
+    if (sp.tmpl == AT_TMPL_GEMM) {
+        // 130 features per row: not a multiple of 4, scalar stores
+        hipLaunchKernelGGL((k_extract<AT_TMPL_GEMM, false, 13>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs, n,
+                           feats, bad);
+    } else if (aligned) {
+        hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, true, 13>), dim3(grid), dim3(WG), 0, stream, sd, fac,
+                           cfgs, n, feats, bad);
+    } else {
+        hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, false, 13>), dim3(grid), dim3(WG), 0, stream, sd, fac,
+                           cfgs, n, feats, bad);
     }
     return hipGetLastError();
 }
