@@ -286,7 +286,8 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(chains shard across GPUs by global chain id; see the design notes)", file=sys.stderr)
+              "(chains are keyed by global chain id, so N GPUs would each run a contiguous block of chains "
+              "and give the same results as one GPU)", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_1805_08166_amd as P
