@@ -285,7 +285,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
               "(chains are keyed by global chain id, so N GPUs would each run a contiguous block of chains "
               "and give the same results as one GPU)", file=sys.stderr)
         sys.exit(2)
