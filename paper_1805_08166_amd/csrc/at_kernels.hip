@@ -157,19 +157,42 @@ __global__ __launch_bounds__(WG) void k_relation(SpaceDesc sd, const uint64_t* _
                                                        : fac[N::axis[p]][N::level[p]];
                 prod *= e;
             }
+            // A sub-nest touches no fewer elements than any sub-nest inside
+            // it, so the loops a threshold t admits (bitlen(touch) <= t) are
+            // the innermost ones from some loop p* on, and each maximum is a
+            // suffix maximum (over p* and the loops inside it).  Visiting the
+            // loops from the innermost outwards, loop p writes its suffix
+            // maxima into every threshold it admits; the outermost admitted
+            // loop, p*, writes last.  Four thresholds share a word: byte j of
+            // word w is t = 4w + 1 + j, admitted when j >= bitlen(touch) - 1 - 4w.
 #pragma unroll
             for (int b = 0; b < 3; ++b) {
+                constexpr int NW = REL_T / 4;
+                uint32_t w0[NW], w1[NW];
 #pragma unroll
-                for (int t = 1; t <= REL_T; ++t) {
-                    uint32_t r0 = 0u, r1 = 0u;
+                for (int w = 0; w < NW; ++w) w0[w] = w1[w] = 0u;
+                uint32_t s0 = 0u, s1 = 0u;
 #pragma unroll
-                    for (int p = 0; p < N::L; ++p) {
-                        const bool in = tc[p][b] <= (uint32_t)t;
-                        r0 = max(r0, in ? ru[p][b] : 0u);
-                        r1 = max(r1, in ? td[p] : 0u);
+                for (int p = N::L - 1; p >= 0; --p) {
+                    s0 = max(s0, ru[p][b]);
+                    s1 = max(s1, td[p]);
+                    const uint32_t b0 = s0 * 0x01010101u, b1 = s1 * 0x01010101u;
+#pragma unroll
+                    for (int w = 0; w < NW; ++w) {
+                        const int kb = min(max((int)tc[p][b] - 1 - 4 * w, 0), 4);
+                        const uint32_t m = (uint32_t)(0xffffffffull << (8 * kb));
+                        w0[w] = (b0 & m) | (w0[w] & ~m);
+                        w1[w] = (b1 & m) | (w1[w] & ~m);
                     }
-                    my[(0 * 3 + b) * REL_T + (t - 1)] = (int8_t)r0;
-                    my[(1 * 3 + b) * REL_T + (t - 1)] = (int8_t)r1;
+                }
+                // rows are dword aligned (REL_RS = 196 bytes) and so is each
+                // 32-byte block
+                uint32_t* d0 = reinterpret_cast<uint32_t*>(my + (0 * 3 + b) * REL_T);
+                uint32_t* d1 = reinterpret_cast<uint32_t*>(my + (1 * 3 + b) * REL_T);
+#pragma unroll
+                for (int w = 0; w < NW; ++w) {
+                    d0[w] = w0[w];
+                    d1[w] = w1[w];
                 }
             }
         }
