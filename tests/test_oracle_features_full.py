@@ -93,3 +93,19 @@ def test_out_of_range_config_is_rejected():
     sp = oracle.Space(workloads.GEMM, (4, 4, 4))
     with pytest.raises(ValueError):
         sp.features_full([sp.n_configs])
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C4", "C7", "C10", "C12", "gemm"])
+def test_touch_counts_never_shrink_outwards(name):
+    # a sub-nest touches every element its inner sub-nests touch, so each
+    # buffer's touch count is non-decreasing from the innermost loop out
+    # (the relation features' thresholds therefore admit innermost runs of
+    # loops)
+    if name == "gemm":
+        sp = oracle.Space(workloads.GEMM, (512, 512, 512))
+    else:
+        sp = oracle.Space(workloads.CONV2D, workloads.conv_shape(name))
+    for c in workloads.make_configs(200, sp.n_configs, seed=17):
+        q = sp.loop_quantities(int(c))
+        for col in (3, 6, 9):
+            assert (np.diff(q[:, col]) <= 0).all(), (name, int(c), col)
