@@ -1,26 +1,34 @@
 """Benchmark of the annealing hot path on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--no-cpu]
 
-A step is one at_sa_run over the whole workload: every chain is initialised
-(knobs drawn, scored, offered to its best list) and then annealed for the
+A step is one at_sa_run over the whole workload: every chain anneals for the
 workload's step count; each annealing step proposes, featurises, scores,
-offers and accepts.  Inputs (ensemble tables, thresholds) are resident on the
-GPU before the timed region; every timed step uses fresh chains with the same
-seed, so every step does identical work.  The headline workload is the C2
-conv2d search (1024 chains x 500 steps, 500 trees of depth 8); the other
-workloads are reported under "extra".
+offers and accepts.  The headline workload is the largest single-GPU search,
+C12 (8192 chains x 1000 steps, 2000 trees of depth 10); the other workloads
+are reported under "extra".  One chains handle serves every run of a
+workload: the warm-up runs initialise its chains and take its one-time
+workspace allocation, and each timed run continues the chains for the
+workload's step count with thresholds computed beforehand for its steps.
+Inputs (ensemble tables, thresholds) are resident on the GPU before the
+timed region, which holds kernel launches only.
 
 Prints one JSON line.  Run times come from HIP events on the stream the
 kernels run on.  The roofline object is for the dominant kernel, the tree
 walk: one further run of each workload attaches start/stop events to every
 kernel launch (at_sa_set_profiling), and the roofline divides the walk's
 algorithmic LDS bytes per launch, (2d+1) x 4 bytes per tree evaluation
-times chains times trees, by its average launch duration.  Its HBM traffic
-comes from the committed rocprofv3 counter summary while the kernel source
-it was taken from is unchanged (null otherwise).  A 256 MiB device copy runs
-once before the timed region; its FETCH_SIZE / WRITE_SIZE readings scale the
-counters.
+times chains times trees, by its average launch duration; "whole_run" does
+the same for the whole run.  Fractions are given against 128 bytes per clock
+per compute unit (4-byte accesses) and against the 202 measured for 16-byte
+reads.  Its HBM traffic comes from the committed rocprofv3 counter summary
+while the kernel source it was taken from is unchanged (null otherwise).  A
+256 MiB device copy runs once before the timed region; its FETCH_SIZE /
+WRITE_SIZE readings scale the counters.
+
+The CPU baseline is the oracle on the first chains of the workload, on one
+core and as P single-threaded processes at once (P = the host cores this
+process may use, at most 16), run before the GPU is touched.
 """
 from __future__ import annotations
 
@@ -43,7 +51,12 @@ METRIC = "SA candidate evals/sec (features+GBT+accept); GBT scores/sec, 1M cfg×
 
 # MI355X: 256 CUs at 2.4 GHz; LDS serves 128 bytes per clock per CU.
 N_CU, CLOCK_HZ = 256, 2.4e9
-LDS_PEAK_BPS = 128 * N_CU * CLOCK_HZ          # 78.6 TB/s
+LDS_PEAK_BPS = 128 * N_CU * CLOCK_HZ          # 78.6 TB/s (4-byte accesses)
+# ds_read_b128 measured 202 bytes per clock per CU on gfx950: the denominator
+# for wide reads (every fraction against it is about 0.63 of the other)
+LDS_B128_BPS = 202 * N_CU * CLOCK_HZ          # 124 TB/s
+# the largest single-GPU annealing workload: the C12 search
+HEADLINE = "conv_c12_sa"
 HBM_PEAK_BPS = 8.0e12
 
 
@@ -113,20 +126,29 @@ class SaWorkload:
         self.ens_tables = W.make_ensemble(wl["trees"], wl["depth"], F, wl["ens_seed"])
         self.ens = P.at_ensemble_create(*self.ens_tables, F)
         self.t_pack = time.perf_counter() - t0
-        t0 = time.perf_counter()
-        thr = P.at_sa_thresholds(self.seed, 0, self.n, 0, self.steps)
-        self.t_thr = time.perf_counter() - t0
-        self.thr = torch.from_numpy(thr).cuda()
+        self.t_thr = None
         self.best = torch.zeros((self.n, self.topk, 4), dtype=torch.int32, device="cuda")
         self.evals = self.n * self.steps
         self.tree_evals = self.evals * wl["trees"]
         self.lds_bytes = self.tree_evals * tree_eval_bytes(wl["depth"])
+        self.chains = P.at_chains_create(self.space, 0, self.n, self.topk, self.seed)
 
-    def make_chains(self, count):
-        return [self.P.at_chains_create(self.space, 0, self.n, self.topk, self.seed) for _ in range(count)]
+    def thresholds(self, runs):
+        """Device threshold tables of the next `runs` runs of the chains
+        (each run continues from where the previous one stopped)."""
+        import torch
+        base = self.P.at_chains_step(self.chains)
+        out = []
+        for r in range(runs):
+            t0 = time.perf_counter()
+            thr = self.P.at_sa_thresholds(self.seed, 0, self.n, base + r * self.steps, self.steps)
+            if self.t_thr is None:
+                self.t_thr = time.perf_counter() - t0
+            out.append(torch.from_numpy(thr).cuda())
+        return out
 
-    def run(self, chains):
-        self.P.at_sa_run(self.space, self.ens, chains, self.steps, self.thr, self.best)
+    def run(self, thr):
+        self.P.at_sa_run(self.space, self.ens, self.chains, self.steps, thr, self.best)
 
 
 def time_events(fn, reps):
@@ -145,29 +167,36 @@ def time_events(fn, reps):
 
 
 def bench_sa(P, name, steps, warmup):
+    """Annealing runs of a workload on one chains handle.  The warm-up runs
+    initialise the chains and take the handle's one-time workspace
+    allocation; every timed run then continues the same chains for the
+    workload's step count with thresholds precomputed for its steps, so the
+    timed region holds kernel launches only."""
     import torch
     w = SaWorkload(P, name)
-    chains = w.make_chains(steps + warmup)
+    warmup = max(1, warmup)
+    thr = w.thresholds(warmup)
     for i in range(warmup):
-        w.run(chains[i])
+        w.run(thr[i])
+    thr = w.thresholds(steps + 1)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev = time_events(lambda r: w.run(chains[warmup + r]), steps)
+    ev = time_events(lambda r: w.run(thr[r]), steps)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     t = float(np.mean(ev))
-    # one profiled run: average launch durations of the kernels.  The walk
-    # kernel is k_local on the chain-local path (one launch per run: the
-    # initial round and every step) and k_trees on the tree-partitioned path
-    # (one launch per scoring round).
-    ch = w.make_chains(1)[0]
-    P.at_sa_set_profiling(ch, True)
-    w.run(ch)
-    kt = P.at_sa_kernel_times(ch)
-    local = P.at_chains_last_path(ch) == P.AT_SA_PATH_LOCAL
-    plan = P.at_chains_last_plan(ch) if local else None
+    # one more run, profiled: average launch durations of the kernels.  The
+    # walk kernel is k_local on the chain-local path (one launch per run, a
+    # scoring round per step) and k_trees on the tree-partitioned path (one
+    # launch per scoring round).
+    P.at_sa_set_profiling(w.chains, True)
+    w.run(thr[steps])
+    kt = P.at_sa_kernel_times(w.chains)
+    P.at_sa_set_profiling(w.chains, False)
+    local = P.at_chains_last_path(w.chains) == P.AT_SA_PATH_LOCAL
+    plan = P.at_chains_last_plan(w.chains)
     tree_s = kt["tree_ms"] / kt["tree_launches"] * 1e-3
-    rounds_per_launch = (w.steps + 1) if local else 1
+    rounds_per_launch = w.steps if local else 1
     tree_bytes = w.n * w.wl["trees"] * rounds_per_launch * tree_eval_bytes(w.wl["depth"])
     return w, dict(
         path="chain-local" if local else "tree-partitioned", plan=plan,
@@ -175,12 +204,12 @@ def bench_sa(P, name, steps, warmup):
         workload=describe(name), ms_per_run=t * 1e3, ms_min=float(np.min(ev)) * 1e3, wall_s=wall,
         evals_per_s=w.evals / t, tree_evals_per_s=w.tree_evals / t,
         run_lds_bytes=w.lds_bytes, run_lds_TBps=w.lds_bytes / t / 1e12,
-        run_lds_frac=w.lds_bytes / t / LDS_PEAK_BPS,
+        run_lds_frac=w.lds_bytes / t / LDS_PEAK_BPS, run_lds_frac_b128=w.lds_bytes / t / LDS_B128_BPS,
         host_threshold_s=w.t_thr, host_ensemble_pack_s=w.t_pack,
         tree_kernel_us=tree_s * 1e6, tree_kernel_launches=kt["tree_launches"],
         chain_kernel_us=(kt["chain_ms"] / kt["chain_launches"] * 1e3) if kt["chain_launches"] else None,
         tree_lds_bytes_per_launch=tree_bytes, tree_lds_TBps=tree_bytes / tree_s / 1e12,
-        tree_lds_frac=tree_bytes / tree_s / LDS_PEAK_BPS)
+        tree_lds_frac=tree_bytes / tree_s / LDS_PEAK_BPS, tree_lds_frac_b128=tree_bytes / tree_s / LDS_B128_BPS)
 
 
 def bench_score(P, reps, warmup):
@@ -253,42 +282,84 @@ def bench_select(P, w, reps=20):
                 read_GBps=n_cand * 16 / t / 1e9)
 
 
-def cpu_baseline(name, budget_s):
-    """The oracle (single-threaded C++) on the first chains of the workload."""
+def oracle_sa_sample(name, chain0, n_chains):
+    """The oracle on chains [chain0, chain0 + n_chains) of a single-space
+    annealing workload, all of its steps; returns (evals, seconds)."""
     import oracle
     wl = W.WORKLOADS[name]
-    spaces = [oracle.Space(t, s) for t, s in wl["spaces"]]
-    F = spaces[0].n_features
-    ens = W.make_ensemble(wl["trees"], wl["depth"], F, wl["ens_seed"])
+    spaces = [oracle.Space(t, s) for t, s in wl["spaces"][:1]]
+    ens = W.make_ensemble(wl["trees"], wl["depth"], spaces[0].n_features, wl["ens_seed"])
     steps, seed, k = wl["steps"], wl["sa_seed"], wl["topk"]
-    chains, done, elapsed = 0, 0, 0.0
-    block = 8
-    while elapsed < budget_s and chains + block <= wl["chains_per_space"]:
-        ch = oracle.Chains(spaces[:1], [0, block], seed=seed, chain0=chains, topk=k)
-        thr = oracle.thresholds(seed, chains, block, 0, steps)
-        t0 = time.perf_counter()
-        ch.run(ens, steps, thr)
-        elapsed += time.perf_counter() - t0
-        chains += block
-        done += block * steps
-    return dict(value=done / elapsed, unit="evals/s", cores=1, kind="oracle",
-                sample=f"first {chains} chains x {steps} steps of {name} ({done} evals, {elapsed:.1f} s)")
+    ch = oracle.Chains(spaces, [0, n_chains], seed=seed, chain0=chain0, topk=k)
+    thr = oracle.thresholds(seed, chain0, n_chains, 0, steps)
+    t0 = time.perf_counter()
+    ch.run(ens, steps, thr)
+    return n_chains * steps, time.perf_counter() - t0
+
+
+def host_cores() -> int:
+    """Host cores this process may use, capped at the one-GPU share of 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(name, chains):
+    """The single-threaded oracle on a bounded sample of the workload: the
+    first `chains` chains, all steps, on one core; then P = host_cores()
+    single-threaded oracle processes at once, shard p taking chains
+    [p * chains, (p + 1) * chains), for the all-cores rate (total evals over
+    the slowest shard's time).  Runs before the GPU is touched."""
+    import subprocess
+    evals, t1 = oracle_sa_sample(name, 0, chains)
+    P = host_cores()
+    procs = [subprocess.Popen([sys.executable, os.path.abspath(__file__), "--oracle-shard", name, str(p * chains),
+                               str(chains)], stdout=subprocess.PIPE, text=True) for p in range(P)]
+    outs = [json.loads(p.communicate()[0].strip().splitlines()[-1]) for p in procs]
+    if any(p.returncode != 0 for p in procs):
+        raise RuntimeError("an oracle shard failed")
+    total = sum(o["evals"] for o in outs)
+    slowest = max(o["s"] for o in outs)
+    steps = W.WORKLOADS[name]["steps"]
+    return dict(value=total / slowest, unit="evals/s", cores=P, kind="oracle",
+                sample=(f"{P} single-threaded oracle processes at once, each {chains} chains x {steps} steps of "
+                        f"{name} (chains 0..{P * chains - 1}, {total} evals, slowest {slowest:.1f} s)"),
+                one_core=dict(value=evals / t1, unit="evals/s", cores=1,
+                              sample=f"first {chains} chains x {steps} steps of {name} ({evals} evals, {t1:.1f} s)"))
+
+
+def oracle_shard_main(argv):
+    """Child process of the all-cores CPU baseline: one oracle shard."""
+    name, chain0, n = argv[0], int(argv[1]), int(argv[2])
+    evals, secs = oracle_sa_sample(name, chain0, n)
+    print(json.dumps({"evals": evals, "s": secs}), flush=True)
 
 
 def main():
+    if len(sys.argv) > 1 and sys.argv[1] == "--oracle-shard":
+        oracle_shard_main(sys.argv[2:])
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="conv_c2_sa")
+    ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--no-extra", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--cpu-chains", type=int, default=64,
+                    help="chains per oracle sample (the C12 workload: 64 chains x 1000 steps, about 9 s a core)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
               "(chains are keyed by global chain id, so N GPUs would each run a contiguous block of chains "
               "and give the same results as one GPU)", file=sys.stderr)
         sys.exit(2)
+    # the oracle baseline runs first, in this process and in child processes,
+    # before anything touches the GPU
+    cpu = None if args.no_cpu else cpu_baseline(args.workload, args.cpu_chains)
+
     import torch
     import paper_1805_08166_amd as P
     torch.cuda.set_device(0)
@@ -299,14 +370,14 @@ def main():
     if not args.no_extra:
         extra["select_" + args.workload] = bench_select(P, head)
         extra["conv_c2_score1m"] = bench_score(P, reps=5, warmup=1)
-        for name in ["gemm512_sa", "conv_c12_sa", "resnet18_12conv_sa"]:
+        for name in ["conv_c2_sa", "gemm512_sa", "conv_c12_sa", "resnet18_12conv_sa"]:
             if name == args.workload:
                 continue
             reps = 2 if name == "conv_c12_sa" else 3
             w, extra[name] = bench_sa(P, name, reps, 1)
-            if name == "conv_c12_sa":
-                extra["select_conv_c12_sa"] = bench_select(P, w)
-    cpu = cpu_baseline(args.workload, args.cpu_budget)
+            if name in ("conv_c2_sa", "conv_c12_sa"):
+                extra["select_" + name] = bench_select(P, w)
+    depth = head.wl["depth"]
     line = {
         "metric": METRIC,
         "value": r["evals_per_s"],
@@ -321,7 +392,7 @@ def main():
         "dtype": "int32+f32",
         "data": "synthetic (seeded ensemble and configurations; Table 1 shapes)",
         "config": {"workload": r["workload"], "evals_per_step": head.evals,
-                   "tree_evals_per_step": head.tree_evals},
+                   "tree_evals_per_step": head.tree_evals, "path": r["path"], "plan": r["plan"]},
         "roofline": {"bound": "lds",
                      "kernel": (f"{r['walk_kernel']} ({r['path']} path: "
                                 + ("one launch runs every step" if r["path"] == "chain-local"
@@ -329,9 +400,15 @@ def main():
                      "achieved": r["tree_lds_TBps"] * 1e3, "peak": LDS_PEAK_BPS / 1e9, "unit": "GB/s",
                      "frac": r["tree_lds_frac"], "traffic": committed_traffic(r["walk_kernel"], args.workload),
                      "launch_us": r["tree_kernel_us"],
-                     "per_unit": f"{tree_eval_bytes(head.wl['depth'])} B LDS per tree evaluation, "
+                     "per_unit": f"{tree_eval_bytes(depth)} B LDS per tree evaluation, "
                                  f"{head.n} chains x {head.wl['trees']} trees x "
-                                 f"{(head.steps + 1) if r['path'] == 'chain-local' else 1} rounds per launch"},
+                                 f"{head.steps if r['path'] == 'chain-local' else 1} rounds per launch",
+                     "peak_b128": LDS_B128_BPS / 1e9, "frac_b128": r["tree_lds_frac_b128"],
+                     "whole_run": {"achieved": r["run_lds_TBps"] * 1e3, "frac": r["run_lds_frac"],
+                                   "frac_b128": r["run_lds_frac_b128"],
+                                   "per_unit": f"{tree_eval_bytes(depth)} B LDS per tree evaluation, "
+                                               f"{head.n} chains x {head.steps} steps x {head.wl['trees']} trees "
+                                               "per run"}},
         "cpu_baseline": cpu,
         "extra": extra,
     }

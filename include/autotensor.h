@@ -83,8 +83,12 @@ typedef struct {
  * more configurations.  Synchronous. */
 at_status at_space_create(int tmpl, const int64_t* shape, int nshape, at_space_t* out);
 
-/* Space metadata.  knob_sizes: host [at least n_knobs], may be NULL; any
- * other output pointer may be NULL. */
+/* Metadata of the schedule space S_e (Section 2): the knobs of the
+ * configuration s = [s_1 .. s_m] and their value counts, the loop count of
+ * the lowered nest and the length of its loop-context feature rows
+ * (Appendix A.2), and |S_e|.  knob_sizes: host [at least n_knobs], may be
+ * NULL; any other output pointer may be NULL.  AT_E_INVALID for a NULL
+ * space.  Host only; nothing is enqueued. */
 at_status at_space_info(at_space_t space, int* n_knobs, int32_t* knob_sizes, int* n_loops,
                         int* n_features, uint64_t* n_configs);
 
@@ -219,14 +223,18 @@ void at_chains_destroy(at_chains_t chains);
 /* Absolute step counter of the chains (the step_base of the next run). */
 at_status at_chains_step(at_chains_t chains, uint64_t* step_abs);
 
-/* Metropolis thresholds for the next `steps` steps of chains
+/* Acceptance thresholds of simulated annealing with the model score as
+ * energy (Section 3.3; the acceptance rule of Algorithm 1's search):
+ * Metropolis thresholds for the next `steps` steps of chains
  * chain0 .. chain0+n_chains-1 starting at absolute step step_base:
  * thr[c][s] = fp32(T_s * ln(u)) computed in double, with
  * T_s = 1 - s/(steps-1) (T = 0 when steps == 1) and u = (r2 + 0.5) / 2^32,
  * r2 the third word of the Philox-4x32-10 block keyed by seed at counter
  * (chain, step_base + s, 0, 0).  A move of score change d (fp32) is then
  * accepted iff d >= thr, i.e. with probability min(1, exp(d / T_s)).
- * thr: host [n_chains][steps] float.  Runs on the host. */
+ * thr: host [n_chains][steps] float, caller-owned.  AT_E_INVALID for
+ * steps < 1, a negative chain0 or n_chains, or a NULL thr with chains to
+ * fill.  Runs on the host; nothing is enqueued. */
 at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint64_t step_base,
                            int steps, float* thr);
 
@@ -322,14 +330,21 @@ at_status at_chains_set_path(at_chains_t chains, int path);
 /* The path the last run on `chains` took (AT_SA_PATH_AUTO before any run). */
 at_status at_chains_last_path(at_chains_t chains, int* path);
 
-/* Launch plan of the last chain-local run (measurement aid; zeros when the
- * last run took the other path): info[0] chains per workgroup, [1] threads
- * per workgroup, [2] workgroups, [3] trees per chunk, [4] chunks streamed
- * per step (0: nothing is streamed), [5] how leaves are reached: 0 from LDS
- * (whole trees resident or streamed), 1 streamed node blocks with leaves
- * read from global memory, 2 tree tops resident in LDS with the last level
- * and its leaves read from global memory, [6] dynamic LDS bytes, [7] bytes
- * one workgroup reads per step from outside its LDS. */
+/* Launch plan of the last run (measurement aid; read at_chains_last_path
+ * to know which layout applies; zeros before any run).
+ * Chain-local run: info[0] chains per workgroup, [1] threads per workgroup,
+ * [2] workgroups, [3] trees per chunk, [4] chunks streamed per step (0:
+ * nothing is streamed), [5] how leaves are reached: 0 from LDS (whole trees
+ * resident or streamed), 1 streamed node blocks with leaves read from
+ * global memory, 2 tree tops resident in LDS with the last level and its
+ * leaves read from global memory, [6] dynamic LDS bytes, [7] bytes one
+ * workgroup reads per step from outside its LDS.
+ * Tree-partitioned run: info[0] trees per tree-kernel workgroup, [1] waves
+ * per tree-kernel workgroup, [2] tree-kernel workgroups, [3] chain slices
+ * per tree group, [4] 64-chain blocks per slice (a wave walks more than one
+ * block when this exceeds [1]), [5] chain-kernel workgroups, [6] LDS bytes
+ * of a tree-kernel workgroup, [7] bytes of leaf values written and read
+ * back per step. */
 at_status at_chains_last_plan(at_chains_t chains, int64_t info[8]);
 
 /* Copies the chains' current configuration indices (device [n_chains]

@@ -50,8 +50,12 @@ class ATError(RuntimeError):
 
 
 def _load():
+    from . import build as _build
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    if _build.stale():
+        raise ImportError(f"{LIB_PATH} was built from other sources than those under csrc/; "
+                          "run __graft_entry__.build() again")
     L = ctypes.CDLL(LIB_PATH)
     vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64
     sig = {
@@ -349,28 +353,41 @@ def at_chains_last_path(chains: Chains) -> int:
     return v.value
 
 
+PLAN_KEYS_LOCAL = ["chains_per_wg", "threads", "workgroups", "trees_per_chunk", "chunks", "gather", "lds_bytes",
+                   "stream_bytes_per_step"]
+PLAN_KEYS_TREES = ["trees_per_wg", "waves", "workgroups", "slices", "slice_blocks", "chain_workgroups",
+                   "lds_bytes", "v_bytes_per_step"]
+
+
 def at_chains_last_plan(chains: Chains) -> dict:
-    """Launch plan of the last chain-local run (zeros after a tree-partitioned one)."""
+    """Launch plan of the last run, keyed by the layout of the path it took
+    (PLAN_KEYS_LOCAL or PLAN_KEYS_TREES), plus "path"."""
     v = np.zeros(8, np.int64)
     _check("at_chains_last_plan", _lib.at_chains_last_plan(chains.h, _np(v)))
-    keys = ["chains_per_wg", "threads", "workgroups", "trees_per_chunk", "chunks", "gather", "lds_bytes",
-            "stream_bytes_per_step"]
-    return dict(zip(keys, (int(x) for x in v)))
+    path = at_chains_last_path(chains)
+    keys = PLAN_KEYS_TREES if path == AT_SA_PATH_TREES else PLAN_KEYS_LOCAL
+    plan = dict(zip(keys, (int(x) for x in v)))
+    plan["path"] = path
+    return plan
 
 
-def at_select_batch(space: Space, cand, pool: int, n_greedy: int, alpha: float, n_random: int, seed: int, out,
-                    stream=None):
-    """cand: device int32 [..., 4] (at_entry, any leading shape); out: device
-    int32 [n_greedy + n_random, 4] (at_entry)."""
+def _select(name, space: Space, cand, pool, n_greedy, alpha, n_random, seed, out, stream):
     import torch
     n_cand = cand.numel() // 4 if cand is not None else 0
     if cand is not None and (cand.dtype != torch.int32 or cand.shape[-1] != 4 or not cand.is_contiguous()):
         raise ValueError("cand must be a contiguous int32 [..., 4] at_entry tensor")
     if out.shape != (n_greedy + n_random, 4):
         raise ValueError("out must be [n_greedy + n_random, 4] int32")
-    _check("at_select_batch", _lib.at_select_batch(
+    _check(name, getattr(_lib, name)(
         space.h, _dev(cand, torch.int32, "cand") if n_cand else None, int(n_cand), int(pool), int(n_greedy),
         float(alpha), int(n_random), int(seed), _dev(out, torch.int32, "out"), _stream(stream)))
+
+
+def at_select_batch(space: Space, cand, pool: int, n_greedy: int, alpha: float, n_random: int, seed: int, out,
+                    stream=None):
+    """cand: device int32 [..., 4] (at_entry, any leading shape); out: device
+    int32 [n_greedy + n_random, 4] (at_entry)."""
+    _select("at_select_batch", space, cand, pool, n_greedy, alpha, n_random, seed, out, stream)
 
 
 def at_sa_thresholds(seed: int, chain0: int, n_chains: int, step_base: int, steps: int) -> np.ndarray:

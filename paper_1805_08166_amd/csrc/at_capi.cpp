@@ -728,7 +728,11 @@ static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t ch
     chains->last_path = path;
     const int64_t plan[8] = {pl.cpb, pl.threads, pl.grid, pl.ct, (pl.resident || pl.tail) ? 0 : pl.n_chunks,
                              pl.tail ? 2 : pl.gather, (int64_t)pl.lds_bytes, (int64_t)pl.round_bytes};
-    for (int i = 0; i < 8; ++i) chains->last_plan[i] = path == AT_SA_PATH_LOCAL ? plan[i] : 0;
+    // the tree-partitioned launcher records its own plan
+    if (path == AT_SA_PATH_LOCAL)
+        for (int i = 0; i < 8; ++i) chains->last_plan[i] = plan[i];
+    else if (chains->n_chains == 0)
+        for (int i = 0; i < 8; ++i) chains->last_plan[i] = 0;
     chains->initialised = true;
     chains->step_abs += (uint64_t)steps;
     return AT_OK;

@@ -1068,6 +1068,12 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
     const size_t chain_lds = RING_BYTES + (size_t)CPW * ch.topk * sizeof(at_entry);
+    {
+        const int64_t tree_grid = (int64_t)(e.n_trees + ta.tpw - 1) / ta.tpw * ta.slices;
+        const int64_t plan[8] = {ta.tpw, nw, tree_grid, ta.slices, ta.slice_blocks, (int64_t)chain_grid,
+                                 (int64_t)MAX_LDS_BYTES, (int64_t)groups * ((n + 15) / 16 * 16) * 16};
+        for (int i = 0; i < 8; ++i) ch.last_plan[i] = plan[i];
+    }
     static bool chain_configured = false;
     if (!chain_configured) {
         for (const void* f : {reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM>),

@@ -193,3 +193,41 @@ def test_best_by_score_matches_exhaustive_search():
     pooled = sorted(pool.items(), key=lambda kv: (-float(kv[1]), kv[0]))[:k]
     assert [c for c, _ in pooled] == order[:k]
     assert all(np.float32(sc[c]) == s for c, s in pooled)
+
+
+def test_initial_configurations_uniform_and_distinct_across_chains():
+    # chain initialisation draws each knob uniformly over its values from the
+    # chain's own random stream: per-knob chi-square over 8192 chains, a
+    # contingency chi-square between the two largest knobs, and distinct
+    # starting configurations (a draw that ignored the chain id would give
+    # every chain the same start)
+    sp = oracle.Space(*workloads.WORKLOADS["conv_c2_sa"]["spaces"][0])
+    ens = workloads.make_ensemble(1, 1, sp.n_features, 5)
+    n = 8192
+    ch = oracle.Chains([sp], [0, n], seed=2001, chain0=0, topk=1)
+    ch.run(ens, 0, np.zeros((n, 0), np.float32))
+    kv = ch.knobs[:, : sp.n_knobs]
+    for j, size in enumerate(sp.knob_sizes):
+        size = int(size)
+        assert kv[:, j].min() >= 0 and kv[:, j].max() < size
+        if size == 1:
+            continue
+        counts = np.bincount(kv[:, j], minlength=size)
+        exp = n / size
+        chi2 = ((counts - exp) ** 2 / exp).sum()
+        dof = size - 1
+        assert chi2 < dof + 6 * np.sqrt(2 * dof), (j, chi2, dof)
+    # knobs 0 and 1 (84 and 80 values) binned into quarters: independent
+    a, b = kv[:, 0] * 4 // int(sp.knob_sizes[0]), kv[:, 1] * 4 // int(sp.knob_sizes[1])
+    table = np.zeros((4, 4))
+    np.add.at(table, (a, b), 1)
+    expt = table.sum(1, keepdims=True) * table.sum(0, keepdims=True) / n
+    chi2 = ((table - expt) ** 2 / expt).sum()
+    assert chi2 < 9 + 6 * np.sqrt(18)
+    # 8192 draws from 90 M configurations: almost surely all distinct
+    cfgs = ch.cur_cfgs()
+    assert len(np.unique(cfgs)) >= n - 2
+    # a chain's start depends on its global id only: chains 100.. started alone agree
+    part = oracle.Chains([sp], [0, 16], seed=2001, chain0=100, topk=1)
+    part.run(ens, 0, np.zeros((16, 0), np.float32))
+    assert np.array_equal(part.knobs, ch.knobs[100:116])
