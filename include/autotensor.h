@@ -314,6 +314,23 @@ at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, i
 at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
                           float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream);
 
+/* at_select_batch for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same kernels and the same result, bit for bit, with the
+ * partial reduction of more than 4096 candidates kept in a fixed scratch
+ * array that the library holds on each device until the process ends (two
+ * buffers of 131072 entries, 4 MiB; looked up with hipGetSymbolAddress on
+ * the first call on a device).  The call allocates and frees nothing.
+ * Limit: ceil(n_cand / 4096) * max(pool, 1) <= 131072 (for example up to
+ * 524288 candidates at pool 1024, 4194304 at pool 128), AT_E_UNSUPPORTED
+ * beyond it; the other arguments and errors are those of at_select_batch.
+ * Every call on a device shares that device's scratch: calls that overlap
+ * on one device (other streams, other threads) race and must be ordered by
+ * the caller.  Nothing in the scratch needs to start at zero: each call
+ * writes every entry it reads. */
+at_status at_select_batch_noalloc(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
+                                  float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream);
+
 /* Execution path of the annealing runs of a chains handle. */
 typedef enum {
     AT_SA_PATH_AUTO = 0,   /* chosen per run from the ensemble and chain count */

@@ -34,7 +34,7 @@ EXPORTED = [
     "at_trees_depth", "at_trees_pad", "at_ensemble_import",
     "at_gbt_predict", "at_gbt_predict_global_local", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
-    "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_last_error",
+    "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_select_batch_noalloc", "at_last_error",
 ]
 
 # at_sa_path
@@ -87,6 +87,7 @@ def _load():
         "at_chains_last_path": [vp, vp],
         "at_chains_last_plan": [vp, vp],
         "at_select_batch": [vp, vp, i64, i32, i32, ctypes.c_float, i32, u64, vp, vp],
+        "at_select_batch_noalloc": [vp, vp, i64, i32, i32, ctypes.c_float, i32, u64, vp, vp],
         "at_last_error": [],
     }
     for name, args in sig.items():
@@ -388,6 +389,13 @@ def at_select_batch(space: Space, cand, pool: int, n_greedy: int, alpha: float, 
     """cand: device int32 [..., 4] (at_entry, any leading shape); out: device
     int32 [n_greedy + n_random, 4] (at_entry)."""
     _select("at_select_batch", space, cand, pool, n_greedy, alpha, n_random, seed, out, stream)
+
+
+def at_select_batch_noalloc(space: Space, cand, pool: int, n_greedy: int, alpha: float, n_random: int, seed: int,
+                            out, stream=None):
+    """at_select_batch without device allocation (the library's fixed
+    per-device scratch; calls that overlap on one device race)."""
+    _select("at_select_batch_noalloc", space, cand, pool, n_greedy, alpha, n_random, seed, out, stream)
 
 
 def at_sa_thresholds(seed: int, chain0: int, n_chains: int, step_base: int, steps: int) -> np.ndarray:

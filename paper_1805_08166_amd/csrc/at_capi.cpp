@@ -634,24 +634,60 @@ at_status at_sa_kernel_times(at_chains_t chains, double* tree_ms, int64_t* tree_
     return AT_OK;
 }
 
-at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
-                          float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream) {
-    if (!space) return fail(AT_E_INVALID, "at_select_batch: NULL space");
-    if (space->n_spaces != 1) return fail(AT_E_INVALID, "at_select_batch: takes a single space, not a set");
-    if (n_cand < 0 || pool < 0 || n_greedy < 0 || n_random < 0) return fail(AT_E_INVALID, "at_select_batch: negative size");
-    if (n_cand > 0 && !cand) return fail(AT_E_INVALID, "at_select_batch: NULL candidates");
-    if (pool > select_pool_max()) return fail(AT_E_UNSUPPORTED, "at_select_batch: pool above 1024");
-    if ((int64_t)n_greedy + n_random > select_pick_max()) return fail(AT_E_UNSUPPORTED, "at_select_batch: more than 2048 picks");
-    if (!std::isfinite(alpha)) return fail(AT_E_INVALID, "at_select_batch: alpha must be finite");
+// Argument checks shared by the two selection entry points; AT_OK with
+// *nothing set when there is nothing to pick.
+static at_status select_args(const char* fn, at_space_t space, const at_entry* cand, int64_t n_cand, int pool,
+                             int n_greedy, float alpha, int n_random, at_entry* out, bool* nothing) {
+    const std::string f(fn);
+    *nothing = false;
+    if (!space) return fail(AT_E_INVALID, f + ": NULL space");
+    if (space->n_spaces != 1) return fail(AT_E_INVALID, f + ": takes a single space, not a set");
+    if (n_cand < 0 || pool < 0 || n_greedy < 0 || n_random < 0) return fail(AT_E_INVALID, f + ": negative size");
+    if (n_cand > 0 && !cand) return fail(AT_E_INVALID, f + ": NULL candidates");
+    if (pool > select_pool_max()) return fail(AT_E_UNSUPPORTED, f + ": pool above 1024");
+    if ((int64_t)n_greedy + n_random > select_pick_max()) return fail(AT_E_UNSUPPORTED, f + ": more than 2048 picks");
+    if (!std::isfinite(alpha)) return fail(AT_E_INVALID, f + ": alpha must be finite");
     const SpaceDesc& d = space->descs[0];
     for (int j = 0; j < d.n_knobs; ++j)
-        if (d.knob_size[j] > 65536u) return fail(AT_E_UNSUPPORTED, "at_select_batch: a knob has more than 65536 values");
-    if (n_greedy + n_random == 0) return AT_OK;
-    if (!out) return fail(AT_E_INVALID, "at_select_batch: NULL output");
-    if (n_cand > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, "at_select_batch: too many candidates");
+        if (d.knob_size[j] > 65536u) return fail(AT_E_UNSUPPORTED, f + ": a knob has more than 65536 values");
+    if (n_greedy + n_random == 0) {
+        *nothing = true;
+        return AT_OK;
+    }
+    if (!out) return fail(AT_E_INVALID, f + ": NULL output");
+    if (n_cand > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, f + ": too many candidates");
+    return AT_OK;
+}
+
+at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
+                          float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream) {
+    bool nothing = false;
+    const at_status st = select_args("at_select_batch", space, cand, n_cand, pool, n_greedy, alpha, n_random, out,
+                                     &nothing);
+    if (st != AT_OK || nothing) return st;
     DeviceGuard g(space->device);
     return finish_launch(launch_select(*space, cand, n_cand, pool, n_greedy, alpha, n_random, seed, out,
-                                       (hipStream_t)stream), "at_select_batch");
+                                       (hipStream_t)stream, nullptr),
+                         "at_select_batch");
+}
+
+at_status at_select_batch_noalloc(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
+                                  float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream) {
+    bool nothing = false;
+    const at_status st = select_args("at_select_batch_noalloc", space, cand, n_cand, pool, n_greedy, alpha,
+                                     n_random, out, &nothing);
+    if (st != AT_OK || nothing) return st;
+    if (select_scratch_entries(n_cand, pool) > select_scratch_max_entries())
+        return fail(AT_E_UNSUPPORTED, "at_select_batch_noalloc: ceil(n_cand / 4096) * max(pool, 1) exceeds the "
+                                      "scratch limit of " + std::to_string(select_scratch_max_entries()) +
+                                      " entries");
+    DeviceGuard g(space->device);
+    at_entry* scratch = nullptr;
+    const hipError_t e = select_scratch_ptr(space->device, &scratch);
+    if (e != hipSuccess) return hip_fail(e, "at_select_batch_noalloc: hipGetSymbolAddress");
+    return finish_launch(launch_select(*space, cand, n_cand, pool, n_greedy, alpha, n_random, seed, out,
+                                       (hipStream_t)stream, scratch),
+                         "at_select_batch_noalloc");
 }
 
 at_status at_chains_set_path(at_chains_t chains, int path) {

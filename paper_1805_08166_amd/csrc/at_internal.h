@@ -267,8 +267,17 @@ hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t&
 // Batch selection (at_select.hip).
 int select_pool_max();
 int select_pick_max();
+// scratch: two buffers of select_scratch_max_entries() entries each (the
+// device's static scratch), or null for stream-ordered allocations.
 hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
-                         float alpha, int n_random, uint64_t seed, at_entry* out, hipStream_t stream);
+                         float alpha, int n_random, uint64_t seed, at_entry* out, hipStream_t stream,
+                         at_entry* scratch);
+// Entries of each partial-result buffer the reduction needs (0: none).
+int64_t select_scratch_entries(int64_t n_cand, int pool);
+int64_t select_scratch_max_entries();
+// Address of the static selection scratch on `device` (which must be
+// current), looked up once per device.
+hipError_t select_scratch_ptr(int device, at_entry** out);
 
 hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score,
                          hipStream_t stream);

@@ -19,6 +19,8 @@
 // one thread per pool candidate runs the greedy rounds (block-wide arg-max
 // of the gains, then every candidate clears the knobs the winner covers),
 // and thread 0 draws the random configurations.
+#include <mutex>
+
 #include "at_chain.h"
 
 namespace at {
@@ -299,8 +301,45 @@ size_t select_lds_bytes() {
 int select_pool_max() { return POOL_MAX; }
 int select_pick_max() { return PICK_MAX; }
 
+// Entries of each of the two partial-result buffers the reduction of n_cand
+// candidates needs (0 when n_cand fits the final workgroup).
+int64_t select_scratch_entries(int64_t n_cand, int pool) {
+    if (n_cand <= MERGE_MAX) return 0;
+    const int keep = pool > 0 ? pool : 1;
+    return (n_cand + SORT_N - 1) / SORT_N * keep;
+}
+
+// Scratch of the entry point that allocates nothing: the two partial-result
+// buffers, each SELECT_SCRATCH_ENTRIES entries (2 MiB), in one array per
+// device that lives as long as the process.  Host code never passes the
+// array's name to a kernel: the address comes from hipGetSymbolAddress,
+// once per device.
+constexpr int64_t SELECT_SCRATCH_ENTRIES = 131072;
+static __device__ __align__(256) at_entry select_scratch[2 * SELECT_SCRATCH_ENTRIES];
+
+int64_t select_scratch_max_entries() { return SELECT_SCRATCH_ENTRIES; }
+
+hipError_t select_scratch_ptr(int device, at_entry** out) {
+    constexpr int MAX_DEVICES = 64;
+    static std::mutex mu;
+    static at_entry* ptr[MAX_DEVICES] = {};
+    if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[device]) {
+        void* p = nullptr;
+        // the caller has made `device` current
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(select_scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        ptr[device] = static_cast<at_entry*>(p);
+    }
+    *out = ptr[device];
+    return hipSuccess;
+}
+
 hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
-                         float alpha, int n_random, uint64_t seed, at_entry* out, hipStream_t stream) {
+                         float alpha, int n_random, uint64_t seed, at_entry* out, hipStream_t stream,
+                         at_entry* scratch) {
     static bool configured = false;
     hipError_t e = hipSuccess;
     if (!configured) {
@@ -315,8 +354,14 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     const at_entry* src = cand;
     int64_t n = n_cand;
     void* bufs[2] = {nullptr, nullptr};
-    if (n > MERGE_MAX) {
-        const size_t bytes = (size_t)((n + SORT_N - 1) / SORT_N) * keep * sizeof(at_entry);
+    const int64_t need = select_scratch_entries(n_cand, pool);
+    const bool own = need > 0 && !scratch;   // stream-ordered buffers of our own
+    if (need > 0 && scratch) {
+        if (need > SELECT_SCRATCH_ENTRIES) return hipErrorInvalidValue;
+        bufs[0] = scratch;
+        bufs[1] = scratch + SELECT_SCRATCH_ENTRIES;
+    } else if (own) {
+        const size_t bytes = (size_t)need * sizeof(at_entry);
         for (void*& b : bufs) {
             e = hipMallocAsync(&b, bytes, stream);
             if (e != hipSuccess) {
@@ -337,8 +382,9 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
         cur ^= 1;
     }
     if (e != hipSuccess) {
-        for (void* x : bufs)
-            if (x) (void)hipFreeAsync(x, stream);
+        if (own)
+            for (void* x : bufs)
+                if (x) (void)hipFreeAsync(x, stream);
         return e;
     }
     SelectArgs a{};
@@ -353,8 +399,9 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     a.out = out;
     hipLaunchKernelGGL(k_select, dim3(1), dim3(SEL_WG), select_lds_bytes(), stream, a);
     e = hipGetLastError();
-    for (void* b : bufs)
-        if (b) (void)hipFreeAsync(b, stream);
+    if (own)
+        for (void* b : bufs)
+            if (b) (void)hipFreeAsync(b, stream);
     return e;
 }
 
