@@ -61,6 +61,8 @@ def lib():
         L.or_select_batch.argtypes = [vp, vp, i64, i32, i32, ctypes.c_float, i32, u64, vp]
         L.or_sa_run.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp, vp, u64, i64, i64, i32,
                                 i32, vp, i32, vp, vp, vp, vp, vp, vp]
+        L.or_sa_run_global_local.argtypes = [vp, i32, vp, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, vp,
+                                             u64, i64, i64, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -235,22 +237,36 @@ class Chains:
                 out[c] = sp.encode(self.knobs[c, : sp.n_knobs])
         return out
 
-    def run(self, ensemble, steps: int, thr, trace=False):
+    @staticmethod
+    def _model(ensemble):
         fid, thr_nodes, leaf = (np.ascontiguousarray(a) for a in ensemble)
         fid = fid.astype(np.uint8, copy=False)
         thr_nodes = thr_nodes.astype(np.uint8, copy=False)
         leaf = leaf.astype(np.float32, copy=False)
         T, n_int = fid.shape
         depth = int(n_int + 1).bit_length() - 1
+        return fid, thr_nodes, leaf, T, depth
+
+    def run(self, ensemble, steps: int, thr, trace=False, global_model=None):
+        """`steps` annealing steps of every chain.  With global_model (a
+        (fid, thr, leaf) ensemble over the 192 context relation features) the
+        energy is Eq. 4's global + local model, `ensemble` being the local
+        one over the loop-context features."""
+        fid, thr_nodes, leaf, T, depth = self._model(ensemble)
         F = self.spaces[0].n_features
         thr = np.ascontiguousarray(thr, dtype=np.float32).reshape(self.n, steps)
         handles = (ctypes.c_void_p * len(self.spaces))(*[s._h.value for s in self.spaces])
         tr = np.zeros((self.n, steps), dtype=TOP_DTYPE) if trace else None
-        st = lib().or_sa_run(handles, len(self.spaces), _p(self.offsets), T, depth, F,
-                             _p(fid), _p(thr_nodes), _p(leaf), self.seed, self.chain0, self.n,
-                             self.topk, steps, _p(thr), self.MAX_KNOBS, _p(self.knobs),
-                             _p(self.score), _p(self.initialised), _p(self.step_abs),
-                             _p(self.top), _p(tr) if trace else None)
+        tail = (self.seed, self.chain0, self.n, self.topk, steps, _p(thr), self.MAX_KNOBS, _p(self.knobs),
+                _p(self.score), _p(self.initialised), _p(self.step_abs), _p(self.top), _p(tr) if trace else None)
+        if global_model is None:
+            st = lib().or_sa_run(handles, len(self.spaces), _p(self.offsets), T, depth, F,
+                                 _p(fid), _p(thr_nodes), _p(leaf), *tail)
+        else:
+            gfid, gthr, gleaf, gT, gdepth = self._model(global_model)
+            st = lib().or_sa_run_global_local(handles, len(self.spaces), _p(self.offsets), gT, gdepth,
+                                              Space.RELATION_THRESHOLDS * 6, _p(gfid), _p(gthr), _p(gleaf),
+                                              T, depth, F, _p(fid), _p(thr_nodes), _p(leaf), *tail)
         _check(st, "sa_run")
         return tr
 

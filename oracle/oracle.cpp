@@ -529,6 +529,20 @@ float score_config(const Space& sp, const Ensemble& e, uint64_t cfg) {
     return predict_row(e, row.data(), nullptr);
 }
 
+// Eq. 4 (Section 4): f_hat = f_hat_global + f_hat_local.  The global model
+// reads the invariant representation (the context relation features), the
+// in-domain local model the loop-context features; each prediction is its
+// own fp32 fold in tree order, and the two are added once, global first.
+float score_config_global_local(const Space& sp, const Ensemble& global, const Ensemble& local, uint64_t cfg) {
+    std::vector<int32_t> rel(n_relation_features_of(sp));
+    relation_features_of(sp, cfg, rel.data());
+    const float g = predict_row(global, rel.data(), nullptr);
+    std::vector<int32_t> row(n_features_of(sp));
+    features_of(sp, cfg, row.data());
+    const float l = predict_row(local, row.data(), nullptr);
+    return g + l;
+}
+
 // ---------------------------------------------------------------------------
 // Picking the batch to measure (Algorithm 1 after the annealing; Section 3.3,
 // Eq. 3).  Q is the set of distinct configurations the chains keep.  From
@@ -778,20 +792,28 @@ int or_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint64_t step
 // chain0 + c.  Per-chain state (in/out): cur knob values [n][max_knobs],
 // cur score, initialised flag, step_abs, top-k [n][k].  thr is [n][steps].
 // trace (optional) receives [n][steps] entries (cfg, score, accepted).
-int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
-              int n_trees, int depth, int n_features, const uint8_t* fid, const uint8_t* thr_nodes,
-              const float* leaf, uint64_t seed, int64_t chain0, int64_t n_chains, int topk,
-              int steps, const float* thr, int max_knobs,
-              int64_t* cur_knobs, float* cur_score, uint8_t* initialised, uint64_t* step_abs,
-              TopEntry* tops, TopEntry* trace) {
+}  // extern "C"
+
+namespace {
+
+// The annealing loop of or_sa_run; `global` set: the energy is Eq. 4's
+// global + local model (score_config_global_local), else the ensemble e
+// alone.
+int sa_run(void** spaces, int n_spaces, const int64_t* offsets, const Ensemble& e, const Ensemble* global,
+           uint64_t seed, int64_t chain0, int64_t n_chains, int topk, int steps, const float* thr, int max_knobs,
+           int64_t* cur_knobs, float* cur_score, uint8_t* initialised, uint64_t* step_abs, TopEntry* tops,
+           TopEntry* trace) {
     if (n_spaces < 1 || topk < 1 || steps < 0) return -1;
     if (offsets[0] != 0 || offsets[n_spaces] != n_chains) return -1;
-    Ensemble e{n_trees, depth, n_features, fid, thr_nodes, leaf};
     for (int64_t c = 0; c < n_chains; ++c) {
         int w = 0;
         while (!(offsets[w] <= c && c < offsets[w + 1])) ++w;
         const Space& sp = *(Space*)spaces[w];
-        if (n_features_of(sp) != n_features) return -6;
+        if (n_features_of(sp) != e.n_features) return -6;
+        if (global && n_relation_features_of(sp) != global->n_features) return -6;
+        auto score = [&](uint64_t cfg) {
+            return global ? score_config_global_local(sp, *global, e, cfg) : score_config(sp, e, cfg);
+        };
         int nk = (int)sp.knobs.size();
         if (nk > max_knobs) return -1;
         uint64_t g = (uint64_t)(chain0 + c);
@@ -807,7 +829,7 @@ int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
             }
             for (int i = 0; i < topk; ++i) list[i] = TopEntry{0, 0.0f, 0u};
             uint64_t cfg0 = encode(sp, cur);
-            cur_score[c] = score_config(sp, e, cfg0);
+            cur_score[c] = score(cfg0);
             topk_offer(list, topk, cfg0, cur_score[c]);
             step_abs[c] = 0;
             initialised[c] = 1;
@@ -827,7 +849,7 @@ int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
                 cand[j] = nv;
             }
             uint64_t cfg = encode(sp, cand);
-            float sc = score_config(sp, e, cfg);
+            float sc = score(cfg);
             topk_offer(list, topk, cfg, sc);
             float delta = sc - cur_score[c];
             bool accept = delta >= thr[c * steps + s];
@@ -841,6 +863,43 @@ int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
         for (int j = 0; j < nk; ++j) v[j] = cur[j];
     }
     return 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Annealing over a set of spaces sharing one ensemble.  Chain c (local index)
+// belongs to space w with offsets[w] <= c < offsets[w+1]; its global id is
+// chain0 + c.  Per-chain state (in/out): cur knob values [n][max_knobs],
+// cur score, initialised flag, step_abs, top-k [n][k].  thr is [n][steps].
+// trace (optional) receives [n][steps] entries (cfg, score, accepted).
+int or_sa_run(void** spaces, int n_spaces, const int64_t* offsets,
+              int n_trees, int depth, int n_features, const uint8_t* fid, const uint8_t* thr_nodes,
+              const float* leaf, uint64_t seed, int64_t chain0, int64_t n_chains, int topk,
+              int steps, const float* thr, int max_knobs,
+              int64_t* cur_knobs, float* cur_score, uint8_t* initialised, uint64_t* step_abs,
+              TopEntry* tops, TopEntry* trace) {
+    const Ensemble e{n_trees, depth, n_features, fid, thr_nodes, leaf};
+    return sa_run(spaces, n_spaces, offsets, e, nullptr, seed, chain0, n_chains, topk, steps, thr, max_knobs,
+                  cur_knobs, cur_score, initialised, step_abs, tops, trace);
+}
+
+// or_sa_run whose energy is Eq. 4's sum of a global model over the context
+// relation features (g_* arrays, g_n_features = 2 * buffers * 32) and the
+// local model over the loop-context features (the usual ensemble arrays).
+int or_sa_run_global_local(void** spaces, int n_spaces, const int64_t* offsets,
+                           int g_n_trees, int g_depth, int g_n_features, const uint8_t* g_fid,
+                           const uint8_t* g_thr, const float* g_leaf,
+                           int n_trees, int depth, int n_features, const uint8_t* fid, const uint8_t* thr_nodes,
+                           const float* leaf, uint64_t seed, int64_t chain0, int64_t n_chains, int topk,
+                           int steps, const float* thr, int max_knobs,
+                           int64_t* cur_knobs, float* cur_score, uint8_t* initialised, uint64_t* step_abs,
+                           TopEntry* tops, TopEntry* trace) {
+    const Ensemble e{n_trees, depth, n_features, fid, thr_nodes, leaf};
+    const Ensemble g{g_n_trees, g_depth, g_n_features, g_fid, g_thr, g_leaf};
+    return sa_run(spaces, n_spaces, offsets, e, &g, seed, chain0, n_chains, topk, steps, thr, max_knobs,
+                  cur_knobs, cur_score, initialised, step_abs, tops, trace);
 }
 
 int or_relation_features(void* h, const uint64_t* cfgs, int64_t n, int32_t* feats) {
