@@ -109,9 +109,13 @@ def describe(name: str) -> str:
 
 
 class SaWorkload:
-    def __init__(self, P, name):
+    """One annealing workload on one chains handle.  transfer: the energy is
+    Eq. 4's global model (as many trees, of the same depth, over the 192
+    relation features) plus the workload's ensemble as the local model."""
+
+    def __init__(self, P, name, transfer=False):
         import torch
-        self.P, self.name = P, name
+        self.P, self.name, self.transfer = P, name, transfer
         wl = self.wl = W.WORKLOADS[name]
         self.spaces = [P.at_space_create(t, s) for t, s in wl["spaces"]]
         F = self.spaces[0].n_features
@@ -125,11 +129,14 @@ class SaWorkload:
         t0 = time.perf_counter()
         self.ens_tables = W.make_ensemble(wl["trees"], wl["depth"], F, wl["ens_seed"])
         self.ens = P.at_ensemble_create(*self.ens_tables, F)
+        if transfer:
+            self.glob = P.at_ensemble_create(*W.make_ensemble(wl["trees"], wl["depth"], P.RELATION_FEATURES,
+                                                              wl["ens_seed"] + 50), P.RELATION_FEATURES)
         self.t_pack = time.perf_counter() - t0
         self.t_thr = None
         self.best = torch.zeros((self.n, self.topk, 4), dtype=torch.int32, device="cuda")
         self.evals = self.n * self.steps
-        self.tree_evals = self.evals * wl["trees"]
+        self.tree_evals = self.evals * wl["trees"] * (2 if transfer else 1)
         self.lds_bytes = self.tree_evals * tree_eval_bytes(wl["depth"])
         self.chains = P.at_chains_create(self.space, 0, self.n, self.topk, self.seed)
 
@@ -148,7 +155,10 @@ class SaWorkload:
         return out
 
     def run(self, thr):
-        self.P.at_sa_run(self.space, self.ens, self.chains, self.steps, thr, self.best)
+        if self.transfer:
+            self.P.at_sa_run_global_local(self.space, self.glob, self.ens, self.chains, self.steps, thr, self.best)
+        else:
+            self.P.at_sa_run(self.space, self.ens, self.chains, self.steps, thr, self.best)
 
 
 def time_events(fn, reps):
@@ -166,14 +176,14 @@ def time_events(fn, reps):
     return out
 
 
-def bench_sa(P, name, steps, warmup):
+def bench_sa(P, name, steps, warmup, transfer=False):
     """Annealing runs of a workload on one chains handle.  The warm-up runs
     initialise the chains and take the handle's one-time workspace
     allocation; every timed run then continues the same chains for the
     workload's step count with thresholds precomputed for its steps, so the
     timed region holds kernel launches only."""
     import torch
-    w = SaWorkload(P, name)
+    w = SaWorkload(P, name, transfer)
     warmup = max(1, warmup)
     thr = w.thresholds(warmup)
     for i in range(warmup):
@@ -198,10 +208,13 @@ def bench_sa(P, name, steps, warmup):
     tree_s = kt["tree_ms"] / kt["tree_launches"] * 1e-3
     rounds_per_launch = w.steps if local else 1
     tree_bytes = w.n * w.wl["trees"] * rounds_per_launch * tree_eval_bytes(w.wl["depth"])
+    if transfer:
+        name += " (Eq. 4: global model on the relation features + local model on the loop features, "
+        name += f"{w.wl['trees']} trees depth {w.wl['depth']} each; two tree launches per step)"
     return w, dict(
         path="chain-local" if local else "tree-partitioned", plan=plan,
         walk_kernel="k_local" if local else "k_trees",
-        workload=describe(name), ms_per_run=t * 1e3, ms_min=float(np.min(ev)) * 1e3, wall_s=wall,
+        workload=describe(name.split(" ")[0]) + name[len(name.split(" ")[0]):], ms_per_run=t * 1e3, ms_min=float(np.min(ev)) * 1e3, wall_s=wall,
         evals_per_s=w.evals / t, tree_evals_per_s=w.tree_evals / t,
         run_lds_bytes=w.lds_bytes, run_lds_TBps=w.lds_bytes / t / 1e12,
         run_lds_frac=w.lds_bytes / t / LDS_PEAK_BPS, run_lds_frac_b128=w.lds_bytes / t / LDS_B128_BPS,
@@ -377,6 +390,7 @@ def main():
             w, extra[name] = bench_sa(P, name, reps, 1)
             if name in ("conv_c2_sa", "conv_c12_sa"):
                 extra["select_" + name] = bench_select(P, w)
+        _, extra["transfer_resnet18_12conv_sa"] = bench_sa(P, "resnet18_12conv_sa", 3, 1, transfer=True)
     depth = head.wl["depth"]
     line = {
         "metric": METRIC,

@@ -271,6 +271,24 @@ at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int
 at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps,
                            const float* thr, at_entry* best, at_entry* trace, at_stream_t stream);
 
+/* at_sa_run whose energy is the transfer model of Section 4, Eq. 4:
+ * f_hat(x) = f_hat_global(x) + f_hat_local(x).  The global model reads a
+ * candidate's context relation features (the invariant representation, as
+ * at_extract_relation_features writes them: 192 per configuration; its
+ * ensemble must have n_features == 192, else AT_E_MISMATCH); the local model
+ * reads its loop-context features (n_features of the space).  Each model's
+ * prediction is its own fp32 left fold over its trees from +0.0f; a
+ * candidate's score is fp32(global + local), the global one first.  Every
+ * other step is at_sa_run's.  The chains keep the scores of the model that
+ * scored them.  trace: device [n_chains][steps] at_entry, or NULL.  These runs
+ * take the tree-partitioned path (two tree-kernel launches per step, one per
+ * model): at_chains_set_path(AT_SA_PATH_LOCAL) makes them fail with
+ * AT_E_UNSUPPORTED.  Workspace as at_sa_run, plus about n_chains *
+ * (16 * ceil(global trees / 4) + 192) bytes on the first such run. */
+at_status at_sa_run_global_local(at_space_t space, at_ensemble_t global, at_ensemble_t local, at_chains_t chains,
+                                 int steps, const float* thr, at_entry* best, at_entry* trace,
+                                 at_stream_t stream);
+
 /* Context relation features (Section 4, "Context Relation Features for
  * GBT"; Appendix A.2 "Relation Feature") of n configurations: the invariant
  * representation the paper transfers across workloads.  Over the loops of

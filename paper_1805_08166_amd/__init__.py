@@ -33,7 +33,7 @@ EXPORTED = [
     "at_extract_features", "at_extract_features_full", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_trees_depth", "at_trees_pad", "at_ensemble_import",
     "at_gbt_predict", "at_gbt_predict_global_local", "at_chains_create", "at_chains_destroy", "at_chains_step",
-    "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_chains_export", "at_sa_set_profiling",
+    "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_sa_run_global_local", "at_chains_export", "at_sa_set_profiling",
     "at_sa_kernel_times", "at_chains_set_path", "at_chains_last_path", "at_chains_last_plan", "at_select_batch", "at_select_batch_noalloc", "at_last_error",
 ]
 
@@ -80,6 +80,7 @@ def _load():
         "at_sa_thresholds": [u64, i64, i64, u64, i32, vp],
         "at_sa_run": [vp, vp, vp, i32, vp, vp, vp],
         "at_sa_run_traced": [vp, vp, vp, i32, vp, vp, vp, vp],
+        "at_sa_run_global_local": [vp, vp, vp, vp, i32, vp, vp, vp, vp],
         "at_chains_export": [vp, vp, vp, vp],
         "at_sa_set_profiling": [vp, i32],
         "at_sa_kernel_times": [vp, vp, vp, vp, vp],
@@ -422,6 +423,21 @@ def at_sa_run_traced(space: Space, ens: Ensemble, chains: Chains, steps: int, th
     _check("at_sa_run_traced", _lib.at_sa_run_traced(
         space.h, ens.h, chains.h, int(steps), _dev(thr, torch.float32, "thr"), _dev(best, torch.int32, "best"),
         _dev(trace, torch.int32, "trace"), _stream(stream)))
+
+
+def at_sa_run_global_local(space: Space, glob: Ensemble, local: Ensemble, chains: Chains, steps: int, thr, best,
+                           trace=None, stream=None):
+    """Annealing with Eq. 4's energy: glob over the 192 relation features
+    plus local over the loop features.  thr: device float32 [n_chains,
+    steps]; best: device int32 [n_chains, topk, 4]; trace: device int32
+    [n_chains, steps, 4] or None."""
+    import torch
+    _check_sa(chains, steps, thr, best)
+    if trace is not None and trace.shape != (chains.n_chains, steps, 4):
+        raise ValueError("trace must be [n_chains, steps, 4] int32")
+    _check("at_sa_run_global_local", _lib.at_sa_run_global_local(
+        space.h, glob.h, local.h, chains.h, int(steps), _dev(thr, torch.float32, "thr"),
+        _dev(best, torch.int32, "best"), _dev(trace, torch.int32, "trace"), _stream(stream)))
 
 
 def _check_sa(chains, steps, thr, best):

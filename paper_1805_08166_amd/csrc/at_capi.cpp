@@ -600,6 +600,9 @@ void at_chains_destroy(at_chains_t chains) {
     release(chains->d_fg);
     release(chains->d_v);
     release(chains->d_tw);
+    release(chains->d_fr);
+    release(chains->d_vg);
+    release(chains->d_twg);
     for (auto& pool : chains->events)
         for (hipEvent_t e : pool) (void)hipEventDestroy(e);
     delete chains;
@@ -733,34 +736,44 @@ at_status at_sa_thresholds(uint64_t seed, int64_t chain0, int64_t n_chains, uint
     return AT_OK;
 }
 
-static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps, const float* thr,
-                             at_entry* best, at_entry* trace, at_stream_t stream) {
-    if (!space || !ens || !chains) return fail(AT_E_INVALID, "at_sa_run: NULL handle");
-    if (steps < 0) return fail(AT_E_INVALID, "at_sa_run: steps < 0");
+static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_ensemble_t global, at_chains_t chains,
+                             int steps, const float* thr, at_entry* best, at_entry* trace, at_stream_t stream,
+                             const char* fn) {
+    const std::string f(fn);
+    if (!space || !ens || !chains) return fail(AT_E_INVALID, f + ": NULL handle");
+    if (steps < 0) return fail(AT_E_INVALID, f + ": steps < 0");
     if (space->n_spaces != chains->n_spaces || space->tmpl != chains->tmpl)
-        return fail(AT_E_INVALID, "at_sa_run: chains were created for another space");
+        return fail(AT_E_INVALID, f + ": chains were created for another space");
     if (space->n_spaces > 1 && chains->n_chains != space->chain_offsets.back())
-        return fail(AT_E_INVALID, "at_sa_run: chain count does not match the space set");
+        return fail(AT_E_INVALID, f + ": chain count does not match the space set");
     if (ens->desc.n_features != space->descs[0].n_features)
-        return fail(AT_E_MISMATCH, "at_sa_run: ensemble and space feature counts differ");
-    if (chains->n_chains > 0 && !best) return fail(AT_E_INVALID, "at_sa_run: NULL best");
-    if (steps > 0 && chains->n_chains > 0 && !thr) return fail(AT_E_INVALID, "at_sa_run: NULL thr");
+        return fail(AT_E_MISMATCH, f + ": ensemble and space feature counts differ");
+    if (global && global->desc.n_features != RELATION_FEATURES)
+        return fail(AT_E_MISMATCH, f + ": the global model must read the 192 context relation features");
+    if (chains->n_chains > 0 && !best) return fail(AT_E_INVALID, f + ": NULL best");
+    if (steps > 0 && chains->n_chains > 0 && !thr) return fail(AT_E_INVALID, f + ": NULL thr");
     if (chains->step_abs + (uint64_t)steps > ((uint64_t)1 << 32))
-        return fail(AT_E_UNSUPPORTED, "at_sa_run: step counter must fit 32 bits");
+        return fail(AT_E_UNSUPPORTED, f + ": step counter must fit 32 bits");
     DeviceGuard g(chains->device);
     const bool init = !chains->initialised;
     // path: chain-local when its plan fits and one workgroup streams at most
-    // LOCAL_AUTO_BYTES per step, else tree-partitioned
+    // LOCAL_AUTO_BYTES per step, else tree-partitioned; Eq. 4 runs take the
+    // tree-partitioned path
     LocalPlan pl;
-    const bool local_fits = chains->n_chains > 0 && plan_local(*space, ens->desc, *chains, pl);
+    const bool local_fits = !global && chains->n_chains > 0 && plan_local(*space, ens->desc, *chains, pl);
     int path = chains->path;
-    if (path == AT_SA_PATH_AUTO) path = (local_fits && pl.round_bytes <= LOCAL_AUTO_BYTES) ? AT_SA_PATH_LOCAL : AT_SA_PATH_TREES;
+    if (path == AT_SA_PATH_AUTO)
+        path = (local_fits && pl.round_bytes <= LOCAL_AUTO_BYTES) ? AT_SA_PATH_LOCAL : AT_SA_PATH_TREES;
+    if (path == AT_SA_PATH_LOCAL && global)
+        return fail(AT_E_UNSUPPORTED, f + ": two-model (Eq. 4) runs take the tree-partitioned path");
     if (path == AT_SA_PATH_LOCAL && chains->n_chains > 0 && !local_fits)
-        return fail(AT_E_UNSUPPORTED, "at_sa_run: the chain-local plan does not fit one workgroup's LDS");
+        return fail(AT_E_UNSUPPORTED, f + ": the chain-local plan does not fit one workgroup's LDS");
     hipError_t e = path == AT_SA_PATH_LOCAL
-                       ? launch_sa_local(*space, ens->desc, *chains, pl, steps, init, thr, best, trace, (hipStream_t)stream)
-                       : launch_sa_tp(*space, ens->desc, *chains, steps, init, thr, best, trace, (hipStream_t)stream);
-    if (e != hipSuccess) return hip_fail(e, "at_sa_run");
+                       ? launch_sa_local(*space, ens->desc, *chains, pl, steps, init, thr, best, trace,
+                                         (hipStream_t)stream)
+                       : launch_sa_tp(*space, ens->desc, global ? &global->desc : nullptr, *chains, steps, init, thr,
+                                      best, trace, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, fn);
     chains->last_path = path;
     const int64_t plan[8] = {pl.cpb, pl.threads, pl.grid, pl.ct, (pl.resident || pl.tail) ? 0 : pl.n_chunks,
                              pl.tail ? 2 : pl.gather, (int64_t)pl.lds_bytes, (int64_t)pl.round_bytes};
@@ -776,13 +789,19 @@ static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_chains_t ch
 
 at_status at_sa_run(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps, const float* thr,
                     at_entry* best, at_stream_t stream) {
-    return sa_run_impl(space, ens, chains, steps, thr, best, nullptr, stream);
+    return sa_run_impl(space, ens, nullptr, chains, steps, thr, best, nullptr, stream, "at_sa_run");
 }
 
 at_status at_sa_run_traced(at_space_t space, at_ensemble_t ens, at_chains_t chains, int steps, const float* thr,
                            at_entry* best, at_entry* trace, at_stream_t stream) {
     if (steps > 0 && chains && chains->n_chains > 0 && !trace) return fail(AT_E_INVALID, "at_sa_run_traced: NULL trace");
-    return sa_run_impl(space, ens, chains, steps, thr, best, trace, stream);
+    return sa_run_impl(space, ens, nullptr, chains, steps, thr, best, trace, stream, "at_sa_run_traced");
+}
+
+at_status at_sa_run_global_local(at_space_t space, at_ensemble_t global, at_ensemble_t local, at_chains_t chains,
+                                 int steps, const float* thr, at_entry* best, at_entry* trace, at_stream_t stream) {
+    if (!global) return fail(AT_E_INVALID, "at_sa_run_global_local: NULL global model");
+    return sa_run_impl(space, local, global, chains, steps, thr, best, trace, stream, "at_sa_run_global_local");
 }
 
 at_status at_chains_export(at_chains_t chains, uint64_t* cur_cfg, float* cur_score, at_stream_t stream) {

@@ -143,10 +143,13 @@ __device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_
 // schedule with one lane per loop.  Same arithmetic as nest_features: the
 // running products over the loops at or inside p are formed by visiting every
 // loop from the innermost outwards and multiplying in only those with index
-// >= p; loop p's own quantities are captured when it is visited.
+// >= p; loop p's own quantities are captured when it is visited.  td, when
+// given, receives bitlen(top-down) of loop p: the product of the lengths of
+// the loops outside it, i.e. the nest's iteration count over bottom-up.
 template <int TMPL>
 __device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4], uint32_t unroll_max,
-                                              uint32_t unroll_id, int p, uint32_t (&out)[11]) {
+                                              uint32_t unroll_id, int p, uint32_t (&out)[11],
+                                              uint32_t* td = nullptr) {
     using N = Nest<TMPL>;
     uint32_t range[6] = {1u, 1u, 1u, 1u, 1u, 1u};
     uint32_t bottom_up = 1u, ext = 1u, bind = 0u;
@@ -181,6 +184,14 @@ __device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_
     }
     uint32_t t[3];
     N::touched(range, (uint32_t)sd.stride, t);
+    if (td) {
+        uint32_t total = 1u;
+#pragma unroll
+        for (int a = 0; a < 6; ++a)
+#pragma unroll
+            for (int l = 0; l < 4; ++l) total *= fac[a][l];
+        *td = bitlen_quot(total, bottom_up);
+    }
     out[0] = bitlen(ext);
     out[1] = bind ? bind : ((unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u);
 #pragma unroll

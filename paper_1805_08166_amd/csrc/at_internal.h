@@ -23,6 +23,9 @@ constexpr int N_BUFFERS = 3;
 // lane of a wave reads its own bank whatever feature it asks for.
 constexpr int TILE_LANES = 256;
 constexpr int MAX_TILE_QUADS = 64;   // up to 256 features
+// Context relation features per configuration (Section 4): 2 pairs x 3
+// buffers x 32 thresholds.
+constexpr int RELATION_FEATURES = 192;
 // Packed ensembles are zero-padded to a multiple of this many words.
 constexpr size_t ENSEMBLE_PAD_WORDS = 8192;
 
@@ -199,6 +202,10 @@ struct at_chains_s {
     at::DeviceBuf d_fg;       // uint32 [Q][n_chains] packed candidate features
     at::DeviceBuf d_v;        // float leaf values, [ceil(T/4)][n_chains][4]
     at::DeviceBuf d_tw;       // uint32 pointer-form trees relocated for the tree kernel's LDS plan
+    // Eq. 4 runs (tree-partitioned): the global model's side
+    at::DeviceBuf d_fr;       // uint32 [48][n_chains] packed candidate relation features
+    at::DeviceBuf d_vg;       // float leaf values of the global model, laid out as d_v
+    at::DeviceBuf d_twg;      // the global model's relocated pointer form
     // launch timing (measurement aid): start/stop events attached to every
     // launch of the last run; kind 0 is the tree kernel, 1 the chain kernel
     bool profiling = false;
@@ -232,9 +239,9 @@ hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n
                           uint16_t* leaves, bool accumulate, hipStream_t stream);
 hipError_t launch_score(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
                         uint16_t* leaves, bool accumulate, hipStream_t stream);
-hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps,
-                        bool init, const float* thr, at_entry* best, at_entry* trace,
-                        hipStream_t stream);
+// eg: the global model of an Eq. 4 run (over the relation features), or null.
+hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const EnsembleDesc* eg, at_chains_s& ch,
+                        int steps, bool init, const float* thr, at_entry* best, at_entry* trace, hipStream_t stream);
 // Chain-local annealing path (at_sa_local.hip): launch geometry and the
 // byte offsets of its dynamic LDS blocks.
 struct LocalPlan {

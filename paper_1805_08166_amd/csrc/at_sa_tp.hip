@@ -75,7 +75,17 @@ struct ChainArgs {
     int draw;                 // what to propose next
     uint32_t draw_step;       // absolute step of the proposal
     at_entry* best;           // copy of the best lists (last launch), or null
+    // Eq. 4 runs: leaf values of the global model (over the candidates'
+    // relation features), folded before the local model's V and added to
+    // its sum; the candidates' relation features go to Fr as packed bytes,
+    // quad-major ([REL_Q][fg_stride]).  Null for one-model runs.
+    const float* Vg;
+    int Tg;
+    uint32_t* Fr;
 };
+
+constexpr int REL_F = 192;              // context relation features per candidate
+constexpr int REL_Q = REL_F / 4;
 
 
 // Score of the pending candidates of chains c0 .. c0+nc-1: lane j < nc of
@@ -253,7 +263,12 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     }
     // the leaf values of the pending candidates start streaming in (after
     // the table staging, whose loads would otherwise queue behind them)
-    if (a.fin != FIN_NONE) fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+    if (a.fin != FIN_NONE) {
+        if (a.Vg)
+            fold_prime(reinterpret_cast<const float4*>(a.Vg), a.Tg, c0, nc, ring, tid);
+        else
+            fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+    }
     // publishes the staged space tables; the first passes of the fold stay
     // in flight
     lds_barrier();
@@ -280,7 +295,20 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
                 lists[e] = z;
             }
         }
-        const float s = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+        float s;
+        if (a.Vg) {
+            // Eq. 4: each model's prediction is its own fold from +0.0f;
+            // the sum adds the global one first
+            const float sg = fold_ring(reinterpret_cast<const float4*>(a.Vg), a.Tg, c0, nc, ring, tid);
+            // wave 0 has read the global model's last pass before the ring
+            // takes the local model's first ones
+            lds_barrier();
+            fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+            const float sl = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+            s = sg + sl;
+        } else {
+            s = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+        }
         __builtin_amdgcn_s_waitcnt(0);
 
         // best lists: the chain's group of 16 lanes inserts the candidate
@@ -389,6 +417,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     __syncthreads();
 
     // features: lane gr of group gj evaluates loop gr of chain gj's candidate
+    __shared__ uint8_t tdrow[CPW][16];
     if (gvalid && gr < N::L) {
         const SpaceDesc& sd = *gsdp;
         uint32_t nx[MAX_KNOBS];
@@ -396,12 +425,44 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (rec[gj].nx[j >> 1] >> (16 * (j & 1))) & 0xffffu;
         uint32_t fac[6][4];
         gather_factors<TMPL>(sd, facp, nx, fac);
-        uint32_t f[11];
-        loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f);
+        uint32_t f[11], td = 0u;
+        loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f, a.Fr ? &td : nullptr);
 #pragma unroll
         for (int i = 0; i < 11; ++i) frow[gj][gr * 11 + i] = (uint8_t)f[i];
+        tdrow[gj][gr] = (uint8_t)td;
     }
     __syncthreads();
+    if (a.Fr) {
+        // context relation features of the candidate (Section 4): output
+        // o = [pair][buffer b][t - 1] is the largest value over the loops
+        // whose touch count of b is below 2^t (bitlen(touch) <= t), the value
+        // being bitlen(reuse ratio of b) for pair 0, bitlen(top-down) for
+        // pair 1; 0 when no loop qualifies.  Lane gr of group gj makes
+        // outputs gr, gr + 16, ...
+        __shared__ __attribute__((aligned(16))) uint8_t rrow[CPW][REL_F];
+        if (gvalid) {
+#pragma unroll 1
+            for (int o = gr; o < REL_F; o += 16) {
+                const int pair = o / 96, b = (o >> 5) % 3;
+                const uint32_t t = (uint32_t)(o & 31) + 1u;
+                uint32_t v = 0u;
+#pragma unroll
+                for (int l = 0; l < N::L; ++l) {
+                    const uint32_t bt = frow[gj][l * 11 + 2 + 3 * b];
+                    const uint32_t x = pair ? (uint32_t)tdrow[gj][l] : (uint32_t)frow[gj][l * 11 + 3 + 3 * b];
+                    v = (bt <= t && x > v) ? x : v;
+                }
+                rrow[gj][o] = (uint8_t)v;
+            }
+        }
+        __syncthreads();
+        for (int idx = tid; idx < CPW * REL_Q; idx += CHAIN_WG) {
+            const int q = idx >> 4, j = idx & (CPW - 1);
+            if (j >= nc) continue;
+            const uint32_t w = (*reinterpret_cast<const uint32_t*>(&rrow[j][4 * q]) << 2) | 0x03030303u;
+            a.Fr[(int64_t)q * a.fg_stride + c0 + j] = w;
+        }
+    }
     // packed rows out (4x+3 per byte, the tree kernel's tile encoding),
     // consecutive lanes on consecutive chains
     // (a feature value x <= 63 makes (x << 2) | 3 stay within its byte)
@@ -929,17 +990,61 @@ hipError_t launch_trees_q(const TreeArgs& a, int depth, int nw, hipStream_t stre
     }
 }
 
-// Tile slot sizes: the smallest power of two holding Q * 256 bytes.
+// Tile slot sizes: the smallest power of two holding Q * 256 bytes.  The
+// relation-feature tile (Eq. 4 runs, 192 features) has REL_Q quads.
 constexpr int GEMM_Q = 28, CONV_Q = 44;
-constexpr int GEMM_SLOT_LOG2 = 13, CONV_SLOT_LOG2 = 14;
+constexpr int GEMM_SLOT_LOG2 = 13, CONV_SLOT_LOG2 = 14, REL_SLOT_LOG2 = 14;
 static_assert((GEMM_Q * 256) <= (1 << GEMM_SLOT_LOG2) && (GEMM_Q * 256) > (1 << (GEMM_SLOT_LOG2 - 1)), "slot");
 static_assert((CONV_Q * 256) <= (1 << CONV_SLOT_LOG2) && (CONV_Q * 256) > (1 << (CONV_SLOT_LOG2 - 1)), "slot");
+static_assert((REL_Q * 256) <= (1 << REL_SLOT_LOG2) && (REL_Q * 256) > (1 << (REL_SLOT_LOG2 - 1)), "slot");
+
+int slot_log2_of(int Q) { return Q == GEMM_Q ? GEMM_SLOT_LOG2 : Q == CONV_Q ? CONV_SLOT_LOG2 : REL_SLOT_LOG2; }
 
 hipError_t launch_trees(const TreeArgs& a, int Q, int depth, int nw, hipStream_t stream, hipEvent_t start,
                         hipEvent_t stop) {
     if (Q == GEMM_Q) return launch_trees_q<GEMM_Q, GEMM_SLOT_LOG2>(a, depth, nw, stream, start, stop);
     if (Q == CONV_Q) return launch_trees_q<CONV_Q, CONV_SLOT_LOG2>(a, depth, nw, stream, start, stop);
+    if (Q == REL_Q) return launch_trees_q<REL_Q, REL_SLOT_LOG2>(a, depth, nw, stream, start, stop);
     return hipErrorInvalidValue;
+}
+
+// Launch plan of the tree kernel for an ensemble walked over Q-quad tiles of
+// n chains: tree groups of tpw trees times chain slices, the layout scoring
+// the walks in flight per compute unit (waves times trees walked together)
+// times the share of compute units its grid fills.  Fills ta's plan fields
+// and nw; false when nothing fits.
+bool plan_tree_launch(int n_trees, int depth, int Q, int64_t n, int n_cu, TreeArgs& ta, int& nw) {
+    const int slot = 1 << slot_log2_of(Q);
+    const int64_t blocks = (n + 63) / 64;
+    double best_score = -1.0;
+    nw = 0;
+    for (int tpw = TREES_MAX; tpw >= 1; tpw /= 2) {
+        const int tg = (n_trees + tpw - 1) / tpw;
+        int64_t slices = n_cu / tg;
+        if (slices < 1) slices = 1;
+        if (slices > blocks) slices = blocks;
+        const int64_t sb = (blocks + slices - 1) / slices;
+        slices = (blocks + sb - 1) / sb;
+        const int cap = sb < TREE_WAVES_MAX ? (int)sb : TREE_WAVES_MAX;
+        uint32_t toff[TREES_MAX];
+        for (int w = cap; w >= 1; --w) {
+            if (!plan_trees(depth, Q, slot, w, tpw, toff)) continue;
+            const double grid = (double)tg * (double)slices;
+            const double score = (double)w * (tpw < 8 ? tpw : 8) * (grid < n_cu ? grid / n_cu : 1.0);
+            if (score > best_score) {
+                best_score = score;
+                nw = w;
+                ta.tpw = tpw;
+                ta.slices = (int)slices;
+                ta.slice_blocks = (int)sb;
+                for (int i = 0; i < TREES_MAX; ++i) ta.toff[i] = toff[i];
+            }
+            break;
+        }
+    }
+    if (nw == 0) return false;
+    ta.mask = (((uint32_t)slot - 1u) & ~0xffu) | 3u;
+    return true;
 }
 
 hipError_t ensure(DeviceBuf& b, size_t bytes) {
@@ -980,18 +1085,54 @@ hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t&
     return hipSuccess;
 }
 
-hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s& ch, int steps, bool init,
-                        const float* thr, at_entry* best, at_entry* trace, hipStream_t stream) {
+// One ensemble's tree kernel for a run: its plan, its pointer form
+// relocated for that plan, and the tile and leaf-value buffers it uses.
+struct TreeLaunch {
+    TreeArgs ta{};
+    int nw = 0;
+    int Q = 0;
+    int depth = 0;
+};
+
+static hipError_t prepare_trees(const EnsembleDesc& e, int Q, int64_t n, int n_cu, DeviceBuf& relocated,
+                         const uint32_t* Fg, int64_t fg_stride, float* V, hipStream_t stream, TreeLaunch& tl) {
+    tl.Q = Q;
+    tl.depth = e.depth;
+    TreeArgs& ta = tl.ta;
+    ta.words32 = e.words32;
+    ta.n_trees = e.n_trees;
+    ta.Fg = Fg;
+    ta.fg_stride = fg_stride;
+    ta.n = n;
+    ta.V = V;
+    if (!plan_tree_launch(e.n_trees, e.depth, Q, n, n_cu, ta, tl.nw)) return hipErrorInvalidConfiguration;
+    const int64_t words = (int64_t)e.n_trees << (e.depth + 1);
+    hipError_t err = ensure(relocated, (size_t)words * 4);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_reloc, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream, e.words32,
+                       static_cast<uint32_t*>(relocated.p), words, e.depth, ta);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    ta.words32 = static_cast<const uint32_t*>(relocated.p);
+    return hipSuccess;
+}
+
+hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const EnsembleDesc* eg, at_chains_s& ch,
+                        int steps, bool init, const float* thr, at_entry* best, at_entry* trace, hipStream_t stream) {
     const int64_t n = ch.n_chains;
     if (n == 0) return hipSuccess;
     const int Q = (sp.descs[0].n_features + 3) / 4;
     const int groups = (e.n_trees + 3) / 4;
+    const int64_t n16 = (n + 15) / 16 * 16;
     hipError_t err;
     if ((err = ensure(ch.d_cand, (size_t)n * MAX_KNOBS * 2)) != hipSuccess) return err;
     if ((err = ensure(ch.d_meta, (size_t)n * sizeof(ChainMeta))) != hipSuccess) return err;
     const int64_t fg_stride = (n + 63) / 64 * 64;
     if ((err = ensure(ch.d_fg, (size_t)Q * fg_stride * 4)) != hipSuccess) return err;
-    if ((err = ensure(ch.d_v, (size_t)groups * ((n + 15) / 16 * 16) * 16)) != hipSuccess) return err;
+    if ((err = ensure(ch.d_v, (size_t)groups * n16 * 16)) != hipSuccess) return err;
+    if (eg) {
+        if ((err = ensure(ch.d_fr, (size_t)REL_Q * fg_stride * 4)) != hipSuccess) return err;
+        if ((err = ensure(ch.d_vg, (size_t)((eg->n_trees + 3) / 4) * n16 * 16)) != hipSuccess) return err;
+    }
 
     ChainArgs ca{};
     ca.descs = static_cast<const SpaceDesc*>(sp.d_descs.p);
@@ -1014,64 +1155,31 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
     ca.steps = steps;
     ca.thr = thr;
     ca.trace = trace;
+    if (eg) {
+        ca.Vg = static_cast<const float*>(ch.d_vg.p);
+        ca.Tg = eg->n_trees;
+        ca.Fr = static_cast<uint32_t*>(ch.d_fr.p);
+    }
 
-    TreeArgs ta{};
-    ta.words32 = e.words32;
-    ta.n_trees = e.n_trees;
-    ta.Fg = ca.Fg;
-    ta.fg_stride = fg_stride;
-    ta.n = n;
-    ta.V = static_cast<float*>(ch.d_v.p);
-    // Tree groups of tpw trees times chain slices: a layout scores the walks
-    // in flight per compute unit (waves times trees walked together) times
-    // the share of compute units its grid fills.
     int n_cu = 256;
     (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, ch.device);
-    const int slot = 1 << (Q == GEMM_Q ? GEMM_SLOT_LOG2 : CONV_SLOT_LOG2);
-    const int64_t blocks = (n + 63) / 64;
-    double best_score = -1.0;
-    int nw = 0;
-    for (int tpw = TREES_MAX; tpw >= 1; tpw /= 2) {
-        const int tg = (e.n_trees + tpw - 1) / tpw;
-        int64_t slices = n_cu / tg;
-        if (slices < 1) slices = 1;
-        if (slices > blocks) slices = blocks;
-        const int64_t sb = (blocks + slices - 1) / slices;
-        slices = (blocks + sb - 1) / sb;
-        const int cap = sb < TREE_WAVES_MAX ? (int)sb : TREE_WAVES_MAX;
-        uint32_t toff[TREES_MAX];
-        for (int w = cap; w >= 1; --w) {
-            if (!plan_trees(e.depth, Q, slot, w, tpw, toff)) continue;
-            const double grid = (double)tg * (double)slices;
-            const double score = (double)w * (tpw < 8 ? tpw : 8) * (grid < n_cu ? grid / n_cu : 1.0);
-            if (score > best_score) {
-                best_score = score;
-                nw = w;
-                ta.tpw = tpw;
-                ta.slices = (int)slices;
-                ta.slice_blocks = (int)sb;
-                for (int i = 0; i < TREES_MAX; ++i) ta.toff[i] = toff[i];
-            }
-            break;
-        }
-    }
-    if (nw == 0) return hipErrorInvalidConfiguration;
-    ta.mask = (((uint32_t)slot - 1u) & ~0xffu) | 3u;
-    {
-        const int64_t words = (int64_t)e.n_trees << (e.depth + 1);
-        if ((err = ensure(ch.d_tw, (size_t)words * 4)) != hipSuccess) return err;
-        hipLaunchKernelGGL(k_reloc, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream, e.words32,
-                           static_cast<uint32_t*>(ch.d_tw.p), words, e.depth, ta);
-        if ((err = hipGetLastError()) != hipSuccess) return err;
-        ta.words32 = static_cast<const uint32_t*>(ch.d_tw.p);
-    }
+    // the local (or only) model over the loop features, then the global model
+    // over the relation features
+    TreeLaunch tl, tg;
+    if ((err = prepare_trees(e, Q, n, n_cu, ch.d_tw, ca.Fg, fg_stride, static_cast<float*>(ch.d_v.p), stream,
+                             tl)) != hipSuccess)
+        return err;
+    if (eg && (err = prepare_trees(*eg, REL_Q, n, n_cu, ch.d_twg, ca.Fr, fg_stride, static_cast<float*>(ch.d_vg.p),
+                                   stream, tg)) != hipSuccess)
+        return err;
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
     const size_t chain_lds = RING_BYTES + (size_t)CPW * ch.topk * sizeof(at_entry);
     {
+        const TreeArgs& ta = tl.ta;
         const int64_t tree_grid = (int64_t)(e.n_trees + ta.tpw - 1) / ta.tpw * ta.slices;
-        const int64_t plan[8] = {ta.tpw, nw, tree_grid, ta.slices, ta.slice_blocks, (int64_t)chain_grid,
-                                 (int64_t)MAX_LDS_BYTES, (int64_t)groups * ((n + 15) / 16 * 16) * 16};
+        const int64_t plan[8] = {ta.tpw, tl.nw, tree_grid, ta.slices, ta.slice_blocks, (int64_t)chain_grid,
+                                 (int64_t)MAX_LDS_BYTES, (int64_t)groups * n16 * 16};
         for (int i = 0; i < 8; ++i) ch.last_plan[i] = plan[i];
     }
     static bool chain_configured = false;
@@ -1098,10 +1206,14 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, at_chains_s
         return hipGetLastError();
     };
     auto trees_kernel = [&]() -> hipError_t {
-        hipEvent_t start, stop;
-        const hipError_t ev = next_events(ch, 0, start, stop);
-        if (ev != hipSuccess) return ev;
-        return launch_trees(ta, Q, e.depth, nw, stream, start, stop);
+        for (const TreeLaunch* t : {eg ? &tg : nullptr, &tl}) {
+            if (!t) continue;
+            hipEvent_t start, stop;
+            hipError_t ev = next_events(ch, 0, start, stop);
+            if (ev != hipSuccess) return ev;
+            if ((ev = launch_trees(t->ta, t->Q, t->depth, t->nw, stream, start, stop)) != hipSuccess) return ev;
+        }
+        return hipSuccess;
     };
 
     int pending = FIN_NONE;
