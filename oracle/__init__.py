@@ -52,6 +52,7 @@ def lib():
         L.or_loop_quantities.argtypes = [vp, u64, vp]
         L.or_features.argtypes = [vp, vp, i64, vp]
         L.or_features_full.argtypes = [vp, vp, i64, vp]
+        L.or_features_onehot.argtypes = [vp, vp, i64, vp]
         L.or_predict.argtypes = [i32, i32, i32, vp, vp, vp, vp, i64, vp, vp]
         L.or_predict_nodes.argtypes = [i32, vp, vp, vp, vp, vp, vp, i32, vp, i64, vp]
         L.or_philox.argtypes = [u64, vp, vp]
@@ -99,6 +100,8 @@ class Space:
         self.n_features = nf.value
         # full Appendix A.2 rows add top-down and bottom-up: 4 + 3 per buffer (3) per loop
         self.n_features_full = self.n_loops * 13
+        # one-hot rows: length, 12 annotation columns, top-down, bottom-up, 3 per buffer
+        self.n_features_onehot = self.n_loops * (3 + 12 + 9)
         self.n_configs = nc.value
 
     def __del__(self):
@@ -149,6 +152,18 @@ class Space:
         c = np.ascontiguousarray(cfgs, dtype=np.uint64)
         out = np.zeros((len(c), self.n_features_full), dtype=np.int32)
         _check(lib().or_features_full(self._h, _p(c), len(c), _p(out)), "features_full")
+        return out
+
+    ANNOTATION_KINDS = 12
+
+    def features_onehot(self, cfgs) -> np.ndarray:
+        """Appendix A.2 rows with a one-hot annotation: per loop
+        bitlen(length), 12 one-hot annotation columns (ids 0..11),
+        bitlen(top-down), bitlen(bottom-up), then per buffer touch, reuse,
+        stride bitlens."""
+        c = np.ascontiguousarray(cfgs, dtype=np.uint64)
+        out = np.zeros((len(c), self.n_features_onehot), dtype=np.int32)
+        _check(lib().or_features_onehot(self._h, _p(c), len(c), _p(out)), "features_onehot")
         return out
 
     def features(self, cfgs) -> np.ndarray:
@@ -217,7 +232,7 @@ def thresholds(seed: int, chain0: int, n_chains: int, step_base: int, steps: int
 class Chains:
     """Persistent annealing chain state (Section 3.3)."""
 
-    MAX_KNOBS = 8
+    MAX_KNOBS = 12
 
     def __init__(self, spaces, offsets, seed: int, chain0: int, topk: int):
         self.spaces = list(spaces)

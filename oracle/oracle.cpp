@@ -81,13 +81,21 @@ int32_t bitlen(int64_t x) {
 // Schedule templates (Section 2: multi-level tiling of every loop axis, loop
 // ordering, thread binding and unrolling annotations).
 // ---------------------------------------------------------------------------
-enum { TMPL_GEMM = 0, TMPL_CONV2D = 1 };
+// Templates 2 and 3 are 0 and 1 with two annotation knobs more (the
+// vectorization annotation of Section 2's search space, and virtual-thread
+// binding): vectorize in {0, 1} and vthread in {0, 1}, in that order after
+// unroll_explicit.
+enum { TMPL_GEMM = 0, TMPL_CONV2D = 1, TMPL_GEMM_VT = 2, TMPL_CONV2D_VT = 3 };
 
 // Annotation ids of the loop-context "annotation" column (Appendix A.2).
+// The one-hot form of the column has one column per id, ANN_KINDS in all
+// (parallel is a CPU annotation that these GPU templates never produce).
 enum {
     ANN_SERIAL = 0, ANN_UNROLL = 1, ANN_UNROLL_EXPLICIT = 2,
     ANN_BLOCK_X = 3, ANN_BLOCK_Y = 4, ANN_BLOCK_Z = 5,
-    ANN_THREAD_X = 6, ANN_THREAD_Y = 7, ANN_THREAD_Z = 8
+    ANN_THREAD_X = 6, ANN_THREAD_Y = 7, ANN_THREAD_Z = 8,
+    ANN_VTHREAD = 9, ANN_VECTORIZE = 10, ANN_PARALLEL = 11,
+    ANN_KINDS = 12
 };
 
 // One term coef * axis inside one dimension of a buffer's index expression.
@@ -119,6 +127,9 @@ struct Space {
     std::vector<Knob> knobs;
     int knob_auto_unroll;               // index of the auto_unroll_max_step knob
     int knob_unroll_explicit;           // index of the unroll_explicit knob
+    int knob_vectorize = -1;            // index of the vectorize knob (templates 2, 3), else -1
+    int knob_vthread = -1;              // index of the vthread knob (templates 2, 3), else -1
+    std::vector<int> spatial_axes;      // axes whose third tiling level a vthread knob binds
     std::vector<int> axis_knob;         // split knob of each axis
     std::vector<Loop> loops;            // outer to inner
     std::vector<Buffer> buffers;
@@ -181,6 +192,7 @@ bool build_gemm(Space& sp, const int64_t* shape, int nshape) {
     sp.axis_knob = {0, 1, 2};
     sp.knob_auto_unroll = 3;
     sp.knob_unroll_explicit = 4;
+    sp.spatial_axes = {I, J};
     auto L = [](int axis, int level, int binding) { Loop l; l.comps = {{axis, level}}; l.binding = binding; return l; };
     sp.loops = {L(I, 0, ANN_BLOCK_Y), L(J, 0, ANN_BLOCK_X), L(I, 1, ANN_THREAD_Y), L(J, 1, ANN_THREAD_X),
                 L(KK, 0, ANN_SERIAL), L(I, 2, ANN_SERIAL), L(J, 2, ANN_SERIAL), L(KK, 1, ANN_SERIAL),
@@ -222,6 +234,7 @@ bool build_conv(Space& sp, const int64_t* shape, int nshape) {
     sp.axis_knob = {0, 1, 2, 3, 4, 5};
     sp.knob_auto_unroll = 6;
     sp.knob_unroll_explicit = 7;
+    sp.spatial_axes = {OC, OHX, OWX};
     auto L = [](int axis, int level, int binding) { Loop l; l.comps = {{axis, level}}; l.binding = binding; return l; };
     auto R = [](int level) { Loop l; l.comps = {{RY, level}, {RX, level}}; l.binding = ANN_SERIAL; return l; };
     sp.loops = {L(OC, 0, ANN_BLOCK_Z), L(OHX, 0, ANN_BLOCK_Y), L(OWX, 0, ANN_BLOCK_X),
@@ -235,6 +248,19 @@ bool build_conv(Space& sp, const int64_t* shape, int nshape) {
     Buffer out{"output", {Dim{OH * OW, {{OC, 1}}}, Dim{OW, {{OHX, 1}}}, Dim{1, {{OWX, 1}}}}};
     sp.buffers = {data, kern, out};
     return true;
+}
+
+// The annotation knobs of templates 2 and 3 (reading of Section 2's
+// "annotations such as unrolling and vectorization"): vectorize = 1 marks
+// the innermost loop vectorized; vthread = 1 binds the third tiling level of
+// every spatial axis (GEMM i3 j3, conv2d oc3 oh3 ow3) to virtual threads.
+// Either annotation takes the place of the unroll rule on its loops; the
+// nest and every other feature are unchanged.
+void add_annotation_knobs(Space& sp) {
+    sp.knob_vectorize = (int)sp.knobs.size();
+    sp.knobs.push_back(value_knob({0, 1}));
+    sp.knob_vthread = (int)sp.knobs.size();
+    sp.knobs.push_back(value_knob({0, 1}));
 }
 
 // Knob values of configuration index cfg: mixed radix, knob 0 most significant.
@@ -279,6 +305,8 @@ void loop_quantities(const Space& sp, const std::vector<int64_t>& v, std::vector
     }
     int64_t auto_unroll = sp.knobs[sp.knob_auto_unroll].values[v[sp.knob_auto_unroll]];
     int64_t explicit_unroll = sp.knobs[sp.knob_unroll_explicit].values[v[sp.knob_unroll_explicit]];
+    const bool vectorize = sp.knob_vectorize >= 0 && sp.knobs[sp.knob_vectorize].values[v[sp.knob_vectorize]] == 1;
+    const bool vthread = sp.knob_vthread >= 0 && sp.knobs[sp.knob_vthread].values[v[sp.knob_vthread]] == 1;
 
     int n_loops = (int)sp.loops.size();
     int n_buf = (int)sp.buffers.size();
@@ -300,7 +328,12 @@ void loop_quantities(const Space& sp, const std::vector<int64_t>& v, std::vector
             for (const LoopComp& c : sp.loops[r].comps) range[c.axis] *= factor[c.axis][c.level];
         // annotation: thread binding, else unrolled when the whole sub-nest has
         // at most auto_unroll_max_step iterations, else serial
+        bool third_spatial = false;
+        for (int a : sp.spatial_axes)
+            if (lp.comps.size() == 1 && lp.comps[0].axis == a && lp.comps[0].level == 2) third_spatial = true;
         if (lp.binding != ANN_SERIAL) o.ann = lp.binding;
+        else if (vthread && third_spatial) o.ann = ANN_VTHREAD;
+        else if (vectorize && p == n_loops - 1) o.ann = ANN_VECTORIZE;
         else if (auto_unroll > 0 && o.bottom_up <= auto_unroll) o.ann = explicit_unroll ? ANN_UNROLL_EXPLICIT : ANN_UNROLL;
         else o.ann = ANN_SERIAL;
 
@@ -404,6 +437,36 @@ void features_full_of(const Space& sp, uint64_t cfg, int32_t* row) {
 }
 
 int n_features_full_of(const Space& sp) { return (int)sp.loops.size() * (4 + 3 * (int)sp.buffers.size()); }
+
+// The loop-context table of Appendix A.2 with its annotation column in
+// one-hot form: per loop, outer to inner: bitlen(length), ANN_KINDS columns
+// holding 1 for the loop's annotation and 0 for every other, bitlen(top-down),
+// bitlen(bottom-up), then for each buffer bitlen(touch count), bitlen(reuse
+// ratio), bitlen(stride).
+void features_onehot_of(const Space& sp, uint64_t cfg, int32_t* row) {
+    std::vector<int64_t> v;
+    decode(sp, cfg, v);
+    std::vector<LoopQ> q;
+    loop_quantities(sp, v, q);
+    int64_t top_down = 1;
+    int k = 0;
+    for (const LoopQ& o : q) {
+        row[k++] = bitlen(o.ext);
+        for (int a = 0; a < ANN_KINDS; ++a) row[k++] = (o.ann == a) ? 1 : 0;
+        row[k++] = bitlen(top_down);
+        row[k++] = bitlen(o.bottom_up);
+        for (size_t b = 0; b < o.touched.size(); ++b) {
+            row[k++] = bitlen(o.touched[b]);
+            row[k++] = bitlen(o.reuse[b]);
+            row[k++] = bitlen(o.stride[b]);
+        }
+        top_down *= o.ext;
+    }
+}
+
+int n_features_onehot_of(const Space& sp) {
+    return (int)sp.loops.size() * (3 + ANN_KINDS + 3 * (int)sp.buffers.size());
+}
 
 // ---------------------------------------------------------------------------
 // Context relation features (Section 4; Appendix A.2 "Relation Feature").
@@ -637,9 +700,10 @@ int or_space_create(int tmpl, const int64_t* shape, int nshape, void** out) {
     Space* sp = new Space();
     sp->tmpl = tmpl;
     sp->shape.assign(shape, shape + nshape);
-    bool ok = (tmpl == TMPL_GEMM) ? build_gemm(*sp, shape, nshape)
-            : (tmpl == TMPL_CONV2D) ? build_conv(*sp, shape, nshape) : false;
+    bool ok = (tmpl == TMPL_GEMM || tmpl == TMPL_GEMM_VT) ? build_gemm(*sp, shape, nshape)
+            : (tmpl == TMPL_CONV2D || tmpl == TMPL_CONV2D_VT) ? build_conv(*sp, shape, nshape) : false;
     if (!ok) { delete sp; return -1; }
+    if (tmpl == TMPL_GEMM_VT || tmpl == TMPL_CONV2D_VT) add_annotation_knobs(*sp);
     sp->n_configs = 1;
     for (const Knob& kb : sp->knobs) sp->n_configs *= (uint64_t)kb.size();
     *out = sp;
@@ -715,6 +779,16 @@ int or_features(void* h, const uint64_t* cfgs, int64_t n, int32_t* feats) {
     for (int64_t i = 0; i < n; ++i) {
         if (cfgs[i] >= sp.n_configs) return -5;
         features_of(sp, cfgs[i], feats + i * F);
+    }
+    return 0;
+}
+
+int or_features_onehot(void* h, const uint64_t* cfgs, int64_t n, int32_t* feats) {
+    const Space& sp = *(Space*)h;
+    int F = n_features_onehot_of(sp);
+    for (int64_t i = 0; i < n; ++i) {
+        if (cfgs[i] >= sp.n_configs) return -5;
+        features_onehot_of(sp, cfgs[i], feats + i * F);
     }
     return 0;
 }
