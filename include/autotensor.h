@@ -63,10 +63,25 @@ typedef enum {
  *    auto_unroll_max_step; unroll_explicit.  Nest oc1 oh1 ow1 oc2 oh2 ow2
  *    rc1 r1 oc3 oh3 ow3 rc2 r2 oc4 oh4 ow4 (r_l fuses ry_l, rx_l; first band
  *    -> blockIdx.z/y/x, second -> threadIdx.z/y/x): 16 loops, 176 features.
+ *  AT_TMPL_GEMM_VT, AT_TMPL_CONV2D_NCHW_VT: the same templates with two
+ *    annotation knobs more (Section 2's search space includes annotations
+ *    such as unrolling and vectorization), after unroll_explicit:
+ *    vectorize in {0, 1} marks the innermost loop (GEMM j4, conv2d ow4)
+ *    vectorized, annotation id 10; vthread in {0, 1} binds the third tiling
+ *    level of every spatial axis (GEMM i3 j3, conv2d oc3 oh3 ow3) to virtual
+ *    threads, annotation id 9.  Either takes the place of the unroll rule on
+ *    its loops; nest, buffers and every other feature are unchanged.  7 and
+ *    10 knobs, four times as many configurations (index = base index * 4 +
+ *    vectorize * 2 + vthread).
  * Ordered splits are enumerated lexicographically (outer level first); a
  * configuration index is the mixed-radix number of the knob values with
  * knob 0 most significant. */
-typedef enum { AT_TMPL_GEMM = 0, AT_TMPL_CONV2D_NCHW = 1 } at_template;
+typedef enum {
+    AT_TMPL_GEMM = 0,
+    AT_TMPL_CONV2D_NCHW = 1,
+    AT_TMPL_GEMM_VT = 2,
+    AT_TMPL_CONV2D_NCHW_VT = 3
+} at_template;
 
 /* One entry of a chain's best list, or of an annealing trace. */
 typedef struct {
@@ -107,7 +122,8 @@ void at_space_destroy(at_space_t space);
  * then for each buffer bitlen(touch count), bitlen(reuse ratio),
  * bitlen(stride).  bitlen(x) = 0 for x = 0, else floor(log2 x) + 1.
  * Annotation ids: 0 serial, 1 unrolled, 2 unrolled explicitly, 3/4/5
- * blockIdx.x/y/z, 6/7/8 threadIdx.x/y/z; a serial loop is unrolled when
+ * blockIdx.x/y/z, 6/7/8 threadIdx.x/y/z, 9 vthread, 10 vectorized (the
+ * annotated templates; 11, parallel, never occurs); a serial loop is unrolled when
  * auto_unroll_max_step > 0 and its sub-nest has at most that many
  * iterations.  Touch counts are distinct elements of the (padded) buffer
  * touched by the sub-nest rooted at the loop; reuse ratio is
@@ -132,6 +148,18 @@ at_status at_extract_features(at_space_t space, const uint64_t* cfgs, int64_t n,
  * at_extract_features.  n == 0 is a no-op. */
 at_status at_extract_features_full(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
                                    at_stream_t stream);
+
+/* The loop-context table of Appendix A.2 with its annotation column one-hot,
+ * as the paper lists it: per loop (outer to inner) bitlen(length), 12
+ * annotation columns (column h is 1 when the loop's annotation id is h, ids
+ * as for at_extract_features, 0 otherwise), bitlen(top-down),
+ * bitlen(bottom-up), then for each buffer bitlen(touch count), bitlen(reuse
+ * ratio), bitlen(stride): 24 int32 per loop, n_loops * 24 per row (GEMM 240,
+ * conv2d 384).  cfgs: device [n] uint64; feats: device [n][n_loops * 24]
+ * int32.  A single space only.  Out-of-range indices fill their row with -1
+ * and are counted as for at_extract_features.  n == 0 is a no-op. */
+at_status at_extract_features_onehot(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                     at_stream_t stream);
 
 /* Number of out-of-range configuration indices seen by at_extract_features
  * since the last call (synchronises the device; resets the counter). */

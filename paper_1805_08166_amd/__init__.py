@@ -21,6 +21,8 @@ LIB_PATH = os.path.join(_HERE, "libautotensor.so")
 
 AT_TMPL_GEMM = 0
 AT_TMPL_CONV2D_NCHW = 1
+AT_TMPL_GEMM_VT = 2
+AT_TMPL_CONV2D_NCHW_VT = 3
 
 STATUS = {0: "AT_OK", -1: "AT_E_INVALID", -2: "AT_E_UNSUPPORTED", -3: "AT_E_OOM", -4: "AT_E_HIP",
           -5: "AT_E_RANGE", -6: "AT_E_MISMATCH"}
@@ -30,7 +32,7 @@ ENTRY_DTYPE = np.dtype([("cfg", "<u8"), ("score", "<f4"), ("flag", "<u4")])
 
 EXPORTED = [
     "at_space_create", "at_space_info", "at_spaceset_create", "at_space_destroy",
-    "at_extract_features", "at_extract_features_full", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
+    "at_extract_features", "at_extract_features_full", "at_extract_features_onehot", "at_extract_relation_features", "at_space_errors", "at_ensemble_create", "at_ensemble_destroy",
     "at_trees_depth", "at_trees_pad", "at_ensemble_import",
     "at_gbt_predict", "at_gbt_predict_global_local", "at_chains_create", "at_chains_destroy", "at_chains_step",
     "at_sa_thresholds", "at_sa_run", "at_sa_run_traced", "at_sa_run_global_local", "at_chains_export", "at_sa_set_profiling",
@@ -66,6 +68,7 @@ def _load():
         "at_extract_features": [vp, vp, i64, vp, vp],
         "at_extract_relation_features": [vp, vp, i64, vp, vp],
         "at_extract_features_full": [vp, vp, i64, vp, vp],
+        "at_extract_features_onehot": [vp, vp, i64, vp, vp],
         "at_space_errors": [vp, vp],
         "at_ensemble_create": [i32, i32, i32, vp, vp, vp, vp],
         "at_ensemble_destroy": [vp],
@@ -221,6 +224,22 @@ def at_extract_features_full(space: Space, cfgs, feats, stream=None):
     if feats.shape != (n, 13 * space.n_loops):
         raise ValueError("feats must be [n, 13 * n_loops]")
     _check("at_extract_features_full", _lib.at_extract_features_full(
+        space.h, _dev(cfgs, torch.int64, "cfgs"), n, _dev(feats, torch.int32, "feats"), _stream(stream)))
+
+
+ONEHOT_PER_LOOP = 24
+
+
+def at_extract_features_onehot(space: Space, cfgs, feats, stream=None):
+    """Appendix A.2 rows with a one-hot annotation (24 per loop: length,
+    12 annotation columns, top-down, bottom-up, touch/reuse/stride per
+    buffer).  cfgs: device uint64 [n] (torch.int64 storage); feats: device
+    int32 [n, 24 * n_loops]."""
+    import torch
+    n = cfgs.numel()
+    if feats.shape != (n, ONEHOT_PER_LOOP * space.n_loops):
+        raise ValueError("feats must be [n, 24 * n_loops]")
+    _check("at_extract_features_onehot", _lib.at_extract_features_onehot(
         space.h, _dev(cfgs, torch.int64, "cfgs"), n, _dev(feats, torch.int32, "feats"), _stream(stream)))
 
 

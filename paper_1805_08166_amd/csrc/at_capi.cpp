@@ -110,7 +110,8 @@ at_status at_space_create(int tmpl, const int64_t* shape, int nshape, at_space_t
     at_space_s* sp = new (std::nothrow) at_space_s();
     if (!sp) return fail(AT_E_OOM, "at_space_create: host allocation");
     sp->device = current_device();
-    sp->tmpl = tmpl;
+    sp->tmpl = d.tmpl;
+    sp->api_tmpl = tmpl;
     sp->n_spaces = 1;
     sp->descs.push_back(d);
     sp->chain_offsets = {0, 0};
@@ -150,12 +151,13 @@ at_status at_spaceset_create(const at_space_t* spaces, int n, const int64_t* cha
     for (int i = 0; i < n; ++i) {
         if (!spaces[i] || spaces[i]->n_spaces != 1) return fail(AT_E_INVALID, "at_spaceset_create: member must be a single space");
         if (chain_offsets[i + 1] < chain_offsets[i]) return fail(AT_E_INVALID, "at_spaceset_create: offsets must ascend");
-        if (spaces[i]->tmpl != spaces[0]->tmpl) return fail(AT_E_MISMATCH, "at_spaceset_create: templates differ");
+        if (spaces[i]->api_tmpl != spaces[0]->api_tmpl) return fail(AT_E_MISMATCH, "at_spaceset_create: templates differ");
     }
     at_space_s* sp = new (std::nothrow) at_space_s();
     if (!sp) return fail(AT_E_OOM, "at_spaceset_create: host allocation");
     sp->device = current_device();
     sp->tmpl = spaces[0]->tmpl;
+    sp->api_tmpl = spaces[0]->api_tmpl;
     sp->n_spaces = n;
     std::vector<uint64_t> all;
     for (int i = 0; i < n; ++i) {
@@ -211,6 +213,19 @@ at_status at_extract_features_full(at_space_t space, const uint64_t* cfgs, int64
     if (n > ((int64_t)1 << 36)) return fail(AT_E_UNSUPPORTED, "at_extract_features_full: n too large for one call");
     DeviceGuard g(space->device);
     return finish_launch(launch_extract_full(*space, cfgs, n, feats, (hipStream_t)stream), "at_extract_features_full");
+}
+
+at_status at_extract_features_onehot(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                     at_stream_t stream) {
+    if (!space) return fail(AT_E_INVALID, "at_extract_features_onehot: NULL space");
+    if (space->n_spaces != 1) return fail(AT_E_INVALID, "at_extract_features_onehot: takes a single space, not a set");
+    if (n < 0) return fail(AT_E_INVALID, "at_extract_features_onehot: n < 0");
+    if (n == 0) return AT_OK;
+    if (!cfgs || !feats) return fail(AT_E_INVALID, "at_extract_features_onehot: NULL buffer");
+    if (n > ((int64_t)1 << 40)) return fail(AT_E_UNSUPPORTED, "at_extract_features_onehot: n too large");
+    DeviceGuard g(space->device);
+    return finish_launch(launch_extract_onehot(*space, cfgs, n, feats, (hipStream_t)stream),
+                         "at_extract_features_onehot");
 }
 
 at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, int64_t n, int32_t* feats,
@@ -564,7 +579,7 @@ at_status at_chains_create(at_space_t space, int64_t chain0, int64_t n_chains, i
     ch->topk = topk;
     ch->seed = seed;
     ch->n_spaces = space->n_spaces;
-    ch->tmpl = space->tmpl;
+    ch->tmpl = space->api_tmpl;
     at_status st;
     if ((st = alloc_zero(ch->d_knobs, (size_t)n_chains * MAX_KNOBS * 2)) != AT_OK ||
         (st = alloc_zero(ch->d_score, (size_t)n_chains * 4)) != AT_OK ||
@@ -742,7 +757,7 @@ static at_status sa_run_impl(at_space_t space, at_ensemble_t ens, at_ensemble_t 
     const std::string f(fn);
     if (!space || !ens || !chains) return fail(AT_E_INVALID, f + ": NULL handle");
     if (steps < 0) return fail(AT_E_INVALID, f + ": steps < 0");
-    if (space->n_spaces != chains->n_spaces || space->tmpl != chains->tmpl)
+    if (space->n_spaces != chains->n_spaces || space->api_tmpl != chains->tmpl)
         return fail(AT_E_INVALID, f + ": chains were created for another space");
     if (space->n_spaces > 1 && chains->n_chains != space->chain_offsets.back())
         return fail(AT_E_INVALID, f + ": chain count does not match the space set");

@@ -20,20 +20,21 @@ __device__ __forceinline__ int space_of(const int64_t* offsets, int n_spaces, in
     return w;
 }
 
+// A chain's knob vector: MAX_KNOBS u16 (24 bytes, three 8-byte words).
+static_assert(MAX_KNOBS == 12, "knob vectors move as three 8-byte words");
 __device__ __forceinline__ void load_knobs(const uint16_t* p, int64_t c, uint32_t (&kv)[MAX_KNOBS]) {
-    const uint4 w = reinterpret_cast<const uint4*>(p)[c];
-    const uint32_t pw[4] = {w.x, w.y, w.z, w.w};
+    const uint2* w = reinterpret_cast<const uint2*>(p) + 3 * c;
+    const uint2 a = w[0], b = w[1], d = w[2];
+    const uint32_t pw[6] = {a.x, a.y, b.x, b.y, d.x, d.y};
 #pragma unroll
     for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = (pw[j >> 1] >> (16 * (j & 1))) & 0xffffu;
 }
 
 __device__ __forceinline__ void store_knobs(uint16_t* p, int64_t c, const uint32_t (&kv)[MAX_KNOBS]) {
-    uint4 w;
-    w.x = kv[0] | (kv[1] << 16);
-    w.y = kv[2] | (kv[3] << 16);
-    w.z = kv[4] | (kv[5] << 16);
-    w.w = kv[6] | (kv[7] << 16);
-    reinterpret_cast<uint4*>(p)[c] = w;
+    uint2* w = reinterpret_cast<uint2*>(p) + 3 * c;
+    w[0] = make_uint2(kv[0] | (kv[1] << 16), kv[2] | (kv[3] << 16));
+    w[1] = make_uint2(kv[4] | (kv[5] << 16), kv[6] | (kv[7] << 16));
+    w[2] = make_uint2(kv[8] | (kv[9] << 16), kv[10] | (kv[11] << 16));
 }
 
 __device__ __forceinline__ bool precedes(float sa, uint64_t ca, float sb, uint64_t cb) {

@@ -32,9 +32,14 @@ __device__ __forceinline__ uint32_t distinct_affine(uint32_t A, uint32_t B, uint
 // Loop nests of the two templates, outer to inner.  Axis ids: GEMM i=0 j=1
 // k=2; conv oc=0 oh=1 ow=2 rc=3 ry=4 rx=5.  FUSED marks the kernel-window
 // loop r_l = (ry_l outer, rx_l inner).  Binding ids follow the annotation
-// column: 3/4/5 blockIdx.x/y/z, 6/7/8 threadIdx.x/y/z, 0 serial.
+// column: 3/4/5 blockIdx.x/y/z, 6/7/8 threadIdx.x/y/z, 0 serial.  The
+// spatial axes (the first SPATIAL) are those whose third tiling level a
+// vthread knob binds to virtual threads (id 9); a vectorize knob marks the
+// innermost loop vectorized (id 10).
 // --------------------------------------------------------------------------
 constexpr int FUSED = -1;
+constexpr uint32_t ANN_VTHREAD = 9u, ANN_VECTORIZE = 10u;
+constexpr int ANN_KINDS = 12;   // one-hot annotation columns (ids 0 .. 11)
 
 template <int TMPL> struct Nest;
 
@@ -44,6 +49,7 @@ template <> struct Nest<AT_TMPL_GEMM> {
     static constexpr int axis[L] = {0, 1, 0, 1, 2, 0, 1, 2, 0, 1};
     static constexpr int level[L] = {0, 0, 1, 1, 0, 2, 2, 1, 3, 3};
     static constexpr int bind[L] = {4, 3, 7, 6, 0, 0, 0, 0, 0, 0};
+    static constexpr int SPATIAL = 2;
     // touch counts from the per-axis ranges of a sub-nest
     __device__ static void touched(const uint32_t (&r)[6], uint32_t, uint32_t (&t)[3]) {
         t[0] = r[2] * r[0];   // A[k][i]
@@ -58,6 +64,7 @@ template <> struct Nest<AT_TMPL_CONV2D_NCHW> {
     static constexpr int axis[L] = {0, 1, 2, 0, 1, 2, 3, FUSED, 0, 1, 2, 3, FUSED, 0, 1, 2};
     static constexpr int level[L] = {0, 0, 0, 1, 1, 1, 0, 0, 2, 2, 2, 1, 1, 3, 3, 3};
     static constexpr int bind[L] = {5, 4, 3, 8, 7, 6, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    static constexpr int SPATIAL = 3;
     __device__ static void touched(const uint32_t (&r)[6], uint32_t S, uint32_t (&t)[3]) {
         // data_pad[rc][oh*S+ry][ow*S+rx], unclipped padded coordinates
         t[0] = r[3] * distinct_affine(r[1], r[4], S) * distinct_affine(r[2], r[5], S);
@@ -65,6 +72,37 @@ template <> struct Nest<AT_TMPL_CONV2D_NCHW> {
         t[2] = r[0] * r[1] * r[2];          // output[oc][oh][ow]
     }
 };
+
+// Annotation id of loop p: its thread or block binding, else virtual
+// threads (vth set, third level of a spatial axis), else vectorized (vec set,
+// innermost loop), else unrolled (id unroll_id) when auto_unroll_max_step is
+// on and its sub-nest has at most that many iterations, else serial.
+template <int TMPL>
+__device__ __forceinline__ uint32_t annotation_of(int p, uint32_t bottom_up, uint32_t unroll_max, uint32_t unroll_id,
+                                                  uint32_t vec, uint32_t vth) {
+    using N = Nest<TMPL>;
+    if (N::bind[p]) return (uint32_t)N::bind[p];
+    if (vth && N::level[p] == 2 && N::axis[p] >= 0 && N::axis[p] < N::SPATIAL) return ANN_VTHREAD;
+    if (vec && p == N::L - 1) return ANN_VECTORIZE;
+    return (unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u;
+}
+
+// The annotation knobs of configuration kv: auto_unroll_max_step,
+// unroll_explicit (id 1 or 2 for unrolled loops) and, for the annotated
+// templates, vectorize and vthread.
+struct AnnKnobs {
+    uint32_t unroll_max, unroll_id, vec, vth;
+};
+template <int TMPL>
+__device__ __forceinline__ AnnKnobs ann_knobs_of(const SpaceDesc& sd, const uint32_t (&kv)[MAX_KNOBS]) {
+    constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
+    AnnKnobs k;
+    k.unroll_max = kv[A] == 0u ? 0u : (kv[A] == 1u ? 512u : 1500u);
+    k.unroll_id = 1u + kv[A + 1];
+    k.vec = sd.ann_knobs ? kv[A + 2] : 0u;
+    k.vth = sd.ann_knobs ? kv[A + 3] : 0u;
+    return k;
+}
 
 // Factors of the chosen split of axis a: four 16-bit fields, outer level first.
 __device__ __forceinline__ void unpack_split(uint64_t w, uint32_t (&f)[4]) {
@@ -82,18 +120,21 @@ __device__ __forceinline__ void unpack_split(uint64_t w, uint32_t (&f)[4]) {
 // PER = 13 gives the full rows of Appendix A.2: bitlen(top-down) and
 // bitlen(bottom-up) follow the annotation.  Top-down is the nest's iteration
 // count (the product of every factor, below 2^31 for any space) divided by
-// bottom-up, the quotient's bitlen taken without a division.
+// bottom-up, the quotient's bitlen taken without a division.  PER = 24 gives
+// the full rows with the annotation one-hot: ANN_KINDS columns, 1 at the
+// loop's annotation id, 0 elsewhere.
 template <int TMPL, int PER = 11, class Emit>
-__device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4],
-                                              uint32_t unroll_max, uint32_t unroll_id, Emit&& emit) {
-    static_assert(PER == 11 || PER == 13, "loop-context rows or full rows");
+__device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4], const AnnKnobs& ak,
+                                              Emit&& emit) {
+    static_assert(PER == 11 || PER == 13 || PER == 24, "loop-context rows, full rows or one-hot rows");
     using N = Nest<TMPL>;
-    constexpr int B0 = PER == 13 ? 4 : 2;   // first buffer column
+    constexpr int HOT = PER == 24 ? ANN_KINDS : 1;          // annotation columns
+    constexpr int B0 = 1 + HOT + (PER == 11 ? 0 : 2);       // first buffer column
     uint32_t range[6] = {1u, 1u, 1u, 1u, 1u, 1u};
     uint32_t bottom_up = 1u;
     const uint32_t S = (uint32_t)sd.stride;
     uint32_t total = 1u;
-    if constexpr (PER == 13) {
+    if constexpr (PER != 11) {
 #pragma unroll
         for (int a = 0; a < 6; ++a)
 #pragma unroll
@@ -122,13 +163,17 @@ __device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_
         bottom_up *= ext;
         uint32_t t[3];
         N::touched(range, S, t);
-        uint32_t ann = N::bind[p] ? (uint32_t)N::bind[p]
-                                  : ((unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u);
+        const uint32_t ann = annotation_of<TMPL>(p, bottom_up, ak.unroll_max, ak.unroll_id, ak.vec, ak.vth);
         emit(p * PER + 0, bitlen(ext));
-        emit(p * PER + 1, ann);
-        if constexpr (PER == 13) {
-            emit(p * PER + 2, bitlen_quot(total, bottom_up));
-            emit(p * PER + 3, bitlen(bottom_up));
+        if constexpr (PER == 24) {
+#pragma unroll
+            for (int h = 0; h < ANN_KINDS; ++h) emit(p * PER + 1 + h, ann == (uint32_t)h ? 1u : 0u);
+        } else {
+            emit(p * PER + 1, ann);
+        }
+        if constexpr (PER != 11) {
+            emit(p * PER + 1 + HOT, bitlen_quot(total, bottom_up));
+            emit(p * PER + 2 + HOT, bitlen(bottom_up));
         }
 #pragma unroll
         for (int b = 0; b < 3; ++b) {
@@ -147,12 +192,11 @@ __device__ __forceinline__ void nest_features(const SpaceDesc& sd, const uint32_
 // given, receives bitlen(top-down) of loop p: the product of the lengths of
 // the loops outside it, i.e. the nest's iteration count over bottom-up.
 template <int TMPL>
-__device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4], uint32_t unroll_max,
-                                              uint32_t unroll_id, int p, uint32_t (&out)[11],
-                                              uint32_t* td = nullptr) {
+__device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_t (&fac)[6][4], const AnnKnobs& ak,
+                                              int p, uint32_t (&out)[11], uint32_t* td = nullptr) {
     using N = Nest<TMPL>;
     uint32_t range[6] = {1u, 1u, 1u, 1u, 1u, 1u};
-    uint32_t bottom_up = 1u, ext = 1u, bind = 0u;
+    uint32_t bottom_up = 1u, ext = 1u;
     uint32_t strd[3] = {0u, 0u, 0u};
 #pragma unroll
     for (int q = N::L - 1; q >= 0; --q) {
@@ -177,7 +221,6 @@ __device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_
         bottom_up *= in ? e : 1u;
         if (at) {
             ext = e;
-            bind = (uint32_t)N::bind[q];
 #pragma unroll
             for (int b = 0; b < 3; ++b) strd[b] = sq[b];
         }
@@ -193,7 +236,7 @@ __device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_
         *td = bitlen_quot(total, bottom_up);
     }
     out[0] = bitlen(ext);
-    out[1] = bind ? bind : ((unroll_max > 0u && bottom_up <= unroll_max) ? unroll_id : 0u);
+    out[1] = annotation_of<TMPL>(p, bottom_up, ak.unroll_max, ak.unroll_id, ak.vec, ak.vth);
 #pragma unroll
     for (int b = 0; b < 3; ++b) {
         out[2 + 3 * b] = bitlen(t[b]);
@@ -202,7 +245,6 @@ __device__ __forceinline__ void loop_features(const SpaceDesc& sd, const uint32_
     }
 }
 
-__device__ __forceinline__ uint32_t unroll_max_of(uint32_t v) { return v == 0u ? 0u : (v == 1u ? 512u : 1500u); }
 
 // Factors of every axis for knob values kv (split knob a = axis a).
 template <int TMPL>

@@ -15,7 +15,10 @@
 
 namespace at {
 
-constexpr int MAX_KNOBS = 8;
+// Knobs of a space: splits (one per axis), auto_unroll_max_step,
+// unroll_explicit, and for the annotated templates vectorize and vthread
+// (conv2d: 6 + 2 + 2).  Chains keep their knob vectors as 12 u16 (24 bytes).
+constexpr int MAX_KNOBS = 12;
 constexpr int MAX_AXES = 6;
 constexpr int N_BUFFERS = 3;
 // Lanes of one feature tile in LDS.  A tile holds the u8 features of 256
@@ -45,7 +48,7 @@ struct SpaceDesc {
                                          // factors[split_off[a]] (u64 each)
     int32_t coef[N_BUFFERS][MAX_AXES];   // weight of axis a in buffer b's flat index
     int32_t stride;                      // conv stride S (1 for GEMM)
-    int32_t pad_;
+    int32_t ann_knobs;                   // 1: knobs n_axes + 2, n_axes + 3 are vectorize and vthread
 };
 
 // Packed ensemble.  Tree t occupies words [t*W, (t+1)*W) with W = 2^(d+1):
@@ -157,7 +160,8 @@ struct DeviceBuf {
 
 struct at_space_s {
     int device = 0;
-    int tmpl = 0;
+    int tmpl = 0;                           // template of the loop nest (AT_TMPL_GEMM or AT_TMPL_CONV2D_NCHW)
+    int api_tmpl = 0;                       // template id the space was created with (0 .. 3)
     int n_spaces = 1;                       // > 1 for a space set
     std::vector<at::SpaceDesc> descs;       // host copies
     std::vector<int64_t> chain_offsets;     // [n_spaces + 1] (sets only)
@@ -230,6 +234,8 @@ at_status build_space(int tmpl, const int64_t* shape, int nshape, SpaceDesc& des
 // Kernel launchers (at_kernels.hip).
 hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                           hipStream_t stream);
+hipError_t launch_extract_onehot(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                 hipStream_t stream);
 hipError_t launch_extract_full(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                                hipStream_t stream);
 hipError_t launch_relation(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,

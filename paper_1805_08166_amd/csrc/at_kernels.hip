@@ -23,8 +23,8 @@ using namespace dev;
 // consecutive lanes covering consecutive 16-byte pieces of the block, so the
 // HBM stores are fully coalesced.
 // ==========================================================================
-// PER columns per loop: 11 (loop-context rows) or 13 (full Appendix A.2 rows
-// with top-down and bottom-up)
+// PER columns per loop: 11 (loop-context rows), 13 (full Appendix A.2 rows
+// with top-down and bottom-up) or 24 (full rows with a one-hot annotation)
 template <int TMPL, int PER = 11>
 struct RowLayout {
     static constexpr int F = Nest<TMPL>::L * PER;
@@ -65,8 +65,7 @@ __global__ __launch_bounds__(WG) void k_extract(SpaceDesc sd, const uint64_t* __
             }
             uint32_t fac[6][4];
             gather_factors<TMPL>(sd, factors, kv, fac);
-            constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
-            nest_features<TMPL, PER>(sd, fac, unroll_max_of(kv[A]), 1u + kv[A + 1],
+            nest_features<TMPL, PER>(sd, fac, ann_knobs_of<TMPL>(sd, kv),
                                      [&](int f, uint32_t v) { my[f] = (int8_t)v; });
         }
     }
@@ -139,10 +138,9 @@ __global__ __launch_bounds__(WG) void k_relation(SpaceDesc sd, const uint64_t* _
             }
             uint32_t fac[6][4];
             gather_factors<TMPL>(sd, factors, kv, fac);
-            constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
             // per loop: bitlen of the touch count (tc) and of the reuse ratio (ru) per buffer
             uint32_t tc[N::L][3], ru[N::L][3];
-            nest_features<TMPL>(sd, fac, unroll_max_of(kv[A]), 1u + kv[A + 1], [&](int f, uint32_t v) {
+            nest_features<TMPL>(sd, fac, ann_knobs_of<TMPL>(sd, kv), [&](int f, uint32_t v) {
                 const int p = f / 11, c = f - p * 11;
                 if (c >= 2 && (c - 2) % 3 == 0) tc[p][(c - 2) / 3] = v;
                 if (c >= 2 && (c - 2) % 3 == 1) ru[p][(c - 2) / 3] = v;
@@ -354,6 +352,32 @@ hipError_t launch_extract_full(const at_space_s& sp, const uint64_t* cfgs, int64
                            cfgs, n, feats, bad);
     } else {
         hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, false, 13>), dim3(grid), dim3(WG), 0, stream, sd, fac,
+                           cfgs, n, feats, bad);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_extract_onehot(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
+                                 hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const SpaceDesc& sd = sp.descs[0];
+    const unsigned grid = (unsigned)((n + WG - 1) / WG);
+    const uint64_t* fac = static_cast<const uint64_t*>(sp.d_factors.p);
+    auto* bad = static_cast<unsigned long long*>(sp.d_errors.p);
+    const bool aligned = (reinterpret_cast<uintptr_t>(feats) & 15u) == 0;
+    // 240 (GEMM) and 384 (conv2d) features per row, both multiples of 4
+    if (sp.tmpl == AT_TMPL_GEMM) {
+        if (aligned)
+            hipLaunchKernelGGL((k_extract<AT_TMPL_GEMM, true, 24>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs, n,
+                               feats, bad);
+        else
+            hipLaunchKernelGGL((k_extract<AT_TMPL_GEMM, false, 24>), dim3(grid), dim3(WG), 0, stream, sd, fac, cfgs,
+                               n, feats, bad);
+    } else if (aligned) {
+        hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, true, 24>), dim3(grid), dim3(WG), 0, stream, sd, fac,
+                           cfgs, n, feats, bad);
+    } else {
+        hipLaunchKernelGGL((k_extract<AT_TMPL_CONV2D_NCHW, false, 24>), dim3(grid), dim3(WG), 0, stream, sd, fac,
                            cfgs, n, feats, bad);
     }
     return hipGetLastError();

@@ -236,7 +236,6 @@ __device__ __forceinline__ void apply_move(const uint32_t (&base)[MAX_KNOBS], ui
 template <int TMPL, int DEPTH, bool FAST>
 __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
     using N = Nest<TMPL>;
-    constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
     constexpr int Q = (N::F + 3) / 4;
     constexpr int RS = Q * 4 + 4;
     constexpr uint32_t NBB = 4u << (DEPTH - 1);   // node block bytes
@@ -432,7 +431,7 @@ __global__ __launch_bounds__(LOCAL_WG_MAX) void k_local(LocalArgs a) {
             uint32_t fac[6][4];
             gather_factors<TMPL>(sd, facp, nx, fac);
             uint32_t f[11];
-            loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr_, f);
+            loop_features<TMPL>(sd, fac, ann_knobs_of<TMPL>(sd, nx), gr_, f);
 #pragma unroll
             for (int i = 0; i < 11; ++i) dst[gr_ * 11 + i] = (uint8_t)f[i];
         };

@@ -199,7 +199,6 @@ __device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int T,
 template <int TMPL>
 __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     using N = Nest<TMPL>;
-    constexpr int A = (TMPL == AT_TMPL_GEMM) ? 3 : 6;
     constexpr int Q = (N::F + 3) / 4;
     constexpr int RS = Q * 4 + 4;                 // feature row stride (bytes) in LDS
     // dynamic LDS: the fold ring, then the chains' best lists [CPW][topk]
@@ -426,7 +425,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         uint32_t fac[6][4];
         gather_factors<TMPL>(sd, facp, nx, fac);
         uint32_t f[11], td = 0u;
-        loop_features<TMPL>(sd, fac, unroll_max_of(nx[A]), 1u + nx[A + 1], gr, f, a.Fr ? &td : nullptr);
+        loop_features<TMPL>(sd, fac, ann_knobs_of<TMPL>(sd, nx), gr, f, a.Fr ? &td : nullptr);
 #pragma unroll
         for (int i = 0; i < 11; ++i) frow[gj][gr * 11 + i] = (uint8_t)f[i];
         tdrow[gj][gr] = (uint8_t)td;

@@ -63,6 +63,9 @@ at_status build_space(int tmpl, const int64_t* shape, int nshape, SpaceDesc& d,
                       std::vector<uint64_t>& factors) {
     std::memset(&d, 0, sizeof(d));
     factors.clear();
+    // templates 2 and 3 are 0 and 1 with the vectorize and vthread knobs
+    const bool annotated = tmpl == AT_TMPL_GEMM_VT || tmpl == AT_TMPL_CONV2D_NCHW_VT;
+    if (annotated) tmpl -= 2;
     d.tmpl = tmpl;
     if (!shape || nshape < 1) return fail(AT_E_INVALID, "missing shape");
     for (int i = 0; i < nshape; ++i)
@@ -136,6 +139,12 @@ at_status build_space(int tmpl, const int64_t* shape, int nshape, SpaceDesc& d,
     d.knob_size[n_axes] = 3;       // auto_unroll_max_step in {0, 512, 1500}
     d.knob_size[n_axes + 1] = 2;   // unroll_explicit in {0, 1}
     d.n_knobs = n_axes + 2;
+    if (annotated) {
+        d.knob_size[n_axes + 2] = 2;   // vectorize in {0, 1}
+        d.knob_size[n_axes + 3] = 2;   // vthread in {0, 1}
+        d.n_knobs = n_axes + 4;
+        d.ann_knobs = 1;
+    }
     unsigned __int128 total = 1;
     for (int j = 0; j < d.n_knobs; ++j) total *= d.knob_size[j];
     if (total >= ((unsigned __int128)1 << 32))
