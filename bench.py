@@ -285,13 +285,16 @@ def bench_select(P, w, reps=20):
     sp = w.spaces[0]
     out = torch.zeros((64, 4), dtype=torch.int32, device="cuda")
     fn = lambda r: P.at_select_batch(sp, w.best, 128, 61, 1.0, 3, 4000 + r, out)
+    fn_na = lambda r: P.at_select_batch_noalloc(sp, w.best, 128, 61, 1.0, 3, 4000 + r, out)
     for r in range(2):
         fn(r)
+        fn_na(r)
     torch.cuda.synchronize()
     t = float(np.median(time_events(fn, reps)))
+    t_na = float(np.median(time_events(fn_na, reps)))
     n_cand = w.best.numel() // 4
     return dict(workload=f"{w.name}: best lists {w.n} x {w.topk}, pool 128, 61 greedy + 3 random, alpha 1",
-                candidates=n_cand, ms=t * 1e3, candidates_per_s=n_cand / t,
+                candidates=n_cand, ms=t * 1e3, ms_noalloc=t_na * 1e3, candidates_per_s=n_cand / t,
                 read_GBps=n_cand * 16 / t / 1e9)
 
 

@@ -354,7 +354,7 @@ at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, i
  * the space runs out have flag 0.
  * Limits: 0 <= pool <= 1024, n_greedy + n_random <= 2048, a single space
  * (not a set) whose knobs have at most 65536 values each; AT_E_INVALID or
- * AT_E_UNSUPPORTED otherwise.  Enqueued on `stream`; more than 4096
+ * AT_E_UNSUPPORTED otherwise.  Enqueued on `stream`; more than 2048
  * candidates use stream-ordered device scratch (hipMallocAsync) for a
  * partial reduction. */
 at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
@@ -363,13 +363,14 @@ at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand
 /* at_select_batch for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation): the same kernels and the same result, bit for bit, with the
- * partial reduction of more than 4096 candidates kept in a fixed scratch
+ * partial reduction of more than 2048 candidates kept in a fixed scratch
  * array that the library holds on each device until the process ends (two
  * buffers of 131072 entries, 4 MiB; looked up with hipGetSymbolAddress on
  * the first call on a device).  The call allocates and frees nothing.
- * Limit: ceil(n_cand / 4096) * max(pool, 1) <= 131072 (for example up to
- * 524288 candidates at pool 1024, 4194304 at pool 128), AT_E_UNSUPPORTED
- * beyond it; the other arguments and errors are those of at_select_batch.
+ * Limit: ceil(n_cand / 2048) * P <= 131072, P the power of two at or above
+ * max(pool, 1) (for example up to 262144 candidates at pool 1024, 2097152
+ * at pool 128), AT_E_UNSUPPORTED beyond it; the other arguments and errors
+ * are those of at_select_batch.
  * Every call on a device shares that device's scratch: calls that overlap
  * on one device (other streams, other threads) race and must be ordered by
  * the caller.  Nothing in the scratch needs to start at zero: each call

@@ -696,9 +696,9 @@ at_status at_select_batch_noalloc(at_space_t space, const at_entry* cand, int64_
                                      n_random, out, &nothing);
     if (st != AT_OK || nothing) return st;
     if (select_scratch_entries(n_cand, pool) > select_scratch_max_entries())
-        return fail(AT_E_UNSUPPORTED, "at_select_batch_noalloc: ceil(n_cand / 4096) * max(pool, 1) exceeds the "
-                                      "scratch limit of " + std::to_string(select_scratch_max_entries()) +
-                                      " entries");
+        return fail(AT_E_UNSUPPORTED, "at_select_batch_noalloc: ceil(n_cand / 2048) * max(pool, 1) rounded up to "
+                                      "a power of two exceeds the scratch limit of " +
+                                      std::to_string(select_scratch_max_entries()) + " entries");
     DeviceGuard g(space->device);
     at_entry* scratch = nullptr;
     const hipError_t e = select_scratch_ptr(space->device, &scratch);

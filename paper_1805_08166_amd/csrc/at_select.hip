@@ -13,12 +13,28 @@
 // yet, draw i from Philox block (i, 0, 5, 0): u = r1 * 2^32 + r0, the
 // floor(u * remaining / 2^64)-th unselected index.
 //
-// k_pool_partial: each workgroup sorts a slice of up to SORT_N entries in
-// LDS (bitonic), drops repeated indices and writes its `pool` best.
-// k_select (one workgroup): merges the partial results the same way, then
-// one thread per pool candidate runs the greedy rounds (block-wide arg-max
-// of the gains, then every candidate clears the knobs the winner covers),
-// and thread 0 draws the random configurations.
+// k_reduce: each workgroup orders a slice of up to CHUNK candidates in LDS
+// (on 16-byte records that carry the score's order bits, the score itself
+// and the index), drops repeated indices and writes its best `keep`
+// candidates as a run of the power of two at or above keep (empty slots
+// after them).  Ordering is a merge sort: at each level every record finds
+// its place in the merged run by a binary search of the partner run (a
+// record of the left run counts the partner's records that precede it, one
+// of the right run also those equal to it, so places are distinct), one
+// barrier per level.  Raw candidates are runs of one; a partial result from
+// the level before is a slice of sorted runs, so later levels and the final
+// workgroup start from longer runs.
+// Levels repeat until at most FINAL_MAX candidates remain.
+// k_select (one workgroup): orders and compacts those the same way into the
+// pool and decodes its knob values; then wave 0 alone runs the greedy
+// rounds, each lane looking after pool candidates lane, lane + 64, ...: a
+// round is a wave-wide arg-max of the gains (DPP steps, no workgroup
+// barrier), then every lane clears the knobs the winner covers in its
+// candidates' masks.  The wave then ranks the picks in parallel (ascending
+// indices) and makes each random draw with one wave-wide count: with S the
+// picks in ascending order, the floor(u * remaining / 2^64) = k-th
+// unselected index is k + j, j the number of positions i with
+// S[i] - i <= k.
 #include <mutex>
 
 #include "at_chain.h"
@@ -28,61 +44,123 @@ namespace {
 
 using namespace dev;
 
-constexpr int SEL_WG = 1024;
-constexpr int SORT_N = 4096;     // entries one workgroup sorts (64 KB of LDS)
-constexpr int MERGE_MAX = 4096;  // entries the final workgroup sorts (64 KB)
-constexpr int POOL_MAX = SEL_WG; // one thread per pool candidate
+constexpr int SEL_WG = 1024;     // threads of both kernels
+constexpr int CHUNK = 2048;      // candidates one reduction workgroup orders
+constexpr int FINAL_MAX = 2048;  // candidates the final workgroup orders
+constexpr int POOL_MAX = 1024;
 constexpr int PICK_MAX = 2048;   // greedy plus random picks
 
-// Sort key: (order of the score, descending; index ascending), invalid
-// entries last.  -0.0 counts as +0.0, as in a float comparison.
-struct Key {
-    uint32_t s;   // larger score -> smaller s
+// A candidate while it is ordered: index, score bits and the score's order
+// bits (smaller for a higher score, -0.0 as +0.0; 0xffffffff for an empty
+// slot, whose index is then ~0).
+struct Rec {
     uint64_t cfg;
+    uint32_t bits;
+    uint32_t ord;
 };
+static_assert(sizeof(Rec) == 16, "16-byte records");
 
-__device__ __forceinline__ Key key_of(const at_entry& e) {
-    Key k;
+__device__ __forceinline__ Rec rec_of(const at_entry& e) {
+    Rec r;
     if (!e.flag) {
-        k.s = 0xffffffffu;
-        k.cfg = ~0ull;
-        return k;
+        r.cfg = ~0ull;
+        r.bits = 0u;
+        r.ord = 0xffffffffu;
+        return r;
     }
-    uint32_t b = __float_as_uint(e.score);
+    r.cfg = e.cfg;
+    r.bits = __float_as_uint(e.score);
+    uint32_t b = r.bits;
     if (b == 0x80000000u) b = 0u;
     const uint32_t asc = (b & 0x80000000u) ? ~b : (b | 0x80000000u);   // ascending float order
-    k.s = ~asc;
-    k.cfg = e.cfg;
-    return k;
+    r.ord = ~asc;
+    return r;
 }
 
-__device__ __forceinline__ bool key_less(const Key& a, const Key& b) {
-    return a.s < b.s || (a.s == b.s && a.cfg < b.cfg);
+__device__ __forceinline__ bool rec_valid(const Rec& r) { return r.ord != 0xffffffffu; }
+
+__device__ __forceinline__ at_entry entry_of(const Rec& r) {
+    at_entry e;
+    e.cfg = r.cfg;
+    e.score = __uint_as_float(r.bits);
+    e.flag = 1u;
+    return e;
 }
 
-// Bitonic sort of n (a power of two) entries in LDS by key; all threads call.
-__device__ void bitonic_sort(at_entry* v, int n) {
-    for (int size = 2; size <= n; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            __syncthreads();
-            for (int i = threadIdx.x; i < n / 2; i += blockDim.x) {
-                const int lo = 2 * i - (i & (stride - 1));
-                const int hi = lo + stride;
-                const bool up = (lo & size) == 0;
-                const at_entry a = v[lo], b = v[hi];
-                const bool swap = up ? key_less(key_of(b), key_of(a)) : key_less(key_of(a), key_of(b));
-                if (swap) {
-                    v[lo] = b;
-                    v[hi] = a;
-                }
+__device__ __forceinline__ at_entry empty_entry() {
+    at_entry z;
+    z.cfg = 0;
+    z.score = 0.0f;
+    z.flag = 0u;
+    return z;
+}
+
+__device__ __forceinline__ bool rec_less(const Rec& a, const Rec& b) {
+    return a.ord < b.ord || (a.ord == b.ord && a.cfg < b.cfg);
+}
+
+// Orders n records (a power of two) made of ascending runs of length run
+// (a power of two, 1 for unordered input) ascending, moving them between
+// the LDS buffers a and b; returns the buffer that holds the result.  All
+// threads call.  A thread takes records tid, tid + blockDim.x, ...; the
+// binary searches of its records go step by step together, so their LDS
+// reads overlap.
+template <int PER>
+__device__ Rec* merge_sort(Rec* a, Rec* b, int n, int run) {
+    const int nt = (int)blockDim.x;
+    Rec* src = a;
+    Rec* dst = b;
+    for (int L = run; L < n; L <<= 1) {
+        __syncthreads();
+        Rec x[PER];
+        int base[PER], own[PER], cnt[PER];
+        bool left[PER], here[PER];
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            const int i = (int)threadIdx.x + e * nt;
+            here[e] = i < n;
+            const int ii = here[e] ? i : 0;
+            x[e] = src[ii];
+            const int blk = ii / (2 * L);
+            const int pos = ii - blk * 2 * L;
+            left[e] = pos < L;
+            own[e] = left[e] ? pos : pos - L;
+            base[e] = blk * 2 * L + (left[e] ? L : 0);   // the partner run
+            cnt[e] = 0;
+        }
+        // branch-free steps: every probe loads (clamped into the run), so
+        // the PER loads of a step issue together
+        for (int step = L; step > 0; step >>= 1) {
+            Rec y[PER];
+            int t[PER];
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                t[e] = cnt[e] + step;
+                y[e] = src[base[e] + (t[e] <= L ? t[e] : L) - 1];
+            }
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                const bool before = left[e] ? rec_less(y[e], x[e]) : !rec_less(x[e], y[e]);
+                cnt[e] = (t[e] <= L && before) ? t[e] : cnt[e];
             }
         }
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            if (here[e]) {
+                const int blk0 = base[e] - (left[e] ? L : 0);
+                dst[blk0 + own[e] + cnt[e]] = x[e];
+            }
+        }
+        Rec* t = src;
+        src = dst;
+        dst = t;
     }
     __syncthreads();
+    return src;
 }
 
 // Exclusive prefix sum of x over the block's threads (thread order); the
-// total goes to *total.  All threads call; uses wsum[SEL_WG / 64].
+// total goes to *total.  All threads call; wsum has a slot per wave.
 __device__ __forceinline__ int block_exclusive_scan(int x, int* wsum, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     int inc = x;
@@ -104,59 +182,55 @@ __device__ __forceinline__ int block_exclusive_scan(int x, int* wsum, int* total
     return before + inc - x;
 }
 
-// Sorted entries v[0..n) (n a power of two): the first `keep` distinct valid
-// ones (an index equal to its predecessor's is dropped) go to out[0..keep),
-// the rest of out is cleared; returns how many were found (at most keep).
-// Thread t looks after the consecutive entries [t * per, (t + 1) * per).
+// Ordered records v[0..n): the first `keep` distinct valid ones (an index
+// equal to its predecessor's is dropped) go to out[0..keep), empty entries
+// fill out[keep..slots); returns how many were found (at most keep).
+// Thread t looks after the consecutive records [t * per, (t + 1) * per).
 // All threads call.
-__device__ int compact_distinct(const at_entry* v, int n, at_entry* out, int keep, int* wsum) {
-    const int per = n > (int)blockDim.x ? n / (int)blockDim.x : 1;
+__device__ int compact_distinct(const Rec* v, int n, at_entry* out, int keep, int slots, int* wsum) {
+    const int nt = (int)blockDim.x;
+    const int per = n > nt ? n / nt : 1;
     const int lo = threadIdx.x * per;
+    auto fresh = [&](int i) { return rec_valid(v[i]) && (i == 0 || v[i].cfg != v[i - 1].cfg); };
     int cnt = 0;
-    for (int i = lo; i < lo + per && i < n; ++i) cnt += (v[i].flag && (i == 0 || v[i].cfg != v[i - 1].cfg)) ? 1 : 0;
+    for (int i = lo; i < lo + per && i < n; ++i) cnt += fresh(i) ? 1 : 0;
     int total = 0;
     int pos = block_exclusive_scan(cnt, wsum, &total);
     for (int i = lo; i < lo + per && i < n; ++i) {
-        if (v[i].flag && (i == 0 || v[i].cfg != v[i - 1].cfg)) {
-            if (pos < keep) out[pos] = v[i];
+        if (fresh(i)) {
+            if (pos < keep) out[pos] = entry_of(v[i]);
             ++pos;
         }
     }
     const int have = total < keep ? total : keep;
-    for (int i = have + (int)threadIdx.x; i < keep; i += blockDim.x) {
-        at_entry z;
-        z.cfg = 0;
-        z.score = 0.0f;
-        z.flag = 0u;
-        out[i] = z;
-    }
+    for (int i = have + (int)threadIdx.x; i < slots; i += nt) out[i] = empty_entry();
     __syncthreads();
     return have;
 }
 
-__device__ __forceinline__ at_entry empty_entry() {
-    at_entry z;
-    z.cfg = 0;
-    z.score = 0.0f;
-    z.flag = 0u;
-    return z;
+// Records of entries [base, base + n) of src (empty past the end); all
+// threads call.
+__device__ __forceinline__ void load_slice(const at_entry* __restrict__ src, int64_t base, int64_t total, int n,
+                                           Rec* v) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) v[i] = rec_of(base + i < total ? src[base + i] : empty_entry());
 }
 
-// Workgroup b: entries [b * SORT_N, ...) of src -> its `keep` best distinct at dst + b * keep.
-__global__ __launch_bounds__(SEL_WG) void k_pool_partial(const at_entry* __restrict__ src, int64_t n, int keep,
-                                                          at_entry* __restrict__ dst) {
-    __shared__ at_entry v[SORT_N];
+// Workgroup b: entries [b * CHUNK, ...) of src, ascending runs of length
+// run -> its `keep` best distinct as the run dst + b * slots.
+__global__ __launch_bounds__(SEL_WG) void k_reduce(const at_entry* __restrict__ src, int64_t n, int run, int keep,
+                                                   int slots, at_entry* __restrict__ dst) {
+    __shared__ Rec v[CHUNK], w[CHUNK];
     __shared__ int wsum[SEL_WG / 64];
-    const int64_t base = (int64_t)blockIdx.x * SORT_N;
-    for (int i = threadIdx.x; i < SORT_N; i += blockDim.x) v[i] = base + i < n ? src[base + i] : empty_entry();
-    bitonic_sort(v, SORT_N);
-    compact_distinct(v, SORT_N, dst + (int64_t)blockIdx.x * keep, keep, wsum);
+    load_slice(src, (int64_t)blockIdx.x * CHUNK, n, CHUNK, v);
+    const Rec* sorted = merge_sort<CHUNK / SEL_WG>(v, w, CHUNK, run);
+    compact_distinct(sorted, CHUNK, dst + (int64_t)blockIdx.x * slots, keep, slots, wsum);
 }
 
 struct SelectArgs {
     const SpaceDesc* desc;
-    const at_entry* src;      // sorted input candidates, or partial results
-    int64_t n;                // entries in src (at most MERGE_MAX)
+    const at_entry* src;      // candidates, or partial results (at most FINAL_MAX)
+    int64_t n;
+    int run;                  // ascending runs of src (1: unordered)
     int pool;
     int n_greedy;
     float alpha;
@@ -165,135 +239,227 @@ struct SelectArgs {
     at_entry* out;            // [n_greedy + n_random]
 };
 
-__global__ __launch_bounds__(SEL_WG) void k_select(SelectArgs a) {
+// Ascending order bits of a finite gain (-0.0 as +0.0).
+__device__ __forceinline__ uint32_t gain_order(float g) {
+    uint32_t b = __float_as_uint(g);
+    if (b == 0x80000000u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ int wave_sum(int x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+    return x;
+}
+
+// Largest 64-bit key of the wave, in every lane: DPP shifts within rows
+// of 16, then row broadcasts, leave the maximum in lane 63.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t dpp_max_step(uint64_t x) {
+    const uint32_t hi = (uint32_t)(x >> 32), lo = (uint32_t)x;
+    const uint32_t ohi = (uint32_t)__builtin_amdgcn_update_dpp((int)hi, (int)hi, CTRL, ROWS, 0xf, false);
+    const uint32_t olo = (uint32_t)__builtin_amdgcn_update_dpp((int)lo, (int)lo, CTRL, ROWS, 0xf, false);
+    const uint64_t o = ((uint64_t)ohi << 32) | olo;
+    return o > x ? o : x;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+    x = dpp_max_step<0x111, 0xf>(x);   // row_shr:1
+    x = dpp_max_step<0x112, 0xf>(x);   // row_shr:2
+    x = dpp_max_step<0x114, 0xf>(x);   // row_shr:4
+    x = dpp_max_step<0x118, 0xf>(x);   // row_shr:8
+    x = dpp_max_step<0x142, 0xa>(x);   // row_bcast:15 into rows 1 and 3
+    x = dpp_max_step<0x143, 0xc>(x);   // row_bcast:31 into rows 2 and 3
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// The greedy rounds of wave 0 for up to 64 * CPL pool candidates; knob
+// values of a lane's candidates (packed in pairs) are held in registers for
+// up to 4 candidates a lane, read from LDS for more.
+template <int CPL>
+__device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const uint32_t* vals, int have, int m,
+                              uint64_t* picked, int rounds) {
+    constexpr int W = MAX_KNOBS / 2;
+    const int lane = threadIdx.x & 63;
+    const uint32_t all = m >= 32 ? 0xffffffffu : (1u << m) - 1u;
+    constexpr bool REG = CPL <= 4;
+    constexpr int KR = REG ? CPL : 1;
+    float sc[CPL];
+    uint32_t fresh[CPL], kv[KR][W];
+    uint32_t taken = 0u;   // bit i: candidate lane + 64 i is picked or absent
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        const int c = lane + 64 * i;
+        const bool mine = c < have;
+        sc[i] = mine ? pool[c].score : 0.0f;
+        fresh[i] = mine ? all : 0u;
+        if constexpr (REG) {
+#pragma unroll
+            for (int j = 0; j < W; ++j) kv[i][j] = mine ? vals[c * W + j] : 0u;
+        }
+        if (!mine) taken |= 1u << i;
+    }
+    for (int r = 0; r < rounds; ++r) {
+        // arg-max of (gain, -index): the key's high half orders the gains,
+        // the low half prefers the earlier candidate
+        uint64_t best = 0;
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+            const float cov = a.alpha * (float)__popc(fresh[i]);
+            const float g = sc[i] + cov;
+            const uint64_t key = ((uint64_t)gain_order(g) << 32) | (uint32_t)~(uint32_t)(lane + 64 * i);
+            if (!((taken >> i) & 1u) && key > best) best = key;
+        }
+        best = wave_max_u64(best);
+        const int win = (int)~(uint32_t)best;
+        const int wl = win & 63, wi = win >> 6;
+        if (wl == lane) taken |= 1u << wi;
+        // the winner's knob values: from its lane's registers, or LDS
+        uint32_t wv[W];
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+            if constexpr (REG) {
+                uint32_t x = 0u;
+#pragma unroll
+                for (int i = 0; i < CPL; ++i)
+                    if (i == wi) x = kv[i][j];
+                wv[j] = (uint32_t)__builtin_amdgcn_readlane((int)x, wl);
+            } else {
+                wv[j] = vals[win * W + j];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+            uint32_t f = fresh[i];
+#pragma unroll
+            for (int j = 0; j < W; ++j) {
+                const uint32_t mine = REG ? kv[REG ? i : 0][j] : vals[(lane + 64 * i) * W + j];
+                const uint32_t x = mine ^ wv[j];
+                if ((x & 0xffffu) == 0u) f &= ~(1u << (2 * j));
+                if ((x >> 16) == 0u) f &= ~(1u << (2 * j + 1));
+            }
+            fresh[i] = f & all;
+        }
+        if (lane == 0) {
+            at_entry e = pool[win];
+            e.flag = 1u;
+            a.out[r] = e;
+            picked[r] = e.cfg;
+        }
+    }
+}
+
+// Four waves per SIMD (the workgroup's sixteen): up to 128 VGPRs, so the
+// greedy wave keeps its candidates in registers without spilling.
+__global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) void k_select(SelectArgs a) {
     extern __shared__ uint4 sel_lds[];
-    at_entry* v = reinterpret_cast<at_entry*>(sel_lds);                  // [MERGE_MAX]
-    at_entry* pool = v + MERGE_MAX;                                      // [POOL_MAX]
-    uint16_t* vals = reinterpret_cast<uint16_t*>(pool + POOL_MAX);       // [POOL_MAX][MAX_KNOBS]
-    uint64_t* picked = reinterpret_cast<uint64_t*>(vals + POOL_MAX * MAX_KNOBS);   // [PICK_MAX], ascending
-    __shared__ float w_gain[SEL_WG / 64];
-    __shared__ int w_idx[SEL_WG / 64];
-    __shared__ int s_win;
+    Rec* v = reinterpret_cast<Rec*>(sel_lds);                                    // [FINAL_MAX]
+    Rec* w = v + FINAL_MAX;                                                      // [FINAL_MAX]
+    at_entry* pool = reinterpret_cast<at_entry*>(w + FINAL_MAX);                 // [POOL_MAX]
+    uint32_t* vals = reinterpret_cast<uint32_t*>(pool + POOL_MAX);               // [POOL_MAX][MAX_KNOBS / 2]
+    uint64_t* picked = reinterpret_cast<uint64_t*>(vals + POOL_MAX * (MAX_KNOBS / 2));   // [PICK_MAX], pick order
+    uint64_t* sorted = picked + PICK_MAX;                                        // [PICK_MAX], ascending
     __shared__ int wsum[SEL_WG / 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
     const SpaceDesc& sd = *a.desc;
 
     // the pool: the `pool` best distinct candidates
     int nsort = 1;
     while (nsort < a.n) nsort <<= 1;
-    for (int i = tid; i < nsort; i += SEL_WG) v[i] = i < a.n ? a.src[i] : empty_entry();
-    bitonic_sort(v, nsort);
-    const int have = compact_distinct(v, nsort, pool, a.pool, wsum);
+    load_slice(a.src, 0, a.n, nsort, v);
+    const Rec* sorted_c = merge_sort<FINAL_MAX / SEL_WG>(v, w, nsort, a.run < nsort ? a.run : nsort);
+    const int have = compact_distinct(sorted_c, nsort, pool, a.pool, a.pool, wsum);
 
-    // knob values of the pool candidates; mask of knobs not yet covered
+    // knob values of the pool candidates, packed in pairs (indices fit 32
+    // bits: a space has fewer than 2^32 configurations)
     const int m = sd.n_knobs;
-    uint32_t fresh = 0u;
-    float score = 0.0f;
-    const bool mine = tid < have;
-    if (mine) {
-        uint64_t cfg = pool[tid].cfg;
-        score = pool[tid].score;
-        for (int j = 0; j < m; ++j) {
-            const uint64_t q = cfg / sd.radix[j];
-            vals[tid * MAX_KNOBS + j] = (uint16_t)q;
-            cfg -= q * sd.radix[j];
-        }
-        fresh = (1u << m) - 1u;
-    }
-    bool taken = !mine;
-    const int rounds = a.n_greedy < have ? a.n_greedy : have;
-    __syncthreads();
-    for (int r = 0; r < rounds; ++r) {
-        // gain of every untaken candidate; block arg-max by (gain, -index)
-        float g = -INFINITY;
-        int gi = 0x7fffffff;
-        if (!taken) {
-            const float cov = a.alpha * (float)__popc(fresh);
-            g = score + cov;
-            gi = tid;
+    for (int c = tid; c < have; c += SEL_WG) {
+        uint32_t cfg = (uint32_t)pool[c].cfg;
+        uint32_t kv[MAX_KNOBS];
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j) {
+            kv[j] = 0u;
+            if (j < m) {
+                const uint32_t rdx = (uint32_t)sd.radix[j];
+                const uint32_t q = cfg / rdx;
+                kv[j] = q;
+                cfg -= q * rdx;
+            }
         }
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            const float og = __shfl_xor(g, off);
-            const int oi = __shfl_xor(gi, off);
-            if (og > g || (og == g && oi < gi)) {
-                g = og;
-                gi = oi;
-            }
+        for (int j = 0; j < MAX_KNOBS / 2; ++j) vals[c * (MAX_KNOBS / 2) + j] = kv[2 * j] | (kv[2 * j + 1] << 16);
+    }
+    __syncthreads();
+    if (tid >= 64) return;   // the rounds and the draws are wave 0's; no barrier follows
+
+    const int rounds = a.n_greedy < have ? a.n_greedy : have;
+    const int cpl = (have + 63) / 64;
+    if (cpl <= 1) greedy_rounds<1>(a, pool, vals, have, m, picked, rounds);
+    else if (cpl <= 2) greedy_rounds<2>(a, pool, vals, have, m, picked, rounds);
+    else if (cpl <= 4) greedy_rounds<4>(a, pool, vals, have, m, picked, rounds);
+    else if (cpl <= 8) greedy_rounds<8>(a, pool, vals, have, m, picked, rounds);
+    else greedy_rounds<16>(a, pool, vals, have, m, picked, rounds);
+
+    // the picks in ascending order: pick i goes to its rank (picks are
+    // distinct)
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    for (int i = lane; i < rounds; i += 64) {
+        const uint64_t x = picked[i];
+        int rank = 0;
+        for (int j = 0; j < rounds; ++j) rank += picked[j] < x ? 1 : 0;
+        sorted[rank] = x;
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+
+    // epsilon-greedy draws, then empty slots
+    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+    int n_sel = rounds, slot = rounds;
+    for (int i = 0; i < a.n_random; ++i) {
+        const uint64_t remaining = sd.n_configs - (uint64_t)n_sel;
+        if (remaining == 0) break;
+        const U4 r = philox(k0, k1, U4{(uint32_t)i, 0u, 5u, 0u});
+        const uint64_t u = ((uint64_t)r.y << 32) | r.x;
+        const uint64_t k = __umul64hi(u, remaining);
+        // j = #{positions p with sorted[p] - p <= k}: those picks lie at or
+        // below the drawn index, which is then k + j
+        int j = 0;
+        for (int p = lane; p < n_sel; p += 64) j += (sorted[p] - (uint64_t)p <= k) ? 1 : 0;
+        j = wave_sum(j);
+        const uint64_t cfg = k + (uint64_t)j;
+        // insert at position j: the picks from j on move up by one, each
+        // lane reading all of its picks before any lane writes
+        for (int base = (n_sel - 1) & ~63; base >= 0; base -= 64) {
+            const int p = base + lane;
+            const uint64_t x = (p < n_sel) ? sorted[p] : 0;
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
+            if (p < n_sel && p >= j) sorted[p + 1] = x;
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
         }
         if (lane == 0) {
-            w_gain[wave] = g;
-            w_idx[wave] = gi;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            float bg = w_gain[0];
-            int bi = w_idx[0];
-            for (int w = 1; w < SEL_WG / 64; ++w)
-                if (w_gain[w] > bg || (w_gain[w] == bg && w_idx[w] < bi)) {
-                    bg = w_gain[w];
-                    bi = w_idx[w];
-                }
-            s_win = bi;
-            at_entry e;
-            e.cfg = pool[bi].cfg;
-            e.score = pool[bi].score;
-            e.flag = 1u;
-            a.out[r] = e;
-            picked[r] = e.cfg;
-        }
-        __syncthreads();
-        const int win = s_win;
-        if (tid == win) taken = true;
-        if (mine) {
-            for (int j = 0; j < m; ++j)
-                if (vals[tid * MAX_KNOBS + j] == vals[win * MAX_KNOBS + j]) fresh &= ~(1u << j);
-        }
-        __syncthreads();
-    }
-
-    // epsilon-greedy, then empty slots
-    if (tid == 0) {
-        int n_sel = rounds;
-        // ascending order of the greedy picks (insertion sort)
-        for (int i = 1; i < n_sel; ++i) {
-            const uint64_t x = picked[i];
-            int j = i - 1;
-            while (j >= 0 && picked[j] > x) {
-                picked[j + 1] = picked[j];
-                --j;
-            }
-            picked[j + 1] = x;
-        }
-        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-        int slot = rounds;
-        for (int i = 0; i < a.n_random; ++i) {
-            const uint64_t remaining = sd.n_configs - (uint64_t)n_sel;
-            if (remaining == 0) break;
-            const U4 r = philox(k0, k1, U4{(uint32_t)i, 0u, 5u, 0u});
-            const uint64_t u = ((uint64_t)r.y << 32) | r.x;
-            uint64_t cfg = __umul64hi(u, remaining);
-            int pos = 0;
-            while (pos < n_sel && picked[pos] <= cfg) {
-                ++cfg;
-                ++pos;
-            }
-            for (int j = n_sel; j > pos; --j) picked[j] = picked[j - 1];
-            picked[pos] = cfg;
-            ++n_sel;
+            sorted[j] = cfg;
             at_entry e;
             e.cfg = cfg;
             e.score = 0.0f;
             e.flag = 2u;
-            a.out[slot++] = e;
+            a.out[slot] = e;
         }
-        for (; slot < a.n_greedy + a.n_random; ++slot) a.out[slot] = empty_entry();
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_wave_barrier();
+        ++n_sel;
+        ++slot;
     }
+    for (int q = slot + lane; q < a.n_greedy + a.n_random; q += 64) a.out[q] = empty_entry();
 }
 
 size_t select_lds_bytes() {
-    return (size_t)MERGE_MAX * sizeof(at_entry) + (size_t)POOL_MAX * sizeof(at_entry) +
-           (size_t)POOL_MAX * MAX_KNOBS * 2 + (size_t)PICK_MAX * 8;
+    return (size_t)FINAL_MAX * sizeof(Rec) * 2 + (size_t)POOL_MAX * sizeof(at_entry) +
+           (size_t)POOL_MAX * (MAX_KNOBS / 2) * 4 + (size_t)PICK_MAX * 8 * 2;
 }
 
 }  // namespace
@@ -301,12 +467,19 @@ size_t select_lds_bytes() {
 int select_pool_max() { return POOL_MAX; }
 int select_pick_max() { return PICK_MAX; }
 
+// Slots of one reduction workgroup's result: the power of two at or above
+// max(pool, 1), so that the results form whole ascending runs.
+static int run_slots(int pool) {
+    int r = 1;
+    while (r < pool) r <<= 1;
+    return r;
+}
+
 // Entries of each of the two partial-result buffers the reduction of n_cand
 // candidates needs (0 when n_cand fits the final workgroup).
 int64_t select_scratch_entries(int64_t n_cand, int pool) {
-    if (n_cand <= MERGE_MAX) return 0;
-    const int keep = pool > 0 ? pool : 1;
-    return (n_cand + SORT_N - 1) / SORT_N * keep;
+    if (n_cand <= FINAL_MAX) return 0;
+    return (n_cand + CHUNK - 1) / CHUNK * run_slots(pool);
 }
 
 // Scratch of the entry point that allocates nothing: the two partial-result
@@ -348,9 +521,12 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
         if (e != hipSuccess) return e;
         configured = true;
     }
-    // reduce the candidates to at most MERGE_MAX entries: each level keeps
-    // the `keep` best distinct of every SORT_N-entry slice (a quarter or less)
+    // reduce the candidates to at most FINAL_MAX entries: each level keeps
+    // the `keep` best distinct of every CHUNK-entry slice as a run of `slots`
+    // (half a slice or less)
     const int keep = pool > 0 ? pool : 1;
+    const int slots = run_slots(pool);
+    int run = 1;
     const at_entry* src = cand;
     int64_t n = n_cand;
     void* bufs[2] = {nullptr, nullptr};
@@ -372,13 +548,14 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
         }
     }
     int cur = 0;
-    while (n > MERGE_MAX) {
-        const int64_t groups = (n + SORT_N - 1) / SORT_N;
-        hipLaunchKernelGGL(k_pool_partial, dim3((unsigned)groups), dim3(SEL_WG), 0, stream, src, n, keep,
+    while (n > FINAL_MAX) {
+        const int64_t groups = (n + CHUNK - 1) / CHUNK;
+        hipLaunchKernelGGL(k_reduce, dim3((unsigned)groups), dim3(SEL_WG), 0, stream, src, n, run, keep, slots,
                            static_cast<at_entry*>(bufs[cur]));
         if ((e = hipGetLastError()) != hipSuccess) break;
         src = static_cast<const at_entry*>(bufs[cur]);
-        n = groups * keep;
+        n = groups * slots;
+        run = slots;
         cur ^= 1;
     }
     if (e != hipSuccess) {
@@ -391,6 +568,7 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     a.desc = static_cast<const SpaceDesc*>(sp.d_descs.p);
     a.src = src;
     a.n = n;
+    a.run = run;
     a.pool = pool;
     a.n_greedy = n_greedy;
     a.alpha = alpha;

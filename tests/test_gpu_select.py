@@ -69,9 +69,12 @@ def test_select_after_annealing_c2(P):
 @pytest.mark.parametrize("n_lists,per_list,pool,n_greedy,alpha", [
     (8192, 32, 128, 61, 1.0),     # the C12 search's lists: two levels of partial reduction
     (1024, 16, 1024, 1024, 0.5),  # the largest pool, every candidate picked
-    (256, 16, 128, 61, 0.0),      # 4096 candidates: one workgroup, no partial level
-    (4097, 1, 64, 32, 2.0),       # one past a workgroup's slice
+    (128, 16, 128, 61, 0.0),      # 2048 candidates: one workgroup, no partial level
+    (2049, 1, 64, 32, 2.0),       # one past a workgroup's slice
+    (256, 16, 128, 61, 0.0),      # 4096 candidates: one partial level
     (300, 7, 200, 150, -0.25),    # negative alpha
+    (6000, 16, 300, 200, 1.0),    # pool not a power of two: runs of 512
+    (4096, 64, 1000, 300, 0.3),   # 262144 candidates, runs of 1024: seven partial levels
 ])
 def test_select_synthetic_candidates(P, n_lists, per_list, pool, n_greedy, alpha):
     say(f"select: {n_lists}x{per_list} synthetic, pool {pool}, greedy {n_greedy}, alpha {alpha}")
