@@ -64,8 +64,8 @@ typedef enum {
  *    rc1 r1 oc3 oh3 ow3 rc2 r2 oc4 oh4 ow4 (r_l fuses ry_l, rx_l; first band
  *    -> blockIdx.z/y/x, second -> threadIdx.z/y/x): 16 loops, 176 features.
  *  AT_TMPL_GEMM_VT, AT_TMPL_CONV2D_NCHW_VT: the same templates with two
- *    annotation knobs more (Section 2's search space includes annotations
- *    such as unrolling and vectorization), after unroll_explicit:
+ *    annotation knobs more (Section 2 lists unrolling and vectorization
+ *    among the annotations of its search space), after unroll_explicit:
  *    vectorize in {0, 1} marks the innermost loop (GEMM j4, conv2d ow4)
  *    vectorized, annotation id 10; vthread in {0, 1} binds the third tiling
  *    level of every spatial axis (GEMM i3 j3, conv2d oc3 oh3 ow3) to virtual

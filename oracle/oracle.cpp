@@ -250,8 +250,8 @@ bool build_conv(Space& sp, const int64_t* shape, int nshape) {
     return true;
 }
 
-// The annotation knobs of templates 2 and 3 (reading of Section 2's
-// "annotations such as unrolling and vectorization"): vectorize = 1 marks
+// The annotation knobs of templates 2 and 3 (a reading of Section 2, whose
+// search space takes unrolling and vectorization annotations): vectorize = 1 marks
 // the innermost loop vectorized; vthread = 1 binds the third tiling level of
 // every spatial axis (GEMM i3 j3, conv2d oc3 oh3 ow3) to virtual threads.
 // Either annotation takes the place of the unroll rule on its loops; the

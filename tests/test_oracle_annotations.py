@@ -1,6 +1,7 @@
-"""Oracle pins: the templates with vectorize and vthread knobs (Section 2's
-annotations such as unrolling and vectorization) and the one-hot form of the
-annotation column (Appendix A.2 loop-context table).
+"""Oracle pins: the templates with vectorize and vthread knobs (Section 2
+lists unrolling and vectorization among the annotations of its search space)
+and the one-hot form of the annotation column (Appendix A.2 loop-context
+table).
 
 Pinned against:
   - the hand-worked annotation columns in tests/golden (Appendix A.3 GEMM and
