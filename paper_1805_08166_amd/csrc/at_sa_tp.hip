@@ -331,9 +331,12 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         } else if (tid < CPW) {
             rec[tid].qual = 0;
         }
+        // the barriers from here on order LDS only: a full __syncthreads
+        // would also wait for this workgroup's global stores (best lists,
+        // trace, state) to drain
         if (__syncthreads_or(qual)) {
             group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
-            __syncthreads();
+            lds_barrier();
             for (int idx = tid; idx < nc * k; idx += CHAIN_WG) {
                 const int j = idx / k;
                 if (rec[j].qual) a.top[c0 * k + idx] = lists[idx];
@@ -413,7 +416,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
 #pragma unroll
         for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = nx[2 * j] | (nx[2 * j + 1] << 16);
     }
-    __syncthreads();
+    lds_barrier();
 
     // features: lane gr of group gj evaluates loop gr of chain gj's candidate
     __shared__ uint8_t tdrow[CPW][16];
@@ -430,7 +433,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         for (int i = 0; i < 11; ++i) frow[gj][gr * 11 + i] = (uint8_t)f[i];
         tdrow[gj][gr] = (uint8_t)td;
     }
-    __syncthreads();
+    lds_barrier();
     if (a.Fr) {
         // context relation features of the candidate (Section 4): output
         // o = [pair][buffer b][t - 1] is the largest value over the loops
@@ -454,7 +457,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
                 rrow[gj][o] = (uint8_t)v;
             }
         }
-        __syncthreads();
+        lds_barrier();
         for (int idx = tid; idx < CPW * REL_Q; idx += CHAIN_WG) {
             const int q = idx >> 4, j = idx & (CPW - 1);
             if (j >= nc) continue;
