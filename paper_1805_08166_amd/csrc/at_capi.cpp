@@ -2,6 +2,7 @@
 // codes and the host-side threshold helper.  Every compute entry point
 // validates its arguments and then enqueues HIP kernels on the caller's
 // stream.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -47,6 +48,48 @@ at_status alloc_zero(DeviceBuf& buf, size_t bytes) {
     e = hipMemset(buf.p, 0, buf.bytes);
     if (e != hipSuccess) return hip_fail(e, "hipMemset");
     return AT_OK;
+}
+
+// LDS images of a space's members and, for a set, the image of each block
+// of STAGE_CHAINS chains (see at_space_s).
+at_status build_stage(at_space_s& sp) {
+    std::vector<int> fits(sp.n_spaces, 0);
+    size_t need = 0;
+    for (int i = 0; i < sp.n_spaces; ++i) {
+        const size_t nf = sp.host_factors[i].size();
+        fits[i] = nf <= (size_t)STAGE_FAC_MAX;
+        if (fits[i]) need = std::max(need, (size_t)STAGE_DESC_BYTES + nf * 8);
+    }
+    const size_t stride = (need + STAGE_ALIGN - 1) / STAGE_ALIGN * STAGE_ALIGN;
+    std::vector<uint8_t> img(stride * sp.n_spaces, 0);
+    for (int i = 0; i < sp.n_spaces && stride; ++i) {
+        if (!fits[i]) continue;
+        SpaceDesc d = sp.descs[i];
+        const int32_t base = d.split_off[0];
+        for (int a = 0; a < d.n_axes; ++a) d.split_off[a] -= base;
+        uint8_t* dst = img.data() + stride * i;
+        std::memcpy(dst, &d, sizeof d);
+        std::memcpy(dst + STAGE_DESC_BYTES, sp.host_factors[i].data(), sp.host_factors[i].size() * 8);
+    }
+    sp.stage_stride = (int)stride;
+    at_status st = upload(sp.d_stage, img.data(), img.size());
+    if (st != AT_OK) return st;
+    if (sp.n_spaces == 1) {
+        sp.stage_single = fits[0] ? 0 : -1;
+        return AT_OK;
+    }
+    const int64_t n = sp.chain_offsets.back();
+    const int64_t blocks = (n + STAGE_CHAINS - 1) / STAGE_CHAINS;
+    std::vector<int32_t> ws((size_t)blocks, -1);
+    int w = 0;
+    for (int64_t b = 0; b < blocks; ++b) {
+        const int64_t lo = b * STAGE_CHAINS, hi = std::min(n, lo + STAGE_CHAINS) - 1;
+        while (w + 1 < sp.n_spaces && sp.chain_offsets[w + 1] <= lo) ++w;
+        int wh = w;
+        while (wh + 1 < sp.n_spaces && sp.chain_offsets[wh + 1] <= hi) ++wh;
+        ws[(size_t)b] = (wh == w && fits[w]) ? w : -1;
+    }
+    return upload(sp.d_wg_space, ws.data(), ws.size());
 }
 
 void release(DeviceBuf& buf) {
@@ -118,7 +161,8 @@ at_status at_space_create(int tmpl, const int64_t* shape, int nshape, at_space_t
     sp->host_factors.push_back(factors);
     int64_t offs[2] = {0, INT64_MAX};
     if ((st = upload(sp->d_descs, &d, 1)) != AT_OK || (st = upload(sp->d_factors, factors.data(), factors.size())) != AT_OK ||
-        (st = upload(sp->d_offsets, offs, 2)) != AT_OK || (st = alloc_zero(sp->d_errors, 8)) != AT_OK) {
+        (st = upload(sp->d_offsets, offs, 2)) != AT_OK || (st = alloc_zero(sp->d_errors, 8)) != AT_OK ||
+        (st = build_stage(*sp)) != AT_OK) {
         at_space_destroy(sp);
         return st;
     }
@@ -174,7 +218,7 @@ at_status at_spaceset_create(const at_space_t* spaces, int n, const int64_t* cha
     if ((st = upload(sp->d_descs, sp->descs.data(), sp->descs.size())) != AT_OK ||
         (st = upload(sp->d_factors, all.data(), all.size())) != AT_OK ||
         (st = upload(sp->d_offsets, sp->chain_offsets.data(), sp->chain_offsets.size())) != AT_OK ||
-        (st = alloc_zero(sp->d_errors, 8)) != AT_OK) {
+        (st = alloc_zero(sp->d_errors, 8)) != AT_OK || (st = build_stage(*sp)) != AT_OK) {
         at_space_destroy(sp);
         return st;
     }
@@ -189,6 +233,8 @@ void at_space_destroy(at_space_t space) {
     release(space->d_factors);
     release(space->d_offsets);
     release(space->d_errors);
+    release(space->d_stage);
+    release(space->d_wg_space);
     delete space;
 }
 

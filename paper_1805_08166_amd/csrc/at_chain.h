@@ -22,12 +22,23 @@ __device__ __forceinline__ int space_of(const int64_t* offsets, int n_spaces, in
 
 // A chain's knob vector: MAX_KNOBS u16 (24 bytes, three 8-byte words).
 static_assert(MAX_KNOBS == 12, "knob vectors move as three 8-byte words");
-__device__ __forceinline__ void load_knobs(const uint16_t* p, int64_t c, uint32_t (&kv)[MAX_KNOBS]) {
-    const uint2* w = reinterpret_cast<const uint2*>(p) + 3 * c;
-    const uint2 a = w[0], b = w[1], d = w[2];
-    const uint32_t pw[6] = {a.x, a.y, b.x, b.y, d.x, d.y};
+__device__ __forceinline__ void load_knob_words(const uint16_t* p, int64_t c, uint2 (&w)[3]) {
+    const uint2* q = reinterpret_cast<const uint2*>(p) + 3 * c;
+    w[0] = q[0];
+    w[1] = q[1];
+    w[2] = q[2];
+}
+
+__device__ __forceinline__ void unpack_knobs(const uint2 (&w)[3], uint32_t (&kv)[MAX_KNOBS]) {
+    const uint32_t pw[6] = {w[0].x, w[0].y, w[1].x, w[1].y, w[2].x, w[2].y};
 #pragma unroll
     for (int j = 0; j < MAX_KNOBS; ++j) kv[j] = (pw[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+}
+
+__device__ __forceinline__ void load_knobs(const uint16_t* p, int64_t c, uint32_t (&kv)[MAX_KNOBS]) {
+    uint2 w[3];
+    load_knob_words(p, c, w);
+    unpack_knobs(w, kv);
 }
 
 __device__ __forceinline__ void store_knobs(uint16_t* p, int64_t c, const uint32_t (&kv)[MAX_KNOBS]) {

@@ -51,6 +51,17 @@ struct SpaceDesc {
     int32_t ann_knobs;                   // 1: knobs n_axes + 2, n_axes + 3 are vectorize and vthread
 };
 
+// LDS image of one space for the annealing chain kernel: the descriptor
+// with its split offsets rebased to 0 in the first STAGE_DESC_BYTES, then
+// the space's split factors (u64), at most STAGE_FAC_MAX of them.  Images
+// of a space set lie STAGE_ALIGN-multiple strides apart; the kernel copies
+// a whole stride with 16-byte direct-to-LDS moves of whole waves.
+constexpr int STAGE_DESC_BYTES = (int)((sizeof(SpaceDesc) + 15) / 16 * 16);
+constexpr int STAGE_FAC_MAX = 1024;
+constexpr int STAGE_ALIGN = 1024;
+constexpr int STAGE_MAX_BYTES = (STAGE_DESC_BYTES + STAGE_FAC_MAX * 8 + STAGE_ALIGN - 1) / STAGE_ALIGN * STAGE_ALIGN;
+constexpr int STAGE_CHAINS = 16;         // chains per chain-kernel workgroup
+
 // Packed ensemble.  Tree t occupies words [t*W, (t+1)*W) with W = 2^(d+1):
 // word m (1 <= m < 2^d) is internal node m (1-based heap order: children 2m
 // and 2m+1) holding (thr << 16) | tile byte offset of its feature; words
@@ -169,6 +180,15 @@ struct at_space_s {
     at::DeviceBuf d_factors;                // uint64 split factor tables
     at::DeviceBuf d_offsets;                // int64 [n_spaces + 1]
     at::DeviceBuf d_errors;                 // uint64 out-of-range counter
+    // LDS images of the member spaces (stage_stride bytes apart, 0 when no
+    // member's image fits), and which image a block of STAGE_CHAINS chains
+    // uses: stage_single for a single space, d_wg_space (int32 per block) for
+    // a set; -1 when the block spans two spaces or its space's image does not
+    // fit
+    at::DeviceBuf d_stage;
+    int stage_stride = 0;
+    int stage_single = -1;
+    at::DeviceBuf d_wg_space;
     // per member space: its factor tables as host data (for building sets)
     std::vector<std::vector<uint64_t>> host_factors;
 };

@@ -38,12 +38,11 @@ __device__ __forceinline__ int64_t v_index(int64_t c, int t, int groups) {
 
 constexpr int CHAIN_WG = 256;           // wave 0 runs the chains, all four waves move data
 constexpr int CPW = 16;                 // chains per chain-kernel workgroup
-static_assert(CPW == 16, "a chain-kernel workgroup reads one 16-chain block of V");
+static_assert(CPW == 16 && CPW == STAGE_CHAINS, "a chain-kernel workgroup reads one 16-chain block of V");
 constexpr int FOLD_P = 32;              // 4-tree groups per fold pass: 32 x 16 chains x 16 B = 8 KB
 constexpr int FOLD_R = 6;               // passes in the LDS ring (five in flight while one is folded)
 constexpr size_t RING_BYTES = (size_t)FOLD_R * FOLD_P * CPW * 16;
 constexpr int KMAX = 64;                // largest best list
-constexpr int FAC_MAX = 1024;           // split choices staged in LDS (8 KB)
 constexpr size_t MAX_LDS_BYTES = 163840; // LDS of one compute unit
 
 enum { FIN_NONE = 0, FIN_INIT = 1, FIN_STEP = 2 };
@@ -54,6 +53,13 @@ struct ChainArgs {
     const int64_t* offsets;
     int n_spaces;
     const uint64_t* factors;
+    // LDS images of the spaces (descriptor rebased, then split factors),
+    // stage_stride bytes apart; the image of a workgroup's chains is
+    // stage_single (one space) or wg_space[workgroup] (sets), -1 for none
+    const uint8_t* stage;
+    int stage_stride;
+    int stage_single;
+    const int32_t* wg_space;
     uint16_t* knobs;          // [n][MAX_KNOBS] current configuration
     uint16_t* cand;           // [n][MAX_KNOBS] candidate being scored
     float* cur_score;         // [n]
@@ -140,21 +146,87 @@ __device__ __forceinline__ void pass_barrier(int later) {
     }
 }
 
-// cnt float4 from src (stride CPW float4) added in order: blocks of sixteen
-// reads, then their adds.
-template <int B>
-__device__ __forceinline__ void fold_strided(float& s, const float4* __restrict__ src) {
-    float4 R[B];
+// Batches of FOLD_B groups (stride CPW float4 in the ring): the reads of a
+// batch, then its adds in tree order.
+constexpr int FOLD_B = 8;
+__device__ __forceinline__ void fold_load(float4 (&R)[FOLD_B], const float4* __restrict__ src) {
 #pragma unroll
-    for (int g = 0; g < B; ++g) R[g] = src[g * CPW];
+    for (int g = 0; g < FOLD_B; ++g) R[g] = src[g * CPW];
+}
+
+__device__ __forceinline__ void fold_add(float& s, const float4 (&R)[FOLD_B]) {
 #pragma unroll
-    for (int g = 0; g < B; ++g) {
+    for (int g = 0; g < FOLD_B; ++g) {
         s = s + R[g].x;
         s = s + R[g].y;
         s = s + R[g].z;
         s = s + R[g].w;
     }
 }
+
+// A whole pass (FOLD_P groups) added in order, two register sets deep: the
+// reads of batch b + 1 are in flight while batch b is added (a dependent
+// fp32 add takes about as long as ten issue slots, an LDS read several
+// adds).  The reads are issued from inline asm at the lane's LDS byte
+// address and waited for explicitly: LDS reads of one wave complete in
+// order, so at most FOLD_B outstanding means the older batch has landed
+// (other outstanding LDS or scalar operations only make the wait longer).
+// Each wait statement takes its batch's registers as operands, so no add
+// can move ahead of it.
+static_assert(FOLD_P == 4 * FOLD_B && FOLD_B == 8, "a pass is four batches of eight reads");
+typedef float fold_v4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t lds_byte_address(const void* p) {
+    // the LDS aperture's base has zero low 32 bits
+    return (uint32_t)reinterpret_cast<uintptr_t>(p);
+}
+
+template <int OFF>
+__device__ __forceinline__ void fold_issue_batch(fold_v4 (&R)[FOLD_B], uint32_t ad) {
+#define AT_FOLD_READ(G) \
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(R[G]) : "v"(ad), "i"(OFF + (G) * CPW * 16))
+    AT_FOLD_READ(0);
+    AT_FOLD_READ(1);
+    AT_FOLD_READ(2);
+    AT_FOLD_READ(3);
+    AT_FOLD_READ(4);
+    AT_FOLD_READ(5);
+    AT_FOLD_READ(6);
+    AT_FOLD_READ(7);
+#undef AT_FOLD_READ
+}
+
+#define AT_FOLD_WAIT(N, R)                                                                                  \
+    asm volatile("s_waitcnt lgkmcnt(" #N ")"                                                                \
+                 : "+v"(R[0]), "+v"(R[1]), "+v"(R[2]), "+v"(R[3]), "+v"(R[4]), "+v"(R[5]), "+v"(R[6]), "+v"(R[7]))
+
+__device__ __forceinline__ void fold_add_v(float& s, const fold_v4 (&R)[FOLD_B]) {
+#pragma unroll
+    for (int g = 0; g < FOLD_B; ++g) {
+        s = s + R[g].x;
+        s = s + R[g].y;
+        s = s + R[g].z;
+        s = s + R[g].w;
+    }
+}
+
+__device__ __forceinline__ void fold_pass(float& s, uint32_t ad) {
+    constexpr int BB = FOLD_B * CPW * 16;   // bytes between batches
+    fold_v4 A[FOLD_B], B[FOLD_B];
+    fold_issue_batch<0>(A, ad);
+    fold_issue_batch<BB>(B, ad);
+    AT_FOLD_WAIT(8, A);
+    fold_add_v(s, A);
+    fold_issue_batch<2 * BB>(A, ad);
+    AT_FOLD_WAIT(8, B);
+    fold_add_v(s, B);
+    fold_issue_batch<3 * BB>(B, ad);
+    AT_FOLD_WAIT(8, A);
+    fold_add_v(s, A);
+    AT_FOLD_WAIT(0, B);
+    fold_add_v(s, B);
+}
+#undef AT_FOLD_WAIT
 
 // Every wave of the workgroup calls this (it holds workgroup barriers); the
 // score is valid in lanes j < nc of wave 0.
@@ -173,18 +245,24 @@ __device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int T,
             const float4* src = ring + (p % FOLD_R) * (FOLD_P * CPW) + lane;
             const int ng = groups - p * FOLD_P < FOLD_P ? groups - p * FOLD_P : FOLD_P;
             const int r = (p == npass - 1) ? (T & 3) : 0;   // trees in a last, partial group
-            int full = r ? ng - 1 : ng;
+            const int full = r ? ng - 1 : ng;
             int g = 0;
-            for (; g + 16 <= full; g += 16) fold_strided<16>(s, src + g * CPW);
-            if (full - g >= 8) {
-                fold_strided<8>(s, src + g * CPW);
-                g += 8;
+            if (full == FOLD_P) {
+                fold_pass(s, lds_byte_address(src));
+                g = FOLD_P;
             }
-            if (full - g >= 4) {
-                fold_strided<4>(s, src + g * CPW);
-                g += 4;
+            for (; g + FOLD_B <= full; g += FOLD_B) {
+                float4 A[FOLD_B];
+                fold_load(A, src + g * CPW);
+                fold_add(s, A);
             }
-            for (; g < full; ++g) fold_strided<1>(s, src + g * CPW);
+            for (; g < full; ++g) {
+                const float4 q = src[g * CPW];
+                s = s + q.x;
+                s = s + q.y;
+                s = s + q.z;
+                s = s + q.w;
+            }
             if (r) {
                 const float4 q = src[full * CPW];
                 s = s + q.x;
@@ -217,60 +295,53 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     const uint64_t gmask = 0xffffull << (16 * (gj & 3));
     const bool gvalid = gj < nc;
 
-    // The workgroup's space: when all its chains share one space whose split
-    // tables fit, the descriptor and tables are staged in LDS; otherwise each
-    // lane reads its own space from global memory.
-    __shared__ SpaceDesc s_desc;
-    __shared__ uint64_t s_fac[FAC_MAX];
-    const int w_lo = space_of(a.offsets, a.n_spaces, c0), w_hi = space_of(a.offsets, a.n_spaces, c0 + nc - 1);
-    int fac_lo = 0, fac_n = 0;
-    if (w_lo == w_hi) {
-        const SpaceDesc& g = a.descs[w_lo];
-        fac_lo = g.split_off[0];
-        for (int ax = 0; ax < g.n_axes; ++ax) fac_n += (int)g.knob_size[ax];
-    }
-    const bool staged = w_lo == w_hi && fac_n <= FAC_MAX;
+    // The workgroup's space: when all its chains share one space whose image
+    // fits, the image (descriptor with rebased split offsets, then the split
+    // factors) moves straight into LDS; otherwise each lane reads its own
+    // space from global memory.  No load of the prologue is waited for before
+    // the fold: the fold's first pass barrier (or, with no fold, the barrier
+    // below) finds them complete.
+    __shared__ __attribute__((aligned(16))) uint8_t s_img[STAGE_MAX_BYTES];
+    const int ws = a.n_spaces == 1 ? a.stage_single : a.wg_space[blockIdx.x];
+    const bool staged = ws >= 0;
     if (staged) {
-        constexpr int DW = (int)(sizeof(SpaceDesc) / 4);
-        constexpr int SO = (int)(offsetof(SpaceDesc, split_off) / 4);
-        const uint32_t* gd = reinterpret_cast<const uint32_t*>(a.descs + w_lo);
-        uint32_t* ld = reinterpret_cast<uint32_t*>(&s_desc);
-        for (int i = tid; i < DW; i += CHAIN_WG)
-            ld[i] = (i >= SO && i < SO + MAX_AXES) ? gd[i] - (uint32_t)fac_lo : gd[i];
-        for (int i = tid; i < fac_n; i += CHAIN_WG) s_fac[i] = a.factors[fac_lo + i];
+        const uint8_t* src = a.stage + (int64_t)ws * a.stage_stride + (tid & 63) * 16;
+        for (int off = wave * 1024; off < a.stage_stride; off += CHAIN_WG * 16)
+            __builtin_amdgcn_global_load_lds(src + off, s_img + off, 16, 0, 0);
     }
-    const uint64_t* facp = staged ? s_fac : a.factors;
+    const SpaceDesc* s_desc = reinterpret_cast<const SpaceDesc*>(s_img);
+    const uint64_t* facp = staged ? reinterpret_cast<const uint64_t*>(s_img + STAGE_DESC_BYTES) : a.factors;
     // owner lanes: their chain's space; group lanes: the space of chain gj
-    const SpaceDesc* sdp = staged ? &s_desc : a.descs + space_of(a.offsets, a.n_spaces, c);
-    const SpaceDesc* gsdp = staged ? &s_desc : a.descs + space_of(a.offsets, a.n_spaces, c0 + (gvalid ? gj : 0));
+    const SpaceDesc* sdp = staged ? s_desc : a.descs + space_of(a.offsets, a.n_spaces, c);
+    const SpaceDesc* gsdp = staged ? s_desc : a.descs + space_of(a.offsets, a.n_spaces, c0 + (gvalid ? gj : 0));
 
-    // per-chain state, fetched before the fold so the loads overlap it
-    uint32_t cur[MAX_KNOBS], cd[MAX_KNOBS];
+    // per-chain state, in flight during the fold (unpacked after it)
+    uint2 kraw[3] = {}, craw[3] = {};
     ChainMeta m;
     m.count = 0;
     m.kth_score = 0.0f;
     m.kth_cfg = 0;
     float cur_s = 0.0f, thr_v = 0.0f;
     if (owner) {
-        load_knobs(a.knobs, c, cur);
-        if (a.fin != FIN_NONE) load_knobs(a.cand, c, cd);
+        load_knob_words(a.knobs, c, kraw);
+        if (a.fin != FIN_NONE) load_knob_words(a.cand, c, craw);
         if (a.fin == FIN_STEP) {
             m = a.meta[c];
             cur_s = a.cur_score[c];
             thr_v = a.thr[c * a.steps + a.fin_step];
         }
     }
-    // the leaf values of the pending candidates start streaming in (after
-    // the table staging, whose loads would otherwise queue behind them)
+    // the leaf values of the pending candidates start streaming in
     if (a.fin != FIN_NONE) {
         if (a.Vg)
             fold_prime(reinterpret_cast<const float4*>(a.Vg), a.Tg, c0, nc, ring, tid);
         else
             fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
+    } else {
+        // no fold: the image lands before the proposal reads it
+        asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     }
-    // publishes the staged space tables; the first passes of the fold stay
-    // in flight
-    lds_barrier();
+    uint32_t cur[MAX_KNOBS], cd[MAX_KNOBS];
 
     if (a.fin != FIN_NONE) {
         // score of the pending candidate (wave 0, fed by every wave); waves
@@ -309,12 +380,15 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             s = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
         }
         __builtin_amdgcn_s_waitcnt(0);
+        unpack_knobs(kraw, cur);
+        unpack_knobs(craw, cd);
 
         // best lists: the chain's group of 16 lanes inserts the candidate
         // into its list in LDS when it qualifies; changed lists are written
         // back.  Skipped when no chain qualifies.
         uint64_t cfg = 0;
         int qual = 0;
+        __shared__ uint32_t s_any;
         if (owner) {
             const SpaceDesc& sd = *sdp;
 #pragma unroll
@@ -331,10 +405,15 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         } else if (tid < CPW) {
             rec[tid].qual = 0;
         }
+        if (wave == 0) {
+            const uint64_t q = __ballot(qual);
+            if (tid == 0) s_any = q != 0 ? 1u : 0u;
+        }
         // the barriers from here on order LDS only: a full __syncthreads
         // would also wait for this workgroup's global stores (best lists,
         // trace, state) to drain
-        if (__syncthreads_or(qual)) {
+        lds_barrier();
+        if (s_any) {
             group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
             lds_barrier();
             for (int idx = tid; idx < nc * k; idx += CHAIN_WG) {
@@ -377,6 +456,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         for (int idx = tid; idx < nc * k; idx += CHAIN_WG) a.best[c0 * k + idx] = a.top[c0 * k + idx];
     }
     if (a.draw == DRAW_NONE) return;
+    if (a.fin == FIN_NONE) unpack_knobs(kraw, cur);
 
     // proposal (owner lanes)
     if (owner) {
@@ -1141,6 +1221,10 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
     ca.offsets = static_cast<const int64_t*>(sp.d_offsets.p);
     ca.n_spaces = sp.n_spaces;
     ca.factors = static_cast<const uint64_t*>(sp.d_factors.p);
+    ca.stage = static_cast<const uint8_t*>(sp.d_stage.p);
+    ca.stage_stride = sp.stage_stride;
+    ca.stage_single = sp.stage_single;
+    ca.wg_space = static_cast<const int32_t*>(sp.d_wg_space.p);
     ca.knobs = static_cast<uint16_t*>(ch.d_knobs.p);
     ca.cand = static_cast<uint16_t*>(ch.d_cand.p);
     ca.cur_score = static_cast<float*>(ch.d_score.p);
