@@ -315,22 +315,19 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     const SpaceDesc* sdp = staged ? s_desc : a.descs + space_of(a.offsets, a.n_spaces, c);
     const SpaceDesc* gsdp = staged ? s_desc : a.descs + space_of(a.offsets, a.n_spaces, c0 + (gvalid ? gj : 0));
 
-    // per-chain state, in flight during the fold (unpacked after it)
-    uint2 kraw[3] = {}, craw[3] = {};
-    ChainMeta m;
-    m.count = 0;
-    m.kth_score = 0.0f;
-    m.kth_cfg = 0;
-    float cur_s = 0.0f, thr_v = 0.0f;
-    if (owner) {
-        load_knob_words(a.knobs, c, kraw);
-        if (a.fin != FIN_NONE) load_knob_words(a.cand, c, craw);
-        if (a.fin == FIN_STEP) {
-            m = a.meta[c];
-            cur_s = a.cur_score[c];
-            thr_v = a.thr[c * a.steps + a.fin_step];
-        }
-    }
+    // per-chain state, in flight during the fold (used after it).  Every
+    // lane loads from valid addresses (c is chain c0 for lanes that own no
+    // chain; the threshold is read from the scores when there is none), so
+    // no branch joins the loaded values: a join would wait for them here.
+    uint2 kraw[3], craw[3];
+    load_knob_words(a.knobs, c, kraw);
+    load_knob_words(a.cand, c, craw);
+    ChainMeta m = a.meta[c];
+    const float cur_s = a.cur_score[c];
+    const float* thr_b = a.fin == FIN_STEP ? a.thr : a.cur_score;
+    int64_t thr_i = a.fin == FIN_STEP ? c * a.steps + a.fin_step : c;
+    asm volatile("" : "+v"(thr_i));   // one load from either table (not two loads and a join)
+    const float thr_v = thr_b[thr_i];
     // the leaf values of the pending candidates start streaming in
     if (a.fin != FIN_NONE) {
         if (a.Vg)
@@ -382,6 +379,12 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         __builtin_amdgcn_s_waitcnt(0);
         unpack_knobs(kraw, cur);
         unpack_knobs(craw, cd);
+        if (a.fin != FIN_STEP) {
+            // a fresh chain: empty best list
+            m.count = 0;
+            m.kth_score = 0.0f;
+            m.kth_cfg = 0;
+        }
 
         // best lists: the chain's group of 16 lanes inserts the candidate
         // into its list in LDS when it qualifies; changed lists are written
