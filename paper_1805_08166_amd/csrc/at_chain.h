@@ -96,7 +96,9 @@ struct ChainRec {
 // the wave must call this (the ballots are wave-wide); gm selects the
 // group's 16 bits of a ballot mask and `active` the lanes of a group whose
 // chain offers.
-__device__ __forceinline__ void group_offer(at_entry* list, ChainRec& rec, int k, int r, uint64_t gm, bool active) {
+// Rec: any record with cfg, score, count, kth_score and kth_cfg.
+template <class Rec>
+__device__ __forceinline__ void group_offer(at_entry* list, Rec& rec, int k, int r, uint64_t gm, bool active) {
     const uint64_t cfg = rec.cfg;
     const float sc = rec.score;
     const int count = active ? (int)rec.count : 0;

@@ -3,10 +3,12 @@
 // One annealing step of every chain is two kernels:
 //   k_chain  one lane per chain: folds the leaf values of the candidate just
 //            scored (tree order, fp32, from +0.0f), offers it to the chain's
-//            best list, applies the Metropolis test, then proposes the next
-//            candidate (one knob changed, Philox block (chain, step, 0, 0)),
-//            evaluates its loop-context features and writes them as packed
-//            bytes 4x+3, quad-major (dword q of chain c at Fg[q * n + c]).
+//            best list, applies the Metropolis test, then publishes the next
+//            candidate (one knob changed, Philox block (chain, step, 0, 0))
+//            and its loop-context features as packed bytes 4x+3,
+//            quad-major (dword q of chain c at Fg[q * n + c]).  The next
+//            candidates of both outcomes of the test, and their features,
+//            are built by the workgroup's other waves while the fold runs.
 //   k_trees  workgroup w holds the pointer form of trees [w*tpw, (w+1)*tpw)
 //            in LDS; each of its waves walks them for 64 chains at a time
 //            through its own LDS feature tile, writing the reached leaf
@@ -94,58 +96,6 @@ constexpr int REL_F = 192;              // context relation features per candida
 constexpr int REL_Q = REL_F / 4;
 
 
-// Score of the pending candidates of chains c0 .. c0+nc-1: lane j < nc of
-// wave 0 adds its chain's leaf values in tree order (fp32, from +0.0f).  All
-// four waves move the values into a ring of FOLD_R LDS buffers, each wave two
-// of a pass's eight direct-to-LDS instructions (one wave alone issues them
-// too slowly to keep the fold fed): pass p (groups p*FOLD_P ..) goes to
-// buffer p % FOLD_R, instruction i of a pass moves groups 4i .. 4i+3 of the
-// 16 chains (lane l: group 4i + l/16, chain c0 + l%16), so buffer entry
-// g * 16 + j holds group g of chain c0 + j.  FOLD_R - 1 passes stay in flight
-// while one is folded; a workgroup barrier per pass tells wave 0 that the
-// pass has landed and the other waves that the buffer they refill is free.
-constexpr int FOLD_SHARE = FOLD_P / 4 / (CHAIN_WG / 64);   // instructions per wave and pass
-static_assert(FOLD_SHARE * (CHAIN_WG / 64) * 4 == FOLD_P, "the waves share a pass evenly");
-
-__device__ __forceinline__ void fold_issue(const float4* __restrict__ V4, int T, int64_t c0, int nc, float4* ring,
-                                           int tid, int p) {
-    const int lane = tid & 63, wave = tid >> 6;
-    const int groups = (T + 3) >> 2;
-    const int j = lane & (CPW - 1);
-    const int64_t cj = c0 + (j < nc ? j : nc - 1);
-    float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
-#pragma unroll
-    for (int q = 0; q < FOLD_SHARE; ++q) {
-        const int ins = wave * FOLD_SHARE + q;
-        const int g = p * FOLD_P + ins * 4 + (lane >> 4);
-        const int gc = g < groups ? g : groups - 1;
-        // non-temporal (cache policy 2): V is read once
-        __builtin_amdgcn_global_load_lds(V4 + (((cj >> 4) * groups + gc) << 4) + (cj & 15), buf + ins * 64, 16, 0, 2);
-    }
-}
-
-// The first FOLD_R - 1 passes, issued at kernel entry so that they overlap
-// the set-up.
-__device__ __forceinline__ void fold_prime(const float4* __restrict__ V4, int T, int64_t c0, int nc, float4* ring,
-                                           int tid) {
-    const int npass = (((T + 3) >> 2) + FOLD_P - 1) / FOLD_P;
-    for (int p = 0; p < FOLD_R - 1 && p < npass; ++p) fold_issue(V4, T, c0, nc, ring, tid, p);
-}
-
-// Wait for this wave's moves up to pass p (later = its passes issued after
-// p), then meet the other waves.
-#define AT_VM_BARRIER(K) asm volatile("s_waitcnt vmcnt(" #K ")\n\ts_barrier" ::: "memory")
-__device__ __forceinline__ void pass_barrier(int later) {
-    static_assert(FOLD_SHARE == 2 && FOLD_R == 6, "the waits below count two moves per pass, at most four passes");
-    switch (later) {
-        case 0: AT_VM_BARRIER(0); break;
-        case 1: AT_VM_BARRIER(2); break;
-        case 2: AT_VM_BARRIER(4); break;
-        case 3: AT_VM_BARRIER(6); break;
-        default: AT_VM_BARRIER(8); break;
-    }
-}
-
 // Batches of FOLD_B groups (stride CPW float4 in the ring): the reads of a
 // batch, then its adds in tree order.
 constexpr int FOLD_B = 8;
@@ -228,20 +178,61 @@ __device__ __forceinline__ void fold_pass(float& s, uint32_t ad) {
 }
 #undef AT_FOLD_WAIT
 
-// Every wave of the workgroup calls this (it holds workgroup barriers); the
-// score is valid in lanes j < nc of wave 0.
-__device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int T, int64_t c0, int nc, float4* ring,
-                                           int tid) {
-    const int lane = tid & 63, wave = tid >> 6;
+// The leaf values of chain block c0 for fold pass p (groups p*FOLD_P ..,
+// one contiguous stretch of FOLD_P * CPW float4) moved by eight 1 KB
+// direct-to-LDS loads of the calling wave into ring buffer p % FOLD_R, so
+// that entry g * CPW + j holds group g of chain c0 + j.  Past the last
+// group the loads repeat the last float4 (never folded).
+__device__ __forceinline__ void ring_issue(const float4* __restrict__ blk, int last, float4* ring, int p, int lane) {
+    float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
+#pragma unroll
+    for (int i = 0; i < FOLD_P * CPW / 64; ++i) {
+        int idx = p * (FOLD_P * CPW) + i * 64 + lane;
+        idx = idx < last ? idx : last;
+        // non-temporal (cache policy 2): V is read once
+        __builtin_amdgcn_global_load_lds(blk + idx, buf + i * 64, 16, 0, 2);
+    }
+}
+
+// Wait until at most `later` passes of this wave's ring moves are
+// outstanding (the moves of older passes, and every older load, have
+// landed).
+#define AT_VM_WAIT(K) asm volatile("s_waitcnt vmcnt(" #K ")" ::: "memory")
+__device__ __forceinline__ void ring_wait(int later) {
+    static_assert(FOLD_P * CPW / 64 == 8 && FOLD_R == 6, "the waits below count eight moves per pass, at most five passes");
+    switch (later) {
+        case 0: AT_VM_WAIT(0); break;
+        case 1: AT_VM_WAIT(8); break;
+        case 2: AT_VM_WAIT(16); break;
+        case 3: AT_VM_WAIT(24); break;
+        case 4: AT_VM_WAIT(32); break;
+        default: AT_VM_WAIT(40); break;
+    }
+}
+#undef AT_VM_WAIT
+
+// Score of the pending candidates of chain block c0 from one model's leaf
+// values V (T trees): lane j < nc of the calling wave adds its chain's
+// values in tree order (fp32, from +0.0f).  The wave alone moves the values
+// into the LDS ring, FOLD_R passes ahead, so no other wave takes part.
+// A pass's buffer is refilled at the start of the next pass, after its
+// reads have completed.
+__device__ __forceinline__ float fold_wave(const float* __restrict__ V, int T, int64_t c0, int nc, float4* ring,
+                                           int lane) {
     const int groups = (T + 3) >> 2;
     const int npass = (groups + FOLD_P - 1) / FOLD_P;
+    const float4* blk = reinterpret_cast<const float4*>(V) + (c0 >> 4) * (int64_t)groups * CPW;
+    const int last = groups * CPW - 1;
+    int issued = 0;
+    for (; issued < FOLD_R - 1 && issued < npass; ++issued) ring_issue(blk, last, ring, issued, lane);
     float s = 0.0f;
     for (int p = 0; p < npass; ++p) {
-        const int issued = p + FOLD_R - 2 < npass - 1 ? p + FOLD_R - 2 : npass - 1;
-        pass_barrier(issued - p);
-        // the buffer pass p + R - 1 takes was folded before the barrier
-        if (p + FOLD_R - 1 < npass) fold_issue(V4, T, c0, nc, ring, tid, p + FOLD_R - 1);
-        if (wave == 0 && lane < nc) {
+        if (issued < npass) {
+            ring_issue(blk, last, ring, issued, lane);
+            ++issued;
+        }
+        ring_wait(issued - 1 - p);
+        if (lane < nc) {
             const float4* src = ring + (p % FOLD_R) * (FOLD_P * CPW) + lane;
             const int ng = groups - p * FOLD_P < FOLD_P ? groups - p * FOLD_P : FOLD_P;
             const int r = (p == npass - 1) ? (T & 3) : 0;   // trees in a last, partial group
@@ -274,51 +265,137 @@ __device__ __forceinline__ float fold_ring(const float4* __restrict__ V4, int T,
     return s;
 }
 
+// The first configuration of a chain: each knob uniform over its values,
+// Philox block (chain, 0, 1, j / 4) word j % 4.
+__device__ __forceinline__ void init_draw(const SpaceDesc& sd, uint32_t k0, uint32_t k1, uint32_t gchain,
+                                          uint32_t (&nx)[MAX_KNOBS]) {
+    U4 r{0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < MAX_KNOBS; ++j) {
+        if ((j & 3) == 0) r = philox(k0, k1, U4{gchain, 0u, 1u, (uint32_t)(j >> 2)});
+        const uint32_t word = (j & 3) == 0 ? r.x : (j & 3) == 1 ? r.y : (j & 3) == 2 ? r.z : r.w;
+        nx[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
+    }
+}
+
+// The move of step `step` from configuration kv: one knob, uniform among
+// those with two or more values, goes to a uniformly chosen other value;
+// Philox block (chain, step, 0, 0).  The block does not depend on kv, so
+// the moves from the two possible states of a step draw the same numbers.
+__device__ __forceinline__ void step_move(const SpaceDesc& sd, uint32_t k0, uint32_t k1, uint32_t gchain,
+                                          uint32_t step, const uint32_t (&kv)[MAX_KNOBS], uint32_t (&nx)[MAX_KNOBS]) {
+    const U4 r = philox(k0, k1, U4{gchain, step, 0u, 0u});
+#pragma unroll
+    for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = kv[j];
+    if (sd.n_mut > 0) {
+        const int jm = sd.mut[uniform_below(r.x, (uint32_t)sd.n_mut)];
+        uint32_t old = 0, size = 2;
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j)
+            if (j == jm) {
+                old = kv[j];
+                size = sd.knob_size[j];
+            }
+        uint32_t nv = uniform_below(r.y, size - 1u);
+        if (nv >= old) nv += 1u;
+#pragma unroll
+        for (int j = 0; j < MAX_KNOBS; ++j)
+            if (j == jm) nx[j] = nv;
+    }
+}
+
+// Loop l's eleven loop-context features of configuration nx into row[l *
+// 11 ..], and bitlen(top-down product) into td[l] when asked for.
+template <int TMPL>
+__device__ __forceinline__ void row_features(const SpaceDesc& sd, const uint64_t* facp, const uint32_t (&nx)[MAX_KNOBS],
+                                             int l, bool want_td, uint8_t* row, uint8_t* td) {
+    uint32_t fac[6][4];
+    gather_factors<TMPL>(sd, facp, nx, fac);
+    uint32_t f[11], t = 0u;
+    loop_features<TMPL>(sd, fac, ann_knobs_of<TMPL>(sd, nx), l, f, want_td ? &t : nullptr);
+#pragma unroll
+    for (int i = 0; i < 11; ++i) row[l * 11 + i] = (uint8_t)f[i];
+    td[l] = (uint8_t)t;
+}
+
+__device__ __forceinline__ uint32_t pack_pair(const uint32_t (&nx)[MAX_KNOBS], int j) {
+    return nx[2 * j] | (nx[2 * j + 1] << 16);
+}
+
+__device__ __forceinline__ void unpack_pairs(const uint32_t* w, uint32_t (&nx)[MAX_KNOBS]) {
+#pragma unroll
+    for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (w[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+}
+
+// Per-chain record of the chain kernel, shared through LDS.
+struct TpRec {
+    uint64_t cfg;                       // the pending candidate's configuration index
+    float score;
+    uint32_t count;                     // best list: entries, k-th entry
+    float kth_score;
+    uint32_t qual;
+    uint64_t kth_cfg;
+    uint32_t nx[2][MAX_KNOBS / 2];      // next candidate after an accept [0] or a reject [1]
+};
+
+// One annealing step of CPW chains (see the top of this file).  With a
+// pending candidate, wave 0 folds its score while waves 1-3 bring the best
+// lists into LDS and build, for every chain, both candidates that can come
+// next (a move from the pending candidate if it is accepted, from the
+// current configuration if not) and the loop-context features of both;
+// once the score is known the owner lanes (wave 0, lane j: chain c0 + j)
+// offer the candidate to the best list, take the Metropolis decision and
+// the rows of the candidate that follows go out.
 template <int TMPL>
 __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     using N = Nest<TMPL>;
+    constexpr int L = N::L;
     constexpr int Q = (N::F + 3) / 4;
     constexpr int RS = Q * 4 + 4;                 // feature row stride (bytes) in LDS
     // dynamic LDS: the fold ring, then the chains' best lists [CPW][topk]
     extern __shared__ float4 ring[];
-    __shared__ ChainRec rec[CPW];
-    __shared__ __attribute__((aligned(16))) uint8_t frow[CPW][RS];
+    __shared__ TpRec rec[CPW];
+    __shared__ __attribute__((aligned(16))) uint8_t frow[2][CPW][RS];
+    __shared__ uint8_t tdrow[2][CPW][16];
+    __shared__ __attribute__((aligned(16))) uint8_t s_img[STAGE_MAX_BYTES];
+    __shared__ __attribute__((aligned(16))) uint16_t s_kv[2][CPW][MAX_KNOBS];   // current, pending knobs
+    __shared__ uint32_t s_sel[CPW];
+    __shared__ uint32_t s_any;
     const int tid = threadIdx.x;
-    const int wave = tid >> 6;
+    const int lane = tid & 63, wave = tid >> 6;
     const int64_t c0 = (int64_t)blockIdx.x * CPW;
     const int nc = (a.n - c0 < CPW) ? (int)(a.n - c0) : CPW;
     const bool owner = tid < nc;                 // lanes of wave 0 that own a chain
     const int64_t c = c0 + (owner ? tid : 0);
     const int k = a.topk;
+    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
     // group of 16 lanes per chain for the best-list offer and the features
     const int gj = tid >> 4, gr = tid & 15;
     const uint64_t gmask = 0xffffull << (16 * (gj & 3));
     const bool gvalid = gj < nc;
+    at_entry* lists = reinterpret_cast<at_entry*>(ring + RING_BYTES / 16);
 
     // The workgroup's space: when all its chains share one space whose image
     // fits, the image (descriptor with rebased split offsets, then the split
     // factors) moves straight into LDS; otherwise each lane reads its own
-    // space from global memory.  No load of the prologue is waited for before
-    // the fold: the fold's first pass barrier (or, with no fold, the barrier
-    // below) finds them complete.
-    __shared__ __attribute__((aligned(16))) uint8_t s_img[STAGE_MAX_BYTES];
+    // chain's space from global memory.
     const int ws = a.n_spaces == 1 ? a.stage_single : a.wg_space[blockIdx.x];
     const bool staged = ws >= 0;
-    if (staged) {
-        const uint8_t* src = a.stage + (int64_t)ws * a.stage_stride + (tid & 63) * 16;
-        for (int off = wave * 1024; off < a.stage_stride; off += CHAIN_WG * 16)
-            __builtin_amdgcn_global_load_lds(src + off, s_img + off, 16, 0, 0);
-    }
     const SpaceDesc* s_desc = reinterpret_cast<const SpaceDesc*>(s_img);
     const uint64_t* facp = staged ? reinterpret_cast<const uint64_t*>(s_img + STAGE_DESC_BYTES) : a.factors;
-    // owner lanes: their chain's space; group lanes: the space of chain gj
-    const SpaceDesc* sdp = staged ? s_desc : a.descs + space_of(a.offsets, a.n_spaces, c);
-    const SpaceDesc* gsdp = staged ? s_desc : a.descs + space_of(a.offsets, a.n_spaces, c0 + (gvalid ? gj : 0));
+    auto desc_of = [&](int j) -> const SpaceDesc& {
+        return staged ? *s_desc : a.descs[space_of(a.offsets, a.n_spaces, c0 + j)];
+    };
+    auto copy_image = [&](int first, int stride) {
+        const uint8_t* src = a.stage + (int64_t)ws * a.stage_stride + lane * 16;
+        for (int off = first * 1024; off < a.stage_stride; off += stride * 1024)
+            __builtin_amdgcn_global_load_lds(src + off, s_img + off, 16, 0, 0);
+    };
 
-    // per-chain state, in flight during the fold (used after it).  Every
-    // lane loads from valid addresses (c is chain c0 for lanes that own no
-    // chain; the threshold is read from the scores when there is none), so
-    // no branch joins the loaded values: a join would wait for them here.
+    // per-chain state of the owner lanes, in flight while the score is
+    // folded.  Every lane loads from valid addresses (c is chain c0 for lanes
+    // that own no chain; the threshold is read from the scores when there is
+    // none), so no branch joins the loaded values: a join would wait for them.
     uint2 kraw[3], craw[3];
     load_knob_words(a.knobs, c, kraw);
     load_knob_words(a.cand, c, craw);
@@ -328,111 +405,144 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     int64_t thr_i = a.fin == FIN_STEP ? c * a.steps + a.fin_step : c;
     asm volatile("" : "+v"(thr_i));   // one load from either table (not two loads and a join)
     const float thr_v = thr_b[thr_i];
-    // the leaf values of the pending candidates start streaming in
-    if (a.fin != FIN_NONE) {
-        if (a.Vg)
-            fold_prime(reinterpret_cast<const float4*>(a.Vg), a.Tg, c0, nc, ring, tid);
-        else
-            fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
-    } else {
-        // no fold: the image lands before the proposal reads it
+
+    if (a.fin == FIN_NONE) {
+        // No pending candidate: the first draw of fresh chains, or a move
+        // from the current configurations, or only the best lists' copy.
+        if (a.best) {
+            for (int idx = tid; idx < nc * k; idx += CHAIN_WG) a.best[c0 * k + idx] = a.top[c0 * k + idx];
+        }
+        if (a.draw == DRAW_NONE) return;
+        if (staged) copy_image(wave, CHAIN_WG / 64);
         asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-    }
-    uint32_t cur[MAX_KNOBS], cd[MAX_KNOBS];
-
-    if (a.fin != FIN_NONE) {
-        // score of the pending candidate (wave 0, fed by every wave); waves
-        // 1-3 first bring the chains' best lists into LDS (an initial list
-        // is empty)
-        at_entry* lists = reinterpret_cast<at_entry*>(ring + RING_BYTES / 16);
-        if (wave == 0) {
-        } else if (a.fin == FIN_STEP) {
-            const at_entry* src = a.top + c0 * k;
-            const int total = nc * k;
-            for (int ins = wave - 1; ins * 64 < total; ins += CHAIN_WG / 64 - 1) {
-                const int e = ins * 64 + (tid & 63);
-                if (e < total) __builtin_amdgcn_global_load_lds(src + e, lists + ins * 64, 16, 0, 0);
-            }
-        } else {
-            for (int e = tid - 64; e < nc * k; e += CHAIN_WG - 64) {
-                at_entry z;
-                z.cfg = 0;
-                z.score = 0.0f;
-                z.flag = 0u;
-                lists[e] = z;
-            }
-        }
-        float s;
-        if (a.Vg) {
-            // Eq. 4: each model's prediction is its own fold from +0.0f;
-            // the sum adds the global one first
-            const float sg = fold_ring(reinterpret_cast<const float4*>(a.Vg), a.Tg, c0, nc, ring, tid);
-            // wave 0 has read the global model's last pass before the ring
-            // takes the local model's first ones
-            lds_barrier();
-            fold_prime(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
-            const float sl = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
-            s = sg + sl;
-        } else {
-            s = fold_ring(reinterpret_cast<const float4*>(a.V), a.T, c0, nc, ring, tid);
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        unpack_knobs(kraw, cur);
-        unpack_knobs(craw, cd);
-        if (a.fin != FIN_STEP) {
-            // a fresh chain: empty best list
-            m.count = 0;
-            m.kth_score = 0.0f;
-            m.kth_cfg = 0;
-        }
-
-        // best lists: the chain's group of 16 lanes inserts the candidate
-        // into its list in LDS when it qualifies; changed lists are written
-        // back.  Skipped when no chain qualifies.
-        uint64_t cfg = 0;
-        int qual = 0;
-        __shared__ uint32_t s_any;
         if (owner) {
-            const SpaceDesc& sd = *sdp;
+            const SpaceDesc& sd = desc_of(tid);
+            const uint32_t gchain = (uint32_t)(a.chain0 + (uint64_t)c);
+            uint32_t nx[MAX_KNOBS];
+            if (a.draw == DRAW_INIT) {
+                init_draw(sd, k0, k1, gchain, nx);
+            } else {
+                uint32_t cur[MAX_KNOBS];
+                unpack_knobs(kraw, cur);
+                step_move(sd, k0, k1, gchain, a.draw_step, cur, nx);
+            }
+            store_knobs(a.cand, c, nx);
 #pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j)
-                if (j < sd.n_knobs) cfg += (uint64_t)cd[j] * sd.radix[j];
+            for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[0][j] = pack_pair(nx, j);
+            s_sel[tid] = 0u;
+        }
+        lds_barrier();
+        // lane gr of group gj: loop gr of chain gj's candidate
+        if (gvalid && gr < L) {
+            uint32_t nx[MAX_KNOBS];
+            unpack_pairs(rec[gj].nx[0], nx);
+            row_features<TMPL>(desc_of(gj), facp, nx, gr, a.Fr != nullptr, frow[0][gj], tdrow[0][gj]);
+        }
+    } else {
+        float s = 0.0f;
+        if (wave == 0) {
+            // the fold is a chain of dependent adds: its wave goes first
+            // whenever it can issue, ahead of the candidate building
+            __builtin_amdgcn_s_setprio(3);
+            // Eq. 4: each model's prediction is its own fold from +0.0f; the
+            // sum adds the global one first
+            if (a.Vg) {
+                const float sg = fold_wave(a.Vg, a.Tg, c0, nc, ring, lane);
+                const float sl = fold_wave(a.V, a.T, c0, nc, ring, lane);
+                s = sg + sl;
+            } else {
+                s = fold_wave(a.V, a.T, c0, nc, ring, lane);
+            }
+            __builtin_amdgcn_s_setprio(0);
+        } else {
+            // waves 1-3: each copies the whole space image and the chains'
+            // knobs (identical bytes, so the copies may overlap) and waits
+            // for its own moves only; the best lists are shared out
+            if (staged) copy_image(0, 1);
+            {
+                const int nb = nc * MAX_KNOBS * 2;           // bytes of one knob array
+                const uint8_t* kp = reinterpret_cast<const uint8_t*>(a.knobs + c0 * MAX_KNOBS);
+                const uint8_t* cp = reinterpret_cast<const uint8_t*>(a.cand + c0 * MAX_KNOBS);
+                uint8_t* d = reinterpret_cast<uint8_t*>(&s_kv[0][0][0]);
+                constexpr int KB = CPW * MAX_KNOBS * 2;      // LDS bytes of one knob array
+                static_assert(2 * KB == 3 * 256, "three dword moves of 64 lanes");
+#pragma unroll
+                for (int i = 0; i < 3; ++i) {
+                    const int byte = i * 256 + lane * 4;     // of the two arrays, current first
+                    const int arr = byte >= KB ? 1 : 0, off = byte - arr * KB;
+                    if (off < nb) __builtin_amdgcn_global_load_lds((arr ? cp : kp) + off, d + i * 256, 4, 0, 0);
+                }
+            }
+            if (a.fin == FIN_STEP) {
+                const at_entry* src = a.top + c0 * k;
+                const int total = nc * k;
+                for (int ins = wave - 1; ins * 64 < total; ins += CHAIN_WG / 64 - 1) {
+                    const int e = ins * 64 + lane;
+                    if (e < total) __builtin_amdgcn_global_load_lds(src + e, lists + ins * 64, 16, 0, 0);
+                }
+            } else {
+                // an initial list is empty
+                for (int e = tid - 64; e < nc * k; e += CHAIN_WG - 64) {
+                    at_entry z;
+                    z.cfg = 0;
+                    z.score = 0.0f;
+                    z.flag = 0u;
+                    lists[e] = z;
+                }
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            // the pending candidates' configuration indices
+            const int t0 = tid - 64;
+            if (t0 < nc) {
+                const SpaceDesc& sd = desc_of(t0);
+                uint64_t cfg = 0;
+#pragma unroll
+                for (int j = 0; j < MAX_KNOBS; ++j)
+                    if (j < sd.n_knobs) cfg += (uint64_t)s_kv[1][t0][j] * sd.radix[j];
+                rec[t0].cfg = cfg;
+            }
+            // both next candidates of every chain and their loop features:
+            // task t is loop t % L of outcome (t / L) & 1 of chain t / (2L)
+            // (an initial candidate is always accepted: no reject outcome)
+            if (a.draw == DRAW_PROPOSE) {
+                for (int t = t0; t < nc * 2 * L; t += CHAIN_WG - 64) {
+                    const int l = t % L, jo = t / L, j = jo >> 1, o = jo & 1;
+                    if (o == 1 && a.fin == FIN_INIT) continue;
+                    const SpaceDesc& sd = desc_of(j);
+                    uint32_t base[MAX_KNOBS], nx[MAX_KNOBS];
+#pragma unroll
+                    for (int i = 0; i < MAX_KNOBS; ++i) base[i] = s_kv[o ^ 1][j][i];
+                    step_move(sd, k0, k1, (uint32_t)(a.chain0 + (uint64_t)(c0 + j)), a.draw_step, base, nx);
+                    if (l == 0) {
+#pragma unroll
+                        for (int i = 0; i < MAX_KNOBS / 2; ++i) rec[j].nx[o][i] = pack_pair(nx, i);
+                    }
+                    row_features<TMPL>(sd, facp, nx, l, a.Fr != nullptr, frow[o][j], tdrow[o][j]);
+                }
+            }
+        }
+        // score known (wave 0), candidates built (waves 1-3)
+        lds_barrier();
+
+        // owner lanes: qualification for the best list, the Metropolis
+        // decision, the chain's state
+        int qual = 0;
+        bool acc = true;
+        if (owner) {
+            if (a.fin != FIN_STEP) {
+                // a fresh chain: empty best list
+                m.count = 0;
+                m.kth_score = 0.0f;
+                m.kth_cfg = 0;
+            }
+            TpRec& R = rec[tid];
+            const uint64_t cfg = R.cfg;
             qual = (a.fin == FIN_INIT || (int)m.count < k || precedes(s, cfg, m.kth_score, m.kth_cfg)) ? 1 : 0;
-            ChainRec& R = rec[tid];
-            R.cfg = cfg;
             R.score = s;
             R.count = m.count;
             R.kth_score = m.kth_score;
             R.kth_cfg = m.kth_cfg;
             R.qual = (uint32_t)qual;
-        } else if (tid < CPW) {
-            rec[tid].qual = 0;
-        }
-        if (wave == 0) {
-            const uint64_t q = __ballot(qual);
-            if (tid == 0) s_any = q != 0 ? 1u : 0u;
-        }
-        // the barriers from here on order LDS only: a full __syncthreads
-        // would also wait for this workgroup's global stores (best lists,
-        // trace, state) to drain
-        lds_barrier();
-        if (s_any) {
-            group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
-            lds_barrier();
-            for (int idx = tid; idx < nc * k; idx += CHAIN_WG) {
-                const int j = idx / k;
-                if (rec[j].qual) a.top[c0 * k + idx] = lists[idx];
-            }
-        }
-        if (owner) {
-            if (qual) {
-                const ChainRec& R = rec[tid];
-                m.count = R.count;
-                m.kth_score = R.kth_score;
-                m.kth_cfg = R.kth_cfg;
-                a.meta[c] = m;
-            }
-            bool acc = true;
             if (a.fin == FIN_STEP) {
                 const float delta = s - cur_s;
                 acc = delta >= thr_v;
@@ -445,78 +555,56 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
                 }
             }
             if (acc) {
-#pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j) cur[j] = cd[j];
-                store_knobs(a.knobs, c, cur);
+                reinterpret_cast<uint2*>(a.knobs)[3 * c] = craw[0];
+                reinterpret_cast<uint2*>(a.knobs)[3 * c + 1] = craw[1];
+                reinterpret_cast<uint2*>(a.knobs)[3 * c + 2] = craw[2];
                 a.cur_score[c] = s;
             }
-        }
-    }
-
-    if (a.best) {
-        // the lists were written back above by this workgroup
-        __syncthreads();
-        for (int idx = tid; idx < nc * k; idx += CHAIN_WG) a.best[c0 * k + idx] = a.top[c0 * k + idx];
-    }
-    if (a.draw == DRAW_NONE) return;
-    if (a.fin == FIN_NONE) unpack_knobs(kraw, cur);
-
-    // proposal (owner lanes)
-    if (owner) {
-        const SpaceDesc& sd = *sdp;
-        const uint64_t gchain = a.chain0 + (uint64_t)c;
-        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-        uint32_t nx[MAX_KNOBS];
-        if (a.draw == DRAW_INIT) {
-            // each knob uniform over its values: block (chain, 0, 1, j / 4)
-            U4 r{0, 0, 0, 0};
-#pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j) {
-                if ((j & 3) == 0) r = philox(k0, k1, U4{(uint32_t)gchain, 0u, 1u, (uint32_t)(j >> 2)});
-                const uint32_t word = (j & 3) == 0 ? r.x : (j & 3) == 1 ? r.y : (j & 3) == 2 ? r.z : r.w;
-                nx[j] = (j < sd.n_knobs) ? uniform_below(word, sd.knob_size[j]) : 0u;
+            const int o = acc ? 0 : 1;
+            s_sel[tid] = (uint32_t)o;
+            if (a.draw == DRAW_PROPOSE) {
+                uint2* w = reinterpret_cast<uint2*>(a.cand) + 3 * c;
+                w[0] = make_uint2(R.nx[o][0], R.nx[o][1]);
+                w[1] = make_uint2(R.nx[o][2], R.nx[o][3]);
+                w[2] = make_uint2(R.nx[o][4], R.nx[o][5]);
             }
-        } else {
-            // one knob, uniform among those with two or more values, moves to a
-            // uniformly chosen other value: block (chain, step, 0, 0)
-            const U4 r = philox(k0, k1, U4{(uint32_t)gchain, a.draw_step, 0u, 0u});
-#pragma unroll
-            for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = cur[j];
-            if (sd.n_mut > 0) {
-                const int jm = sd.mut[uniform_below(r.x, (uint32_t)sd.n_mut)];
-                uint32_t old = 0, size = 2;
-#pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j)
-                    if (j == jm) { old = cur[j]; size = sd.knob_size[j]; }
-                uint32_t nv = uniform_below(r.y, size - 1u);
-                if (nv >= old) nv += 1u;
-#pragma unroll
-                for (int j = 0; j < MAX_KNOBS; ++j)
-                    if (j == jm) nx[j] = nv;
+        } else if (tid < CPW) {
+            rec[tid].qual = 0;
+        }
+        if (wave == 0) {
+            const uint64_t q = __ballot(qual);
+            if (tid == 0) s_any = q != 0 ? 1u : 0u;
+        }
+        // the barriers from here on order LDS only: a full __syncthreads
+        // would also wait for this workgroup's global stores (best lists,
+        // trace, state) to drain
+        lds_barrier();
+
+        // best lists: the chain's group of 16 lanes inserts the candidate
+        // into its list in LDS when it qualifies; changed lists are written
+        // back.  Skipped when no chain qualifies.
+        if (s_any) {
+            group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
+            lds_barrier();
+            for (int idx = tid; idx < nc * k; idx += CHAIN_WG) {
+                const int j = idx / k;
+                if (rec[j].qual) a.top[c0 * k + idx] = lists[idx];
+            }
+            if (owner && qual) {
+                const TpRec& R = rec[tid];
+                m.count = R.count;
+                m.kth_score = R.kth_score;
+                m.kth_cfg = R.kth_cfg;
+                a.meta[c] = m;
             }
         }
-        store_knobs(a.cand, c, nx);
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS / 2; ++j) rec[tid].nx[j] = nx[2 * j] | (nx[2 * j + 1] << 16);
+        if (a.best) {
+            for (int idx = tid; idx < nc * k; idx += CHAIN_WG) a.best[c0 * k + idx] = lists[idx];
+        }
+        if (a.draw == DRAW_NONE) return;
     }
-    lds_barrier();
 
-    // features: lane gr of group gj evaluates loop gr of chain gj's candidate
-    __shared__ uint8_t tdrow[CPW][16];
-    if (gvalid && gr < N::L) {
-        const SpaceDesc& sd = *gsdp;
-        uint32_t nx[MAX_KNOBS];
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j) nx[j] = (rec[gj].nx[j >> 1] >> (16 * (j & 1))) & 0xffffu;
-        uint32_t fac[6][4];
-        gather_factors<TMPL>(sd, facp, nx, fac);
-        uint32_t f[11], td = 0u;
-        loop_features<TMPL>(sd, fac, ann_knobs_of<TMPL>(sd, nx), gr, f, a.Fr ? &td : nullptr);
-#pragma unroll
-        for (int i = 0; i < 11; ++i) frow[gj][gr * 11 + i] = (uint8_t)f[i];
-        tdrow[gj][gr] = (uint8_t)td;
-    }
-    lds_barrier();
+    // the rows of each chain's next candidate: outcome s_sel[j]
     if (a.Fr) {
         // context relation features of the candidate (Section 4): output
         // o = [pair][buffer b][t - 1] is the largest value over the loops
@@ -526,15 +614,17 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         // outputs gr, gr + 16, ...
         __shared__ __attribute__((aligned(16))) uint8_t rrow[CPW][REL_F];
         if (gvalid) {
+            const uint8_t* fr = frow[s_sel[gj]][gj];
+            const uint8_t* tr = tdrow[s_sel[gj]][gj];
 #pragma unroll 1
             for (int o = gr; o < REL_F; o += 16) {
                 const int pair = o / 96, b = (o >> 5) % 3;
                 const uint32_t t = (uint32_t)(o & 31) + 1u;
                 uint32_t v = 0u;
 #pragma unroll
-                for (int l = 0; l < N::L; ++l) {
-                    const uint32_t bt = frow[gj][l * 11 + 2 + 3 * b];
-                    const uint32_t x = pair ? (uint32_t)tdrow[gj][l] : (uint32_t)frow[gj][l * 11 + 3 + 3 * b];
+                for (int l = 0; l < L; ++l) {
+                    const uint32_t bt = fr[l * 11 + 2 + 3 * b];
+                    const uint32_t x = pair ? (uint32_t)tr[l] : (uint32_t)fr[l * 11 + 3 + 3 * b];
                     v = (bt <= t && x > v) ? x : v;
                 }
                 rrow[gj][o] = (uint8_t)v;
@@ -547,6 +637,8 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             const uint32_t w = (*reinterpret_cast<const uint32_t*>(&rrow[j][4 * q]) << 2) | 0x03030303u;
             a.Fr[(int64_t)q * a.fg_stride + c0 + j] = w;
         }
+    } else {
+        lds_barrier();
     }
     // packed rows out (4x+3 per byte, the tree kernel's tile encoding),
     // consecutive lanes on consecutive chains
@@ -555,7 +647,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     for (int idx = tid; idx < CPW * Q; idx += CHAIN_WG) {
         const int q = idx >> 4, j = idx & (CPW - 1);
         if (j >= nc) continue;
-        uint32_t w = (*reinterpret_cast<const uint32_t*>(&frow[j][4 * q]) << 2) | 0x03030303u;
+        uint32_t w = (*reinterpret_cast<const uint32_t*>(&frow[s_sel[j]][j][4 * q]) << 2) | 0x03030303u;
         if (q == Q - 1) w &= LAST;
         a.Fg[(int64_t)q * a.fg_stride + c0 + j] = w;
     }
