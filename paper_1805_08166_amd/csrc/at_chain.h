@@ -97,8 +97,12 @@ struct ChainRec {
 // group's 16 bits of a ballot mask and `active` the lanes of a group whose
 // chain offers.
 // Rec: any record with cfg, score, count, kth_score and kth_cfg.
+// gout / gmeta (optional): the chain's list and ChainMeta in global memory;
+// every entry the offer changes and the list's new count and k-th entry are
+// also written there by the lane that makes them.
 template <class Rec>
-__device__ __forceinline__ void group_offer(at_entry* list, Rec& rec, int k, int r, uint64_t gm, bool active) {
+__device__ __forceinline__ void group_offer(at_entry* list, Rec& rec, int k, int r, uint64_t gm, bool active,
+                                            at_entry* gout = nullptr, ChainMeta* gmeta = nullptr) {
     const uint64_t cfg = rec.cfg;
     const float sc = rec.score;
     const int count = active ? (int)rec.count : 0;
@@ -136,10 +140,18 @@ __device__ __forceinline__ void group_offer(at_entry* list, Rec& rec, int k, int
                 e = prev[u];
             }
             list[i] = e;
+            if (gout) gout[i] = e;
             if (i == n_new - 1) {
                 rec.count = (uint32_t)n_new;
                 rec.kth_score = e.score;
                 rec.kth_cfg = e.cfg;
+                if (gmeta) {
+                    ChainMeta m;
+                    m.count = (uint32_t)n_new;
+                    m.kth_score = e.score;
+                    m.kth_cfg = e.cfg;
+                    *gmeta = m;
+                }
             }
         }
     }

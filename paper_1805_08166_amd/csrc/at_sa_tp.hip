@@ -438,6 +438,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             unpack_pairs(rec[gj].nx[0], nx);
             row_features<TMPL>(desc_of(gj), facp, nx, gr, a.Fr != nullptr, frow[0][gj], tdrow[0][gj]);
         }
+        lds_barrier();
     } else {
         float s = 0.0f;
         if (wave == 0) {
@@ -581,30 +582,23 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
         lds_barrier();
 
         // best lists: the chain's group of 16 lanes inserts the candidate
-        // into its list in LDS when it qualifies; changed lists are written
-        // back.  Skipped when no chain qualifies.
+        // into its list in LDS when it qualifies, each lane writing the
+        // entries it changes (and the new count and k-th entry) to global
+        // memory as well.  Skipped when no chain qualifies.
         if (s_any) {
-            group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0);
-            lds_barrier();
-            for (int idx = tid; idx < nc * k; idx += CHAIN_WG) {
-                const int j = idx / k;
-                if (rec[j].qual) a.top[c0 * k + idx] = lists[idx];
-            }
-            if (owner && qual) {
-                const TpRec& R = rec[tid];
-                m.count = R.count;
-                m.kth_score = R.kth_score;
-                m.kth_cfg = R.kth_cfg;
-                a.meta[c] = m;
-            }
+            const int64_t cg = c0 + (gvalid ? gj : 0);
+            group_offer(lists + gj * k, rec[gj], k, gr, gmask, gvalid && rec[gj].qual != 0, a.top + cg * k,
+                        a.meta + cg);
         }
         if (a.best) {
+            lds_barrier();
             for (int idx = tid; idx < nc * k; idx += CHAIN_WG) a.best[c0 * k + idx] = lists[idx];
         }
         if (a.draw == DRAW_NONE) return;
     }
 
-    // the rows of each chain's next candidate: outcome s_sel[j]
+    // the rows of each chain's next candidate: outcome s_sel[j] (rows and
+    // choices are in LDS since the last barrier)
     if (a.Fr) {
         // context relation features of the candidate (Section 4): output
         // o = [pair][buffer b][t - 1] is the largest value over the loops
@@ -637,8 +631,6 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             const uint32_t w = (*reinterpret_cast<const uint32_t*>(&rrow[j][4 * q]) << 2) | 0x03030303u;
             a.Fr[(int64_t)q * a.fg_stride + c0 + j] = w;
         }
-    } else {
-        lds_barrier();
     }
     // packed rows out (4x+3 per byte, the tree kernel's tile encoding),
     // consecutive lanes on consecutive chains
