@@ -38,7 +38,9 @@ __device__ __forceinline__ int64_t v_index(int64_t c, int t, int groups) {
     return ((((c >> 4) * groups + (t >> 2)) << 6) + ((c & 15) << 2) + (t & 3));
 }
 
-constexpr int CHAIN_WG = 256;           // wave 0 runs the chains, all four waves move data
+// Chain-kernel workgroups have 256 or 512 threads (template argument
+// CHAIN_WG): wave 0 folds, the others build the next candidates (see
+// launch_sa_tp for the choice).
 constexpr int CPW = 16;                 // chains per chain-kernel workgroup
 static_assert(CPW == 16 && CPW == STAGE_CHAINS, "a chain-kernel workgroup reads one 16-chain block of V");
 constexpr int FOLD_P = 32;              // 4-tree groups per fold pass: 32 x 16 chains x 16 B = 8 KB
@@ -346,7 +348,7 @@ struct TpRec {
 // once the score is known the owner lanes (wave 0, lane j: chain c0 + j)
 // offer the candidate to the best list, take the Metropolis decision and
 // the rows of the candidate that follows go out.
-template <int TMPL>
+template <int TMPL, int CHAIN_WG>
 __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     using N = Nest<TMPL>;
     constexpr int L = N::L;
@@ -1357,8 +1359,10 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
     }
     static bool chain_configured = false;
     if (!chain_configured) {
-        for (const void* f : {reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM>),
-                              reinterpret_cast<const void*>(&k_chain<AT_TMPL_CONV2D_NCHW>)}) {
+        for (const void* f : {reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM, 256>),
+                              reinterpret_cast<const void*>(&k_chain<AT_TMPL_CONV2D_NCHW, 256>),
+                              reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM, 512>),
+                              reinterpret_cast<const void*>(&k_chain<AT_TMPL_CONV2D_NCHW, 512>)}) {
             if ((err = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)(RING_BYTES + (size_t)CPW * KMAX * sizeof(at_entry)))) != hipSuccess)
                 return err;
@@ -1366,16 +1370,25 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
         chain_configured = true;
     }
     ch.events_used[0] = ch.events_used[1] = 0;
+    // While wave 0 folds, the other waves build both next candidates of 16
+    // chains (2 x 16 x L loop-feature tasks).  With a short fold (under 1500
+    // trees in all) that building is the longer of the two and eight waves
+    // take it (twelve conv2d workloads, 1000 trees: 14.2 -> 13.3 ms a run);
+    // with a long fold four waves leave the folding wave more of its SIMD
+    // (C12, 2000 trees: 56.6 against 57.1 ms).
+    const bool wide = e.n_trees + (eg ? eg->n_trees : 0) < 1500;
     auto chain_kernel = [&](const ChainArgs& x) -> hipError_t {
         const size_t lds = x.fin == FIN_NONE ? 0 : chain_lds;
         hipEvent_t start, stop;
         const hipError_t ev = next_events(ch, 1, start, stop);
         if (ev != hipSuccess) return ev;
-        auto kern = sp.tmpl == AT_TMPL_GEMM ? k_chain<AT_TMPL_GEMM> : k_chain<AT_TMPL_CONV2D_NCHW>;
+        auto kern = sp.tmpl == AT_TMPL_GEMM ? (wide ? k_chain<AT_TMPL_GEMM, 512> : k_chain<AT_TMPL_GEMM, 256>)
+                                            : (wide ? k_chain<AT_TMPL_CONV2D_NCHW, 512> : k_chain<AT_TMPL_CONV2D_NCHW, 256>);
+        const int wg = wide ? 512 : 256;
         if (start)
-            hipExtLaunchKernelGGL(kern, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, start, stop, 0, x);
+            hipExtLaunchKernelGGL(kern, dim3(chain_grid), dim3(wg), lds, stream, start, stop, 0, x);
         else
-            hipLaunchKernelGGL(kern, dim3(chain_grid), dim3(CHAIN_WG), lds, stream, x);
+            hipLaunchKernelGGL(kern, dim3(chain_grid), dim3(wg), lds, stream, x);
         return hipGetLastError();
     };
     auto trees_kernel = [&]() -> hipError_t {
