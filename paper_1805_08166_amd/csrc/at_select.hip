@@ -105,13 +105,25 @@ __device__ __forceinline__ bool rec_less(const Rec& a, const Rec& b) {
 // threads call.  A thread takes records tid, tid + blockDim.x, ...; the
 // binary searches of its records go step by step together, so their LDS
 // reads overlap.
+// A level whose pairs of runs are already in order (the last record of
+// every left run precedes or equals the first of its right run, so the
+// merge would only concatenate them) is skipped: best lists arrive as
+// ordered runs of the list length.
 template <int PER>
 __device__ Rec* merge_sort(Rec* a, Rec* b, int n, int run) {
     const int nt = (int)blockDim.x;
     Rec* src = a;
     Rec* dst = b;
+    bool check = true;   // until a level is found out of order
     for (int L = run; L < n; L <<= 1) {
-        __syncthreads();
+        __syncthreads();   // the last level's records are in place
+        if (check) {
+            int ordered = 1;
+            for (int blk = (int)threadIdx.x; blk * 2 * L < n; blk += nt)
+                ordered &= rec_less(src[blk * 2 * L + L], src[blk * 2 * L + L - 1]) ? 0 : 1;
+            if (__syncthreads_and(ordered)) continue;
+            check = false;
+        }
         Rec x[PER];
         int base[PER], own[PER], cnt[PER];
         bool left[PER], here[PER];
@@ -252,35 +264,36 @@ __device__ __forceinline__ int wave_sum(int x) {
     return x;
 }
 
-// Largest 64-bit key of the wave, in every lane: DPP shifts within rows
-// of 16, then row broadcasts, leave the maximum in lane 63.
+// Largest unsigned value of the wave, in every lane: DPP shifts within
+// rows of 16, then row broadcasts, leave the maximum in lane 63 (a lane
+// with no source takes 0, which never wins).
 template <int CTRL, int ROWS>
-__device__ __forceinline__ uint64_t dpp_max_step(uint64_t x) {
-    const uint32_t hi = (uint32_t)(x >> 32), lo = (uint32_t)x;
-    const uint32_t ohi = (uint32_t)__builtin_amdgcn_update_dpp((int)hi, (int)hi, CTRL, ROWS, 0xf, false);
-    const uint32_t olo = (uint32_t)__builtin_amdgcn_update_dpp((int)lo, (int)lo, CTRL, ROWS, 0xf, false);
-    const uint64_t o = ((uint64_t)ohi << 32) | olo;
+__device__ __forceinline__ uint32_t dpp_max_step(uint32_t x) {
+    const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, true);
     return o > x ? o : x;
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
     x = dpp_max_step<0x111, 0xf>(x);   // row_shr:1
     x = dpp_max_step<0x112, 0xf>(x);   // row_shr:2
     x = dpp_max_step<0x114, 0xf>(x);   // row_shr:4
     x = dpp_max_step<0x118, 0xf>(x);   // row_shr:8
     x = dpp_max_step<0x142, 0xa>(x);   // row_bcast:15 into rows 1 and 3
     x = dpp_max_step<0x143, 0xc>(x);   // row_bcast:31 into rows 2 and 3
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
-    return ((uint64_t)hi << 32) | lo;
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
 // The greedy rounds of wave 0 for up to 64 * CPL pool candidates; knob
 // values of a lane's candidates (packed in pairs) are held in registers for
-// up to 4 candidates a lane, read from LDS for more.
+// up to 4 candidates a lane, read from LDS for more.  A round takes the
+// largest gain's order bits over the wave (0 marks a candidate already
+// picked or absent: every finite gain orders above 0), then the earliest
+// candidate that has it: candidate lane + 64 i comes before every candidate
+// of a later i, so the first i whose ballot is not empty, and its lowest
+// lane, give the winner.  The winners' indices go to win_idx.
 template <int CPL>
 __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const uint32_t* vals, int have, int m,
-                              uint64_t* picked, int rounds) {
+                              int* win_idx, int rounds) {
     constexpr int W = MAX_KNOBS / 2;
     const int lane = threadIdx.x & 63;
     const uint32_t all = m >= 32 ? 0xffffffffu : (1u << m) - 1u;
@@ -302,52 +315,51 @@ __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const u
         if (!mine) taken |= 1u << i;
     }
     for (int r = 0; r < rounds; ++r) {
-        // arg-max of (gain, -index): the key's high half orders the gains,
-        // the low half prefers the earlier candidate
-        uint64_t best = 0;
+        uint32_t go[CPL], best = 0u;
 #pragma unroll
         for (int i = 0; i < CPL; ++i) {
-            const float cov = a.alpha * (float)__popc(fresh[i]);
-            const float g = sc[i] + cov;
-            const uint64_t key = ((uint64_t)gain_order(g) << 32) | (uint32_t)~(uint32_t)(lane + 64 * i);
-            if (!((taken >> i) & 1u) && key > best) best = key;
+            const float g = sc[i] + a.alpha * (float)__popc(fresh[i]);
+            const uint32_t o = gain_order(g);
+            go[i] = ((taken >> i) & 1u) ? 0u : o;
+            best = go[i] > best ? go[i] : best;
         }
-        best = wave_max_u64(best);
-        const int win = (int)~(uint32_t)best;
+        best = wave_max_u32(best);
+        int win = -1;
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+            const uint64_t bal = __ballot(go[i] == best);
+            if (win < 0 && bal != 0) win = 64 * i + (int)__builtin_ctzll(bal);
+        }
         const int wl = win & 63, wi = win >> 6;
         if (wl == lane) taken |= 1u << wi;
-        // the winner's knob values: from its lane's registers, or LDS
-        uint32_t wv[W];
+        // the knobs whose value the winner adds (its fresh knobs): only
+        // candidates with the same value at those knobs lose them
+        uint32_t wf = 0u;
 #pragma unroll
-        for (int j = 0; j < W; ++j) {
+        for (int i = 0; i < CPL; ++i)
+            if (i == wi) wf = fresh[i];
+        uint32_t added = (uint32_t)__builtin_amdgcn_readlane((int)wf, wl);
+        while (added) {
+            const int j = __builtin_ctz(added);
+            added &= added - 1u;
+            const int jw = j >> 1, sh = 16 * (j & 1);
+            uint32_t wv;
             if constexpr (REG) {
                 uint32_t x = 0u;
 #pragma unroll
                 for (int i = 0; i < CPL; ++i)
-                    if (i == wi) x = kv[i][j];
-                wv[j] = (uint32_t)__builtin_amdgcn_readlane((int)x, wl);
+                    if (i == wi) x = kv[i][jw];
+                wv = ((uint32_t)__builtin_amdgcn_readlane((int)x, wl) >> sh) & 0xffffu;
             } else {
-                wv[j] = vals[win * W + j];
+                wv = (vals[win * W + jw] >> sh) & 0xffffu;
+            }
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) {
+                const uint32_t mine = REG ? kv[REG ? i : 0][jw] : vals[(lane + 64 * i) * W + jw];
+                if (((mine >> sh) & 0xffffu) == wv) fresh[i] &= ~(1u << j);
             }
         }
-#pragma unroll
-        for (int i = 0; i < CPL; ++i) {
-            uint32_t f = fresh[i];
-#pragma unroll
-            for (int j = 0; j < W; ++j) {
-                const uint32_t mine = REG ? kv[REG ? i : 0][j] : vals[(lane + 64 * i) * W + j];
-                const uint32_t x = mine ^ wv[j];
-                if ((x & 0xffffu) == 0u) f &= ~(1u << (2 * j));
-                if ((x >> 16) == 0u) f &= ~(1u << (2 * j + 1));
-            }
-            fresh[i] = f & all;
-        }
-        if (lane == 0) {
-            at_entry e = pool[win];
-            e.flag = 1u;
-            a.out[r] = e;
-            picked[r] = e.cfg;
-        }
+        if (lane == 0) win_idx[r] = win;
     }
 }
 
@@ -396,11 +408,21 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
 
     const int rounds = a.n_greedy < have ? a.n_greedy : have;
     const int cpl = (have + 63) / 64;
-    if (cpl <= 1) greedy_rounds<1>(a, pool, vals, have, m, picked, rounds);
-    else if (cpl <= 2) greedy_rounds<2>(a, pool, vals, have, m, picked, rounds);
-    else if (cpl <= 4) greedy_rounds<4>(a, pool, vals, have, m, picked, rounds);
-    else if (cpl <= 8) greedy_rounds<8>(a, pool, vals, have, m, picked, rounds);
-    else greedy_rounds<16>(a, pool, vals, have, m, picked, rounds);
+    int* win_idx = reinterpret_cast<int*>(sorted);   // free until the ranking below
+    if (cpl <= 1) greedy_rounds<1>(a, pool, vals, have, m, win_idx, rounds);
+    else if (cpl <= 2) greedy_rounds<2>(a, pool, vals, have, m, win_idx, rounds);
+    else if (cpl <= 4) greedy_rounds<4>(a, pool, vals, have, m, win_idx, rounds);
+    else if (cpl <= 8) greedy_rounds<8>(a, pool, vals, have, m, win_idx, rounds);
+    else greedy_rounds<16>(a, pool, vals, have, m, win_idx, rounds);
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    // the picks out, in pick order
+    for (int r = lane; r < rounds; r += 64) {
+        at_entry e = pool[win_idx[r]];
+        e.flag = 1u;
+        a.out[r] = e;
+        picked[r] = e.cfg;
+    }
 
     // the picks in ascending order: pick i goes to its rank (picks are
     // distinct)

@@ -83,6 +83,25 @@ def test_select_synthetic_candidates(P, n_lists, per_list, pool, n_greedy, alpha
     run_both(P, W.CONV2D, C12, cand, pool=pool, n_greedy=n_greedy, alpha=alpha, n_random=5, seed=n_lists)
 
 
+def in_list_order(cand):
+    """Each list in best-list order: valid entries by score descending, then
+    index ascending, empty slots last."""
+    out = cand.copy()
+    for i in range(len(out)):
+        row = out[i]
+        out[i] = row[np.lexsort((row["cfg"], -row["score"].astype(np.float64), row["flag"] == 0))]
+    return out
+
+
+def test_select_lists_in_list_order_through_reduction(P):
+    # lists that are already ordered runs (as best lists are): the first
+    # merge levels of every reduction workgroup find their runs in order
+    say("select: 512x32 lists in best-list order")
+    osp = oracle.Space(W.CONV2D, C12)
+    cand = in_list_order(W.make_candidates(512, 32, osp.n_configs, seed=91))
+    run_both(P, W.CONV2D, C12, cand, pool=128, n_greedy=61, alpha=1.0, n_random=3, seed=9)
+
+
 @pytest.mark.parametrize("kind", ["empty", "all_invalid", "pool_smaller", "pool_zero", "exhaust_space", "one_pick"])
 def test_select_edge_cases(P, kind):
     gemm = (2, 2, 2)   # 192 configurations
