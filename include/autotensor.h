@@ -347,8 +347,10 @@ at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, i
  * seed, u = r1 * 2^32 + r0, and the floor(u * remaining / 2^64)-th
  * unselected index in ascending order.
  * cand: device [n_cand] at_entry, for example the best lists written by
- * at_sa_run ([n_chains][topk]); an index listed more than once must carry
- * the same score each time (as best lists do).  out: device
+ * at_sa_run ([n_chains][topk]); the index of a valid entry must lie below
+ * the space's configuration count (spaces hold fewer than 2^32), and an
+ * index listed more than once must carry the same score each time (as best
+ * lists do).  out: device
  * [n_greedy + n_random] at_entry: the greedy picks (flag 1) in pick order,
  * then the random ones (flag 2, score 0); slots left over when the pool or
  * the space runs out have flag 0.

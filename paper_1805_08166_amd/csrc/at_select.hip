@@ -50,39 +50,36 @@ constexpr int FINAL_MAX = 2048;  // candidates the final workgroup orders
 constexpr int POOL_MAX = 1024;
 constexpr int PICK_MAX = 2048;   // greedy plus random picks
 
-// A candidate while it is ordered: index, score bits and the score's order
-// bits (smaller for a higher score, -0.0 as +0.0; 0xffffffff for an empty
-// slot, whose index is then ~0).
-struct Rec {
-    uint64_t cfg;
-    uint32_t bits;
-    uint32_t ord;
-};
-static_assert(sizeof(Rec) == 16, "16-byte records");
+// A candidate while it is ordered: a 64-bit order key, the score's order
+// bits (smaller for a higher score, -0.0 as +0.0) in the high half and the
+// configuration index in the low half (indices fit 32 bits: a space holds
+// fewer than 2^32 configurations), ~0 for an empty slot; the score's own
+// bits travel beside it in a second array.  Binary searches read the keys
+// only (8-byte LDS reads).
+constexpr uint64_t KEY_EMPTY = ~0ull;
 
-__device__ __forceinline__ Rec rec_of(const at_entry& e) {
-    Rec r;
+struct RecBuf {
+    uint64_t* key;
+    uint32_t* bits;
+};
+
+__device__ __forceinline__ void rec_of(const at_entry& e, uint64_t& key, uint32_t& bits) {
     if (!e.flag) {
-        r.cfg = ~0ull;
-        r.bits = 0u;
-        r.ord = 0xffffffffu;
-        return r;
+        key = KEY_EMPTY;
+        bits = 0u;
+        return;
     }
-    r.cfg = e.cfg;
-    r.bits = __float_as_uint(e.score);
-    uint32_t b = r.bits;
+    bits = __float_as_uint(e.score);
+    uint32_t b = bits;
     if (b == 0x80000000u) b = 0u;
     const uint32_t asc = (b & 0x80000000u) ? ~b : (b | 0x80000000u);   // ascending float order
-    r.ord = ~asc;
-    return r;
+    key = ((uint64_t)~asc << 32) | (uint32_t)e.cfg;
 }
 
-__device__ __forceinline__ bool rec_valid(const Rec& r) { return r.ord != 0xffffffffu; }
-
-__device__ __forceinline__ at_entry entry_of(const Rec& r) {
+__device__ __forceinline__ at_entry entry_of(uint64_t key, uint32_t bits) {
     at_entry e;
-    e.cfg = r.cfg;
-    e.score = __uint_as_float(r.bits);
+    e.cfg = (uint32_t)key;
+    e.score = __uint_as_float(bits);
     e.flag = 1u;
     return e;
 }
@@ -95,10 +92,6 @@ __device__ __forceinline__ at_entry empty_entry() {
     return z;
 }
 
-__device__ __forceinline__ bool rec_less(const Rec& a, const Rec& b) {
-    return a.ord < b.ord || (a.ord == b.ord && a.cfg < b.cfg);
-}
-
 // Orders n records (a power of two) made of ascending runs of length run
 // (a power of two, 1 for unordered input) ascending, moving them between
 // the LDS buffers a and b; returns the buffer that holds the result.  All
@@ -107,24 +100,26 @@ __device__ __forceinline__ bool rec_less(const Rec& a, const Rec& b) {
 // reads overlap.
 // A level whose pairs of runs are already in order (the last record of
 // every left run precedes or equals the first of its right run, so the
-// merge would only concatenate them) is skipped: best lists arrive as
-// ordered runs of the list length.
+// merge would only concatenate them) is skipped, until the first level
+// that is not: best lists arrive as ordered runs of the list length.
 template <int PER>
-__device__ Rec* merge_sort(Rec* a, Rec* b, int n, int run) {
+__device__ RecBuf merge_sort(RecBuf a, RecBuf b, int n, int run) {
     const int nt = (int)blockDim.x;
-    Rec* src = a;
-    Rec* dst = b;
-    bool check = true;   // until a level is found out of order
-    for (int L = run; L < n; L <<= 1) {
+    RecBuf src = a, dst = b;
+    bool check = true;
+    int lg = 0;   // log2(L)
+    while ((1 << lg) < run) ++lg;
+    for (int L = run; L < n; L <<= 1, ++lg) {
         __syncthreads();   // the last level's records are in place
         if (check) {
             int ordered = 1;
             for (int blk = (int)threadIdx.x; blk * 2 * L < n; blk += nt)
-                ordered &= rec_less(src[blk * 2 * L + L], src[blk * 2 * L + L - 1]) ? 0 : 1;
+                ordered &= src.key[blk * 2 * L + L] < src.key[blk * 2 * L + L - 1] ? 0 : 1;
             if (__syncthreads_and(ordered)) continue;
             check = false;
         }
-        Rec x[PER];
+        uint64_t x[PER];
+        uint32_t xb[PER];
         int base[PER], own[PER], cnt[PER];
         bool left[PER], here[PER];
 #pragma unroll
@@ -132,27 +127,30 @@ __device__ Rec* merge_sort(Rec* a, Rec* b, int n, int run) {
             const int i = (int)threadIdx.x + e * nt;
             here[e] = i < n;
             const int ii = here[e] ? i : 0;
-            x[e] = src[ii];
-            const int blk = ii / (2 * L);
-            const int pos = ii - blk * 2 * L;
+            x[e] = src.key[ii];
+            xb[e] = src.bits[ii];
+            const int blk = ii >> (lg + 1);
+            const int pos = ii & (2 * L - 1);
             left[e] = pos < L;
             own[e] = left[e] ? pos : pos - L;
             base[e] = blk * 2 * L + (left[e] ? L : 0);   // the partner run
             cnt[e] = 0;
         }
         // branch-free steps: every probe loads (clamped into the run), so
-        // the PER loads of a step issue together
+        // the PER loads of a step issue together.  A record of the left run
+        // counts the partner's records below it, one of the right run also
+        // those equal to it, so places are distinct.
         for (int step = L; step > 0; step >>= 1) {
-            Rec y[PER];
+            uint64_t y[PER];
             int t[PER];
 #pragma unroll
             for (int e = 0; e < PER; ++e) {
                 t[e] = cnt[e] + step;
-                y[e] = src[base[e] + (t[e] <= L ? t[e] : L) - 1];
+                y[e] = src.key[base[e] + (t[e] <= L ? t[e] : L) - 1];
             }
 #pragma unroll
             for (int e = 0; e < PER; ++e) {
-                const bool before = left[e] ? rec_less(y[e], x[e]) : !rec_less(x[e], y[e]);
+                const bool before = left[e] ? y[e] < x[e] : y[e] <= x[e];
                 cnt[e] = (t[e] <= L && before) ? t[e] : cnt[e];
             }
         }
@@ -160,10 +158,11 @@ __device__ Rec* merge_sort(Rec* a, Rec* b, int n, int run) {
         for (int e = 0; e < PER; ++e) {
             if (here[e]) {
                 const int blk0 = base[e] - (left[e] ? L : 0);
-                dst[blk0 + own[e] + cnt[e]] = x[e];
+                dst.key[blk0 + own[e] + cnt[e]] = x[e];
+                dst.bits[blk0 + own[e] + cnt[e]] = xb[e];
             }
         }
-        Rec* t = src;
+        const RecBuf t = src;
         src = dst;
         dst = t;
     }
@@ -199,18 +198,20 @@ __device__ __forceinline__ int block_exclusive_scan(int x, int* wsum, int* total
 // fill out[keep..slots); returns how many were found (at most keep).
 // Thread t looks after the consecutive records [t * per, (t + 1) * per).
 // All threads call.
-__device__ int compact_distinct(const Rec* v, int n, at_entry* out, int keep, int slots, int* wsum) {
+__device__ int compact_distinct(RecBuf v, int n, at_entry* out, int keep, int slots, int* wsum) {
     const int nt = (int)blockDim.x;
     const int per = n > nt ? n / nt : 1;
     const int lo = threadIdx.x * per;
-    auto fresh = [&](int i) { return rec_valid(v[i]) && (i == 0 || v[i].cfg != v[i - 1].cfg); };
+    auto fresh = [&](int i) {
+        return v.key[i] != KEY_EMPTY && (i == 0 || (uint32_t)v.key[i] != (uint32_t)v.key[i - 1]);
+    };
     int cnt = 0;
     for (int i = lo; i < lo + per && i < n; ++i) cnt += fresh(i) ? 1 : 0;
     int total = 0;
     int pos = block_exclusive_scan(cnt, wsum, &total);
     for (int i = lo; i < lo + per && i < n; ++i) {
         if (fresh(i)) {
-            if (pos < keep) out[pos] = entry_of(v[i]);
+            if (pos < keep) out[pos] = entry_of(v.key[i], v.bits[i]);
             ++pos;
         }
     }
@@ -223,18 +224,21 @@ __device__ int compact_distinct(const Rec* v, int n, at_entry* out, int keep, in
 // Records of entries [base, base + n) of src (empty past the end); all
 // threads call.
 __device__ __forceinline__ void load_slice(const at_entry* __restrict__ src, int64_t base, int64_t total, int n,
-                                           Rec* v) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) v[i] = rec_of(base + i < total ? src[base + i] : empty_entry());
+                                           RecBuf v) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x)
+        rec_of(base + i < total ? src[base + i] : empty_entry(), v.key[i], v.bits[i]);
 }
 
 // Workgroup b: entries [b * CHUNK, ...) of src, ascending runs of length
 // run -> its `keep` best distinct as the run dst + b * slots.
 __global__ __launch_bounds__(SEL_WG) void k_reduce(const at_entry* __restrict__ src, int64_t n, int run, int keep,
                                                    int slots, at_entry* __restrict__ dst) {
-    __shared__ Rec v[CHUNK], w[CHUNK];
+    __shared__ uint64_t k0[CHUNK], k1[CHUNK];
+    __shared__ uint32_t b0[CHUNK], b1[CHUNK];
     __shared__ int wsum[SEL_WG / 64];
+    const RecBuf v{k0, b0}, w{k1, b1};
     load_slice(src, (int64_t)blockIdx.x * CHUNK, n, CHUNK, v);
-    const Rec* sorted = merge_sort<CHUNK / SEL_WG>(v, w, CHUNK, run);
+    const RecBuf sorted = merge_sort<CHUNK / SEL_WG>(v, w, CHUNK, run);
     compact_distinct(sorted, CHUNK, dst + (int64_t)blockIdx.x * slots, keep, slots, wsum);
 }
 
@@ -367,9 +371,11 @@ __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const u
 // greedy wave keeps its candidates in registers without spilling.
 __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) void k_select(SelectArgs a) {
     extern __shared__ uint4 sel_lds[];
-    Rec* v = reinterpret_cast<Rec*>(sel_lds);                                    // [FINAL_MAX]
-    Rec* w = v + FINAL_MAX;                                                      // [FINAL_MAX]
-    at_entry* pool = reinterpret_cast<at_entry*>(w + FINAL_MAX);                 // [POOL_MAX]
+    uint64_t* key0 = reinterpret_cast<uint64_t*>(sel_lds);                       // [FINAL_MAX]
+    uint64_t* key1 = key0 + FINAL_MAX;                                           // [FINAL_MAX]
+    uint32_t* bits0 = reinterpret_cast<uint32_t*>(key1 + FINAL_MAX);             // [FINAL_MAX]
+    uint32_t* bits1 = bits0 + FINAL_MAX;                                         // [FINAL_MAX]
+    at_entry* pool = reinterpret_cast<at_entry*>(bits1 + FINAL_MAX);             // [POOL_MAX]
     uint32_t* vals = reinterpret_cast<uint32_t*>(pool + POOL_MAX);               // [POOL_MAX][MAX_KNOBS / 2]
     uint64_t* picked = reinterpret_cast<uint64_t*>(vals + POOL_MAX * (MAX_KNOBS / 2));   // [PICK_MAX], pick order
     uint64_t* sorted = picked + PICK_MAX;                                        // [PICK_MAX], ascending
@@ -380,8 +386,9 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
     // the pool: the `pool` best distinct candidates
     int nsort = 1;
     while (nsort < a.n) nsort <<= 1;
+    const RecBuf v{key0, bits0}, w{key1, bits1};
     load_slice(a.src, 0, a.n, nsort, v);
-    const Rec* sorted_c = merge_sort<FINAL_MAX / SEL_WG>(v, w, nsort, a.run < nsort ? a.run : nsort);
+    const RecBuf sorted_c = merge_sort<FINAL_MAX / SEL_WG>(v, w, nsort, a.run < nsort ? a.run : nsort);
     const int have = compact_distinct(sorted_c, nsort, pool, a.pool, a.pool, wsum);
 
     // knob values of the pool candidates, packed in pairs (indices fit 32
@@ -480,7 +487,7 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
 }
 
 size_t select_lds_bytes() {
-    return (size_t)FINAL_MAX * sizeof(Rec) * 2 + (size_t)POOL_MAX * sizeof(at_entry) +
+    return (size_t)FINAL_MAX * (8 + 4) * 2 + (size_t)POOL_MAX * sizeof(at_entry) +
            (size_t)POOL_MAX * (MAX_KNOBS / 2) * 4 + (size_t)PICK_MAX * 8 * 2;
 }
 
