@@ -344,6 +344,34 @@ def test_sa_ragged_set_offsets(P, path):
     assert_same_run(best, tr, och, otr, cur=export(P, ch))
 
 
+def test_sa_split_tables_past_the_lds_image(P, path):
+    # GEMM (720, 720, 64): 2807 split choices, more than an LDS space image
+    # holds, so the tree path's chain kernel reads the space from global
+    # memory; a set pairs it with a space whose image fits (blocks of 16
+    # chains take either)
+    big, small = (720, 720, 64), (64, 32, 128)
+    fid, thr, leaf = W.make_ensemble(40, 6, 110, 17)
+    ens = P.at_ensemble_create(fid, thr, leaf, 110)
+    sp = P.at_space_create(W.GEMM, big)
+    osp = oracle.Space(W.GEMM, big)
+    assert sum(int(x) for x in osp.knob_sizes[:3]) > 1024
+    n, steps, seed, k = 100, 30, 23, 5
+    ch = mk_chains(P, sp, 0, n, k, seed, path)
+    best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
+    och = oracle.Chains([osp], [0, n], seed=seed, chain0=0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
+    if path != "trees":
+        return
+    off = np.array([0, 48, 96], np.int64)
+    sset = P.at_spaceset_create([sp, P.at_space_create(W.GEMM, small)], off)
+    ch = mk_chains(P, sset, 0, 96, k, seed, path)
+    best, tr = gpu_sa(P, sset, ens, ch, steps, P.at_sa_thresholds(seed, 0, 96, 0, steps))
+    och = oracle.Chains([osp, oracle.Space(W.GEMM, small)], off, seed=seed, chain0=0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, 96, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
+
+
 def test_sa_ragged_set_tail_mode(P):
     # workgroups of two chains straddle the space boundaries (chains 4-5 and
     # 300), so the chain-local tail mode reads each chain's own space tables
