@@ -256,10 +256,11 @@ struct SelectArgs {
 };
 
 // Ascending order bits of a finite gain (-0.0 as +0.0).
+// (g + 0.0f is g for every g but -0.0, which it turns into +0.0; a negative
+// value's bits are all flipped, a positive value's sign bit set.)
 __device__ __forceinline__ uint32_t gain_order(float g) {
-    uint32_t b = __float_as_uint(g);
-    if (b == 0x80000000u) b = 0u;
-    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+    const uint32_t b = __float_as_uint(g + 0.0f);
+    return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
 }
 
 __device__ __forceinline__ int wave_sum(int x) {
@@ -413,7 +414,8 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
     __syncthreads();
     if (tid >= 64) return;   // the rounds and the draws are wave 0's; no barrier follows
 
-    const int rounds = a.n_greedy < have ? a.n_greedy : have;
+    // the same in every lane; readfirstlane lets the compiler see it
+    const int rounds = __builtin_amdgcn_readfirstlane(a.n_greedy < have ? a.n_greedy : have);
     const int cpl = (have + 63) / 64;
     int* win_idx = reinterpret_cast<int*>(sorted);   // free until the ranking below
     if (cpl <= 1) greedy_rounds<1>(a, pool, vals, have, m, win_idx, rounds);
