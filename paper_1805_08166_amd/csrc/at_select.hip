@@ -13,20 +13,28 @@
 // yet, draw i from Philox block (i, 0, 5, 0): u = r1 * 2^32 + r0, the
 // floor(u * remaining / 2^64)-th unselected index.
 //
-// k_reduce: each workgroup orders a slice of up to CHUNK candidates in LDS
-// (on 16-byte records that carry the score's order bits, the score itself
-// and the index), drops repeated indices and writes its best `keep`
-// candidates as a run of the power of two at or above keep (empty slots
-// after them).  Ordering is a merge sort: at each level every record finds
-// its place in the merged run by a binary search of the partner run (a
-// record of the left run counts the partner's records that precede it, one
-// of the right run also those equal to it, so places are distinct), one
-// barrier per level.  Raw candidates are runs of one; a partial result from
-// the level before is a slice of sorted runs, so later levels and the final
-// workgroup start from longer runs.
+// k_reduce: each workgroup takes a slice of up to CHUNK candidates and
+// writes its `keep` best distinct (score descending, index ascending,
+// an index equal to its predecessor's in that order dropped) as a run of
+// the power of two at or above keep (empty slots after them).  Best lists
+// repeat configurations many times over and only the few best of a slice
+// can reach its result, so the slice is not ordered whole:
+//  1. exact repeats (the same 64-bit order key: score order bits, index)
+//     are dropped, the first in entry order kept: they would be neighbours
+//     once ordered, the first one first.  An LDS hash table holds the keys
+//     and, per key, the smallest entry position;
+//  2. a histogram of the remaining records' score order bits (scaled into
+//     NBINS bins over their range: a bin is a range of order bits) gives the
+//     smallest bin b whose bins up to b hold `keep` records;
+//  3. the records up to bin b (a prefix of the ordered sequence) are
+//     ordered, by counting (a record's place is the number of keys below
+//     it) or for large sets by a merge sort, and the distinct ones taken;
+//  4. should fewer than keep come out (the same index with different
+//     scores, dropped as a neighbour's repeat) while records are left, the
+//     prefix grows and 2-3 run again.
 // Levels repeat until at most FINAL_MAX candidates remain.
-// k_select (one workgroup): orders and compacts those the same way into the
-// pool and decodes its knob values; then wave 0 alone runs the greedy
+// k_select (one workgroup): takes the pool from those the same way and
+// decodes its knob values; then wave 0 alone runs the greedy
 // rounds, each lane looking after pool candidates lane, lane + 64, ...: a
 // round is a wave-wide arg-max of the gains (DPP steps, no workgroup
 // barrier), then every lane clears the knobs the winner covers in its
@@ -49,6 +57,15 @@ constexpr int CHUNK = 2048;      // candidates one reduction workgroup orders
 constexpr int FINAL_MAX = 2048;  // candidates the final workgroup orders
 constexpr int POOL_MAX = 1024;
 constexpr int PICK_MAX = 2048;   // greedy plus random picks
+constexpr int PER = FINAL_MAX / SEL_WG;   // records a thread holds in the pool stage
+static_assert(CHUNK == FINAL_MAX && PER * SEL_WG == FINAL_MAX, "both kernels take the same slice size");
+constexpr int HASH_LOG2 = 12;
+constexpr int HASH_SLOTS = 1 << HASH_LOG2;   // exact-key table: at most half full
+constexpr int NBINS_LOG2 = 11;
+constexpr int NBINS = 1 << NBINS_LOG2;       // score histogram
+static_assert(NBINS == 2 * SEL_WG, "the bin scan takes two bins a thread");
+constexpr int RANK_MAX = SEL_WG;             // prefixes up to this size are ordered by counting
+constexpr int RED_WORDS = 3 * (SEL_WG / 64) + 2;
 
 // A candidate while it is ordered: a 64-bit order key, the score's order
 // bits (smaller for a higher score, -0.0 as +0.0) in the high half and the
@@ -63,17 +80,15 @@ struct RecBuf {
     uint32_t* bits;
 };
 
-__device__ __forceinline__ void rec_of(const at_entry& e, uint64_t& key, uint32_t& bits) {
-    if (!e.flag) {
-        key = KEY_EMPTY;
-        bits = 0u;
-        return;
-    }
-    bits = __float_as_uint(e.score);
-    uint32_t b = bits;
-    if (b == 0x80000000u) b = 0u;
-    const uint32_t asc = (b & 0x80000000u) ? ~b : (b | 0x80000000u);   // ascending float order
-    key = ((uint64_t)~asc << 32) | (uint32_t)e.cfg;
+// The record of entry e, or an empty one when e is not valid or not here
+// (no branches, so that the loads that feed it are all in flight first).
+__device__ __forceinline__ void rec_bits(const at_entry& e, bool here, uint64_t& key, uint32_t& bits) {
+    const bool valid = here && e.flag != 0u;
+    uint32_t b = __float_as_uint(e.score);
+    const uint32_t z = b == 0x80000000u ? 0u : b;
+    const uint32_t asc = (z & 0x80000000u) ? ~z : (z | 0x80000000u);
+    key = valid ? (((uint64_t)~asc << 32) | (uint32_t)e.cfg) : KEY_EMPTY;
+    bits = valid ? b : 0u;
 }
 
 __device__ __forceinline__ at_entry entry_of(uint64_t key, uint32_t bits) {
@@ -92,32 +107,58 @@ __device__ __forceinline__ at_entry empty_entry() {
     return z;
 }
 
-// Orders n records (a power of two) made of ascending runs of length run
-// (a power of two, 1 for unordered input) ascending, moving them between
-// the LDS buffers a and b; returns the buffer that holds the result.  All
-// threads call.  A thread takes records tid, tid + blockDim.x, ...; the
-// binary searches of its records go step by step together, so their LDS
-// reads overlap.
-// A level whose pairs of runs are already in order (the last record of
-// every left run precedes or equals the first of its right run, so the
-// merge would only concatenate them) is skipped, until the first level
-// that is not: best lists arrive as ordered runs of the list length.
-template <int PER>
-__device__ RecBuf merge_sort(RecBuf a, RecBuf b, int n, int run) {
+// Wave-wide primitives on DPP lane moves (no LDS round trip): a row
+// shift or broadcast of x, lanes without a source taking 0.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_move(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, true);
+}
+
+// Largest unsigned value of the wave, in every lane: shifts within rows of
+// 16, then row broadcasts, leave the maximum in lane 63 (a lane with no
+// source takes 0, which never wins).
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+    uint32_t o;
+    o = dpp_move<0x111, 0xf>(x); x = o > x ? o : x;   // row_shr:1
+    o = dpp_move<0x112, 0xf>(x); x = o > x ? o : x;   // row_shr:2
+    o = dpp_move<0x114, 0xf>(x); x = o > x ? o : x;   // row_shr:4
+    o = dpp_move<0x118, 0xf>(x); x = o > x ? o : x;   // row_shr:8
+    o = dpp_move<0x142, 0xa>(x); x = o > x ? o : x;   // row_bcast:15 into rows 1 and 3
+    o = dpp_move<0x143, 0xc>(x); x = o > x ? o : x;   // row_bcast:31 into rows 2 and 3
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// Inclusive prefix sum over the wave's lanes (the same steps with adds:
+// after the row shifts a lane holds the sum of its row up to it, the row
+// broadcasts add the rows before).
+__device__ __forceinline__ uint32_t wave_inclusive_add(uint32_t x) {
+    x += dpp_move<0x111, 0xf>(x);
+    x += dpp_move<0x112, 0xf>(x);
+    x += dpp_move<0x114, 0xf>(x);
+    x += dpp_move<0x118, 0xf>(x);
+    x += dpp_move<0x142, 0xa>(x);
+    x += dpp_move<0x143, 0xc>(x);
+    return x;
+}
+
+__device__ __forceinline__ int wave_sum(int x) {
+    return __builtin_amdgcn_readlane((int)wave_inclusive_add((uint32_t)x), 63);
+}
+
+// Orders n records (a power of two) ascending, moving them between the LDS
+// buffers a and b; returns the buffer that holds the result.  All threads
+// call.  A level merges pairs of ascending runs of length L: every record
+// finds its place in the merged run by a binary search of the partner run
+// (a record of the left run counts the partner's records below it, one of
+// the right run also those equal to it, so places are distinct).  A thread
+// takes records tid, tid + blockDim.x, ...; the binary searches of its
+// records go step by step together, so their LDS reads overlap.
+__device__ RecBuf merge_sort(RecBuf a, RecBuf b, int n) {
     const int nt = (int)blockDim.x;
     RecBuf src = a, dst = b;
-    bool check = true;
     int lg = 0;   // log2(L)
-    while ((1 << lg) < run) ++lg;
-    for (int L = run; L < n; L <<= 1, ++lg) {
+    for (int L = 1; L < n; L <<= 1, ++lg) {
         __syncthreads();   // the last level's records are in place
-        if (check) {
-            int ordered = 1;
-            for (int blk = (int)threadIdx.x; blk * 2 * L < n; blk += nt)
-                ordered &= src.key[blk * 2 * L + L] < src.key[blk * 2 * L + L - 1] ? 0 : 1;
-            if (__syncthreads_and(ordered)) continue;
-            check = false;
-        }
         uint64_t x[PER];
         uint32_t xb[PER];
         int base[PER], own[PER], cnt[PER];
@@ -137,9 +178,7 @@ __device__ RecBuf merge_sort(RecBuf a, RecBuf b, int n, int run) {
             cnt[e] = 0;
         }
         // branch-free steps: every probe loads (clamped into the run), so
-        // the PER loads of a step issue together.  A record of the left run
-        // counts the partner's records below it, one of the right run also
-        // those equal to it, so places are distinct.
+        // the PER loads of a step issue together
         for (int step = L; step > 0; step >>= 1) {
             uint64_t y[PER];
             int t[PER];
@@ -170,16 +209,44 @@ __device__ RecBuf merge_sort(RecBuf a, RecBuf b, int n, int run) {
     return src;
 }
 
+// Orders the c distinct keys of src[0..c) (c <= SEL_WG) into dst[0..c) by
+// counting: g threads look after a record (g = SEL_WG / the power of two
+// at or above c, at most 64), each counting the keys below it in every
+// g-th position, and the record goes to the sum.  All threads call.
+__device__ void rank_sort(RecBuf src, RecBuf dst, int c) {
+    int c2 = 1;
+    while (c2 < c) c2 <<= 1;
+    int g = SEL_WG / c2;
+    g = g > 64 ? 64 : g;
+    const int r = (int)threadIdx.x / g, p = (int)threadIdx.x & (g - 1);
+    const bool mine = r < c;
+    const uint64_t xr = src.key[mine ? r : 0];
+    int cnt = 0;
+    if (mine) {
+        int j = p;
+        // eight reads in flight, then their compares
+        for (; j + 7 * g < c; j += 8 * g) {
+            uint64_t y[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) y[u] = src.key[j + u * g];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) cnt += y[u] < xr ? 1 : 0;
+        }
+        for (; j < c; j += g) cnt += src.key[j] < xr ? 1 : 0;
+    }
+    for (int off = 1; off < g; off <<= 1) cnt += __shfl_xor(cnt, off);
+    if (mine && p == 0) {
+        dst.key[cnt] = xr;
+        dst.bits[cnt] = src.bits[r];
+    }
+    __syncthreads();
+}
+
 // Exclusive prefix sum of x over the block's threads (thread order); the
 // total goes to *total.  All threads call; wsum has a slot per wave.
 __device__ __forceinline__ int block_exclusive_scan(int x, int* wsum, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    int inc = x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(inc, off);
-        if (lane >= off) inc += y;
-    }
+    const int inc = (int)wave_inclusive_add((uint32_t)x);
     if (lane == 63) wsum[wave] = inc;
     __syncthreads();
     int before = 0, all = 0;
@@ -221,32 +288,204 @@ __device__ int compact_distinct(RecBuf v, int n, at_entry* out, int keep, int sl
     return have;
 }
 
-// Records of entries [base, base + n) of src (empty past the end); all
-// threads call.
-__device__ __forceinline__ void load_slice(const at_entry* __restrict__ src, int64_t base, int64_t total, int n,
-                                           RecBuf v) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x)
-        rec_of(base + i < total ? src[base + i] : empty_entry(), v.key[i], v.bits[i]);
+// LDS of the pool stage.  The hash table (keys, first positions) lies over
+// the two record buffers, which are written only once the table is done.
+struct PoolLds {
+    RecBuf v, w;        // [FINAL_MAX] each
+    uint64_t* hkey;     // [HASH_SLOTS]
+    uint32_t* hfirst;   // [HASH_SLOTS]
+    uint32_t* hist;     // [NBINS]
+    int* wsum;          // [SEL_WG / 64]
+    uint32_t* red;      // [RED_WORDS]
+};
+constexpr size_t POOL_REGION_BYTES = (size_t)FINAL_MAX * (8 + 4) * 2;
+static_assert((size_t)HASH_SLOTS * (8 + 4) <= POOL_REGION_BYTES, "the table fits over the record buffers");
+
+__device__ __forceinline__ PoolLds pool_lds(uint64_t* region, uint32_t* hist, int* wsum, uint32_t* red) {
+    PoolLds s;
+    s.v.key = region;
+    s.w.key = region + FINAL_MAX;
+    s.v.bits = reinterpret_cast<uint32_t*>(region + 2 * FINAL_MAX);
+    s.w.bits = s.v.bits + FINAL_MAX;
+    s.hkey = region;
+    s.hfirst = reinterpret_cast<uint32_t*>(region + HASH_SLOTS);
+    s.hist = hist;
+    s.wsum = wsum;
+    s.red = red;
+    return s;
 }
 
-// Workgroup b: entries [b * CHUNK, ...) of src, ascending runs of length
-// run -> its `keep` best distinct as the run dst + b * slots.
-__global__ __launch_bounds__(SEL_WG) void k_reduce(const at_entry* __restrict__ src, int64_t n, int run, int keep,
-                                                   int slots, at_entry* __restrict__ dst) {
-    __shared__ uint64_t k0[CHUNK], k1[CHUNK];
-    __shared__ uint32_t b0[CHUNK], b1[CHUNK];
+__device__ __forceinline__ uint32_t key_hash(uint64_t k) {
+    return (((uint32_t)k * 0x9e3779b1u) ^ ((uint32_t)(k >> 32) * 0x85ebca6bu)) >> (32 - HASH_LOG2);
+}
+
+// The `keep` best distinct of entries [base, base + n) of src (n <=
+// FINAL_MAX, entries past total empty) -> out[0..keep) in order, empty
+// entries up to out[slots); returns how many were found.  All threads call
+// (the steps are in the comment at the top of this file).
+__device__ int top_distinct(const at_entry* __restrict__ src, int64_t base, int64_t total, int n, at_entry* out,
+                            int keep, int slots, const PoolLds& s) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int NW = SEL_WG / 64;
+    if (keep <= 0) {
+        for (int i = tid; i < slots; i += SEL_WG) out[i] = empty_entry();
+        return 0;
+    }
+    uint64_t x[PER];
+    uint32_t xb[PER];
+    for (int i = tid; i < HASH_SLOTS; i += SEL_WG) {
+        s.hkey[i] = KEY_EMPTY;
+        s.hfirst[i] = 0xffffffffu;
+    }
+    for (int i = tid; i < NBINS; i += SEL_WG) s.hist[i] = 0u;
+    // loads from valid addresses on every lane (no branch around a load),
+    // records past the end made empty afterwards
+    at_entry en[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) en[e] = empty_entry();
+    if (total > 0) {
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            const int64_t i = base + tid + e * SEL_WG;
+            en[e] = src[i < total ? i : total - 1];
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+        const int i = tid + e * SEL_WG;
+        const bool here = i < n && base + i < total;
+        rec_bits(en[e], here, x[e], xb[e]);
+    }
+    __syncthreads();
+    // 1. exact repeats: linear probing from the key's hash; every copy of a
+    // key lands on its slot, which keeps the smallest entry position
+    uint32_t slot[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+        slot[e] = 0u;
+        if (x[e] != KEY_EMPTY) {
+            uint32_t h = key_hash(x[e]);
+            while (true) {
+                const uint64_t prev = atomicCAS(&s.hkey[h], KEY_EMPTY, x[e]);
+                if (prev == KEY_EMPTY || prev == x[e]) break;
+                h = (h + 1u) & (HASH_SLOTS - 1u);
+            }
+            slot[e] = h;
+            atomicMin(&s.hfirst[h], (uint32_t)(tid + e * SEL_WG));
+        }
+    }
+    __syncthreads();
+    bool kept[PER];
+    uint32_t ob[PER];
+    uint32_t mn = 0xffffffffu, mx = 0u, nk = 0u;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+        kept[e] = x[e] != KEY_EMPTY && s.hfirst[slot[e]] == (uint32_t)(tid + e * SEL_WG);
+        ob[e] = (uint32_t)(x[e] >> 32);
+        if (kept[e]) {
+            mn = ob[e] < mn ? ob[e] : mn;
+            mx = ob[e] > mx ? ob[e] : mx;
+            ++nk;
+        }
+    }
+    mn = ~wave_max_u32(~mn);
+    mx = wave_max_u32(mx);
+    nk = (uint32_t)wave_sum((int)nk);
+    if (lane == 0) {
+        s.red[wave] = mn;
+        s.red[NW + wave] = mx;
+        s.red[2 * NW + wave] = nk;
+    }
+    __syncthreads();
+    mn = 0xffffffffu;
+    mx = 0u;
+    nk = 0u;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        const uint32_t a = s.red[w], b = s.red[NW + w];
+        mn = a < mn ? a : mn;
+        mx = b > mx ? b : mx;
+        nk += s.red[2 * NW + w];
+    }
+    if (nk == 0u) {
+        for (int i = tid; i < slots; i += SEL_WG) out[i] = empty_entry();
+        __syncthreads();
+        return 0;
+    }
+    // 2. histogram: bin (ob - mn) >> sh < NBINS
+    const uint32_t range = mx - mn;
+    const int bits = range ? 32 - __clz((int)range) : 0;
+    const int sh = bits > NBINS_LOG2 ? bits - NBINS_LOG2 : 0;
+    uint32_t bin[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+        bin[e] = (ob[e] - mn) >> sh;
+        if (kept[e]) atomicAdd(&s.hist[bin[e]], 1u);
+    }
+    __syncthreads();
+    const int h0 = (int)s.hist[2 * tid], h1 = (int)s.hist[2 * tid + 1];
+    int all = 0;
+    const int before = block_exclusive_scan(h0 + h1, s.wsum, &all);
+    int target = keep < (int)nk ? keep : (int)nk;
+    int have = 0;
+    while (true) {
+        // the smallest bin whose bins up to it hold `target` records
+        if (before < target && target <= before + h0 + h1) {
+            s.red[3 * NW] = before + h0 >= target ? 2u * tid : 2u * tid + 1u;
+            s.red[3 * NW + 1] = 0u;
+        }
+        __syncthreads();
+        const uint32_t last = s.red[3 * NW];
+        // 3. the records up to that bin into w (in any order)
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+            const bool in = kept[e] && bin[e] <= last;
+            const uint64_t bal = __ballot(in);
+            uint32_t at = 0u;
+            if (lane == 0 && bal) at = atomicAdd(&s.red[3 * NW + 1], (uint32_t)__popcll(bal));
+            at = (uint32_t)__builtin_amdgcn_readfirstlane((int)at);
+            if (in) {
+                const uint32_t p = at + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+                s.w.key[p] = x[e];
+                s.w.bits[p] = xb[e];
+            }
+        }
+        __syncthreads();
+        const int c = (int)s.red[3 * NW + 1];
+        if (c <= RANK_MAX) {
+            rank_sort(s.w, s.v, c);
+            have = compact_distinct(s.v, c, out, keep, slots, s.wsum);
+        } else {
+            int c2 = 1;
+            while (c2 < c) c2 <<= 1;
+            for (int i = c + tid; i < c2; i += SEL_WG) s.w.key[i] = KEY_EMPTY;
+            const RecBuf sorted = merge_sort(s.w, s.v, c2);
+            have = compact_distinct(sorted, c2, out, keep, slots, s.wsum);
+        }
+        // 4. too few distinct while records are left: a longer prefix
+        if (have >= keep || c >= (int)nk) break;
+        target = c + 2 * (keep - have);
+        target = target < (int)nk ? target : (int)nk;
+    }
+    return have;
+}
+
+// Workgroup b: entries [b * CHUNK, ...) of src -> its `keep` best distinct
+// as the run dst + b * slots.
+__global__ __launch_bounds__(SEL_WG) void k_reduce(const at_entry* __restrict__ src, int64_t n, int keep, int slots,
+                                                   at_entry* __restrict__ dst) {
+    __shared__ uint64_t region[POOL_REGION_BYTES / 8];
+    __shared__ uint32_t hist[NBINS];
     __shared__ int wsum[SEL_WG / 64];
-    const RecBuf v{k0, b0}, w{k1, b1};
-    load_slice(src, (int64_t)blockIdx.x * CHUNK, n, CHUNK, v);
-    const RecBuf sorted = merge_sort<CHUNK / SEL_WG>(v, w, CHUNK, run);
-    compact_distinct(sorted, CHUNK, dst + (int64_t)blockIdx.x * slots, keep, slots, wsum);
+    __shared__ uint32_t red[RED_WORDS];
+    const PoolLds s = pool_lds(region, hist, wsum, red);
+    top_distinct(src, (int64_t)blockIdx.x * CHUNK, n, CHUNK, dst + (int64_t)blockIdx.x * slots, keep, slots, s);
 }
 
 struct SelectArgs {
     const SpaceDesc* desc;
     const at_entry* src;      // candidates, or partial results (at most FINAL_MAX)
     int64_t n;
-    int run;                  // ascending runs of src (1: unordered)
     int pool;
     int n_greedy;
     float alpha;
@@ -261,31 +500,6 @@ struct SelectArgs {
 __device__ __forceinline__ uint32_t gain_order(float g) {
     const uint32_t b = __float_as_uint(g + 0.0f);
     return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
-}
-
-__device__ __forceinline__ int wave_sum(int x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-    return x;
-}
-
-// Largest unsigned value of the wave, in every lane: DPP shifts within
-// rows of 16, then row broadcasts, leave the maximum in lane 63 (a lane
-// with no source takes 0, which never wins).
-template <int CTRL, int ROWS>
-__device__ __forceinline__ uint32_t dpp_max_step(uint32_t x) {
-    const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, true);
-    return o > x ? o : x;
-}
-
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-    x = dpp_max_step<0x111, 0xf>(x);   // row_shr:1
-    x = dpp_max_step<0x112, 0xf>(x);   // row_shr:2
-    x = dpp_max_step<0x114, 0xf>(x);   // row_shr:4
-    x = dpp_max_step<0x118, 0xf>(x);   // row_shr:8
-    x = dpp_max_step<0x142, 0xa>(x);   // row_bcast:15 into rows 1 and 3
-    x = dpp_max_step<0x143, 0xc>(x);   // row_bcast:31 into rows 2 and 3
-    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
 // The greedy rounds of wave 0 for up to 64 * CPL pool candidates; knob
@@ -372,25 +586,21 @@ __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const u
 // greedy wave keeps its candidates in registers without spilling.
 __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) void k_select(SelectArgs a) {
     extern __shared__ uint4 sel_lds[];
-    uint64_t* key0 = reinterpret_cast<uint64_t*>(sel_lds);                       // [FINAL_MAX]
-    uint64_t* key1 = key0 + FINAL_MAX;                                           // [FINAL_MAX]
-    uint32_t* bits0 = reinterpret_cast<uint32_t*>(key1 + FINAL_MAX);             // [FINAL_MAX]
-    uint32_t* bits1 = bits0 + FINAL_MAX;                                         // [FINAL_MAX]
-    at_entry* pool = reinterpret_cast<at_entry*>(bits1 + FINAL_MAX);             // [POOL_MAX]
+    uint64_t* region = reinterpret_cast<uint64_t*>(sel_lds);                     // the pool stage's buffers
+    at_entry* pool = reinterpret_cast<at_entry*>(region + POOL_REGION_BYTES / 8);   // [POOL_MAX]
     uint32_t* vals = reinterpret_cast<uint32_t*>(pool + POOL_MAX);               // [POOL_MAX][MAX_KNOBS / 2]
-    uint64_t* picked = reinterpret_cast<uint64_t*>(vals + POOL_MAX * (MAX_KNOBS / 2));   // [PICK_MAX], pick order
+    // after the pool stage its buffers hold the picks
+    uint64_t* picked = region;                                                   // [PICK_MAX], pick order
     uint64_t* sorted = picked + PICK_MAX;                                        // [PICK_MAX], ascending
+    static_assert((size_t)PICK_MAX * 8 * 2 <= POOL_REGION_BYTES, "the picks fit the pool stage's buffers");
+    __shared__ uint32_t hist[NBINS];
     __shared__ int wsum[SEL_WG / 64];
+    __shared__ uint32_t red[RED_WORDS];
     const int tid = threadIdx.x, lane = tid & 63;
     const SpaceDesc& sd = *a.desc;
 
     // the pool: the `pool` best distinct candidates
-    int nsort = 1;
-    while (nsort < a.n) nsort <<= 1;
-    const RecBuf v{key0, bits0}, w{key1, bits1};
-    load_slice(a.src, 0, a.n, nsort, v);
-    const RecBuf sorted_c = merge_sort<FINAL_MAX / SEL_WG>(v, w, nsort, a.run < nsort ? a.run : nsort);
-    const int have = compact_distinct(sorted_c, nsort, pool, a.pool, a.pool, wsum);
+    const int have = top_distinct(a.src, 0, a.n, (int)a.n, pool, a.pool, a.pool, pool_lds(region, hist, wsum, red));
 
     // knob values of the pool candidates, packed in pairs (indices fit 32
     // bits: a space has fewer than 2^32 configurations)
@@ -489,8 +699,7 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
 }
 
 size_t select_lds_bytes() {
-    return (size_t)FINAL_MAX * (8 + 4) * 2 + (size_t)POOL_MAX * sizeof(at_entry) +
-           (size_t)POOL_MAX * (MAX_KNOBS / 2) * 4 + (size_t)PICK_MAX * 8 * 2;
+    return POOL_REGION_BYTES + (size_t)POOL_MAX * sizeof(at_entry) + (size_t)POOL_MAX * (MAX_KNOBS / 2) * 4;
 }
 
 }  // namespace
@@ -557,7 +766,6 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     // (half a slice or less)
     const int keep = pool > 0 ? pool : 1;
     const int slots = run_slots(pool);
-    int run = 1;
     const at_entry* src = cand;
     int64_t n = n_cand;
     void* bufs[2] = {nullptr, nullptr};
@@ -581,12 +789,11 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     int cur = 0;
     while (n > FINAL_MAX) {
         const int64_t groups = (n + CHUNK - 1) / CHUNK;
-        hipLaunchKernelGGL(k_reduce, dim3((unsigned)groups), dim3(SEL_WG), 0, stream, src, n, run, keep, slots,
+        hipLaunchKernelGGL(k_reduce, dim3((unsigned)groups), dim3(SEL_WG), 0, stream, src, n, keep, slots,
                            static_cast<at_entry*>(bufs[cur]));
         if ((e = hipGetLastError()) != hipSuccess) break;
         src = static_cast<const at_entry*>(bufs[cur]);
         n = groups * slots;
-        run = slots;
         cur ^= 1;
     }
     if (e != hipSuccess) {
@@ -599,7 +806,6 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     a.desc = static_cast<const SpaceDesc*>(sp.d_descs.p);
     a.src = src;
     a.n = n;
-    a.run = run;
     a.pool = pool;
     a.n_greedy = n_greedy;
     a.alpha = alpha;

@@ -102,6 +102,49 @@ def test_select_lists_in_list_order_through_reduction(P):
     run_both(P, W.CONV2D, C12, cand, pool=128, n_greedy=61, alpha=1.0, n_random=3, seed=9)
 
 
+def repeats_and_ties(kind, n_lists, per_list, n_configs, seed):
+    """Candidate lists that stress the pool stage: exact repeats, the same
+    index with different scores, ties, signed zeros, outlying scores."""
+    rng = np.random.default_rng(seed)
+    cand = W.make_candidates(n_lists, per_list, n_configs, seed=seed).reshape(-1)
+    valid = np.flatnonzero(cand["flag"] == 1)
+    if kind == "few_configs":
+        # every entry one of 40 configurations, a score per configuration
+        cfgs = rng.choice(n_configs, 40, replace=False).astype(np.uint64)
+        scores = rng.normal(0.0, 1.0, 40).astype(np.float32)
+        pick = rng.integers(0, 40, len(valid))
+        cand["cfg"][valid] = cfgs[pick]
+        cand["score"][valid] = scores[pick]
+    elif kind == "same_index_other_score":
+        # a quarter of the entries take another entry's index, keeping
+        # their own score
+        idx = rng.choice(valid, len(valid) // 4, replace=False)
+        cand["cfg"][idx] = cand["cfg"][rng.choice(valid, len(idx))]
+    elif kind == "all_tied":
+        cand["score"][valid] = np.float32(1.5)
+    elif kind == "signed_zero":
+        # scores +0.0 and -0.0 (equal in the order), repeats of an index
+        # with either sign, and a few nonzero scores
+        z = np.where(rng.random(len(valid)) < 0.5, np.float32(0.0), np.float32(-0.0))
+        cand["score"][valid] = z
+        few = rng.choice(valid, len(valid) // 50, replace=False)
+        cand["score"][few] = rng.normal(0.0, 1.0, len(few)).astype(np.float32)
+    elif kind == "outliers":
+        # most scores in one histogram bin next to a handful of huge ones
+        few = rng.choice(valid, 5, replace=False)
+        cand["score"][few] = np.float32([1e30, -1e30, 3e29, -2e25, 1e20])
+    return cand.reshape(n_lists, per_list)
+
+
+@pytest.mark.parametrize("kind", ["few_configs", "same_index_other_score", "all_tied", "signed_zero", "outliers"])
+@pytest.mark.parametrize("n_lists,per_list", [(100, 16), (8192, 32)])
+def test_select_repeats_and_ties(P, kind, n_lists, per_list):
+    say(f"select: {kind}, {n_lists}x{per_list}")
+    osp = oracle.Space(W.CONV2D, C12)
+    cand = repeats_and_ties(kind, n_lists, per_list, osp.n_configs, seed=len(kind) + n_lists)
+    run_both(P, W.CONV2D, C12, cand, pool=128, n_greedy=61, alpha=1.0, n_random=3, seed=17)
+
+
 @pytest.mark.parametrize("kind", ["empty", "all_invalid", "pool_smaller", "pool_zero", "exhaust_space", "one_pick"])
 def test_select_edge_cases(P, kind):
     gemm = (2, 2, 2)   # 192 configurations
