@@ -356,9 +356,16 @@ at_status at_extract_relation_features(at_space_t space, const uint64_t* cfgs, i
  * the space runs out have flag 0.
  * Limits: 0 <= pool <= 1024, n_greedy + n_random <= 2048, a single space
  * (not a set) whose knobs have at most 65536 values each; AT_E_INVALID or
- * AT_E_UNSUPPORTED otherwise.  Enqueued on `stream`; more than 2048
- * candidates use stream-ordered device scratch (hipMallocAsync) for a
- * partial reduction. */
+ * AT_E_UNSUPPORTED otherwise.  Enqueued on `stream`.  More than 2048
+ * candidates use stream-ordered device scratch for a partial reduction:
+ * 32 * ceil(n_cand / 2048) * P bytes, P the power of two at or above
+ * max(pool, 1) (512 KiB for 262144 candidates at pool 128), taken with
+ * hipMallocFromPoolAsync from a memory pool that the library creates on the
+ * device.  The library keeps that scratch for the next such call on the
+ * device (growing it when a call needs more) until the process ends, with
+ * an event recorded after each call's kernels: a call makes its stream wait
+ * for the previous call's event, so calls on different streams take their
+ * turns on the scratch. */
 at_status at_select_batch(at_space_t space, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
                           float alpha, int n_random, uint64_t seed, at_entry* out, at_stream_t stream);
 

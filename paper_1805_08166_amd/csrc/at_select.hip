@@ -504,12 +504,15 @@ __device__ __forceinline__ uint32_t gain_order(float g) {
 
 // The greedy rounds of wave 0 for up to 64 * CPL pool candidates; knob
 // values of a lane's candidates (packed in pairs) are held in registers for
-// up to 4 candidates a lane, read from LDS for more.  A round takes the
-// largest gain's order bits over the wave (0 marks a candidate already
-// picked or absent: every finite gain orders above 0), then the earliest
-// candidate that has it: candidate lane + 64 i comes before every candidate
-// of a later i, so the first i whose ballot is not empty, and its lowest
-// lane, give the winner.  The winners' indices go to win_idx.
+// up to 4 candidates a lane, read from LDS for more.  Each candidate's
+// gain is kept as its order bits (0: picked or absent; every finite gain
+// orders above 0) and computed again only in rounds that take knobs from
+// some candidate (the winner usually adds no knob, so most rounds are just
+// the arg-max).  A round takes the largest order bits over the wave, then
+// the earliest candidate that has them: candidate lane + 64 i comes before
+// every candidate of a later i, so the first i whose ballot is not empty,
+// and its lowest lane, give the winner.  The winners' indices go to
+// win_idx.
 template <int CPL>
 __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const uint32_t* vals, int have, int m,
                               int* win_idx, int rounds) {
@@ -519,8 +522,7 @@ __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const u
     constexpr bool REG = CPL <= 4;
     constexpr int KR = REG ? CPL : 1;
     float sc[CPL];
-    uint32_t fresh[CPL], kv[KR][W];
-    uint32_t taken = 0u;   // bit i: candidate lane + 64 i is picked or absent
+    uint32_t fresh[CPL], go[CPL], kv[KR][W];
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
         const int c = lane + 64 * i;
@@ -531,26 +533,26 @@ __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const u
 #pragma unroll
             for (int j = 0; j < W; ++j) kv[i][j] = mine ? vals[c * W + j] : 0u;
         }
-        if (!mine) taken |= 1u << i;
+        go[i] = mine ? gain_order(sc[i] + a.alpha * (float)__popc(fresh[i])) : 0u;
     }
+    int wins = 0;
     for (int r = 0; r < rounds; ++r) {
-        uint32_t go[CPL], best = 0u;
+        uint32_t best = 0u;
 #pragma unroll
-        for (int i = 0; i < CPL; ++i) {
-            const float g = sc[i] + a.alpha * (float)__popc(fresh[i]);
-            const uint32_t o = gain_order(g);
-            go[i] = ((taken >> i) & 1u) ? 0u : o;
-            best = go[i] > best ? go[i] : best;
-        }
+        for (int i = 0; i < CPL; ++i) best = go[i] > best ? go[i] : best;
         best = wave_max_u32(best);
-        int win = -1;
+        // the first i whose ballot is not empty, and its lowest lane
+        int wi = CPL - 1;
+        uint64_t mw = __ballot(go[CPL - 1] == best);
 #pragma unroll
-        for (int i = 0; i < CPL; ++i) {
+        for (int i = CPL - 2; i >= 0; --i) {
             const uint64_t bal = __ballot(go[i] == best);
-            if (win < 0 && bal != 0) win = 64 * i + (int)__builtin_ctzll(bal);
+            if (bal) {
+                wi = i;
+                mw = bal;
+            }
         }
-        const int wl = win & 63, wi = win >> 6;
-        if (wl == lane) taken |= 1u << wi;
+        const int wl = (int)__builtin_ctzll(mw), win = 64 * wi + wl;
         // the knobs whose value the winner adds (its fresh knobs): only
         // candidates with the same value at those knobs lose them
         uint32_t wf = 0u;
@@ -558,27 +560,38 @@ __device__ void greedy_rounds(const SelectArgs& a, const at_entry* pool, const u
         for (int i = 0; i < CPL; ++i)
             if (i == wi) wf = fresh[i];
         uint32_t added = (uint32_t)__builtin_amdgcn_readlane((int)wf, wl);
-        while (added) {
-            const int j = __builtin_ctz(added);
-            added &= added - 1u;
-            const int jw = j >> 1, sh = 16 * (j & 1);
-            uint32_t wv;
-            if constexpr (REG) {
-                uint32_t x = 0u;
 #pragma unroll
-                for (int i = 0; i < CPL; ++i)
-                    if (i == wi) x = kv[i][jw];
-                wv = ((uint32_t)__builtin_amdgcn_readlane((int)x, wl) >> sh) & 0xffffu;
-            } else {
-                wv = (vals[win * W + jw] >> sh) & 0xffffu;
+        for (int i = 0; i < CPL; ++i)
+            if (i == wi && lane == wl) go[i] = 0u;
+        if (added) {
+            while (added) {
+                const int j = __builtin_ctz(added);
+                added &= added - 1u;
+                const int jw = j >> 1, sh = 16 * (j & 1);
+                uint32_t wv;
+                if constexpr (REG) {
+                    uint32_t x = 0u;
+#pragma unroll
+                    for (int i = 0; i < CPL; ++i)
+                        if (i == wi) x = kv[i][jw];
+                    wv = ((uint32_t)__builtin_amdgcn_readlane((int)x, wl) >> sh) & 0xffffu;
+                } else {
+                    wv = (vals[win * W + jw] >> sh) & 0xffffu;
+                }
+#pragma unroll
+                for (int i = 0; i < CPL; ++i) {
+                    const uint32_t mine = REG ? kv[REG ? i : 0][jw] : vals[(lane + 64 * i) * W + jw];
+                    if (((mine >> sh) & 0xffffu) == wv) fresh[i] &= ~(1u << j);
+                }
             }
 #pragma unroll
-            for (int i = 0; i < CPL; ++i) {
-                const uint32_t mine = REG ? kv[REG ? i : 0][jw] : vals[(lane + 64 * i) * W + jw];
-                if (((mine >> sh) & 0xffffu) == wv) fresh[i] &= ~(1u << j);
-            }
+            for (int i = 0; i < CPL; ++i)
+                go[i] = go[i] ? gain_order(sc[i] + a.alpha * (float)__popc(fresh[i])) : 0u;
         }
-        if (lane == 0) win_idx[r] = win;
+        // lane r % 64 keeps the winner of round r, 64 rounds to a store
+        wins = lane == (r & 63) ? win : wins;
+        if ((r & 63) == 63 || r == rounds - 1)
+            if ((r & ~63) + lane <= r) win_idx[(r & ~63) + lane] = wins;
     }
 }
 
@@ -602,24 +615,17 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
     // the pool: the `pool` best distinct candidates
     const int have = top_distinct(a.src, 0, a.n, (int)a.n, pool, a.pool, a.pool, pool_lds(region, hist, wsum, red));
 
-    // knob values of the pool candidates, packed in pairs (indices fit 32
+    // knob values of the pool candidates, packed in pairs (knob j of
+    // candidate c is 16-bit half c * MAX_KNOBS + j), a thread per knob:
+    // value j of index x is floor(x / radix_j) mod size_j (indices fit 32
     // bits: a space has fewer than 2^32 configurations)
     const int m = sd.n_knobs;
-    for (int c = tid; c < have; c += SEL_WG) {
-        uint32_t cfg = (uint32_t)pool[c].cfg;
-        uint32_t kv[MAX_KNOBS];
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS; ++j) {
-            kv[j] = 0u;
-            if (j < m) {
-                const uint32_t rdx = (uint32_t)sd.radix[j];
-                const uint32_t q = cfg / rdx;
-                kv[j] = q;
-                cfg -= q * rdx;
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < MAX_KNOBS / 2; ++j) vals[c * (MAX_KNOBS / 2) + j] = kv[2 * j] | (kv[2 * j + 1] << 16);
+    uint16_t* vals16 = reinterpret_cast<uint16_t*>(vals);
+    for (int t = tid; t < have * MAX_KNOBS; t += SEL_WG) {
+        const int c = t / MAX_KNOBS, j = t - c * MAX_KNOBS;
+        uint32_t v = 0u;
+        if (j < m) v = ((uint32_t)pool[c].cfg / (uint32_t)sd.radix[j]) % sd.knob_size[j];
+        vals16[t] = (uint16_t)v;
     }
     __syncthreads();
     if (tid >= 64) return;   // the rounds and the draws are wave 0's; no barrier follows
@@ -649,51 +655,93 @@ __global__ __launch_bounds__(SEL_WG) __attribute__((amdgpu_waves_per_eu(1, 4))) 
     __builtin_amdgcn_wave_barrier();
     for (int i = lane; i < rounds; i += 64) {
         const uint64_t x = picked[i];
-        int rank = 0;
-        for (int j = 0; j < rounds; ++j) rank += picked[j] < x ? 1 : 0;
+        int rank = 0, j = 0;
+        // eight reads in flight, then their compares
+        for (; j + 8 <= rounds; j += 8) {
+            uint64_t y[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) y[u] = picked[j + u];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) rank += y[u] < x ? 1 : 0;
+        }
+        for (; j < rounds; ++j) rank += picked[j] < x ? 1 : 0;
         sorted[rank] = x;
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
 
-    // epsilon-greedy draws, then empty slots
+    // epsilon-greedy draws, then empty slots.  The draws' random words do
+    // not depend on the picks: each lane makes one, 64 draws at a time.
     const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
     int n_sel = rounds, slot = rounds;
-    for (int i = 0; i < a.n_random; ++i) {
-        const uint64_t remaining = sd.n_configs - (uint64_t)n_sel;
-        if (remaining == 0) break;
-        const U4 r = philox(k0, k1, U4{(uint32_t)i, 0u, 5u, 0u});
-        const uint64_t u = ((uint64_t)r.y << 32) | r.x;
-        const uint64_t k = __umul64hi(u, remaining);
-        // j = #{positions p with sorted[p] - p <= k}: those picks lie at or
-        // below the drawn index, which is then k + j
-        int j = 0;
-        for (int p = lane; p < n_sel; p += 64) j += (sorted[p] - (uint64_t)p <= k) ? 1 : 0;
-        j = wave_sum(j);
-        const uint64_t cfg = k + (uint64_t)j;
-        // insert at position j: the picks from j on move up by one, each
-        // lane reading all of its picks before any lane writes
-        for (int base = (n_sel - 1) & ~63; base >= 0; base -= 64) {
-            const int p = base + lane;
-            const uint64_t x = (p < n_sel) ? sorted[p] : 0;
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            __builtin_amdgcn_wave_barrier();
-            if (p < n_sel && p >= j) sorted[p + 1] = x;
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            __builtin_amdgcn_wave_barrier();
+    uint64_t u_lane = 0;
+    auto draw_word = [&](int i) -> uint64_t {
+        if ((i & 63) == 0 && i + lane < a.n_random) {
+            const U4 r = philox(k0, k1, U4{(uint32_t)(i + lane), 0u, 5u, 0u});
+            u_lane = ((uint64_t)r.y << 32) | r.x;
         }
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u_lane, i & 63);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u_lane >> 32), i & 63);
+        return ((uint64_t)hi << 32) | lo;
+    };
+    auto put = [&](uint64_t cfg) {
         if (lane == 0) {
-            sorted[j] = cfg;
             at_entry e;
             e.cfg = cfg;
             e.score = 0.0f;
             e.flag = 2u;
             a.out[slot] = e;
         }
-        __builtin_amdgcn_s_waitcnt(0xc07f);
-        __builtin_amdgcn_wave_barrier();
-        ++n_sel;
-        ++slot;
+    };
+    if (rounds + a.n_random <= 64) {
+        // every selected index fits the wave: lane p holds sorted[p]
+        uint64_t sv = lane < rounds ? sorted[lane] : ~0ull;
+        for (int i = 0; i < a.n_random; ++i) {
+            const uint64_t remaining = sd.n_configs - (uint64_t)n_sel;
+            if (remaining == 0) break;
+            const uint64_t k = __umul64hi(draw_word(i), remaining);
+            // j = #{positions p with sorted[p] - p <= k}: those picks lie at
+            // or below the drawn index, which is then k + j
+            const int j = (int)__popcll(__ballot(lane < n_sel && sv - (uint64_t)lane <= k));
+            const uint64_t cfg = k + (uint64_t)j;
+            // insert at position j: lanes above it take their lower
+            // neighbour's value (a wave shift right by one lane)
+            const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)sv, 0x138, 0xf, 0xf, false);
+            const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(sv >> 32), 0x138, 0xf, 0xf,
+                                                                      false);
+            const uint64_t below = ((uint64_t)hi << 32) | lo;
+            sv = lane > j ? below : (lane == j ? cfg : sv);
+            put(cfg);
+            ++n_sel;
+            ++slot;
+        }
+    } else {
+        for (int i = 0; i < a.n_random; ++i) {
+            const uint64_t remaining = sd.n_configs - (uint64_t)n_sel;
+            if (remaining == 0) break;
+            const uint64_t k = __umul64hi(draw_word(i), remaining);
+            int j = 0;
+            for (int p = lane; p < n_sel; p += 64) j += (sorted[p] - (uint64_t)p <= k) ? 1 : 0;
+            j = wave_sum(j);
+            const uint64_t cfg = k + (uint64_t)j;
+            // insert at position j: the picks from j on move up by one, each
+            // lane reading all of its picks before any lane writes
+            for (int base = (n_sel - 1) & ~63; base >= 0; base -= 64) {
+                const int p = base + lane;
+                const uint64_t x = (p < n_sel) ? sorted[p] : 0;
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                __builtin_amdgcn_wave_barrier();
+                if (p < n_sel && p >= j) sorted[p + 1] = x;
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                __builtin_amdgcn_wave_barrier();
+            }
+            if (lane == 0) sorted[j] = cfg;
+            put(cfg);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
+            ++n_sel;
+            ++slot;
+        }
     }
     for (int q = slot + lane; q < a.n_greedy + a.n_random; q += 64) a.out[q] = empty_entry();
 }
@@ -750,6 +798,52 @@ hipError_t select_scratch_ptr(int device, at_entry** out) {
     return hipSuccess;
 }
 
+// The allocating entry point's scratch comes from a memory pool of the
+// library's own on each device, whose release threshold is unlimited:
+// memory freed back to it stays reserved, so that later calls take it again
+// without mapping new memory.  Created by the first call that needs scratch
+// on the device (which is current), kept until the process ends.
+static hipError_t select_mem_pool(int device, hipMemPool_t* out) {
+    constexpr int MAX_DEVICES = 64;
+    static std::mutex mu;
+    static hipMemPool_t pools[MAX_DEVICES] = {};
+    if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!pools[device]) {
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = device;
+        hipMemPool_t p = nullptr;
+        hipError_t e = hipMemPoolCreate(&p, &props);
+        if (e != hipSuccess) return e;
+        uint64_t keep_all = UINT64_MAX;
+        e = hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep_all);
+        if (e != hipSuccess) {
+            (void)hipMemPoolDestroy(p);
+            return e;
+        }
+        pools[device] = p;
+    }
+    *out = pools[device];
+    return hipSuccess;
+}
+
+// The allocating entry point keeps, on each device, the scratch of its
+// last call that needed one (grown when a call needs more) and an event
+// recorded after that call's kernels on the call's stream.  A call first
+// makes its own stream wait for that event, so calls on any streams use
+// (or free) the scratch one after the other.  Both live until the process
+// ends.
+struct SelectCache {
+    at_entry* ptr = nullptr;
+    int64_t entries = 0;
+    hipEvent_t done = nullptr;
+    hipStream_t last = nullptr;   // stream of the last call (its order covers the next call there)
+    bool used = false;
+};
+
 hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
                          float alpha, int n_random, uint64_t seed, at_entry* out, hipStream_t stream,
                          at_entry* scratch) {
@@ -768,38 +862,59 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     const int slots = run_slots(pool);
     const at_entry* src = cand;
     int64_t n = n_cand;
-    void* bufs[2] = {nullptr, nullptr};
+    at_entry* bufs[2] = {nullptr, nullptr};
     const int64_t need = select_scratch_entries(n_cand, pool);
-    const bool own = need > 0 && !scratch;   // stream-ordered buffers of our own
+    const bool own = need > 0 && !scratch;   // scratch of our own (both buffers in one)
+    static std::mutex cache_mu;
+    static SelectCache caches[64];
+    std::unique_lock<std::mutex> lock(cache_mu, std::defer_lock);   // held while the kernels are enqueued
+    SelectCache* cache = nullptr;
     if (need > 0 && scratch) {
         if (need > SELECT_SCRATCH_ENTRIES) return hipErrorInvalidValue;
         bufs[0] = scratch;
         bufs[1] = scratch + SELECT_SCRATCH_ENTRIES;
     } else if (own) {
-        const size_t bytes = (size_t)need * sizeof(at_entry);
-        for (void*& b : bufs) {
-            e = hipMallocAsync(&b, bytes, stream);
-            if (e != hipSuccess) {
-                for (void* x : bufs)
-                    if (x) (void)hipFreeAsync(x, stream);
-                return e;
-            }
+        if (sp.device < 0 || sp.device >= 64) return hipErrorInvalidDevice;
+        lock.lock();
+        cache = &caches[sp.device];
+        if (!cache->done && (e = hipEventCreateWithFlags(&cache->done, hipEventDisableTiming)) != hipSuccess) {
+            cache->done = nullptr;
+            return e;
         }
+        // the last call's kernels are done with the scratch first (on the
+        // same stream they come first anyway)
+        if (cache->used && stream != cache->last && (e = hipStreamWaitEvent(stream, cache->done, 0)) != hipSuccess)
+            return e;
+        if (cache->entries < 2 * need) {
+            if (cache->ptr) (void)hipFreeAsync(cache->ptr, stream);
+            cache->ptr = nullptr;
+            cache->entries = 0;
+            hipMemPool_t mp = nullptr;
+            if ((e = select_mem_pool(sp.device, &mp)) != hipSuccess) return e;
+            void* b = nullptr;
+            if ((e = hipMallocFromPoolAsync(&b, 2 * (size_t)need * sizeof(at_entry), mp, stream)) != hipSuccess)
+                return e;
+            cache->ptr = static_cast<at_entry*>(b);
+            cache->entries = 2 * need;
+        }
+        bufs[0] = cache->ptr;
+        bufs[1] = cache->ptr + need;
     }
     int cur = 0;
     while (n > FINAL_MAX) {
         const int64_t groups = (n + CHUNK - 1) / CHUNK;
-        hipLaunchKernelGGL(k_reduce, dim3((unsigned)groups), dim3(SEL_WG), 0, stream, src, n, keep, slots,
-                           static_cast<at_entry*>(bufs[cur]));
+        hipLaunchKernelGGL(k_reduce, dim3((unsigned)groups), dim3(SEL_WG), 0, stream, src, n, keep, slots, bufs[cur]);
         if ((e = hipGetLastError()) != hipSuccess) break;
-        src = static_cast<const at_entry*>(bufs[cur]);
+        src = bufs[cur];
         n = groups * slots;
         cur ^= 1;
     }
     if (e != hipSuccess) {
-        if (own)
-            for (void* x : bufs)
-                if (x) (void)hipFreeAsync(x, stream);
+        if (own) {
+            (void)hipEventRecord(cache->done, stream);
+            cache->last = stream;
+            cache->used = true;
+        }
         return e;
     }
     SelectArgs a{};
@@ -814,9 +929,12 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     a.out = out;
     hipLaunchKernelGGL(k_select, dim3(1), dim3(SEL_WG), select_lds_bytes(), stream, a);
     e = hipGetLastError();
-    if (own)
-        for (void* b : bufs)
-            if (b) (void)hipFreeAsync(b, stream);
+    if (own) {
+        const hipError_t r = hipEventRecord(cache->done, stream);
+        if (e == hipSuccess) e = r;
+        cache->last = stream;
+        cache->used = true;
+    }
     return e;
 }
 
