@@ -840,8 +840,6 @@ struct SelectCache {
     at_entry* ptr = nullptr;
     int64_t entries = 0;
     hipEvent_t done = nullptr;
-    hipStream_t last = nullptr;   // stream of the last call (its order covers the next call there)
-    bool used = false;
 };
 
 hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_cand, int pool, int n_greedy,
@@ -877,14 +875,15 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
         if (sp.device < 0 || sp.device >= 64) return hipErrorInvalidDevice;
         lock.lock();
         cache = &caches[sp.device];
-        if (!cache->done && (e = hipEventCreateWithFlags(&cache->done, hipEventDisableTiming)) != hipSuccess) {
+        // the event orders calls only (a later call's kernels overwrite what
+        // an earlier call's kernels read), so it needs no system-scope fence
+        if (!cache->done && (e = hipEventCreateWithFlags(&cache->done, hipEventDisableTiming |
+                                                                           hipEventDisableSystemFence)) != hipSuccess) {
             cache->done = nullptr;
             return e;
         }
-        // the last call's kernels are done with the scratch first (on the
-        // same stream they come first anyway)
-        if (cache->used && stream != cache->last && (e = hipStreamWaitEvent(stream, cache->done, 0)) != hipSuccess)
-            return e;
+        // the last call's kernels are done with the scratch first
+        if ((e = hipStreamWaitEvent(stream, cache->done, 0)) != hipSuccess) return e;
         if (cache->entries < 2 * need) {
             if (cache->ptr) (void)hipFreeAsync(cache->ptr, stream);
             cache->ptr = nullptr;
@@ -910,11 +909,7 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
         cur ^= 1;
     }
     if (e != hipSuccess) {
-        if (own) {
-            (void)hipEventRecord(cache->done, stream);
-            cache->last = stream;
-            cache->used = true;
-        }
+        if (own) (void)hipEventRecord(cache->done, stream);
         return e;
     }
     SelectArgs a{};
@@ -932,8 +927,6 @@ hipError_t launch_select(const at_space_s& sp, const at_entry* cand, int64_t n_c
     if (own) {
         const hipError_t r = hipEventRecord(cache->done, stream);
         if (e == hipSuccess) e = r;
-        cache->last = stream;
-        cache->used = true;
     }
     return e;
 }
