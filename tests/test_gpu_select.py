@@ -117,7 +117,8 @@ def repeats_and_ties(kind, n_lists, per_list, n_configs, seed):
         cand["score"][valid] = scores[pick]
     elif kind == "same_index_other_score":
         # a quarter of the entries take another entry's index, keeping
-        # their own score
+        # their own score (outside what at_select_batch asks of its input;
+        # the library still drops exactly what the oracle drops)
         idx = rng.choice(valid, len(valid) // 4, replace=False)
         cand["cfg"][idx] = cand["cfg"][rng.choice(valid, len(idx))]
     elif kind == "all_tied":
@@ -170,6 +171,31 @@ def test_select_edge_cases(P, kind):
     else:
         cand = W.make_candidates(3, 5, 192, seed=7)
         run_both(P, W.GEMM, gemm, cand, pool=1, n_greedy=1, alpha=3.0, n_random=0, seed=6)
+
+
+def test_select_batch_on_two_streams(P):
+    """The allocating call keeps one scratch per device and orders its calls
+    through an event: calls on two streams, started so that their kernels
+    would interleave, each give the oracle's batch."""
+    import torch
+    osp = oracle.Space(W.CONV2D, C12)
+    sp = P.at_space_create(W.CONV2D, C12)
+    cands = [W.make_candidates(4096, 16, osp.n_configs, seed=s) for s in (301, 302)]
+    wants = [oracle.select_batch(osp, c.view(oracle.TOP_DTYPE), 128, 61, 1.0, 3, 11 + i) for i, c in enumerate(cands)]
+    dev = [to_dev(c) for c in cands]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [torch.full((64, 4), -1, dtype=torch.int32, device=DEV) for _ in range(2)]
+    torch.cuda.synchronize()
+    for rep in range(6):
+        for i in range(2):
+            with torch.cuda.stream(streams[i]):
+                torch.cuda._sleep(200000 + 30000 * i)
+                P.at_select_batch(sp, dev[i], 128, 61, 1.0, 3, 11 + i, outs[i], stream=streams[i])
+        torch.cuda.synchronize()
+        for i in range(2):
+            got = P.entries(outs[i])
+            assert np.array_equal(got["cfg"], wants[i]["cfg"]) and np.array_equal(got["flag"], wants[i]["valid"])
+            assert np.array_equal(got["score"].view(np.uint32), wants[i]["score"].view(np.uint32))
 
 
 def test_select_argument_errors(P):
