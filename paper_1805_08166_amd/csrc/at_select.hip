@@ -38,7 +38,8 @@
 // rounds, each lane looking after pool candidates lane, lane + 64, ...: a
 // round is a wave-wide arg-max of the gains (DPP steps, no workgroup
 // barrier), then every lane clears the knobs the winner covers in its
-// candidates' masks.  The wave then ranks the picks in parallel (ascending
+// candidates' masks (and computes again the gains of the candidates whose
+// masks changed).  The wave then ranks the picks in parallel (ascending
 // indices) and makes each random draw with one wave-wide count: with S the
 // picks in ascending order, the floor(u * remaining / 2^64) = k-th
 // unselected index is k + j, j the number of positions i with
@@ -53,8 +54,8 @@ namespace {
 using namespace dev;
 
 constexpr int SEL_WG = 1024;     // threads of both kernels
-constexpr int CHUNK = 2048;      // candidates one reduction workgroup orders
-constexpr int FINAL_MAX = 2048;  // candidates the final workgroup orders
+constexpr int CHUNK = 2048;      // candidates one reduction workgroup takes
+constexpr int FINAL_MAX = 2048;  // candidates the final workgroup takes
 constexpr int POOL_MAX = 1024;
 constexpr int PICK_MAX = 2048;   // greedy plus random picks
 constexpr int PER = FINAL_MAX / SEL_WG;   // records a thread holds in the pool stage
@@ -71,7 +72,7 @@ constexpr int RED_WORDS = 3 * (SEL_WG / 64) + 2;
 // bits (smaller for a higher score, -0.0 as +0.0) in the high half and the
 // configuration index in the low half (indices fit 32 bits: a space holds
 // fewer than 2^32 configurations), ~0 for an empty slot; the score's own
-// bits travel beside it in a second array.  Binary searches read the keys
+// bits travel beside it in a second array.  Orderings compare the keys
 // only (8-byte LDS reads).
 constexpr uint64_t KEY_EMPTY = ~0ull;
 
