@@ -508,19 +508,33 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             // task t is loop t % L of outcome (t / L) & 1 of chain t / (2L)
             // (an initial candidate is always accepted: no reject outcome)
             if (a.draw == DRAW_PROPOSE) {
-                for (int t = t0; t < nc * 2 * L; t += CHAIN_WG - 64) {
-                    const int l = t % L, jo = t / L, j = jo >> 1, o = jo & 1;
-                    if (o == 1 && a.fin == FIN_INIT) continue;
+                // the moves first, lane i < 2 nc of every building wave making
+                // the move of chain i / 2 from state i & 1 into the wave's own
+                // rows (the same values in every wave, so none waits for
+                // another), then the loop tasks from those rows
+                __shared__ uint32_t s_mv[CHAIN_WG / 64 - 1][2 * CPW][MAX_KNOBS / 2];
+                uint32_t(*mv)[MAX_KNOBS / 2] = s_mv[wave - 1];
+                if (lane < 2 * nc && !((lane & 1) == 1 && a.fin == FIN_INIT)) {
+                    const int j = lane >> 1, o = lane & 1;
                     const SpaceDesc& sd = desc_of(j);
                     uint32_t base[MAX_KNOBS], nx[MAX_KNOBS];
 #pragma unroll
                     for (int i = 0; i < MAX_KNOBS; ++i) base[i] = s_kv[o ^ 1][j][i];
                     step_move(sd, k0, k1, (uint32_t)(a.chain0 + (uint64_t)(c0 + j)), a.draw_step, base, nx);
-                    if (l == 0) {
 #pragma unroll
-                        for (int i = 0; i < MAX_KNOBS / 2; ++i) rec[j].nx[o][i] = pack_pair(nx, i);
+                    for (int i = 0; i < MAX_KNOBS / 2; ++i) {
+                        mv[lane][i] = pack_pair(nx, i);
+                        if (wave == 1) rec[j].nx[o][i] = pack_pair(nx, i);
                     }
-                    row_features<TMPL>(sd, facp, nx, l, a.Fr != nullptr, frow[o][j], tdrow[o][j]);
+                }
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                __builtin_amdgcn_wave_barrier();
+                for (int t = t0; t < nc * 2 * L; t += CHAIN_WG - 64) {
+                    const int l = t % L, jo = t / L, j = jo >> 1, o = jo & 1;
+                    if (o == 1 && a.fin == FIN_INIT) continue;
+                    uint32_t nx[MAX_KNOBS];
+                    unpack_pairs(mv[jo], nx);
+                    row_features<TMPL>(desc_of(j), facp, nx, l, a.Fr != nullptr, frow[o][j], tdrow[o][j]);
                 }
             }
         }
