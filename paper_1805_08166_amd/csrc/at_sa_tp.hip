@@ -92,6 +92,13 @@ struct ChainArgs {
     const float* Vg;
     int Tg;
     uint32_t* Fr;
+    // trees of the next tree launch, relocated (pf_tree_bytes each, pf_tpw
+    // a tree workgroup, pf_trees in all): the building waves bring them
+    // into their XCD's L2 before the tree kernel copies them; null: none
+    const uint8_t* pf_trees;
+    int pf_tree_bytes;
+    int pf_tpw;
+    int pf_ntrees;
 };
 
 constexpr int REL_F = 192;              // context relation features per candidate
@@ -535,6 +542,40 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
                     uint32_t nx[MAX_KNOBS];
                     unpack_pairs(mv[jo], nx);
                     row_features<TMPL>(desc_of(j), facp, nx, l, a.Fr != nullptr, frow[o][j], tdrow[o][j]);
+                }
+            }
+            if (a.pf_trees) {
+                // the next tree launch copies its trees from the L2: chain
+                // workgroup b takes half of the trees of tree workgroup
+                // 8 * (b / 16) + b % 8, which runs on the same XCD when
+                // workgroups go round the eight XCDs in turn (a wrong guess
+                // only warms another XCD's L2)
+                const int b = (int)blockIdx.x;
+                const int tw = 8 * (b / 16) + b % 8, half = (b / 8) & 1;
+                const int per = a.pf_tpw / 2 > 0 ? a.pf_tpw / 2 : 1;
+                const int first = tw * a.pf_tpw + half * per;
+                int cnt = a.pf_ntrees - first < per ? a.pf_ntrees - first : per;
+                if (half == 1 && a.pf_tpw == 1) cnt = 0;
+                if (cnt > 0) {
+                    const int64_t bytes = (int64_t)cnt * a.pf_tree_bytes;
+                    const uint8_t* src = a.pf_trees + (int64_t)first * a.pf_tree_bytes;
+                    // plain loads, all in flight before one wait: each lane
+                    // takes 16 bytes of every 1 KB line its wave covers (at most
+                    // PF_LINES lines a wave), from a valid address on every
+                    // lane, the values folded into one that is kept
+                    constexpr int PF_LINES = 12;
+                    const int nbw = CHAIN_WG / 64 - 1;
+                    uint32_t keep = 0u;
+                    uint4 v[PF_LINES];
+#pragma unroll
+                    for (int u = 0; u < PF_LINES; ++u) {
+                        int64_t off = ((int64_t)u * nbw + (wave - 1)) * 1024 + lane * 16;
+                        off = off < bytes ? off : bytes - 16;
+                        v[u] = *reinterpret_cast<const uint4*>(src + off);
+                    }
+#pragma unroll
+                    for (int u = 0; u < PF_LINES; ++u) keep ^= v[u].x;
+                    asm volatile("" ::"v"(keep));
                 }
             }
         }
@@ -1431,6 +1472,15 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
         x.fin_step = s - 1;
         x.draw = DRAW_PROPOSE;
         x.draw_step = (uint32_t)(ch.step_abs + (uint64_t)s);
+        if (!eg && !wide) {
+            // a long fold leaves the building waves time to spare: they bring
+            // the next tree launch's trees into the L2 (with a short fold the
+            // building is the longer side and this would lengthen the step)
+            x.pf_trees = reinterpret_cast<const uint8_t*>(tl.ta.words32);
+            x.pf_tree_bytes = 8 << e.depth;
+            x.pf_tpw = tl.ta.tpw;
+            x.pf_ntrees = e.n_trees;
+        }
         if ((err = chain_kernel(x)) != hipSuccess) return err;
         if ((err = trees_kernel()) != hipSuccess) return err;
         pending = FIN_STEP;
