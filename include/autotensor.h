@@ -92,7 +92,11 @@ typedef struct {
 
 /* Builds the schedule space S_e of an index expression e (Section 2):
  * knob tables, loop nest and buffer index expressions, uploaded once to the
- * current device.  shape: host [nshape] int64 (see at_template).
+ * current device.  A space of at most 2^28 configurations is also scanned
+ * whole on the device (one kernel on the null stream) for the loop-context
+ * features that take one value over it: the tree-partitioned annealing
+ * path leaves those out of its feature tiles (at_chains_last_plan).
+ * shape: host [nshape] int64 (see at_template).
  * Errors: AT_E_INVALID for bad shapes; AT_E_UNSUPPORTED when the nest's
  * iteration count or a buffer size reaches 2^31, or the space holds 2^32 or
  * more configurations.  Synchronous. */
@@ -112,7 +116,9 @@ at_status at_space_info(at_space_t space, int* n_knobs, int32_t* knob_sizes, int
  * chain_offsets: host [n + 1] int64, ascending, chain_offsets[0] == 0: space
  * i owns the chains [chain_offsets[i], chain_offsets[i+1]).  The set keeps
  * its own copies of the member spaces' tables; members may be destroyed
- * afterwards.  AT_E_MISMATCH if the templates differ.  Synchronous. */
+ * afterwards.  A loop-context feature counts as constant over the set when
+ * every member fixes it at the same value.  AT_E_MISMATCH if the templates
+ * differ.  Synchronous. */
 at_status at_spaceset_create(const at_space_t* spaces, int n, const int64_t* chain_offsets,
                              at_space_t* out);
 void at_space_destroy(at_space_t space);
@@ -415,9 +421,10 @@ at_status at_chains_last_path(at_chains_t chains, int* path);
  * Tree-partitioned run: info[0] trees per tree-kernel workgroup, [1] waves
  * per tree-kernel workgroup, [2] tree-kernel workgroups, [3] chain slices
  * per tree group, [4] 64-chain blocks per slice (a wave walks more than one
- * block when this exceeds [1]), [5] chain-kernel workgroups, [6] LDS bytes
- * of a tree-kernel workgroup, [7] bytes of leaf values written and read
- * back per step. */
+ * block when this exceeds [1]), [5] chain-kernel workgroups, [6] quads (4
+ * features) per chain in a feature tile: the loop-context features that are
+ * not constant over the space (set), when dropping the constant ones saves a
+ * quad, [7] bytes of leaf values written and read back per step. */
 at_status at_chains_last_plan(at_chains_t chains, int64_t info[8]);
 
 /* Copies the chains' current configuration indices (device [n_chains]

@@ -377,7 +377,7 @@ def at_chains_last_path(chains: Chains) -> int:
 PLAN_KEYS_LOCAL = ["chains_per_wg", "threads", "workgroups", "trees_per_chunk", "chunks", "gather", "lds_bytes",
                    "stream_bytes_per_step"]
 PLAN_KEYS_TREES = ["trees_per_wg", "waves", "workgroups", "slices", "slice_blocks", "chain_workgroups",
-                   "lds_bytes", "v_bytes_per_step"]
+                   "tile_quads", "v_bytes_per_step"]
 
 
 def at_chains_last_plan(chains: Chains) -> dict:

@@ -50,6 +50,63 @@ at_status alloc_zero(DeviceBuf& buf, size_t bytes) {
     return AT_OK;
 }
 
+// Largest single space whose configurations are all scanned for constant
+// loop-context features (a few milliseconds of one GPU at this size).
+constexpr uint64_t FEATURE_SCAN_MAX = (uint64_t)1 << 28;
+
+void release(DeviceBuf& buf);
+
+// Constant loop-context features of a single space (see at_space_s).
+at_status scan_constant_features(at_space_s& sp) {
+    const SpaceDesc& d = sp.descs[0];
+    sp.fconst.clear();
+    if (d.n_configs > FEATURE_SCAN_MAX) return AT_OK;
+    const int F = d.n_features;
+    DeviceBuf buf;
+    at_status st = alloc_zero(buf, (size_t)2 * F * 4);
+    if (st != AT_OK) return st;
+    uint32_t* flags = static_cast<uint32_t*>(buf.p);
+    hipError_t e = launch_feature_scan(sp, flags, flags + F, nullptr);
+    std::vector<uint32_t> host((size_t)2 * F);
+    if (e == hipSuccess) e = hipMemcpy(host.data(), buf.p, host.size() * 4, hipMemcpyDeviceToHost);
+    release(buf);
+    if (e != hipSuccess) return hip_fail(e, "feature scan");
+    sp.fconst.resize(F);
+    for (int f = 0; f < F; ++f) sp.fconst[f] = (host[f] != 0u || host[F + f] > 63u) ? 0xff : (uint8_t)host[F + f];
+    return AT_OK;
+}
+
+// Tile layout of the tree-partitioned path (see at_space_s): the varying
+// features only, in feature order, when that halves the tile slot (a power
+// of two of at least 256 bytes per wave: more waves or trees fit in LDS);
+// otherwise every feature in order.
+at_status build_feature_tables(at_space_s& sp) {
+    const int F = sp.descs[0].n_features, Q = (F + 3) / 4;
+    int nvar = 0;
+    for (uint8_t v : sp.fconst) nvar += v == 0xff;
+    const int qc = nvar > 0 ? (nvar + 3) / 4 : 1;
+    auto slot = [](int q) {
+        int s = 256;
+        while (s < q * 256) s <<= 1;
+        return s;
+    };
+    const bool compact = !sp.fconst.empty() && slot(qc) < slot(Q);
+    sp.tile_q = compact ? qc : Q;
+    std::vector<uint16_t> map(256, 0);
+    std::vector<uint8_t> src((size_t)4 * sp.tile_q, 0xff);
+    for (int f = 0, p = 0; f < F; ++f) {
+        if (compact && sp.fconst[f] != 0xff) {
+            map[f] = (uint16_t)(0x100 | sp.fconst[f]);
+        } else {
+            map[f] = (uint16_t)p;
+            src[p++] = (uint8_t)f;
+        }
+    }
+    at_status st = upload(sp.d_fmap, map.data(), map.size());
+    if (st == AT_OK) st = upload(sp.d_fsrc, src.data(), src.size());
+    return st;
+}
+
 // LDS images of a space's members and, for a set, the image of each block
 // of STAGE_CHAINS chains (see at_space_s).
 at_status build_stage(at_space_s& sp) {
@@ -162,7 +219,8 @@ at_status at_space_create(int tmpl, const int64_t* shape, int nshape, at_space_t
     int64_t offs[2] = {0, INT64_MAX};
     if ((st = upload(sp->d_descs, &d, 1)) != AT_OK || (st = upload(sp->d_factors, factors.data(), factors.size())) != AT_OK ||
         (st = upload(sp->d_offsets, offs, 2)) != AT_OK || (st = alloc_zero(sp->d_errors, 8)) != AT_OK ||
-        (st = build_stage(*sp)) != AT_OK) {
+        (st = build_stage(*sp)) != AT_OK || (st = scan_constant_features(*sp)) != AT_OK ||
+        (st = build_feature_tables(*sp)) != AT_OK) {
         at_space_destroy(sp);
         return st;
     }
@@ -214,11 +272,24 @@ at_status at_spaceset_create(const at_space_t* spaces, int n, const int64_t* cha
         sp->host_factors.push_back(f);
     }
     sp->chain_offsets.assign(chain_offsets, chain_offsets + n + 1);
+    // a feature is constant over the set when every member gives it the same
+    // value
+    sp->fconst = spaces[0]->fconst;
+    for (int i = 1; i < n && !sp->fconst.empty(); ++i) {
+        const std::vector<uint8_t>& m = spaces[i]->fconst;
+        if (m.size() != sp->fconst.size()) {
+            sp->fconst.clear();
+            break;
+        }
+        for (size_t f = 0; f < m.size(); ++f)
+            if (m[f] != sp->fconst[f]) sp->fconst[f] = 0xff;
+    }
     at_status st;
     if ((st = upload(sp->d_descs, sp->descs.data(), sp->descs.size())) != AT_OK ||
         (st = upload(sp->d_factors, all.data(), all.size())) != AT_OK ||
         (st = upload(sp->d_offsets, sp->chain_offsets.data(), sp->chain_offsets.size())) != AT_OK ||
-        (st = alloc_zero(sp->d_errors, 8)) != AT_OK || (st = build_stage(*sp)) != AT_OK) {
+        (st = alloc_zero(sp->d_errors, 8)) != AT_OK || (st = build_stage(*sp)) != AT_OK ||
+        (st = build_feature_tables(*sp)) != AT_OK) {
         at_space_destroy(sp);
         return st;
     }
@@ -235,6 +306,8 @@ void at_space_destroy(at_space_t space) {
     release(space->d_errors);
     release(space->d_stage);
     release(space->d_wg_space);
+    release(space->d_fsrc);
+    release(space->d_fmap);
     delete space;
 }
 

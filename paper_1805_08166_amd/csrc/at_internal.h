@@ -191,6 +191,18 @@ struct at_space_s {
     at::DeviceBuf d_wg_space;
     // per member space: its factor tables as host data (for building sets)
     std::vector<std::vector<uint64_t>> host_factors;
+    // Loop-context features constant over the space (set): fconst[f] is the
+    // value every configuration gives feature f, 0xff when it varies; empty
+    // when the space was too large to scan.
+    std::vector<uint8_t> fconst;
+    // Feature tiles of the tree-partitioned path: tile_q quads (4 features)
+    // per chain.  d_fsrc (uint8 [4 * tile_q]) names the feature at each tile
+    // position (0xff: padding); d_fmap (uint16 [256]) gives each feature's
+    // tile position, or 0x100 | value for a constant feature, whose tree
+    // nodes are settled when the trees are relocated.
+    int tile_q = 0;
+    at::DeviceBuf d_fsrc;
+    at::DeviceBuf d_fmap;
 };
 
 struct at_ensemble_s {
@@ -260,6 +272,9 @@ hipError_t launch_extract_full(const at_space_s& sp, const uint64_t* cfgs, int64
                                hipStream_t stream);
 hipError_t launch_relation(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
                            hipStream_t stream);
+// flags[f] = 1 when loop-context feature f is not the same for every
+// configuration of a single space; ref[f] = configuration 0's value.
+hipError_t launch_feature_scan(const at_space_s& sp, uint32_t* flags, uint32_t* ref, hipStream_t stream);
 // accumulate: add to scores (fp32, the stored value first) instead of storing
 hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n, float* scores,
                           uint16_t* leaves, bool accumulate, hipStream_t stream);

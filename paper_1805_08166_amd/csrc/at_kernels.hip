@@ -311,6 +311,54 @@ __global__ __launch_bounds__(WG) void k_export(const SpaceDesc* descs, const int
     if (cur_score) cur_score[c] = score[c];
 }
 
+// ==========================================================================
+// Which loop-context features are constant over a space.  Every
+// configuration index below n is visited (grid-stride loop, one per lane);
+// flags[f] becomes 1 when some configuration's feature f differs from that
+// of configuration 0, and workgroup 0 writes configuration 0's row to ref.
+// A feature left unflagged therefore takes one value over the whole space.
+// ==========================================================================
+template <int TMPL>
+__global__ __launch_bounds__(WG) void k_feature_scan(SpaceDesc sd, const uint64_t* __restrict__ factors, uint64_t n,
+                                                     uint32_t* __restrict__ flags, uint32_t* __restrict__ ref_out) {
+    constexpr int F = RowLayout<TMPL>::F;
+    __shared__ uint32_t ref[F];
+    __shared__ uint32_t diff[F];
+    const int tid = threadIdx.x;
+    auto row_of = [&](uint64_t cfg, auto&& put) {
+        // mixed radix, knob 0 most significant (indices below n fit 32 bits)
+        uint32_t rest = (uint32_t)cfg;
+        uint32_t kv[MAX_KNOBS];
+#pragma unroll
+        for (int j = MAX_KNOBS - 1; j >= 0; --j) {
+            if (j < sd.n_knobs) {
+                const uint32_t sz = sd.knob_size[j];
+                const uint32_t q = rest / sz;
+                kv[j] = rest - q * sz;
+                rest = q;
+            } else {
+                kv[j] = 0u;
+            }
+        }
+        uint32_t fac[6][4];
+        gather_factors<TMPL>(sd, factors, kv, fac);
+        nest_features<TMPL, 11>(sd, fac, ann_knobs_of<TMPL>(sd, kv), put);
+    };
+    for (int f = tid; f < F; f += WG) diff[f] = 0u;
+    if (tid == 0) row_of(0, [&](int f, uint32_t v) { ref[f] = v; });
+    __syncthreads();
+    const uint64_t stride = (uint64_t)gridDim.x * WG;
+    for (uint64_t cfg = (uint64_t)blockIdx.x * WG + tid; cfg < n; cfg += stride)
+        row_of(cfg, [&](int f, uint32_t v) {
+            if (v != ref[f]) diff[f] = 1u;
+        });
+    __syncthreads();
+    for (int f = tid; f < F; f += WG) {
+        if (diff[f]) flags[f] = 1u;
+        if (blockIdx.x == 0) ref_out[f] = ref[f];
+    }
+}
+
 }  // namespace
 
 hipError_t launch_extract(const at_space_s& sp, const uint64_t* cfgs, int64_t n, int32_t* feats,
@@ -439,6 +487,21 @@ hipError_t launch_predict(const EnsembleDesc& e, const int32_t* feats, int64_t n
         case 12: return predict_depth<12>(e, feats, n, scores, leaves, accumulate, stream);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_feature_scan(const at_space_s& sp, uint32_t* flags, uint32_t* ref, hipStream_t stream) {
+    const SpaceDesc& sd = sp.descs[0];
+    const uint64_t n = sd.n_configs;
+    if (n == 0) return hipSuccess;
+    const uint64_t blocks = (n + WG - 1) / WG;
+    const unsigned grid = (unsigned)(blocks < 4096 ? blocks : 4096);
+    const uint64_t* fac = static_cast<const uint64_t*>(sp.d_factors.p);
+    if (sp.tmpl == AT_TMPL_GEMM)
+        hipLaunchKernelGGL(k_feature_scan<AT_TMPL_GEMM>, dim3(grid), dim3(WG), 0, stream, sd, fac, n, flags, ref);
+    else
+        hipLaunchKernelGGL(k_feature_scan<AT_TMPL_CONV2D_NCHW>, dim3(grid), dim3(WG), 0, stream, sd, fac, n, flags,
+                           ref);
+    return hipGetLastError();
 }
 
 hipError_t launch_export(const at_chains_s& ch, uint64_t* cur_cfg, float* cur_score, hipStream_t stream) {

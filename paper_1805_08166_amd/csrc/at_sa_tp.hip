@@ -99,6 +99,11 @@ struct ChainArgs {
     int pf_tree_bytes;
     int pf_tpw;
     int pf_ntrees;
+    // tile layout of Fg: fq quads, position p holding loop-context feature
+    // fsrc[p] (0xff: padding); fident: position p holds feature p
+    const uint8_t* fsrc;
+    int fq;
+    int fident;
 };
 
 constexpr int REL_F = 192;              // context relation features per candidate
@@ -414,6 +419,20 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     int64_t thr_i = a.fin == FIN_STEP ? c * a.steps + a.fin_step : c;
     asm volatile("" : "+v"(thr_i));   // one load from either table (not two loads and a join)
     const float thr_v = thr_b[thr_i];
+    // tile-layout words of the packed rows this thread writes at the end
+    // (quads (tid + m * CHAIN_WG) / 16, clamped to the last so that every
+    // lane loads)
+    constexpr int PACK_ITERS = (CPW * Q + CHAIN_WG - 1) / CHAIN_WG;
+    uint32_t src4[PACK_ITERS];
+#pragma unroll
+    for (int m = 0; m < PACK_ITERS; ++m) src4[m] = 0u;
+    if (!a.fident) {
+#pragma unroll
+        for (int m = 0; m < PACK_ITERS; ++m) {
+            const int q = (tid + m * CHAIN_WG) >> 4;
+            src4[m] = *reinterpret_cast<const uint32_t*>(a.fsrc + 4 * (q < a.fq ? q : a.fq - 1));
+        }
+    }
 
     if (a.fin == FIN_NONE) {
         // No pending candidate: the first draw of fresh chains, or a move
@@ -689,15 +708,27 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             a.Fr[(int64_t)q * a.fg_stride + c0 + j] = w;
         }
     }
-    // packed rows out (4x+3 per byte, the tree kernel's tile encoding),
-    // consecutive lanes on consecutive chains
+    // packed rows out in the tree kernel's tile layout (4x+3 per byte,
+    // padding 0), consecutive lanes on consecutive chains
     // (a feature value x <= 63 makes (x << 2) | 3 stay within its byte)
-    constexpr uint32_t LAST = (N::F & 3) ? (1u << (8 * (N::F & 3))) - 1u : 0xffffffffu;
-    for (int idx = tid; idx < CPW * Q; idx += CHAIN_WG) {
+#pragma unroll
+    for (int m = 0; m < PACK_ITERS; ++m) {
+        const int idx = tid + m * CHAIN_WG;
         const int q = idx >> 4, j = idx & (CPW - 1);
-        if (j >= nc) continue;
-        uint32_t w = (*reinterpret_cast<const uint32_t*>(&frow[s_sel[j]][j][4 * q]) << 2) | 0x03030303u;
-        if (q == Q - 1) w &= LAST;
+        if (q >= a.fq || j >= nc) continue;
+        const uint8_t* row = frow[s_sel[j]][j];
+        uint32_t w = 0u;
+        if (a.fident) {
+            constexpr uint32_t LAST = (N::F & 3) ? (1u << (8 * (N::F & 3))) - 1u : 0xffffffffu;
+            w = (*reinterpret_cast<const uint32_t*>(row + 4 * q) << 2) | 0x03030303u;
+            if (q == Q - 1) w &= LAST;
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t f = (src4[m] >> (8 * i)) & 0xffu;
+                if (f != 0xffu) w |= (((uint32_t)row[f] << 2) | 3u) << (8 * i);
+            }
+        }
         a.Fg[(int64_t)q * a.fg_stride + c0 + j] = w;
     }
 }
@@ -705,19 +736,20 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
 // ---------------------------------------------------------------------------
 // Tree kernel.  A workgroup holds the pointer form of its trees in LDS and
 // walks them for every chain.  Each wave owns a feature tile of 64 chains in
-// a slot of SLOT bytes at wave * SLOT: byte (f & 3) of dword (f >> 2) * 64 +
-// lane holds 4x+3 for feature value x, so lanes read distinct banks whatever
-// features they ask for, and the tile byte address of feature f is
-// (node & mask) | (wave * SLOT + 4 * lane) for a node of that feature,
-// mask = 3 | (SLOT - 1) & ~0xff.
+// a slot of SLOT bytes (a power of two) at wave * SLOT: byte (p & 3) of
+// dword (p >> 2) * 64 + lane holds 4x+3 for the value x of the feature at
+// tile position p, so lanes read distinct banks whatever features they ask
+// for, and the tile byte address of position p is (node & mask) | (wave *
+// SLOT + 4 * lane) for a node of that feature, mask = 3 | (SLOT - 1) & ~0xff.
+// A tile holds the space's varying loop-context features only: a node on a
+// feature that is constant over the space was settled when the trees were
+// relocated (both children made the one it reaches).
 // With 4x+3 in the tile, x >= thr is (4x+3) >= (low byte of the node) for
 // x, thr <= 63.  Tiles are private to their wave, so the walk loop needs no
 // barrier; tree blocks go into the gaps after the tiles.
 // ---------------------------------------------------------------------------
 constexpr int TREES_MAX = 16;          // trees per workgroup
 constexpr int TREE_WAVES_MAX = 16;
-// the last 16 bytes of the tree kernel's LDS hold its block counter
-constexpr uint32_t TREE_LDS_FREE = (uint32_t)MAX_LDS_BYTES - 16u;
 
 struct TreeArgs {
     const uint32_t* words32;   // pointer form relocated for toff (k_reloc)
@@ -729,6 +761,9 @@ struct TreeArgs {
     float* V;
     int slices;                // chain slices per tree group
     int slice_blocks;          // 64-chain blocks per slice
+    int q;                     // quads (4 features) per chain in a tile
+    uint32_t slot;             // bytes per wave's tile slot
+    uint32_t counter;          // LDS byte offset of the block counter
     uint32_t mask;             // node bits of a tile address: 3 | (slot - 1) & ~0xff
     // LDS dword offsets of tree i's node block (low half) and leaf block (high half)
     uint32_t toff[TREES_MAX];
@@ -1005,10 +1040,12 @@ __device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const T
 // cs = b % slices.  Wave w starts with block w of the slice and then takes
 // the next unclaimed block from a counter in LDS, so waves that share a
 // SIMD with fewer others take more blocks.
-template <int DEPTH, int Q, int SLOT_LOG2>
+// QT: the tile's quads when known at compile time (the whole-feature tiles),
+// else 0 (a.q).
+template <int DEPTH, int QT>
 __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
-    constexpr uint32_t SLOT = 1u << SLOT_LOG2;
     constexpr int G = 8;
+    const int tq = QT ? QT : a.q;
     __shared__ uint32_t lds[MAX_LDS_BYTES / 4];
     const uint8_t* L = reinterpret_cast<const uint8_t*>(lds);
     const int tid = threadIdx.x;
@@ -1017,22 +1054,25 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     const int nt = (a.n_trees - t0 < a.tpw) ? (a.n_trees - t0) : a.tpw;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int nw = (int)(blockDim.x >> 6);
-    uint32_t* counter = lds + TREE_LDS_FREE / 4;
+    uint32_t* counter = lds + a.counter / 4;
     const int64_t n = a.n;
     const int64_t blocks = (n + 63) >> 6;
     const int64_t b_end0 = (int64_t)(cs + 1) * a.slice_blocks;
     const int64_t b_end = b_end0 < blocks ? b_end0 : blocks;
-    uint32_t* tile = lds + wave * (SLOT / 4);
-    const uint32_t fb = (uint32_t)wave * SLOT + (uint32_t)lane * 4u;
+    uint32_t* tile = lds + wave * (a.slot / 4);
+    const uint32_t fb = (uint32_t)wave * a.slot + (uint32_t)lane * 4u;
     // tile fill straight from global memory into LDS: instruction k moves
     // quads 4k..4k+3, lane i the 16 bytes of chains 4(i & 15) .. +3 of quad
     // 4k + i/16, which land on tile dwords 256k + 4i .. +3 = quad * 64 + chain
+    // (in a last, partial group the lanes past the last quad stay idle)
     const uint32_t* fsrc = a.Fg + (int64_t)(lane >> 4) * a.fg_stride + 4 * (lane & 15);
-    static_assert(Q % 4 == 0, "whole quad groups");
+    const int full = tq >> 2;
+    const bool part = (lane >> 4) < (tq & 3);
     auto fill = [&](int64_t blk) {
-#pragma unroll
-        for (int k = 0; k < Q / 4; ++k)
-            __builtin_amdgcn_global_load_lds(fsrc + (int64_t)(4 * k) * a.fg_stride + blk * 64, tile + 256 * k, 16, 0, 0);
+        const uint32_t* src = fsrc + blk * 64;
+        int k = 0;
+        for (; k < full; ++k) __builtin_amdgcn_global_load_lds(src + (int64_t)(4 * k) * a.fg_stride, tile + 256 * k, 16, 0, 0);
+        if (part) __builtin_amdgcn_global_load_lds(src + (int64_t)(4 * k) * a.fg_stride, tile + 256 * k, 16, 0, 0);
     };
     const int64_t b_first = (int64_t)cs * a.slice_blocks;
     const int64_t nblk = b_end - b_first;
@@ -1120,39 +1160,69 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     }
 }
 
-// The pointer form relocated for one LDS plan: every node-block word of tree
-// t gets, in its high half, the LDS word address of the block its children's
-// slot lies in (local tree t % tpw; the leaf block for slots p >= NB / 2,
-// whose nodes are on the last internal level, and for the root when DEPTH is
-// 1); leaf words are copied.  Runs once per annealing run, so that the tree
-// kernel copies its trees into LDS unchanged.
+// The pointer form relocated for one LDS plan and tile layout.  Word j of a
+// tree holds heap node j (the root, node 1, is word 0; word 1 is unused;
+// leaves are words 2^DEPTH and up), so node j's parent is node j / 2.
+//  - Settling: when a node's feature is constant over the space (fmap
+//    entry 0x100 | value), the child it reaches is known, and both of its
+//    children become that child (the slot's other word takes a copy of it),
+//    so the walk reaches the same leaf whatever the tile holds there.
+//  - Every node word gets its feature's tile position (position 0 for a
+//    settled node, whose byte is read but decides nothing) and, in its high
+//    half, the LDS word address of the block its children's slot lies in
+//    (local tree t % tpw; the leaf block for slots p >= NB / 2, whose nodes
+//    are on the last internal level, and for the root when DEPTH is 1).
+// fmap null: identity tile layout, nothing settled.  Runs once per
+// annealing run, so that the tree kernel copies its trees into LDS
+// unchanged.
 __global__ void k_reloc(const uint32_t* __restrict__ src, uint32_t* __restrict__ dst, int64_t words, int depth,
-                        TreeArgs a) {
+                        const uint16_t* __restrict__ fmap, TreeArgs a) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= words) return;
     const uint32_t nb = 1u << (depth - 1);
     const int64_t t = i >> (depth + 1);
     const uint32_t j = (uint32_t)(i & ((2 << depth) - 1));
-    uint32_t v = src[i];
+    const uint32_t* tw = src + (t << (depth + 1));
+    auto feature_of = [](uint32_t c) { return (c & 3u) | ((c >> 8) << 2); };   // compact node c
+    uint32_t js = j;
+    if (fmap && j >= 2u) {
+        const uint32_t p = j >> 1;
+        const uint32_t pc = tw[p == 1u ? 0u : p] & 0xffffu;
+        const uint32_t m = fmap[feature_of(pc)];
+        if (m & 0x100u) js = (j & ~1u) | ((m & 0xffu) >= ((pc >> 2) & 0x3fu) ? 1u : 0u);
+    }
+    uint32_t v = tw[js];
     if (j < 2u * nb) {
+        if (fmap) {
+            const uint32_t c = v & 0xffffu;
+            const uint32_t m = fmap[feature_of(c)];
+            const uint32_t pos = (m & 0x100u) ? 0u : m;
+            v = (v & 0xffff00fcu) | (pos & 3u) | ((pos >> 2) << 8);
+        }
         const uint32_t o = a.toff[t % a.tpw];
         v += ((j >> 1) >= nb / 2u ? (o >> 16) : (o & 0xffffu)) << 16;
     }
     dst[i] = v;
 }
 
-// LDS plan of a tree workgroup: nw feature tiles, one per SLOT, and the
-// node and leaf blocks of tpw trees placed first-fit (largest first) in the
-// space the tiles leave free.  Returns false when they do not fit.
-bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TREES_MAX]) {
+// LDS plan of a tree workgroup: nw feature tiles of Q quads, one per slot,
+// the block counter (16 bytes: at the end of the LDS, or with in_slot in the
+// first slot's spare bytes), and the node and leaf blocks of tpw trees placed
+// first-fit (largest first) in the space left free.  Returns false when they
+// do not fit.
+bool plan_trees(int depth, int Q, uint32_t slot, int nw, int tpw, bool in_slot, uint32_t (&toff)[TREES_MAX],
+                uint32_t& counter) {
     const uint32_t tile = (uint32_t)Q * 256u;
+    if (in_slot && (nw < 2 || slot - tile < 16u)) return false;
+    counter = in_slot ? slot - 16u : (uint32_t)MAX_LDS_BYTES - 16u;
+    const uint32_t end = in_slot ? (uint32_t)MAX_LDS_BYTES : (uint32_t)MAX_LDS_BYTES - 16u;
     struct Gap { uint32_t lo, hi; };
     Gap gaps[TREE_WAVES_MAX];
     int ng = 0;
     for (int w = 0; w < nw; ++w) {
         const uint32_t lo = (uint32_t)w * slot + tile;
-        const uint32_t hi = (w + 1 < nw) ? (uint32_t)(w + 1) * slot : TREE_LDS_FREE;
-        if (lo > TREE_LDS_FREE) return false;
+        const uint32_t hi = (w + 1 < nw) ? (w == 0 && in_slot ? counter : (uint32_t)(w + 1) * slot) : end;
+        if (lo > end) return false;
         gaps[ng++] = Gap{lo, hi};
     }
     // node and leaf blocks: 2^(depth-1) slots of 8 bytes each
@@ -1172,11 +1242,21 @@ bool plan_trees(int depth, int Q, int slot, int nw, int tpw, uint32_t (&toff)[TR
         if (!place(lbytes, loff[t])) return false;
     for (int t = 0; t < tpw; ++t)
         if (!place(nbytes, noff[t])) return false;
+    // every block clear of the tiles and the counter
+    auto clear = [&](uint32_t off, uint32_t bytes) {
+        if (off + bytes > (uint32_t)MAX_LDS_BYTES) return false;
+        if (off < counter + 16u && counter < off + bytes) return false;
+        for (int w = 0; w < nw; ++w)
+            if (off < (uint32_t)w * slot + tile && (uint32_t)w * slot < off + bytes) return false;
+        return true;
+    };
+    for (int t = 0; t < tpw; ++t)
+        if (!clear(loff[t], lbytes) || !clear(noff[t], nbytes)) return false;
     for (int t = 0; t < tpw; ++t) toff[t] = (noff[t] / 4u) | ((loff[t] / 4u) << 16);
     return true;
 }
 
-template <int DEPTH, int Q, int SLOT_LOG2>
+template <int DEPTH, int QT>
 hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     const int grid = (a.n_trees + a.tpw - 1) / a.tpw * a.slices;
     static bool checked = false;
@@ -1184,54 +1264,54 @@ hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEven
         // the walk's asm takes offsets into the kernel's LDS array as LDS
         // addresses: the array must be the kernel's only LDS object
         hipFuncAttributes fa;
-        hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(&k_trees<DEPTH, Q, SLOT_LOG2>));
+        hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(&k_trees<DEPTH, QT>));
         if (e != hipSuccess) return e;
         if (fa.sharedSizeBytes != MAX_LDS_BYTES) return hipErrorInvalidKernelFile;
         checked = true;
     }
     if (start)
-        hipExtLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, start, stop, 0, a);
+        hipExtLaunchKernelGGL((k_trees<DEPTH, QT>), dim3(grid), dim3(nw * 64), 0, stream, start, stop, 0, a);
     else
-        hipLaunchKernelGGL((k_trees<DEPTH, Q, SLOT_LOG2>), dim3(grid), dim3(nw * 64), 0, stream, a);
+        hipLaunchKernelGGL((k_trees<DEPTH, QT>), dim3(grid), dim3(nw * 64), 0, stream, a);
     return hipGetLastError();
 }
 
-template <int Q, int SLOT_LOG2>
+template <int QT>
 hipError_t launch_trees_q(const TreeArgs& a, int depth, int nw, hipStream_t stream, hipEvent_t start,
                           hipEvent_t stop) {
     switch (depth) {
-        case 1: return launch_trees_t<1, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 2: return launch_trees_t<2, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 3: return launch_trees_t<3, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 4: return launch_trees_t<4, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 5: return launch_trees_t<5, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 6: return launch_trees_t<6, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 7: return launch_trees_t<7, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 8: return launch_trees_t<8, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 9: return launch_trees_t<9, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 10: return launch_trees_t<10, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 11: return launch_trees_t<11, Q, SLOT_LOG2>(a, nw, stream, start, stop);
-        case 12: return launch_trees_t<12, Q, SLOT_LOG2>(a, nw, stream, start, stop);
+        case 1: return launch_trees_t<1, QT>(a, nw, stream, start, stop);
+        case 2: return launch_trees_t<2, QT>(a, nw, stream, start, stop);
+        case 3: return launch_trees_t<3, QT>(a, nw, stream, start, stop);
+        case 4: return launch_trees_t<4, QT>(a, nw, stream, start, stop);
+        case 5: return launch_trees_t<5, QT>(a, nw, stream, start, stop);
+        case 6: return launch_trees_t<6, QT>(a, nw, stream, start, stop);
+        case 7: return launch_trees_t<7, QT>(a, nw, stream, start, stop);
+        case 8: return launch_trees_t<8, QT>(a, nw, stream, start, stop);
+        case 9: return launch_trees_t<9, QT>(a, nw, stream, start, stop);
+        case 10: return launch_trees_t<10, QT>(a, nw, stream, start, stop);
+        case 11: return launch_trees_t<11, QT>(a, nw, stream, start, stop);
+        case 12: return launch_trees_t<12, QT>(a, nw, stream, start, stop);
         default: return hipErrorInvalidValue;
     }
 }
 
-// Tile slot sizes: the smallest power of two holding Q * 256 bytes.  The
-// relation-feature tile (Eq. 4 runs, 192 features) has REL_Q quads.
-constexpr int GEMM_Q = 28, CONV_Q = 44;
-constexpr int GEMM_SLOT_LOG2 = 13, CONV_SLOT_LOG2 = 14, REL_SLOT_LOG2 = 14;
-static_assert((GEMM_Q * 256) <= (1 << GEMM_SLOT_LOG2) && (GEMM_Q * 256) > (1 << (GEMM_SLOT_LOG2 - 1)), "slot");
-static_assert((CONV_Q * 256) <= (1 << CONV_SLOT_LOG2) && (CONV_Q * 256) > (1 << (CONV_SLOT_LOG2 - 1)), "slot");
-static_assert((REL_Q * 256) <= (1 << REL_SLOT_LOG2) && (REL_Q * 256) > (1 << (REL_SLOT_LOG2 - 1)), "slot");
+// Whole-feature tiles (GEMM and conv2d loop-context rows, relation rows)
+// have their quad count compiled in; compact tiles take it at run time.
+hipError_t launch_trees(const TreeArgs& a, int depth, int nw, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+    switch (a.q) {
+        case 28: return launch_trees_q<28>(a, depth, nw, stream, start, stop);
+        case 44: return launch_trees_q<44>(a, depth, nw, stream, start, stop);
+        case REL_Q: return launch_trees_q<REL_Q>(a, depth, nw, stream, start, stop);
+        default: return launch_trees_q<0>(a, depth, nw, stream, start, stop);
+    }
+}
 
-int slot_log2_of(int Q) { return Q == GEMM_Q ? GEMM_SLOT_LOG2 : Q == CONV_Q ? CONV_SLOT_LOG2 : REL_SLOT_LOG2; }
-
-hipError_t launch_trees(const TreeArgs& a, int Q, int depth, int nw, hipStream_t stream, hipEvent_t start,
-                        hipEvent_t stop) {
-    if (Q == GEMM_Q) return launch_trees_q<GEMM_Q, GEMM_SLOT_LOG2>(a, depth, nw, stream, start, stop);
-    if (Q == CONV_Q) return launch_trees_q<CONV_Q, CONV_SLOT_LOG2>(a, depth, nw, stream, start, stop);
-    if (Q == REL_Q) return launch_trees_q<REL_Q, REL_SLOT_LOG2>(a, depth, nw, stream, start, stop);
-    return hipErrorInvalidValue;
+// Tile slot of Q quads: the smallest power of two holding Q * 256 bytes.
+uint32_t slot_bytes(int Q) {
+    uint32_t s = 256u;
+    while (s < (uint32_t)Q * 256u) s <<= 1;
+    return s;
 }
 
 // Launch plan of the tree kernel for an ensemble walked over Q-quad tiles of
@@ -1240,7 +1320,7 @@ hipError_t launch_trees(const TreeArgs& a, int Q, int depth, int nw, hipStream_t
 // times the share of compute units its grid fills.  Fills ta's plan fields
 // and nw; false when nothing fits.
 bool plan_tree_launch(int n_trees, int depth, int Q, int64_t n, int n_cu, TreeArgs& ta, int& nw) {
-    const int slot = 1 << slot_log2_of(Q);
+    const uint32_t slot = slot_bytes(Q);
     const int64_t blocks = (n + 63) / 64;
     double best_score = -1.0;
     nw = 0;
@@ -1252,9 +1332,13 @@ bool plan_tree_launch(int n_trees, int depth, int Q, int64_t n, int n_cu, TreeAr
         const int64_t sb = (blocks + slices - 1) / slices;
         slices = (blocks + sb - 1) / sb;
         const int cap = sb < TREE_WAVES_MAX ? (int)sb : TREE_WAVES_MAX;
-        uint32_t toff[TREES_MAX];
+        uint32_t toff[TREES_MAX], counter = 0;
         for (int w = cap; w >= 1; --w) {
-            if (!plan_trees(depth, Q, slot, w, tpw, toff)) continue;
+            // the counter at the end of the LDS, or in a tile slot's spare
+            // bytes when only that leaves room
+            if (!plan_trees(depth, Q, slot, w, tpw, false, toff, counter) &&
+                !plan_trees(depth, Q, slot, w, tpw, true, toff, counter))
+                continue;
             const double grid = (double)tg * (double)slices;
             const double score = (double)w * (tpw < 8 ? tpw : 8) * (grid < n_cu ? grid / n_cu : 1.0);
             if (score > best_score) {
@@ -1263,13 +1347,16 @@ bool plan_tree_launch(int n_trees, int depth, int Q, int64_t n, int n_cu, TreeAr
                 ta.tpw = tpw;
                 ta.slices = (int)slices;
                 ta.slice_blocks = (int)sb;
+                ta.counter = counter;
                 for (int i = 0; i < TREES_MAX; ++i) ta.toff[i] = toff[i];
             }
             break;
         }
     }
     if (nw == 0) return false;
-    ta.mask = (((uint32_t)slot - 1u) & ~0xffu) | 3u;
+    ta.q = Q;
+    ta.slot = slot;
+    ta.mask = ((slot - 1u) & ~0xffu) | 3u;
     return true;
 }
 
@@ -1316,13 +1403,14 @@ hipError_t next_events(at_chains_s& ch, int kind, hipEvent_t& start, hipEvent_t&
 struct TreeLaunch {
     TreeArgs ta{};
     int nw = 0;
-    int Q = 0;
     int depth = 0;
 };
 
-static hipError_t prepare_trees(const EnsembleDesc& e, int Q, int64_t n, int n_cu, DeviceBuf& relocated,
-                         const uint32_t* Fg, int64_t fg_stride, float* V, hipStream_t stream, TreeLaunch& tl) {
-    tl.Q = Q;
+// Q: quads per chain in a tile; fmap: the space's tile layout (null for
+// the relation features, which are tiled whole).
+static hipError_t prepare_trees(const EnsembleDesc& e, int Q, const uint16_t* fmap, int64_t n, int n_cu,
+                                DeviceBuf& relocated, const uint32_t* Fg, int64_t fg_stride, float* V,
+                                hipStream_t stream, TreeLaunch& tl) {
     tl.depth = e.depth;
     TreeArgs& ta = tl.ta;
     ta.words32 = e.words32;
@@ -1336,7 +1424,7 @@ static hipError_t prepare_trees(const EnsembleDesc& e, int Q, int64_t n, int n_c
     hipError_t err = ensure(relocated, (size_t)words * 4);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(k_reloc, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream, e.words32,
-                       static_cast<uint32_t*>(relocated.p), words, e.depth, ta);
+                       static_cast<uint32_t*>(relocated.p), words, e.depth, fmap, ta);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     ta.words32 = static_cast<const uint32_t*>(relocated.p);
     return hipSuccess;
@@ -1385,6 +1473,9 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
     ca.steps = steps;
     ca.thr = thr;
     ca.trace = trace;
+    ca.fsrc = static_cast<const uint8_t*>(sp.d_fsrc.p);
+    ca.fq = sp.tile_q;
+    ca.fident = sp.tile_q == Q ? 1 : 0;
     if (eg) {
         ca.Vg = static_cast<const float*>(ch.d_vg.p);
         ca.Tg = eg->n_trees;
@@ -1396,11 +1487,11 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
     // the local (or only) model over the loop features, then the global model
     // over the relation features
     TreeLaunch tl, tg;
-    if ((err = prepare_trees(e, Q, n, n_cu, ch.d_tw, ca.Fg, fg_stride, static_cast<float*>(ch.d_v.p), stream,
-                             tl)) != hipSuccess)
+    if ((err = prepare_trees(e, sp.tile_q, static_cast<const uint16_t*>(sp.d_fmap.p), n, n_cu, ch.d_tw, ca.Fg,
+                             fg_stride, static_cast<float*>(ch.d_v.p), stream, tl)) != hipSuccess)
         return err;
-    if (eg && (err = prepare_trees(*eg, REL_Q, n, n_cu, ch.d_twg, ca.Fr, fg_stride, static_cast<float*>(ch.d_vg.p),
-                                   stream, tg)) != hipSuccess)
+    if (eg && (err = prepare_trees(*eg, REL_Q, nullptr, n, n_cu, ch.d_twg, ca.Fr, fg_stride,
+                                   static_cast<float*>(ch.d_vg.p), stream, tg)) != hipSuccess)
         return err;
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
@@ -1409,7 +1500,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
         const TreeArgs& ta = tl.ta;
         const int64_t tree_grid = (int64_t)(e.n_trees + ta.tpw - 1) / ta.tpw * ta.slices;
         const int64_t plan[8] = {ta.tpw, tl.nw, tree_grid, ta.slices, ta.slice_blocks, (int64_t)chain_grid,
-                                 (int64_t)MAX_LDS_BYTES, (int64_t)groups * n16 * 16};
+                                 (int64_t)ta.q, (int64_t)groups * n16 * 16};
         for (int i = 0; i < 8; ++i) ch.last_plan[i] = plan[i];
     }
     static bool chain_configured = false;
@@ -1452,7 +1543,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
             hipEvent_t start, stop;
             hipError_t ev = next_events(ch, 0, start, stop);
             if (ev != hipSuccess) return ev;
-            if ((ev = launch_trees(t->ta, t->Q, t->depth, t->nw, stream, start, stop)) != hipSuccess) return ev;
+            if ((ev = launch_trees(t->ta, t->depth, t->nw, stream, start, stop)) != hipSuccess) return ev;
         }
         return hipSuccess;
     };
