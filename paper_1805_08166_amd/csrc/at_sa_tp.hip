@@ -1076,7 +1076,7 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     };
     const int64_t b_first = (int64_t)cs * a.slice_blocks;
     const int64_t nblk = b_end - b_first;
-    int64_t r = wave, nr = nblk;
+    int64_t r = wave;
     // the first block's tile is in flight while the trees are copied
     if (r < nblk) fill(b_first + r);
     // Trees, already relocated for this LDS plan (a.words32 holds per tree
@@ -1127,15 +1127,16 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
         if (lane == 0) r = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         return r;
     };
-    // r: the block walked now; nr: the next one, claimed a block ahead so
-    // that the claim's answer is never waited for
-    if (r < nblk) nr = (int64_t)__builtin_amdgcn_readfirstlane(claim_next());
+    // r: the block walked now.  At the start of each block the wave claims
+    // the one it walks next; the claim's answer arrives during the walk, so
+    // it is never waited for, and no wave holds a block it has not started
+    // while others run out of work.
     bool first = true;
     while (r < nblk) {
         // every earlier read of this wave's tile has returned before the
         // tile is overwritten (s_waitcnt lgkmcnt(0))
         if (!first) __builtin_amdgcn_s_waitcnt(0xc07f);
-        const uint32_t claim = nr < nblk ? claim_next() : 0u;
+        const uint32_t claim = claim_next();
         const int64_t b = b_first + r;
         if (!first) {
             fill(b);
@@ -1155,8 +1156,7 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
         }
         for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
         walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
-        r = nr;
-        if (r < nblk) nr = (int64_t)__builtin_amdgcn_readfirstlane(claim);
+        r = (int64_t)__builtin_amdgcn_readfirstlane(claim);
     }
 }
 

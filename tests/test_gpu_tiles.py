@@ -126,3 +126,22 @@ def test_c12_tile_and_plan(P):
     say(f"C12 plan {plan}")
     assert plan["path"] == P.AT_SA_PATH_TREES
     assert plan["tile_quads"] == 31 and plan["trees_per_wg"] == 8 and plan["waves"] == 12
+
+
+def test_space_past_the_scan_limit_keeps_whole_tiles(P):
+    # the annotated C2 space holds 361,267,200 configurations, more than the
+    # 2^28 a space creation scans: its tiles keep all 44 quads
+    shape = W.conv_shape("C2")
+    osp = oracle.Space(CONV_VT, shape)
+    assert osp.n_configs > 1 << 28
+    sp = P.at_space_create(CONV_VT, shape)
+    fid, thr, leaf = W.make_ensemble(60, 6, 176, 62)
+    ens = P.at_ensemble_create(fid, thr, leaf, 176)
+    n, steps, seed, k = 128, 12, 23, 4
+    ch = mk_chains(P, sp, 0, n, k, seed, "trees")
+    best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
+    plan = P.at_chains_last_plan(ch)
+    assert plan["path"] == P.AT_SA_PATH_TREES and plan["tile_quads"] == 44
+    och = oracle.Chains([osp], [0, n], seed=seed, chain0=0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
