@@ -197,8 +197,9 @@ __device__ __forceinline__ void fold_pass(float& s, uint32_t ad) {
 // direct-to-LDS loads of the calling wave into ring buffer p % FOLD_R, so
 // that entry g * CPW + j holds group g of chain c0 + j.  Past the last
 // group the loads repeat the last float4 (never folded).
-__device__ __forceinline__ void ring_issue(const float4* __restrict__ blk, int last, float4* ring, int p, int lane) {
-    float4* buf = ring + (p % FOLD_R) * (FOLD_P * CPW);
+__device__ __forceinline__ void ring_issue_buf(const float4* __restrict__ blk, int last, float4* ring, int p, int b,
+                                               int lane) {
+    float4* buf = ring + b * (FOLD_P * CPW);
 #pragma unroll
     for (int i = 0; i < FOLD_P * CPW / 64; ++i) {
         int idx = p * (FOLD_P * CPW) + i * 64 + lane;
@@ -206,6 +207,10 @@ __device__ __forceinline__ void ring_issue(const float4* __restrict__ blk, int l
         // non-temporal (cache policy 2): V is read once
         __builtin_amdgcn_global_load_lds(blk + idx, buf + i * 64, 16, 0, 2);
     }
+}
+
+__device__ __forceinline__ void ring_issue(const float4* __restrict__ blk, int last, float4* ring, int p, int lane) {
+    ring_issue_buf(blk, last, ring, p, p % FOLD_R, lane);
 }
 
 // Wait until at most `later` passes of this wave's ring moves are
@@ -224,6 +229,108 @@ __device__ __forceinline__ void ring_wait(int later) {
     }
 }
 #undef AT_VM_WAIT
+
+// Groups (of four trees) in pass p of a model with `groups` groups.
+__device__ __forceinline__ int pass_groups(int groups, int p) {
+    return groups - p * FOLD_P < FOLD_P ? groups - p * FOLD_P : FOLD_P;
+}
+
+// One pass from the ring at src (the lane's column): ng groups, the last of
+// them holding r trees when r > 0, added in tree order.
+__device__ __forceinline__ void fold_pass_any(float& s, const float4* src, int ng, int r) {
+    const int full = r ? ng - 1 : ng;
+    int g = 0;
+    if (full == FOLD_P) {
+        fold_pass(s, lds_byte_address(src));
+        g = FOLD_P;
+    }
+    for (; g + FOLD_B <= full; g += FOLD_B) {
+        float4 A[FOLD_B];
+        fold_load(A, src + g * CPW);
+        fold_add(s, A);
+    }
+    for (; g < full; ++g) {
+        const float4 q = src[g * CPW];
+        s = s + q.x;
+        s = s + q.y;
+        s = s + q.z;
+        s = s + q.w;
+    }
+    if (r) {
+        const float4 q = src[full * CPW];
+        s = s + q.x;
+        if (r > 1) s = s + q.y;
+        if (r > 2) s = s + q.z;
+    }
+}
+
+// A full pass of each of two models (their ring buffers at LDS byte
+// addresses ag and al), in batches of four groups of each, two register
+// sets deep; the adds of the two sums alternate, so that each dependent add
+// has the other sum's add beside it.
+template <int OFF>
+__device__ __forceinline__ void fold_issue_pair(fold_v4 (&R)[FOLD_B], uint32_t ag, uint32_t al) {
+#define AT_FOLD_READ2(G, AD, O) \
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(R[G]) : "v"(AD), "i"(OFF + (O) * CPW * 16))
+    AT_FOLD_READ2(0, ag, 0);
+    AT_FOLD_READ2(1, ag, 1);
+    AT_FOLD_READ2(2, ag, 2);
+    AT_FOLD_READ2(3, ag, 3);
+    AT_FOLD_READ2(4, al, 0);
+    AT_FOLD_READ2(5, al, 1);
+    AT_FOLD_READ2(6, al, 2);
+    AT_FOLD_READ2(7, al, 3);
+#undef AT_FOLD_READ2
+}
+
+__device__ __forceinline__ void fold_add_pair(float& sg, float& sl, const fold_v4 (&R)[FOLD_B]) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        sg = sg + R[g].x;
+        sl = sl + R[4 + g].x;
+        sg = sg + R[g].y;
+        sl = sl + R[4 + g].y;
+        sg = sg + R[g].z;
+        sl = sl + R[4 + g].z;
+        sg = sg + R[g].w;
+        sl = sl + R[4 + g].w;
+    }
+}
+
+#define AT_FOLD_WAIT2(N, R)                                                                                 \
+    asm volatile("s_waitcnt lgkmcnt(" #N ")"                                                                \
+                 : "+v"(R[0]), "+v"(R[1]), "+v"(R[2]), "+v"(R[3]), "+v"(R[4]), "+v"(R[5]), "+v"(R[6]), "+v"(R[7]))
+
+__device__ __forceinline__ void fold_pass2(float& sg, uint32_t ag, float& sl, uint32_t al) {
+    constexpr int BB = 4 * CPW * 16;   // bytes between batches of four groups
+    static_assert(FOLD_P == 8 * 4, "a pass is eight batches of four groups");
+    fold_v4 A[FOLD_B], B[FOLD_B];
+    fold_issue_pair<0>(A, ag, al);
+    fold_issue_pair<BB>(B, ag, al);
+    AT_FOLD_WAIT2(8, A);
+    fold_add_pair(sg, sl, A);
+    fold_issue_pair<2 * BB>(A, ag, al);
+    AT_FOLD_WAIT2(8, B);
+    fold_add_pair(sg, sl, B);
+    fold_issue_pair<3 * BB>(B, ag, al);
+    AT_FOLD_WAIT2(8, A);
+    fold_add_pair(sg, sl, A);
+    fold_issue_pair<4 * BB>(A, ag, al);
+    AT_FOLD_WAIT2(8, B);
+    fold_add_pair(sg, sl, B);
+    fold_issue_pair<5 * BB>(B, ag, al);
+    AT_FOLD_WAIT2(8, A);
+    fold_add_pair(sg, sl, A);
+    fold_issue_pair<6 * BB>(A, ag, al);
+    AT_FOLD_WAIT2(8, B);
+    fold_add_pair(sg, sl, B);
+    fold_issue_pair<7 * BB>(B, ag, al);
+    AT_FOLD_WAIT2(8, A);
+    fold_add_pair(sg, sl, A);
+    AT_FOLD_WAIT2(0, B);
+    fold_add_pair(sg, sl, B);
+}
+#undef AT_FOLD_WAIT2
 
 // Score of the pending candidates of chain block c0 from one model's leaf
 // values V (T trees): lane j < nc of the calling wave adds its chain's
@@ -248,35 +355,72 @@ __device__ __forceinline__ float fold_wave(const float* __restrict__ V, int T, i
         ring_wait(issued - 1 - p);
         if (lane < nc) {
             const float4* src = ring + (p % FOLD_R) * (FOLD_P * CPW) + lane;
-            const int ng = groups - p * FOLD_P < FOLD_P ? groups - p * FOLD_P : FOLD_P;
-            const int r = (p == npass - 1) ? (T & 3) : 0;   // trees in a last, partial group
-            const int full = r ? ng - 1 : ng;
-            int g = 0;
-            if (full == FOLD_P) {
-                fold_pass(s, lds_byte_address(src));
-                g = FOLD_P;
-            }
-            for (; g + FOLD_B <= full; g += FOLD_B) {
-                float4 A[FOLD_B];
-                fold_load(A, src + g * CPW);
-                fold_add(s, A);
-            }
-            for (; g < full; ++g) {
-                const float4 q = src[g * CPW];
-                s = s + q.x;
-                s = s + q.y;
-                s = s + q.z;
-                s = s + q.w;
-            }
-            if (r) {
-                const float4 q = src[full * CPW];
-                s = s + q.x;
-                if (r > 1) s = s + q.y;
-                if (r > 2) s = s + q.z;
-            }
+            fold_pass_any(s, src, pass_groups(groups, p), (p == npass - 1) ? (T & 3) : 0);
         }
     }
     return s;
+}
+
+// Eq. 4: both models' scores, each its own fold in tree order from +0.0f.
+// The two leaf-value arrays go through the one ring pass by pass in turn
+// (pass m / 2 of the global model, then of the local one, while both have
+// passes; then the longer one's last passes), and a pair of full passes is
+// added with the two chains of dependent adds interleaved.
+__device__ __forceinline__ void fold_wave2(const float* __restrict__ Vg, int Tg, const float* __restrict__ Vl, int Tl,
+                                           int64_t c0, int nc, float4* ring, int lane, float& sg, float& sl) {
+    const int gg = (Tg + 3) >> 2, gl = (Tl + 3) >> 2;
+    const int npg = (gg + FOLD_P - 1) / FOLD_P, npl = (gl + FOLD_P - 1) / FOLD_P;
+    const float4* bg = reinterpret_cast<const float4*>(Vg) + (c0 >> 4) * (int64_t)gg * CPW;
+    const float4* bl = reinterpret_cast<const float4*>(Vl) + (c0 >> 4) * (int64_t)gl * CPW;
+    const int pmin = npg < npl ? npg : npl, total = npg + npl;
+    auto pass_of = [&](int m, bool& glob) -> int {
+        if (m < 2 * pmin) {
+            glob = (m & 1) == 0;
+            return m >> 1;
+        }
+        glob = npg > npl;
+        return m - pmin;
+    };
+    auto issue = [&](int m) {
+        bool glob;
+        const int p = pass_of(m, glob);
+        ring_issue_buf(glob ? bg : bl, (glob ? gg : gl) * CPW - 1, ring, p, m % FOLD_R, lane);
+    };
+    int issued = 0;
+    for (; issued < FOLD_R - 1 && issued < total; ++issued) issue(issued);
+    sg = 0.0f;
+    sl = 0.0f;
+    for (int m = 0; m < total;) {
+        const bool pair = m < 2 * pmin;
+        const int use = pair ? 2 : 1;
+        // a pass's buffer is free once the pass six before it was added
+        for (; issued < total && issued < m + FOLD_R; ++issued) issue(issued);
+        ring_wait(issued - m - use);
+        if (lane < nc) {
+            if (pair) {
+                const int p = m >> 1;
+                const float4* srcg = ring + (m % FOLD_R) * (FOLD_P * CPW) + lane;
+                const float4* srcl = ring + ((m + 1) % FOLD_R) * (FOLD_P * CPW) + lane;
+                const int ngg = pass_groups(gg, p), ngl = pass_groups(gl, p);
+                const int rg = (p == npg - 1) ? (Tg & 3) : 0, rl = (p == npl - 1) ? (Tl & 3) : 0;
+                if (ngg == FOLD_P && ngl == FOLD_P && rg == 0 && rl == 0) {
+                    fold_pass2(sg, lds_byte_address(srcg), sl, lds_byte_address(srcl));
+                } else {
+                    fold_pass_any(sg, srcg, ngg, rg);
+                    fold_pass_any(sl, srcl, ngl, rl);
+                }
+            } else {
+                bool glob;
+                const int p = pass_of(m, glob);
+                const float4* src = ring + (m % FOLD_R) * (FOLD_P * CPW) + lane;
+                if (glob)
+                    fold_pass_any(sg, src, pass_groups(gg, p), (p == npg - 1) ? (Tg & 3) : 0);
+                else
+                    fold_pass_any(sl, src, pass_groups(gl, p), (p == npl - 1) ? (Tl & 3) : 0);
+            }
+        }
+        m += use;
+    }
 }
 
 // The first configuration of a chain: each knob uniform over its values,
@@ -476,8 +620,8 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
             // Eq. 4: each model's prediction is its own fold from +0.0f; the
             // sum adds the global one first
             if (a.Vg) {
-                const float sg = fold_wave(a.Vg, a.Tg, c0, nc, ring, lane);
-                const float sl = fold_wave(a.V, a.T, c0, nc, ring, lane);
+                float sg, sl;
+                fold_wave2(a.Vg, a.Tg, a.V, a.T, c0, nc, ring, lane, sg, sl);
                 s = sg + sl;
             } else {
                 s = fold_wave(a.V, a.T, c0, nc, ring, lane);
