@@ -22,15 +22,17 @@ from test_gpu_parity import DEV, P, assert_same_run, export, gpu_sa, say  # noqa
 pytestmark = pytest.mark.gpu
 
 
-def oracle_slice(wl_spaces, offsets, ens_t, seed, topk, steps, lo, hi):
-    """Oracle run of global chains [lo, hi) of a (possibly ragged) space set."""
+def oracle_slice(wl_spaces, offsets, ens_t, seed, topk, steps, lo, hi, global_model=None):
+    """Oracle run of global chains [lo, hi) of a (possibly ragged) space set
+    (with global_model: the Eq. 4 energy, global model first)."""
     offsets = np.asarray(offsets, np.int64)
     sp_lo = int(np.searchsorted(offsets, lo, side="right") - 1)
     sp_hi = int(np.searchsorted(offsets, hi - 1, side="right") - 1)
     spaces = [oracle.Space(t, s) for t, s in wl_spaces[sp_lo:sp_hi + 1]]
     off = [0] + [int(offsets[w + 1]) - lo for w in range(sp_lo, sp_hi)] + [hi - lo]
     och = oracle.Chains(spaces, off, seed=seed, chain0=lo, topk=topk)
-    otr = och.run(ens_t, steps, oracle.thresholds(seed, lo, hi - lo, 0, steps), trace=True)
+    otr = och.run(ens_t, steps, oracle.thresholds(seed, lo, hi - lo, 0, steps), trace=True,
+                  global_model=global_model)
     return och, otr
 
 
@@ -49,11 +51,11 @@ def run_workload(P, name, n_per_space, steps):
     return wl, off, (fid, thr, leaf), ch, best, tr, plan
 
 
-def check_slices(P, wl, off, ens_t, ch, best, tr, steps, slices):
+def check_slices(P, wl, off, ens_t, ch, best, tr, steps, slices, global_model=None):
     cur = export(P, ch)
     for lo, hi in slices:
         say(f"oracle slice [{lo}, {hi})")
-        och, otr = oracle_slice(wl["spaces"], off, ens_t, wl["sa_seed"], wl["topk"], steps, lo, hi)
+        och, otr = oracle_slice(wl["spaces"], off, ens_t, wl["sa_seed"], wl["topk"], steps, lo, hi, global_model)
         assert_same_run(best, tr, och, otr, rows=slice(lo, hi), cur=cur)
 
 
@@ -91,3 +93,30 @@ def test_twelve_conv_sixteen_trees_every_chain(P):
     assert plan["path"] == P.AT_SA_PATH_TREES and plan["trees_per_wg"] == 16
     assert plan["slice_blocks"] > plan["waves"]
     check_slices(P, wl, off, ens_t, ch, best, tr, 3, [(0, int(off[-1]))])
+
+
+def test_twelve_conv_transfer_production_launch_sliced_oracle(P):
+    # the bench's Eq. 4 leg: the twelve-workload set, 12 x 512 chains x 500
+    # steps, a 1000-tree global model over the relation features beside the
+    # 1000-tree local model (two tree launches a step, the two folds
+    # interleaved in the chain kernel)
+    import torch
+    wl = W.WORKLOADS["resnet18_12conv_sa"]
+    spaces = [P.at_space_create(t, s) for t, s in wl["spaces"]]
+    off = W.chain_offsets(12, 512)
+    sset = P.at_spaceset_create(spaces, off)
+    loc = W.make_ensemble(wl["trees"], wl["depth"], 176, wl["ens_seed"])
+    glob = W.make_ensemble(wl["trees"], wl["depth"], P.RELATION_FEATURES, wl["ens_seed"] + 50)
+    n, steps, seed, k = int(off[-1]), wl["steps"], wl["sa_seed"], wl["topk"]
+    ch = P.at_chains_create(sset, 0, n, k, seed)
+    thr = torch.from_numpy(P.at_sa_thresholds(seed, 0, n, 0, steps)).to(DEV)
+    best = torch.zeros((n, k, 4), dtype=torch.int32, device=DEV)
+    trace = torch.zeros((n, steps, 4), dtype=torch.int32, device=DEV)
+    P.at_sa_run_global_local(sset, P.at_ensemble_create(*glob, P.RELATION_FEATURES), P.at_ensemble_create(*loc, 176),
+                             ch, steps, thr, best, trace)
+    torch.cuda.synchronize()
+    plan = P.at_chains_last_plan(ch)
+    say(f"transfer {n} chains x {steps} steps: plan {plan}")
+    assert plan["path"] == P.AT_SA_PATH_TREES
+    slices = [(0, 4)] + [(int(b) - 2, int(b) + 2) for b in off[1:-1:3]] + [(n - 4, n)]
+    check_slices(P, wl, off, loc, ch, P.entries(best), P.entries(trace), steps, slices, global_model=glob)
