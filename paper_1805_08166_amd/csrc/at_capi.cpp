@@ -72,7 +72,10 @@ at_status scan_constant_features(at_space_s& sp) {
     release(buf);
     if (e != hipSuccess) return hip_fail(e, "feature scan");
     sp.fconst.resize(F);
-    for (int f = 0; f < F; ++f) sp.fconst[f] = (host[f] != 0u || host[F + f] > 63u) ? 0xff : (uint8_t)host[F + f];
+    // a constant above the annealing features' range stays in the tile (the
+    // walk's threshold compare is exact only within that range)
+    for (int f = 0; f < F; ++f)
+        sp.fconst[f] = (host[f] != 0u || host[F + f] > SA_FEATURE_MAX) ? 0xff : (uint8_t)host[F + f];
     return AT_OK;
 }
 

@@ -44,8 +44,16 @@ __device__ __forceinline__ int64_t v_index(int64_t c, int t, int groups) {
 constexpr int CPW = 16;                 // chains per chain-kernel workgroup
 static_assert(CPW == 16 && CPW == STAGE_CHAINS, "a chain-kernel workgroup reads one 16-chain block of V");
 constexpr int FOLD_P = 32;              // 4-tree groups per fold pass: 32 x 16 chains x 16 B = 8 KB
-constexpr int FOLD_R = 6;               // passes in the LDS ring (five in flight while one is folded)
-constexpr size_t RING_BYTES = (size_t)FOLD_R * FOLD_P * CPW * 16;
+// Passes in the LDS ring: one model's fold keeps one pass in flight while
+// it adds the other (deeper rings measured slower: C12 chain kernel 16.3 us
+// with two passes, 16.6 with three, 16.7 with four, 17.1 with six); Eq. 4's
+// two folds take a pass of each at a time and keep a pair in flight.
+constexpr int FOLD_R1 = 2;
+constexpr int FOLD_R2 = 4;
+constexpr size_t PASS_BYTES = (size_t)FOLD_P * CPW * 16;
+__host__ __device__ constexpr size_t ring_bytes(bool two_models) {
+    return (two_models ? FOLD_R2 : FOLD_R1) * PASS_BYTES;
+}
 constexpr int KMAX = 64;                // largest best list
 constexpr size_t MAX_LDS_BYTES = 163840; // LDS of one compute unit
 
@@ -194,7 +202,7 @@ __device__ __forceinline__ void fold_pass(float& s, uint32_t ad) {
 
 // The leaf values of chain block c0 for fold pass p (groups p*FOLD_P ..,
 // one contiguous stretch of FOLD_P * CPW float4) moved by eight 1 KB
-// direct-to-LDS loads of the calling wave into ring buffer p % FOLD_R, so
+// direct-to-LDS loads of the calling wave into ring buffer p % FOLD_R1, so
 // that entry g * CPW + j holds group g of chain c0 + j.  Past the last
 // group the loads repeat the last float4 (never folded).
 __device__ __forceinline__ void ring_issue_buf(const float4* __restrict__ blk, int last, float4* ring, int p, int b,
@@ -210,7 +218,7 @@ __device__ __forceinline__ void ring_issue_buf(const float4* __restrict__ blk, i
 }
 
 __device__ __forceinline__ void ring_issue(const float4* __restrict__ blk, int last, float4* ring, int p, int lane) {
-    ring_issue_buf(blk, last, ring, p, p % FOLD_R, lane);
+    ring_issue_buf(blk, last, ring, p, p % FOLD_R1, lane);
 }
 
 // Wait until at most `later` passes of this wave's ring moves are
@@ -218,7 +226,8 @@ __device__ __forceinline__ void ring_issue(const float4* __restrict__ blk, int l
 // landed).
 #define AT_VM_WAIT(K) asm volatile("s_waitcnt vmcnt(" #K ")" ::: "memory")
 __device__ __forceinline__ void ring_wait(int later) {
-    static_assert(FOLD_P * CPW / 64 == 8 && FOLD_R == 6, "the waits below count eight moves per pass, at most five passes");
+    static_assert(FOLD_P * CPW / 64 == 8 && FOLD_R1 <= 6 && FOLD_R2 <= 6,
+                  "the waits below count eight moves per pass, at most five passes");
     switch (later) {
         case 0: AT_VM_WAIT(0); break;
         case 1: AT_VM_WAIT(8); break;
@@ -335,7 +344,7 @@ __device__ __forceinline__ void fold_pass2(float& sg, uint32_t ag, float& sl, ui
 // Score of the pending candidates of chain block c0 from one model's leaf
 // values V (T trees): lane j < nc of the calling wave adds its chain's
 // values in tree order (fp32, from +0.0f).  The wave alone moves the values
-// into the LDS ring, FOLD_R passes ahead, so no other wave takes part.
+// into the LDS ring, FOLD_R1 passes ahead, so no other wave takes part.
 // A pass's buffer is refilled at the start of the next pass, after its
 // reads have completed.
 __device__ __forceinline__ float fold_wave(const float* __restrict__ V, int T, int64_t c0, int nc, float4* ring,
@@ -345,7 +354,7 @@ __device__ __forceinline__ float fold_wave(const float* __restrict__ V, int T, i
     const float4* blk = reinterpret_cast<const float4*>(V) + (c0 >> 4) * (int64_t)groups * CPW;
     const int last = groups * CPW - 1;
     int issued = 0;
-    for (; issued < FOLD_R - 1 && issued < npass; ++issued) ring_issue(blk, last, ring, issued, lane);
+    for (; issued < FOLD_R1 - 1 && issued < npass; ++issued) ring_issue(blk, last, ring, issued, lane);
     float s = 0.0f;
     for (int p = 0; p < npass; ++p) {
         if (issued < npass) {
@@ -354,7 +363,7 @@ __device__ __forceinline__ float fold_wave(const float* __restrict__ V, int T, i
         }
         ring_wait(issued - 1 - p);
         if (lane < nc) {
-            const float4* src = ring + (p % FOLD_R) * (FOLD_P * CPW) + lane;
+            const float4* src = ring + (p % FOLD_R1) * (FOLD_P * CPW) + lane;
             fold_pass_any(s, src, pass_groups(groups, p), (p == npass - 1) ? (T & 3) : 0);
         }
     }
@@ -384,23 +393,23 @@ __device__ __forceinline__ void fold_wave2(const float* __restrict__ Vg, int Tg,
     auto issue = [&](int m) {
         bool glob;
         const int p = pass_of(m, glob);
-        ring_issue_buf(glob ? bg : bl, (glob ? gg : gl) * CPW - 1, ring, p, m % FOLD_R, lane);
+        ring_issue_buf(glob ? bg : bl, (glob ? gg : gl) * CPW - 1, ring, p, m % FOLD_R2, lane);
     };
     int issued = 0;
-    for (; issued < FOLD_R - 1 && issued < total; ++issued) issue(issued);
+    for (; issued < FOLD_R2 - 1 && issued < total; ++issued) issue(issued);
     sg = 0.0f;
     sl = 0.0f;
     for (int m = 0; m < total;) {
         const bool pair = m < 2 * pmin;
         const int use = pair ? 2 : 1;
         // a pass's buffer is free once the pass six before it was added
-        for (; issued < total && issued < m + FOLD_R; ++issued) issue(issued);
+        for (; issued < total && issued < m + FOLD_R2; ++issued) issue(issued);
         ring_wait(issued - m - use);
         if (lane < nc) {
             if (pair) {
                 const int p = m >> 1;
-                const float4* srcg = ring + (m % FOLD_R) * (FOLD_P * CPW) + lane;
-                const float4* srcl = ring + ((m + 1) % FOLD_R) * (FOLD_P * CPW) + lane;
+                const float4* srcg = ring + (m % FOLD_R2) * (FOLD_P * CPW) + lane;
+                const float4* srcl = ring + ((m + 1) % FOLD_R2) * (FOLD_P * CPW) + lane;
                 const int ngg = pass_groups(gg, p), ngl = pass_groups(gl, p);
                 const int rg = (p == npg - 1) ? (Tg & 3) : 0, rl = (p == npl - 1) ? (Tl & 3) : 0;
                 if (ngg == FOLD_P && ngl == FOLD_P && rg == 0 && rl == 0) {
@@ -412,7 +421,7 @@ __device__ __forceinline__ void fold_wave2(const float* __restrict__ Vg, int Tg,
             } else {
                 bool glob;
                 const int p = pass_of(m, glob);
-                const float4* src = ring + (m % FOLD_R) * (FOLD_P * CPW) + lane;
+                const float4* src = ring + (m % FOLD_R2) * (FOLD_P * CPW) + lane;
                 if (glob)
                     fold_pass_any(sg, src, pass_groups(gg, p), (p == npg - 1) ? (Tg & 3) : 0);
                 else
@@ -531,7 +540,7 @@ __global__ __launch_bounds__(CHAIN_WG) void k_chain(ChainArgs a) {
     const int gj = tid >> 4, gr = tid & 15;
     const uint64_t gmask = 0xffffull << (16 * (gj & 3));
     const bool gvalid = gj < nc;
-    at_entry* lists = reinterpret_cast<at_entry*>(ring + RING_BYTES / 16);
+    at_entry* lists = reinterpret_cast<at_entry*>(ring + ring_bytes(a.Vg != nullptr) / 16);
 
     // The workgroup's space: when all its chains share one space whose image
     // fits, the image (descriptor with rebased split offsets, then the split
@@ -1639,7 +1648,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
         return err;
 
     const unsigned chain_grid = (unsigned)((n + CPW - 1) / CPW);
-    const size_t chain_lds = RING_BYTES + (size_t)CPW * ch.topk * sizeof(at_entry);
+    const size_t chain_lds = ring_bytes(eg != nullptr) + (size_t)CPW * ch.topk * sizeof(at_entry);
     {
         const TreeArgs& ta = tl.ta;
         const int64_t tree_grid = (int64_t)(e.n_trees + ta.tpw - 1) / ta.tpw * ta.slices;
@@ -1654,7 +1663,7 @@ hipError_t launch_sa_tp(const at_space_s& sp, const EnsembleDesc& e, const Ensem
                               reinterpret_cast<const void*>(&k_chain<AT_TMPL_GEMM, 512>),
                               reinterpret_cast<const void*>(&k_chain<AT_TMPL_CONV2D_NCHW, 512>)}) {
             if ((err = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)(RING_BYTES + (size_t)CPW * KMAX * sizeof(at_entry)))) != hipSuccess)
+                                           (int)(ring_bytes(true) + (size_t)CPW * KMAX * sizeof(at_entry)))) != hipSuccess)
                 return err;
         }
         chain_configured = true;
