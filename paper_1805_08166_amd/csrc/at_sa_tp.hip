@@ -402,7 +402,7 @@ __device__ __forceinline__ void fold_wave2(const float* __restrict__ Vg, int Tg,
     for (int m = 0; m < total;) {
         const bool pair = m < 2 * pmin;
         const int use = pair ? 2 : 1;
-        // a pass's buffer is free once the pass six before it was added
+        // a pass's buffer is free once the pass FOLD_R2 before it was added
         for (; issued < total && issued < m + FOLD_R2; ++issued) issue(issued);
         ring_wait(issued - m - use);
         if (lane < nc) {
