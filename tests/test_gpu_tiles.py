@@ -145,3 +145,24 @@ def test_space_past_the_scan_limit_keeps_whole_tiles(P):
     och = oracle.Chains([osp], [0, n], seed=seed, chain0=0, topk=k)
     otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
     assert_same_run(best, tr, och, otr, cur=export(P, ch))
+
+
+def test_set_with_an_unscanned_member_keeps_whole_tiles(P):
+    # one member past the scan limit: nothing is known constant over the
+    # set, so its tiles keep all 44 quads; chains on both members compared
+    members = [(CONV_VT, (1, 2, 6, 6, 2, 1, 1, 0, 2)), (CONV_VT, W.conv_shape("C2"))]
+    ospaces = [oracle.Space(t, s) for t, s in members]
+    assert ospaces[1].n_configs > 1 << 28
+    spaces = [P.at_space_create(t, s) for t, s in members]
+    off = np.array([0, 64, 128], np.int64)
+    sset = P.at_spaceset_create(spaces, off)
+    fid, thr, leaf = W.make_ensemble(60, 6, 176, 63)
+    ens = P.at_ensemble_create(fid, thr, leaf, 176)
+    n, steps, seed, k = 128, 12, 29, 4
+    ch = mk_chains(P, sset, 0, n, k, seed, "trees")
+    best, tr = gpu_sa(P, sset, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
+    plan = P.at_chains_last_plan(ch)
+    assert plan["path"] == P.AT_SA_PATH_TREES and plan["tile_quads"] == 44
+    och = oracle.Chains(ospaces, off, seed=seed, chain0=0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
