@@ -68,6 +68,11 @@ CASES = {
     "set": [(W.CONV2D, (1, 2, 6, 6, 2, 1, 1, 0, 2)), (W.CONV2D, (1, 2, 4, 4, 2, 1, 1, 0, 1))],
     # 145 vary over this set: 37 quads, a 16 KB slot as for all 44
     "set_wide": [(W.CONV2D, (1, 2, 6, 6, 2, 1, 1, 0, 2)), (W.CONV2D, (1, 2, 6, 6, 2, 3, 3, 1, 1))],
+    # degenerate spaces: six configurations (only the unroll knobs move),
+    # 10 features vary, 3 quads in a 1 KB slot; twelve configurations, 29
+    # vary, 8 quads in a 2 KB slot
+    "tiny_six": [(W.CONV2D, (1, 1, 1, 1, 1, 1, 1, 0, 1))],
+    "tiny_twelve": [(W.CONV2D, (1, 2, 1, 1, 1, 1, 1, 0, 1))],
 }
 
 
