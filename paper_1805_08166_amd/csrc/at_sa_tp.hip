@@ -1194,8 +1194,8 @@ __device__ __forceinline__ void walk_tail(const uint8_t* __restrict__ L, const T
 // the next unclaimed block from a counter in LDS, so waves that share a
 // SIMD with fewer others take more blocks.
 // QT: the tile's quads when known at compile time (the whole-feature tiles),
-// else 0 (a.q).
-template <int DEPTH, int QT>
+// else 0 (a.q).  ONE: the plan puts one group of G trees on each workgroup.
+template <int DEPTH, int QT, bool ONE>
 __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     constexpr int G = 8;
     const int tq = QT ? QT : a.q;
@@ -1285,6 +1285,16 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
     // it is never waited for, and no wave holds a block it has not started
     // while others run out of work.
     bool first = true;
+    // When a workgroup's trees are one group of G (tree index a multiple of
+    // four, so a lane's values go out as two 16-byte stores), a block's leaf
+    // values are stored after the next block's fill is issued: the wait for
+    // the fill (memory operations complete in the order they were issued)
+    // then leaves those two stores in flight.  Every block has an active
+    // lane 0, so both stores are always issued.
+    const bool defer = ONE && ROOTS && nt == G && (t0 & 3) == 0;
+    uint32_t pv[G];
+    int64_t pc = 0;
+    bool pact = false, pend = false;
     while (r < nblk) {
         // every earlier read of this wave's tile has returned before the
         // tile is overwritten (s_waitcnt lgkmcnt(0))
@@ -1293,7 +1303,13 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
         const int64_t b = b_first + r;
         if (!first) {
             fill(b);
-            __builtin_amdgcn_s_waitcnt(0);
+            if (pend) {
+                if (pact) store_vals<G>(a, t0, pc, pv);
+                __builtin_amdgcn_s_waitcnt(0x0002);     // vmcnt(2) expcnt(0) lgkmcnt(0)
+                pend = false;
+            } else {
+                __builtin_amdgcn_s_waitcnt(0);
+            }
         }
         first = false;
         const int64_t c = b * 64 + lane;
@@ -1304,13 +1320,22 @@ __global__ __launch_bounds__(TREE_WAVES_MAX * 64) void k_trees(TreeArgs a) {
 #pragma unroll
             for (int g = 0; g < G; ++g) nbr[g] = 0u;
             walk8_roll<(ROOTS ? DEPTH : 2), true>(L, nbr, fb, a.mask, rnode, rlo, rhi, v);
-            if (active) store_vals<G>(a, t0, c, v);
+            if (defer) {
+#pragma unroll
+                for (int g = 0; g < G; ++g) pv[g] = v[g];
+                pc = c;
+                pact = active;
+                pend = true;
+            } else if (active) {
+                store_vals<G>(a, t0, c, v);
+            }
             t = G;
         }
         for (; t + G <= nt; t += G) walk_group<DEPTH, G>(L, a, t, t0 + t, fb, c, active);
         walk_tail<DEPTH, G / 2>(L, a, t, t0 + t, nt - t, fb, c, active);
         r = (int64_t)__builtin_amdgcn_readfirstlane(claim);
     }
+    if (pend && pact) store_vals<G>(a, t0, pc, pv);
 }
 
 // The pointer form relocated for one LDS plan and tile layout.  Word j of a
@@ -1409,7 +1434,7 @@ bool plan_trees(int depth, int Q, uint32_t slot, int nw, int tpw, bool in_slot, 
     return true;
 }
 
-template <int DEPTH, int QT>
+template <int DEPTH, int QT, bool ONE>
 hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     const int grid = (a.n_trees + a.tpw - 1) / a.tpw * a.slices;
     static bool checked = false;
@@ -1417,36 +1442,45 @@ hipError_t launch_trees_t(const TreeArgs& a, int nw, hipStream_t stream, hipEven
         // the walk's asm takes offsets into the kernel's LDS array as LDS
         // addresses: the array must be the kernel's only LDS object
         hipFuncAttributes fa;
-        hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(&k_trees<DEPTH, QT>));
+        hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(&k_trees<DEPTH, QT, ONE>));
         if (e != hipSuccess) return e;
         if (fa.sharedSizeBytes != MAX_LDS_BYTES) return hipErrorInvalidKernelFile;
         checked = true;
     }
     if (start)
-        hipExtLaunchKernelGGL((k_trees<DEPTH, QT>), dim3(grid), dim3(nw * 64), 0, stream, start, stop, 0, a);
+        hipExtLaunchKernelGGL((k_trees<DEPTH, QT, ONE>), dim3(grid), dim3(nw * 64), 0, stream, start, stop, 0, a);
     else
-        hipLaunchKernelGGL((k_trees<DEPTH, QT>), dim3(grid), dim3(nw * 64), 0, stream, a);
+        hipLaunchKernelGGL((k_trees<DEPTH, QT, ONE>), dim3(grid), dim3(nw * 64), 0, stream, a);
     return hipGetLastError();
 }
 
+template <int QT, bool ONE>
+hipError_t launch_trees_o(const TreeArgs& a, int depth, int nw, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop) {
+    switch (depth) {
+        case 1: return launch_trees_t<1, QT, ONE>(a, nw, stream, start, stop);
+        case 2: return launch_trees_t<2, QT, ONE>(a, nw, stream, start, stop);
+        case 3: return launch_trees_t<3, QT, ONE>(a, nw, stream, start, stop);
+        case 4: return launch_trees_t<4, QT, ONE>(a, nw, stream, start, stop);
+        case 5: return launch_trees_t<5, QT, ONE>(a, nw, stream, start, stop);
+        case 6: return launch_trees_t<6, QT, ONE>(a, nw, stream, start, stop);
+        case 7: return launch_trees_t<7, QT, ONE>(a, nw, stream, start, stop);
+        case 8: return launch_trees_t<8, QT, ONE>(a, nw, stream, start, stop);
+        case 9: return launch_trees_t<9, QT, ONE>(a, nw, stream, start, stop);
+        case 10: return launch_trees_t<10, QT, ONE>(a, nw, stream, start, stop);
+        case 11: return launch_trees_t<11, QT, ONE>(a, nw, stream, start, stop);
+        case 12: return launch_trees_t<12, QT, ONE>(a, nw, stream, start, stop);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+// Workgroups of one group of trees (eight) keep a block's leaf values until
+// the next block's fill is issued.
 template <int QT>
 hipError_t launch_trees_q(const TreeArgs& a, int depth, int nw, hipStream_t stream, hipEvent_t start,
                           hipEvent_t stop) {
-    switch (depth) {
-        case 1: return launch_trees_t<1, QT>(a, nw, stream, start, stop);
-        case 2: return launch_trees_t<2, QT>(a, nw, stream, start, stop);
-        case 3: return launch_trees_t<3, QT>(a, nw, stream, start, stop);
-        case 4: return launch_trees_t<4, QT>(a, nw, stream, start, stop);
-        case 5: return launch_trees_t<5, QT>(a, nw, stream, start, stop);
-        case 6: return launch_trees_t<6, QT>(a, nw, stream, start, stop);
-        case 7: return launch_trees_t<7, QT>(a, nw, stream, start, stop);
-        case 8: return launch_trees_t<8, QT>(a, nw, stream, start, stop);
-        case 9: return launch_trees_t<9, QT>(a, nw, stream, start, stop);
-        case 10: return launch_trees_t<10, QT>(a, nw, stream, start, stop);
-        case 11: return launch_trees_t<11, QT>(a, nw, stream, start, stop);
-        case 12: return launch_trees_t<12, QT>(a, nw, stream, start, stop);
-        default: return hipErrorInvalidValue;
-    }
+    return a.tpw == 8 ? launch_trees_o<QT, true>(a, depth, nw, stream, start, stop)
+                      : launch_trees_o<QT, false>(a, depth, nw, stream, start, stop);
 }
 
 // Whole-feature tiles (GEMM and conv2d loop-context rows, relation rows)
