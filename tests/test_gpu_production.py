@@ -17,7 +17,7 @@ import pytest
 
 import oracle
 import workloads as W
-from test_gpu_parity import DEV, P, assert_same_run, export, gpu_sa, say  # noqa: F401
+from test_gpu_parity import DEV, P, assert_same_run, export, gpu_sa, mk_chains, say  # noqa: F401
 
 pytestmark = pytest.mark.gpu
 
@@ -84,6 +84,28 @@ def test_c12_ensemble_block_claiming_every_chain(P):
     wl, off, ens_t, ch, best, tr, plan = run_workload(P, "conv_c12_sa", 1024, 4)
     assert plan["path"] == P.AT_SA_PATH_TREES and plan["slice_blocks"] > plan["waves"]
     check_slices(P, wl, off, ens_t, ch, best, tr, 4, [(0, 1024)])
+
+
+def test_one_group_form_with_ragged_trees_and_chains(P):
+    # eight trees a workgroup, the form in which a block's leaf values are
+    # stored after the next block's fill is issued: 2005 trees leave a last
+    # workgroup of five (its values go out at once), 1000 chains a last
+    # block of 40 active lanes, and 16 blocks against the waves make every
+    # wave carry values over from one block to the next
+    t, s = W.WORKLOADS["conv_c12_sa"]["spaces"][0]
+    sp = P.at_space_create(t, s)
+    fid, thr, leaf = W.make_ensemble(2005, 10, 176, 71)
+    ens = P.at_ensemble_create(fid, thr, leaf, 176)
+    n, steps, seed, k = 1000, 4, 31, 8
+    ch = mk_chains(P, sp, 0, n, k, seed, "trees")
+    best, tr = gpu_sa(P, sp, ens, ch, steps, P.at_sa_thresholds(seed, 0, n, 0, steps))
+    plan = P.at_chains_last_plan(ch)
+    say(f"2005 trees, {n} chains: plan {plan}")
+    assert plan["path"] == P.AT_SA_PATH_TREES and plan["trees_per_wg"] == 8
+    assert plan["slice_blocks"] > plan["waves"]
+    och = oracle.Chains([oracle.Space(t, s)], [0, n], seed=seed, chain0=0, topk=k)
+    otr = och.run((fid, thr, leaf), steps, oracle.thresholds(seed, 0, n, 0, steps), trace=True)
+    assert_same_run(best, tr, och, otr, cur=export(P, ch))
 
 
 def test_twelve_conv_sixteen_trees_every_chain(P):
